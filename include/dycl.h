@@ -1,0 +1,145 @@
+/*
+ * dycl.h - C ABI of the batched dynamic-routing executor for MI355X (gfx950).
+ *
+ * DyCL (ISSTA'23, arXiv 2307.04963) compiles a dynamic neural network into
+ * conditional-free sub-networks plus a host program that keeps the
+ * conditionals and calls the compiled pieces (Sec. 5, Fig. 5 steps 1-5).
+ * The host program must be semantically identical to the dynamic network
+ * for every input (Sec. 5, Eq. 2) and is called like a compiled module:
+ * set the input, run, read the output (Listing 2; Sec. 5: "call the API
+ * using a similar way").  This library executes that compiled form on a
+ * BATCH: each sample follows the branch its own decision selects, the
+ * samples of one branch are compacted into a packed buffer, and the host
+ * code reads only the per-branch counts.
+ *
+ * The plan is built from a specification whose nodes are the two kinds of
+ * node of the paper's heterogeneous control-flow graph (Sec. 5.3): runs of
+ * tensor statements (sub-DNNs) and single logic statements.  Shapes are
+ * propagated from the input in topological order, a logic node keeping its
+ * predecessor's shape (Alg. 2).
+ *
+ * Threading: calls on different plans may run concurrently; one plan runs
+ * one batch at a time.  No C++ exception crosses this interface; the
+ * library never aborts the process.  Every function returns a dycl_status
+ * (0 on success); the message of the calling thread's last failure is
+ * available from dycl_last_error().
+ */
+#ifndef DYCL_H_
+#define DYCL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct dycl_plan dycl_plan; /* opaque; owns device weights + workspace */
+
+typedef enum {
+  DYCL_OK = 0,
+  DYCL_E_INVALID = -1, /* null pointer, bad argument, misaligned buffer    */
+  DYCL_E_SPEC = -2,    /* specification does not parse or is inconsistent */
+  DYCL_E_WEIGHTS = -3, /* weight blob too small for what the spec reads   */
+  DYCL_E_BATCH = -4,   /* batch < 0 or batch > max_batch                  */
+  DYCL_E_OOM = -5,     /* device memory allocation failed                 */
+  DYCL_E_HIP = -6      /* a HIP runtime call failed (message has details) */
+} dycl_status;
+
+/* Per-sample record of what the dynamic network did (16 bytes). */
+typedef struct {
+  int32_t exit_index;  /* 0-based exit head that produced the logits; -1 if none */
+  int32_t iterations;  /* bounded-loop steps executed (1..max_steps); 0 if no loop */
+  uint64_t skip_mask;  /* bit i set <=> gate i chose the identity / shortcut path */
+} dycl_record;
+
+/*
+ * Build a plan (the paper's sub-DNN compilation, Alg. 2, for a fixed
+ * maximum batch).
+ *   spec_json     NUL-terminated JSON specification: the input shape and
+ *                 dtype, and a list of nodes - "conv" (convolution or
+ *                 linear layer with folded BatchNorm / bias, optional
+ *                 residual, ReLU or GELU), "maxpool", "exit" (global
+ *                 average pool, linear head, softmax, confidence test),
+ *                 "gate" (pool, linear, sigmoid, run a sub-list of nodes
+ *                 on the samples that execute), "halt" (halting unit of a
+ *                 bounded loop, unrolled) and "output" (final linear on the
+ *                 loop's parked states).  Copied, not retained.
+ *   weights       host pointer to the weight blob the spec's offsets index;
+ *                 copied to the device, not retained.
+ *   weights_bytes size of that blob.
+ *   max_batch     largest batch a later dycl_run may pass (>= 1); the
+ *                 workspace is sized for it.
+ *   device        HIP device ordinal.
+ *   out           receives the plan; set to NULL on failure.
+ * The spec and the blob size are validated before any HIP call.
+ */
+int dycl_plan_create(const char* spec_json, const void* weights, size_t weights_bytes, int max_batch,
+                     int device, dycl_plan** out);
+
+/*
+ * Run one batch (asynchronously on `hip_stream`, a hipStream_t; NULL is the
+ * default stream).
+ *   x_dev       device pointer, [batch, per-sample input] in the spec's
+ *               input dtype (bf16 NHWC images or vectors; fp32 for fp32
+ *               specs), 16-byte aligned, caller-owned.
+ *   batch       0 <= batch <= max_batch; 0 returns immediately.
+ *   aux_dev     device fp32 [batch] per-sample scalars for specs that read
+ *               them (a halting bias), else may be NULL.
+ *   logits_dev  device fp32 [batch, n_out], written in the original sample
+ *               order.
+ *   records_dev device dycl_record [batch], original order.
+ * The host code waits only for the per-decision branch counts; when the call
+ * returns, the remaining work may still be queued on the stream.  Results are
+ * valid after the stream is synchronised.
+ */
+int dycl_run(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev, float* logits_dev,
+             dycl_record* records_dev, void* hip_stream);
+
+/*
+ * Branch counts of the last dycl_run: for decision point d (in program
+ * order, loop steps unrolled) counts[2d] = samples that took the "true"
+ * branch (exit / execute / halt) and counts[2d+1] = the others; decisions
+ * the batch never reached read 0.  Writes min(n, 2 * decisions) entries and
+ * returns the number of decision points.
+ */
+int dycl_last_counts(const dycl_plan* plan, int32_t* counts, int n);
+
+/*
+ * Plan facts, info[0..n): 0 n_out, 1 input bytes per sample, 2 decision
+ * points, 3 device workspace bytes, 4 device weight bytes, 5 max_batch,
+ * 6 aux required (0/1), 7 number of nodes.  Returns the number written.
+ */
+int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n);
+
+/*
+ * Per-kernel-class timing of later runs: when enabled, every kernel launch
+ * of dycl_run is bracketed by HIP events on its stream and its algorithmic
+ * work (FLOPs of the executed rows, bytes it must move) is accumulated.
+ * dycl_profile_read fills up to `cap` rows of
+ *   { launches, total_ms, flops, bytes }  (4 doubles per row)
+ * for the classes named by dycl_profile_class(i) and returns the number of
+ * classes.  Reading synchronises the plan's last stream.
+ */
+int dycl_profile_enable(dycl_plan* plan, int on);
+int dycl_profile_read(dycl_plan* plan, double* rows, int cap);
+const char* dycl_profile_class(int i);
+
+/*
+ * Host-only validation of a spec against a blob size and a batch bound (no
+ * HIP call): parses, checks every reference and weight range, propagates
+ * shapes, and writes a one-line summary into `summary` (may be NULL).
+ */
+int dycl_spec_check(const char* spec_json, size_t weights_bytes, int max_batch, char* summary, size_t cap);
+
+/* Releases the plan's device memory; NULL-safe. */
+void dycl_plan_destroy(dycl_plan* plan);
+
+/* Message of the calling thread's last failure ("" if none). */
+const char* dycl_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DYCL_H_ */

@@ -1,0 +1,72 @@
+"""ctypes binding of libdycl.so: the same names as include/dycl.h.
+
+Argument marshalling only.  The library is loaded from this package's
+directory; if it is missing, importing the binding raises at once (there is
+no fallback path).
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdycl.so")
+
+DYCL_OK = 0
+STATUS = {0: "DYCL_OK", -1: "DYCL_E_INVALID", -2: "DYCL_E_SPEC", -3: "DYCL_E_WEIGHTS", -4: "DYCL_E_BATCH",
+          -5: "DYCL_E_OOM", -6: "DYCL_E_HIP"}
+
+# every symbol include/dycl.h declares
+EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_last_counts", "dycl_plan_info", "dycl_profile_enable",
+           "dycl_profile_read", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
+
+
+class DyclError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Record(C.Structure):
+    _fields_ = [("exit_index", C.c_int32), ("iterations", C.c_int32), ("skip_mask", C.c_uint64)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2307_04963_amd.build` (needs hipcc)")
+    lib = C.CDLL(LIB_PATH)
+    vp, i32, i64p = C.c_void_p, C.c_int, C.POINTER(C.c_int64)
+    lib.dycl_plan_create.argtypes = [C.c_char_p, vp, C.c_size_t, i32, i32, C.POINTER(vp)]
+    lib.dycl_plan_create.restype = i32
+    lib.dycl_run.argtypes = [vp, vp, i32, vp, vp, vp, vp]
+    lib.dycl_run.restype = i32
+    lib.dycl_last_counts.argtypes = [vp, C.POINTER(C.c_int32), i32]
+    lib.dycl_last_counts.restype = i32
+    lib.dycl_plan_info.argtypes = [vp, i64p, i32]
+    lib.dycl_plan_info.restype = i32
+    lib.dycl_profile_enable.argtypes = [vp, i32]
+    lib.dycl_profile_enable.restype = i32
+    lib.dycl_profile_read.argtypes = [vp, C.POINTER(C.c_double), i32]
+    lib.dycl_profile_read.restype = i32
+    lib.dycl_profile_class.argtypes = [i32]
+    lib.dycl_profile_class.restype = C.c_char_p
+    lib.dycl_spec_check.argtypes = [C.c_char_p, C.c_size_t, i32, C.c_char_p, C.c_size_t]
+    lib.dycl_spec_check.restype = i32
+    lib.dycl_plan_destroy.argtypes = [vp]
+    lib.dycl_plan_destroy.restype = None
+    lib.dycl_last_error.argtypes = []
+    lib.dycl_last_error.restype = C.c_char_p
+    return lib
+
+
+lib = _load()
+
+
+def check(rc: int) -> int:
+    if rc < 0:
+        raise DyclError(rc, lib.dycl_last_error().decode())
+    return rc
+
+
+def last_error() -> str:
+    return lib.dycl_last_error().decode()

@@ -1,0 +1,171 @@
+// C ABI: argument checks, error mapping, and the thread-local message.
+// Nothing thrown inside the library crosses this boundary.
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "plan.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+bool valid(const dycl_plan* p) { return p != nullptr && p->magic == 0x44594350u; }
+
+const char* kClassNames[dycl::P_COUNT] = {"conv_bf16_mfma", "linear_f32", "decision_heads", "compaction",
+                                          "gather_scatter", "maxpool", "misc"};
+
+template <class F>
+int guarded(F&& f) {
+  try {
+    return f();
+  } catch (const dycl::WeightsError& e) {
+    return fail(DYCL_E_WEIGHTS, e.what());
+  } catch (const dycl::SpecError& e) {
+    return fail(DYCL_E_SPEC, e.what());
+  } catch (const dycl::OomError& e) {
+    return fail(DYCL_E_OOM, e.what());
+  } catch (const dycl::HipError& e) {
+    return fail(DYCL_E_HIP, e.what());
+  } catch (const std::bad_alloc&) {
+    return fail(DYCL_E_OOM, "host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(DYCL_E_INVALID, e.what());
+  } catch (...) {
+    return fail(DYCL_E_INVALID, "unknown failure");
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+int dycl_plan_create(const char* spec_json, const void* weights, size_t weights_bytes, int max_batch, int device,
+                     dycl_plan** out) {
+  if (out) *out = nullptr;
+  if (!spec_json || !out) return fail(DYCL_E_INVALID, "dycl_plan_create: null spec or out pointer");
+  if (!weights && weights_bytes) return fail(DYCL_E_INVALID, "dycl_plan_create: null weights");
+  if (max_batch < 1) return fail(DYCL_E_BATCH, "dycl_plan_create: max_batch must be >= 1");
+  if (device < 0) return fail(DYCL_E_INVALID, "dycl_plan_create: negative device");
+  dycl_plan* p = new (std::nothrow) dycl_plan();
+  if (!p) return fail(DYCL_E_OOM, "host allocation failed");
+  p->device = device;
+  p->max_batch = max_batch;
+  int rc = guarded([&] { return dycl::plan_build(p, spec_json, weights, weights_bytes); });
+  if (rc != DYCL_OK) {
+    dycl::plan_free(p);
+    p->magic = 0;
+    delete p;
+    return rc;
+  }
+  *out = p;
+  g_err.clear();
+  return DYCL_OK;
+}
+
+int dycl_run(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev, float* logits_dev,
+             dycl_record* records_dev, void* hip_stream) {
+  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_run: invalid plan handle");
+  if (batch < 0 || batch > plan->max_batch)
+    return fail(DYCL_E_BATCH, "dycl_run: batch " + std::to_string(batch) + " outside [0, " +
+                                  std::to_string(plan->max_batch) + "]");
+  if (batch == 0) return DYCL_OK;
+  if (!x_dev || !logits_dev || !records_dev) return fail(DYCL_E_INVALID, "dycl_run: null input or output pointer");
+  if (plan->spec.aux && !aux_dev) return fail(DYCL_E_INVALID, "dycl_run: this plan reads per-sample aux inputs");
+  if ((reinterpret_cast<uintptr_t>(x_dev) & 15) || (reinterpret_cast<uintptr_t>(logits_dev) & 3) ||
+      (reinterpret_cast<uintptr_t>(records_dev) & 7))
+    return fail(DYCL_E_INVALID, "dycl_run: x must be 16-byte aligned, logits 4, records 8");
+  return guarded([&] {
+    dycl::plan_run(plan, x_dev, batch, aux_dev, logits_dev, records_dev, static_cast<hipStream_t>(hip_stream));
+    return DYCL_OK;
+  });
+}
+
+int dycl_last_counts(const dycl_plan* plan, int32_t* counts, int n) {
+  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_last_counts: invalid plan handle");
+  if (n < 0 || (n > 0 && !counts)) return fail(DYCL_E_INVALID, "dycl_last_counts: bad buffer");
+  const int total = 2 * plan->spec.decisions;
+  for (int i = 0; i < n && i < total; ++i) counts[i] = plan->h_counts[i];
+  return plan->spec.decisions;
+}
+
+int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n) {
+  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_plan_info: invalid plan handle");
+  if (n < 0 || (n > 0 && !info)) return fail(DYCL_E_INVALID, "dycl_plan_info: bad buffer");
+  const dycl::Spec& sp = plan->spec;
+  const dycl::TensorInfo& in = sp.tensors[sp.input];
+  const int64_t v[8] = {sp.n_out,
+                        static_cast<int64_t>(in.row_bytes(sp.dt)),
+                        sp.decisions,
+                        static_cast<int64_t>(plan->workspace_bytes),
+                        static_cast<int64_t>(plan->weight_bytes),
+                        plan->max_batch,
+                        sp.aux ? 1 : 0,
+                        sp.nodes_total};
+  int w = 0;
+  for (; w < n && w < 8; ++w) info[w] = v[w];
+  return w;
+}
+
+int dycl_profile_enable(dycl_plan* plan, int on) {
+  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_profile_enable: invalid plan handle");
+  return guarded([&] {
+    dycl::profile_flush(plan);
+    for (auto& r : plan->prof) r = dycl::ProfileRow();
+    plan->profile = on != 0;
+    return DYCL_OK;
+  });
+}
+
+int dycl_profile_read(dycl_plan* plan, double* rows, int cap) {
+  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_profile_read: invalid plan handle");
+  if (cap < 0 || (cap > 0 && !rows)) return fail(DYCL_E_INVALID, "dycl_profile_read: bad buffer");
+  int rc = guarded([&] {
+    hipSetDevice(plan->device);
+    dycl::profile_flush(plan);
+    return DYCL_OK;
+  });
+  if (rc != DYCL_OK) return rc;
+  for (int c = 0; c < dycl::P_COUNT && c < cap; ++c) {
+    rows[4 * c + 0] = plan->prof[c].launches;
+    rows[4 * c + 1] = plan->prof[c].ms;
+    rows[4 * c + 2] = plan->prof[c].flops;
+    rows[4 * c + 3] = plan->prof[c].bytes;
+  }
+  return dycl::P_COUNT;
+}
+
+const char* dycl_profile_class(int i) {
+  if (i < 0 || i >= dycl::P_COUNT) return "";
+  return kClassNames[i];
+}
+
+int dycl_spec_check(const char* spec_json, size_t weights_bytes, int max_batch, char* summary, size_t cap) {
+  if (!spec_json) return fail(DYCL_E_INVALID, "dycl_spec_check: null spec");
+  if (max_batch < 1) return fail(DYCL_E_BATCH, "dycl_spec_check: max_batch must be >= 1");
+  return guarded([&] {
+    dycl::Spec sp;
+    sp.parse(spec_json, weights_bytes, max_batch);
+    if (summary && cap) {
+      std::strncpy(summary, sp.summary.c_str(), cap - 1);
+      summary[cap - 1] = '\0';
+    }
+    return DYCL_OK;
+  });
+}
+
+void dycl_plan_destroy(dycl_plan* plan) {
+  if (!valid(plan)) return;
+  dycl::plan_free(plan);
+  plan->magic = 0;
+  delete plan;
+}
+
+const char* dycl_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

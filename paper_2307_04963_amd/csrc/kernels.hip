@@ -1,0 +1,410 @@
+// Decision heads, stream compaction, row movement and small kernels for
+// gfx950.  The logic nodes of the compiled network (Sec. 5.3: a node that
+// holds a single conditional reading an intermediate tensor, Sec. 2.2) are
+// evaluated here per sample, on the device, for a whole batch at once; the
+// branch each sample takes is then materialised by a stable compaction and
+// row gathers, so the next sub-network runs on a packed subset.
+#include "kernels.hpp"
+
+namespace dycl {
+namespace k {
+
+namespace {
+
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Sum over HW of one row [HW, C] (bf16) into per-channel floats in `red`
+// (shared, C floats).  256 threads; C is a power of two >= 8 and <= 2048.
+__device__ void row_channel_sums(const uint16_t* __restrict__ x, int HW, int C, float* red, float* part) {
+  const int tid = threadIdx.x;
+  const int C8 = C >> 3;              // 16-byte vectors per position
+  const int PG = 256 / C8 > 0 ? 256 / C8 : 1;
+  const int cv = tid % C8, pg = tid / C8;
+  float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (pg < PG) {
+    for (int pos = pg; pos < HW; pos += PG) {
+      const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)pos * C + cv * 8);
+      s[0] += __uint_as_float(v.x << 16);
+      s[1] += __uint_as_float(v.x & 0xffff0000u);
+      s[2] += __uint_as_float(v.y << 16);
+      s[3] += __uint_as_float(v.y & 0xffff0000u);
+      s[4] += __uint_as_float(v.z << 16);
+      s[5] += __uint_as_float(v.z & 0xffff0000u);
+      s[6] += __uint_as_float(v.w << 16);
+      s[7] += __uint_as_float(v.w & 0xffff0000u);
+    }
+  }
+  // part: [PG][C]
+  if (pg < PG) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) part[pg * C + cv * 8 + j] = s[j];
+  }
+  __syncthreads();
+  for (int c = tid; c < C; c += 256) {
+    float t = 0.f;
+    for (int g = 0; g < PG; ++g) t += part[g * C + c];
+    red[c] = t;
+  }
+  __syncthreads();
+}
+
+}  // namespace
+
+// ----------------------------------------------------------------- GAP ----
+
+__global__ __launch_bounds__(256) void gap_kernel(const uint16_t* __restrict__ x, int HW, int C, float* G) {
+  __shared__ float part[2048];
+  __shared__ float red[2048];
+  const int r = blockIdx.x;
+  row_channel_sums(x + (size_t)r * HW * C, HW, C, red, part);
+  const float inv = 1.0f / static_cast<float>(HW);
+  for (int c = threadIdx.x; c < C; c += 256) G[(size_t)r * C + c] = red[c] * inv;
+}
+
+void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, hipStream_t s) {
+  hipLaunchKernelGGL(gap_kernel, dim3(n), dim3(256), 0, s, x, HW, C, G);
+}
+
+// -------------------------------------------------------------- linear ----
+
+__global__ __launch_bounds__(256) void linear_f32_kernel(const float* __restrict__ X, int n, int K,
+                                                         const float* __restrict__ W, const float* __restrict__ bias,
+                                                         int N, int act, float* __restrict__ Y) {
+  __shared__ float Xs[16][68];
+  __shared__ float Ws[16][68];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64;
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+  for (int k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = threadIdx.x + i * 256;
+      const int rr = e >> 4, kk = e & 15;
+      Xs[kk][rr] = (m0 + rr < n && k0 + kk < K) ? X[(size_t)(m0 + rr) * K + k0 + kk] : 0.f;
+      Ws[kk][rr] = (n0 + rr < N && k0 + kk < K) ? W[(size_t)(n0 + rr) * K + k0 + kk] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = Xs[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Ws[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i;
+    if (m >= n) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = n0 + tx * 4 + j;
+      if (c >= N) continue;
+      float v = acc[i][j] + (bias ? bias[c] : 0.f);
+      if (act == ACT_RELU) v = v > 0.f ? v : 0.f;
+      Y[(size_t)m * N + c] = v;
+    }
+  }
+}
+
+void linear_f32(const float* X, int n, int K, const float* W, const float* bias, int N, int act, float* Y,
+                hipStream_t s) {
+  dim3 grid((n + 63) / 64, (N + 63) / 64);
+  hipLaunchKernelGGL(linear_f32_kernel, grid, dim3(256), 0, s, X, n, K, W, bias, N, act, Y);
+}
+
+// --------------------------------------------------------- exit decide ----
+
+__global__ __launch_bounds__(64) void exit_decide_kernel(const float* __restrict__ Z, int ncls,
+                                                         const float* __restrict__ Tp, float tau, int final_, int head,
+                                                         const int32_t* __restrict__ orig, uint8_t* flags,
+                                                         float* __restrict__ logits, int n_out, dycl_record* rec) {
+  const int r = blockIdx.x, lane = threadIdx.x;
+  const float* z = Z + (size_t)r * ncls;
+  bool ex = final_ != 0;
+  if (!ex) {
+    const float T = *Tp;
+    float m = -INFINITY;
+    for (int j = lane; j < ncls; j += 64) m = fmaxf(m, z[j]);
+    m = wave_max(m);
+    float s = 0.f;
+    for (int j = lane; j < ncls; j += 64) s += expf((z[j] - m) / T);
+    s = wave_sum(s);
+    ex = (1.0f / s) >= tau;
+  }
+  if (ex) {
+    const int o = orig ? orig[r] : r;
+    for (int j = lane; j < ncls; j += 64) logits[(size_t)o * n_out + j] = z[j];
+    if (lane == 0 && head >= 0) rec[o].exit_index = head;
+  }
+  if (lane == 0) flags[r] = ex ? 1 : 0;
+}
+
+void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int final_, int head, const int32_t* orig,
+                 uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s) {
+  hipLaunchKernelGGL(exit_decide_kernel, dim3(n), dim3(64), 0, s, Z, ncls, T, tau, final_, head, orig, flags,
+                     logits, n_out, rec);
+}
+
+// ---------------------------------------------------------------- gate ----
+
+__global__ __launch_bounds__(256) void gate_kernel(const uint16_t* __restrict__ x, int HW, int C,
+                                                   const float* __restrict__ u, const float* __restrict__ v,
+                                                   float thr, int gate, const int32_t* __restrict__ orig,
+                                                   uint8_t* flags, dycl_record* rec) {
+  __shared__ float part[2048];
+  __shared__ float red[2048];
+  __shared__ float wsum[4];
+  const int r = blockIdx.x;
+  row_channel_sums(x + (size_t)r * HW * C, HW, C, red, part);
+  const float inv = 1.0f / static_cast<float>(HW);
+  float d = 0.f;
+  for (int c = threadIdx.x; c < C; c += 256) d = fmaf(u[c], red[c] * inv, d);
+  d = wave_sum(d);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = d;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float pre = wsum[0] + wsum[1] + wsum[2] + wsum[3] + *v;
+    const float q = 1.0f / (1.0f + expf(-pre));
+    const bool run = q > thr;
+    flags[r] = run ? 1 : 0;
+    if (!run) {
+      const int o = orig ? orig[r] : r;
+      rec[o].skip_mask |= (1ull << gate);
+    }
+  }
+}
+
+void gate_head(const uint16_t* x, int n, int HW, int C, const float* u, const float* v, float thr, int gate,
+               const int32_t* orig, uint8_t* flags, dycl_record* rec, hipStream_t s) {
+  hipLaunchKernelGGL(gate_kernel, dim3(n), dim3(256), 0, s, x, HW, C, u, v, thr, gate, orig, flags, rec);
+}
+
+// ---------------------------------------------------------------- halt ----
+
+__global__ __launch_bounds__(64) void halt_kernel(const uint16_t* __restrict__ h, int C, const float* __restrict__ w,
+                                                  const float* __restrict__ aux, const int32_t* __restrict__ orig,
+                                                  float* S, int step, int max_steps, float tau, uint8_t* flags,
+                                                  dycl_record* rec) {
+  const int r = blockIdx.x, lane = threadIdx.x;
+  const uint16_t* row = h + (size_t)r * C;
+  float d = 0.f;
+  for (int c = lane * 8; c < C; c += 64 * 8) {
+    const uint4 v = *reinterpret_cast<const uint4*>(row + c);
+    d = fmaf(__uint_as_float(v.x << 16), w[c + 0], d);
+    d = fmaf(__uint_as_float(v.x & 0xffff0000u), w[c + 1], d);
+    d = fmaf(__uint_as_float(v.y << 16), w[c + 2], d);
+    d = fmaf(__uint_as_float(v.y & 0xffff0000u), w[c + 3], d);
+    d = fmaf(__uint_as_float(v.z << 16), w[c + 4], d);
+    d = fmaf(__uint_as_float(v.z & 0xffff0000u), w[c + 5], d);
+    d = fmaf(__uint_as_float(v.w << 16), w[c + 6], d);
+    d = fmaf(__uint_as_float(v.w & 0xffff0000u), w[c + 7], d);
+  }
+  d = wave_sum(d);
+  if (lane == 0) {
+    const int o = orig ? orig[r] : r;
+    const float p = 1.0f / (1.0f + expf(-(d + aux[o])));
+    const float Sn = S[o] + p;
+    S[o] = Sn;
+    const bool stop = (Sn >= tau) || (step == max_steps);
+    flags[r] = stop ? 1 : 0;
+    if (stop) rec[o].iterations = step;
+  }
+}
+
+void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux, const int32_t* orig, float* S,
+               int step, int max_steps, float tau, uint8_t* flags, dycl_record* rec, hipStream_t s) {
+  hipLaunchKernelGGL(halt_kernel, dim3(n), dim3(64), 0, s, h, C, w, aux, orig, S, step, max_steps, tau, flags, rec);
+}
+
+// ---------------------------------------------------------- compaction ----
+// One workgroup of 16 wave64s walks the flags 1024 at a time.  Within a wave
+// the rank of a row among the rows of its branch is the popcount of the
+// 64-bit ballot below its lane (mbcnt); the waves' totals are prefix-summed
+// through LDS.  Rows keep their order in both lists (stable partition).
+
+__global__ __launch_bounds__(1024) void compact_kernel(const uint8_t* __restrict__ flags,
+                                                       const int32_t* __restrict__ orig, int n, int32_t* idx1,
+                                                       int32_t* org1, int32_t* idx0, int32_t* org0, int32_t* counts) {
+  __shared__ int wc1[16], wc0[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int base1 = 0, base0 = 0;
+  for (int start = 0; start < n; start += 1024) {
+    const int i = start + tid;
+    const bool valid = i < n;
+    const bool f = valid && flags[i] != 0;
+    const bool g = valid && flags[i] == 0;
+    const uint64_t b1 = __ballot(f);
+    const uint64_t b0 = __ballot(g);
+    const int r1 = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b1 >> 32),
+                                             __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(b1), 0));
+    const int r0 = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b0 >> 32),
+                                             __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(b0), 0));
+    if (lane == 0) {
+      wc1[wave] = __popcll(b1);
+      wc0[wave] = __popcll(b0);
+    }
+    __syncthreads();
+    int off1 = base1, off0 = base0, t1 = 0, t0 = 0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+      const int c1 = wc1[w], c0 = wc0[w];
+      if (w < wave) {
+        off1 += c1;
+        off0 += c0;
+      }
+      t1 += c1;
+      t0 += c0;
+    }
+    if (f) {
+      idx1[off1 + r1] = i;
+      org1[off1 + r1] = orig ? orig[i] : i;
+    }
+    if (g) {
+      idx0[off0 + r0] = i;
+      org0[off0 + r0] = orig ? orig[i] : i;
+    }
+    base1 += t1;
+    base0 += t0;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    counts[0] = base1;
+    counts[1] = base0;
+  }
+}
+
+void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, int32_t* org1, int32_t* idx0,
+             int32_t* org0, int32_t* counts, hipStream_t s) {
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, flags, orig, n, idx1, org1, idx0, org0, counts);
+}
+
+// ------------------------------------------------------------ row moves ---
+
+__global__ __launch_bounds__(256) void move_rows_kernel(uint4* __restrict__ dst, const int32_t* __restrict__ dst_idx,
+                                                        const uint4* __restrict__ src,
+                                                        const int32_t* __restrict__ src_idx, size_t vpr) {
+  const int r = blockIdx.x;
+  const size_t d = dst_idx ? static_cast<size_t>(dst_idx[r]) : static_cast<size_t>(r);
+  const size_t s = src_idx ? static_cast<size_t>(src_idx[r]) : static_cast<size_t>(r);
+  const uint4* sp = src + s * vpr;
+  uint4* dp = dst + d * vpr;
+  const size_t v0 = static_cast<size_t>(blockIdx.y) * 1024 + threadIdx.x;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const size_t v = v0 + static_cast<size_t>(j) * 256;
+    if (v < vpr) dp[v] = sp[v];
+  }
+}
+
+void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,
+               hipStream_t s) {
+  const size_t vpr = row_bytes / 16;
+  dim3 grid(n, static_cast<unsigned>((vpr + 1023) / 1024));
+  hipLaunchKernelGGL(move_rows_kernel, grid, dim3(256), 0, s, static_cast<uint4*>(dst), dst_idx,
+                     static_cast<const uint4*>(src), src_idx, vpr);
+}
+
+// ------------------------------------------------------------- maxpool ----
+
+__global__ __launch_bounds__(256) void maxpool_kernel(const uint16_t* __restrict__ x, int H, int W, int C, int Ho,
+                                                      int Wo, uint16_t* __restrict__ y, size_t total) {
+  const size_t t = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;   // one 8-channel vector
+  if (t >= total) return;
+  const int C8 = C >> 3;
+  const int cv = static_cast<int>(t % C8);
+  size_t pix = t / C8;
+  const int ow = static_cast<int>(pix % Wo);
+  pix /= Wo;
+  const int oh = static_cast<int>(pix % Ho);
+  const size_t img = pix / Ho;
+  float m[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) m[j] = -INFINITY;
+  for (int i = 0; i < 3; ++i) {
+    const int ih = 2 * oh - 1 + i;
+    if ((unsigned)ih >= (unsigned)H) continue;
+    for (int jw = 0; jw < 3; ++jw) {
+      const int iw = 2 * ow - 1 + jw;
+      if ((unsigned)iw >= (unsigned)W) continue;
+      const uint4 v = *reinterpret_cast<const uint4*>(x + ((img * H + ih) * W + iw) * C + cv * 8);
+      const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        m[2 * q] = fmaxf(m[2 * q], __uint_as_float(w4[q] << 16));
+        m[2 * q + 1] = fmaxf(m[2 * q + 1], __uint_as_float(w4[q] & 0xffff0000u));
+      }
+    }
+  }
+  uint4 o;
+  uint32_t* op = reinterpret_cast<uint32_t*>(&o);
+#pragma unroll
+  for (int q = 0; q < 4; ++q)   // maxima of bf16 values are bf16 values: exact
+    op[q] = (__float_as_uint(m[2 * q]) >> 16) | (__float_as_uint(m[2 * q + 1]) & 0xffff0000u);
+  *reinterpret_cast<uint4*>(y + t * 8) = o;
+}
+
+void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s) {
+  const int Ho = (H + 2 - 3) / 2 + 1, Wo = (W + 2 - 3) / 2 + 1;
+  const size_t total = static_cast<size_t>(n) * Ho * Wo * (C / 8);
+  hipLaunchKernelGGL(maxpool_kernel, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, x, H, W, C,
+                     Ho, Wo, y, total);
+}
+
+// --------------------------------------------------------------- small ----
+
+__global__ void init_records_kernel(dycl_record* rec, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) {
+    rec[i].exit_index = -1;
+    rec[i].iterations = 0;
+    rec[i].skip_mask = 0;
+  }
+}
+
+void init_records(dycl_record* rec, int n, hipStream_t s) {
+  hipLaunchKernelGGL(init_records_kernel, dim3((n + 255) / 256), dim3(256), 0, s, rec, n);
+}
+
+__global__ void fill_f32_kernel(float* p, float v, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+void fill_f32(float* p, float v, int n, hipStream_t s) {
+  hipLaunchKernelGGL(fill_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, p, v, n);
+}
+
+__global__ void iota_kernel(int32_t* p, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = i;
+}
+
+void iota_i32(int32_t* p, int n, hipStream_t s) {
+  hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, s, p, n);
+}
+
+}  // namespace k
+}  // namespace dycl

@@ -1,0 +1,84 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher checks nothing
+// about shapes: the plan builder validates them before any launch, and each
+// launcher is called only with n >= 1 rows.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/dycl.h"
+
+namespace dycl {
+namespace k {
+
+enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_GELU = 2 };
+
+// Tile shape of the implicit-GEMM convolution (rows = output pixels,
+// columns = output channels).  The packed weights are padded to a multiple
+// of bn rows and kBK columns.
+struct ConvTile {
+  int bm, bn;
+};
+constexpr int kBK = 32;
+ConvTile conv_pick_tile(int M, int cout);
+
+struct ConvArgs {
+  const uint16_t* src;   // [n, H, W, cin1] bf16 NHWC
+  const uint16_t* src2;  // [n, 1, 1, cin2] (channel concat, k == 1 only) or null
+  int cin1, cin2;        // cin = cin1 + cin2
+  int n, H, W, cin, Ho, Wo, cout, k, stride, pad;
+  const uint16_t* w;     // packed [cout_pad][Kp] bf16, K order (kh, kw, ci)
+  int Kp;
+  ConvTile tile;
+  const float* scale;    // [cout] or null (1)
+  const float* shift;    // [cout] or null (0)
+  const uint16_t* res;   // [n, Ho, Wo, cout] bf16 or null
+  int act;
+  void* dst;             // [n, Ho, Wo, cout] bf16, or fp32 when out_f32
+  int out_f32;
+};
+void conv_bf16(const ConvArgs& a, hipStream_t s);
+
+// Y[m, j] = act(sum_k X[m, k] W[j, k] + bias[j]), fp32
+void linear_f32(const float* X, int n, int K, const float* W, const float* bias, int N, int act, float* Y,
+                hipStream_t s);
+
+// G[r, c] = sum_{hw} x[r, hw, c] / HW
+void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, hipStream_t s);
+
+// Exit decision from head logits Z [n, ncls]: p = max softmax(Z / T); rows
+// with p >= tau (or all rows when final) write their logits and exit index at
+// their original position.
+void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int final_, int head,
+                 const int32_t* orig, uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s);
+
+// Gate: q = sigmoid(u . GAP(x) + v); flag = q > thr (execute); skipped rows set
+// bit `gate` of their record.
+void gate_head(const uint16_t* x, int n, int HW, int C, const float* u, const float* v, float thr, int gate,
+               const int32_t* orig, uint8_t* flags, dycl_record* rec, hipStream_t s);
+
+// Halting unit of step `step`: p = sigmoid(w . h + aux[orig]); S[orig] += p;
+// flag = S >= tau or step == max_steps (halt); halted rows record step.
+void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux, const int32_t* orig, float* S,
+               int step, int max_steps, float tau, uint8_t* flags, dycl_record* rec, hipStream_t s);
+
+// Stable two-way partition of rows 0..n-1 by flag: idx1/org1 list the rows
+// (and their original ids) with flag != 0, idx0/org0 the others, in order;
+// counts[0] = |flag != 0|, counts[1] = the rest.
+void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, int32_t* org1, int32_t* idx0,
+             int32_t* org0, int32_t* counts, hipStream_t s);
+
+// dst row (dst_idx ? dst_idx[r] : r) = src row (src_idx ? src_idx[r] : r),
+// r < n; row_bytes is a multiple of 16.
+void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,
+               hipStream_t s);
+
+void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s);
+void init_records(dycl_record* rec, int n, hipStream_t s);
+void fill_f32(float* p, float v, int n, hipStream_t s);
+void iota_i32(int32_t* p, int n, hipStream_t s);
+
+}  // namespace k
+}  // namespace dycl

@@ -1,0 +1,150 @@
+// Plan = the compiled form of a dynamic network for one maximum batch.
+//
+// The specification lists the nodes of the paper's heterogeneous control
+// flow graph (Sec. 5.3): sub-DNN nodes (runs of tensor statements; here
+// "conv", "maxpool", "output") and logic nodes, each a single conditional
+// that reads an intermediate tensor ("exit", "gate", "halt").  Loops are
+// already unrolled, as the paper's rewriting step does (Sec. 5.2).  Building
+// the plan walks the nodes in program order and propagates each tensor's
+// per-sample shape from its producer; a logic node passes its input's shape
+// on unchanged (Alg. 2).  Then every tensor gets a device buffer sized for
+// max_batch rows, with buffers reused once their tensor is dead.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/dycl.h"
+#include "json.hpp"
+#include "kernels.hpp"
+
+namespace dycl {
+
+enum class DType { BF16, F32 };
+
+struct TensorInfo {
+  std::string name;
+  int H = 1, W = 1, C = 1;
+  int space = 0;       // row space it lives in (changes at every compaction)
+  bool external = false;   // the caller's input
+  bool parked = false;     // full batch, original sample order
+  int first = -1, last = -1;   // liveness (node sequence numbers)
+  int buf = -1;
+  size_t row_bytes(DType dt) const { return (size_t)H * W * C * (dt == DType::BF16 ? 2 : 4); }
+};
+
+enum class NodeKind { Conv, MaxPool, Exit, Gate, Halt, Output };
+
+struct Node {
+  NodeKind kind = NodeKind::Conv;
+  int seq_pre = 0, seq_post = 0;
+  // tensors
+  int src = -1, src2 = -1, dst = -1, res = -1;
+  // conv / linear
+  int k = 1, stride = 1, pad = 0, cin1 = 0, cin2 = 0, cout = 0;
+  int H = 1, W = 1, Ho = 1, Wo = 1;
+  int act = 0;
+  int64_t w_off = -1, w_ldk = 0, w_k0 = 0;   // weight tensor byte offset, row length, first column
+  int64_t scale_off = -1, shift_off = -1;    // fp32 [cout] byte offsets (or -1)
+  int packed = -1;                           // index of packed bf16 weights
+  k::ConvTile tile{128, 128};
+  // heads: exit W [ncls][C], b [ncls], T [1]; gate u [C], v [1]; halt w [C]
+  int64_t h_w = -1, h_b = -1, h_T = -1;
+  int ncls = 0, hc = 0;
+  float tau = 0.f;
+  bool final_ = false;
+  int index = 0;        // exit head / gate / loop step
+  int max_steps = 0;
+  int decision = -1;    // slot in the per-run counts
+  std::vector<std::pair<int, int>> pairs;     // exit/halt carry (old, new); gate gather (outer, inner)
+  std::vector<std::pair<int, int>> scatter;   // gate: (inner, outer)
+  int park_src = -1, park_dst = -1;           // halt
+  std::vector<Node> body;                     // gate
+};
+
+struct Packed {
+  int64_t w_off, w_ldk, w_k0;
+  int cout, K, cout_pad, Kp;
+  uint16_t* dev = nullptr;
+};
+
+struct ProfileRow {
+  double launches = 0, ms = 0, flops = 0, bytes = 0;
+};
+
+enum ProfileClass { P_CONV = 0, P_LINEAR32, P_HEAD, P_COMPACT, P_MOVE, P_POOL, P_MISC, P_COUNT };
+
+struct Spec {
+  DType dt = DType::BF16;
+  int n_out = 0;
+  bool aux = false;
+  int input = -1;
+  std::vector<TensorInfo> tensors;
+  std::vector<Node> nodes;
+  std::vector<Packed> packed;
+  int decisions = 0;
+  int seq = 0;
+  bool any_halt = false;
+  int max_head_c = 8, max_ncls = 8;
+  int nodes_total = 0;
+  std::string summary;
+
+  void parse(const std::string& json, size_t weights_bytes, int max_batch);
+};
+
+}  // namespace dycl
+
+struct dycl_plan {
+  uint32_t magic = 0x44594350u;  // "DYCP"
+  dycl::Spec spec;
+  int device = 0;
+  int max_batch = 0;
+  // device memory
+  uint8_t* d_blob = nullptr;
+  size_t blob_bytes = 0;
+  std::vector<void*> buffers;
+  std::vector<size_t> buffer_bytes;
+  uint8_t* d_flags = nullptr;
+  int32_t *d_idx1 = nullptr, *d_org1 = nullptr, *d_idx0 = nullptr, *d_org0 = nullptr;
+  int32_t* d_orig[2] = {nullptr, nullptr};
+  int32_t* d_iota = nullptr;      // 0..max_batch-1: original ids of a fresh batch
+  int32_t* d_counts = nullptr;
+  int32_t* h_counts = nullptr;   // pinned
+  float* d_G = nullptr;          // [max_batch, max_head_c]
+  float* d_Z = nullptr;          // [max_batch, max_ncls]
+  float* d_S = nullptr;          // [max_batch]
+  size_t workspace_bytes = 0, weight_bytes = 0;
+  // profiling
+  bool profile = false;
+  std::vector<hipEvent_t> ev_free;
+  struct Pending {
+    int cls;
+    hipEvent_t a, b;
+    double flops, bytes;
+  };
+  std::vector<Pending> pending;
+  dycl::ProfileRow prof[dycl::P_COUNT];
+  hipStream_t last_stream = nullptr;
+};
+
+namespace dycl {
+int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_t weights_bytes);
+void plan_free(dycl_plan* p);
+void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logits, dycl_record* rec,
+              hipStream_t s);
+void profile_flush(dycl_plan* p);
+
+struct HipError : std::runtime_error {
+  explicit HipError(const std::string& m) : std::runtime_error(m) {}
+};
+struct OomError : std::runtime_error {
+  explicit OomError(const std::string& m) : std::runtime_error(m) {}
+};
+struct WeightsError : std::runtime_error {
+  explicit WeightsError(const std::string& m) : std::runtime_error(m) {}
+};
+}  // namespace dycl

@@ -1,0 +1,423 @@
+// Specification parsing, validation and shape propagation (host only; no
+// HIP call happens here, so every check runs without a GPU).
+#include <algorithm>
+#include <map>
+#include <sstream>
+
+#include "plan.hpp"
+
+namespace dycl {
+
+namespace {
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+struct Builder {
+  Spec& sp;
+  size_t blob;
+  std::map<std::string, int> names;
+  int space = 0;
+  int next_space = 1;
+  bool in_body = false;
+
+  Builder(Spec& s, size_t b) : sp(s), blob(b) {}
+
+  [[noreturn]] void fail(const std::string& m) { throw SpecError(m); }
+
+  void need_bytes(int64_t off, int64_t bytes, int64_t align, const char* what) {
+    if (off < 0) fail(std::string(what) + ": negative offset");
+    if (off % align != 0) fail(std::string(what) + ": offset not aligned to " + std::to_string(align));
+    if (bytes < 0 || static_cast<uint64_t>(off) + static_cast<uint64_t>(bytes) > blob)
+      throw WeightsError(std::string(what) + ": weight range [" + std::to_string(off) + ", +" +
+                         std::to_string(bytes) + ") exceeds the blob of " + std::to_string(blob) + " bytes");
+  }
+
+  int lookup(const Json& j, const char* what) {
+    const std::string& n = j.as_str(what);
+    auto it = names.find(n);
+    if (it == names.end()) fail(std::string(what) + ": unknown tensor '" + n + "'");
+    return it->second;
+  }
+
+  int use(const Json& j, const char* what, int seq) {
+    int t = lookup(j, what);
+    TensorInfo& ti = sp.tensors[t];
+    if (!ti.parked && ti.space != space)
+      fail(std::string(what) + ": tensor '" + ti.name +
+           "' belongs to rows that were regrouped by a decision; carry it through that decision");
+    touch(t, seq);
+    return t;
+  }
+
+  void touch(int t, int seq) {
+    TensorInfo& ti = sp.tensors[t];
+    if (ti.first < 0 || seq < ti.first) ti.first = seq;
+    ti.last = std::max(ti.last, seq);
+  }
+
+  int define(const Json& j, int H, int W, int C, int seq, const char* what) {
+    const std::string& n = j.as_str(what);
+    if (names.count(n)) fail(std::string(what) + ": tensor '" + n + "' is defined twice");
+    if (H < 1 || W < 1 || C < 1) fail(std::string(what) + ": empty shape for '" + n + "'");
+    TensorInfo ti;
+    ti.name = n;
+    ti.H = H;
+    ti.W = W;
+    ti.C = C;
+    ti.space = space;
+    sp.tensors.push_back(ti);
+    int id = static_cast<int>(sp.tensors.size()) - 1;
+    names[n] = id;
+    touch(id, seq);
+    return id;
+  }
+
+  int act_of(const std::string& a) {
+    if (a == "none") return k::ACT_NONE;
+    if (a == "relu") return k::ACT_RELU;
+    if (a == "gelu") return k::ACT_GELU;
+    fail("unknown activation '" + a + "'");
+  }
+
+  int64_t f32_vec(const Json& n, const char* key, int64_t count) {
+    if (!n.has(key) || n.at(key).is_null()) return -1;
+    int64_t off = n.at(key).as_int(key);
+    need_bytes(off, count * 4, 4, key);
+    return off;
+  }
+
+  int pack_index(int64_t off, int64_t ldk, int64_t k0, int cout, int K, int bn) {
+    for (size_t i = 0; i < sp.packed.size(); ++i) {
+      const Packed& q = sp.packed[i];
+      if (q.w_off == off && q.w_ldk == ldk && q.w_k0 == k0 && q.cout == cout && q.K == K && q.cout_pad % bn == 0)
+        return static_cast<int>(i);
+    }
+    Packed q;
+    q.w_off = off;
+    q.w_ldk = ldk;
+    q.w_k0 = k0;
+    q.cout = cout;
+    q.K = K;
+    q.cout_pad = (cout + bn - 1) / bn * bn;
+    q.Kp = (K + k::kBK - 1) / k::kBK * k::kBK;
+    sp.packed.push_back(q);
+    return static_cast<int>(sp.packed.size()) - 1;
+  }
+
+  Node conv(const Json& n, int max_batch) {
+    Node nd;
+    nd.kind = NodeKind::Conv;
+    nd.seq_pre = nd.seq_post = sp.seq++;
+    nd.src = use(n.at("src"), "conv.src", nd.seq_pre);
+    const TensorInfo src = sp.tensors[nd.src];
+    nd.H = src.H;
+    nd.W = src.W;
+    nd.cin1 = src.C;
+    if (n.has("src2") && !n.at("src2").is_null()) {
+      nd.src2 = use(n.at("src2"), "conv.src2", nd.seq_pre);
+      const TensorInfo& s2 = sp.tensors[nd.src2];
+      if (s2.H != src.H || s2.W != src.W) fail("conv.src2: spatial shape differs from src");
+      nd.cin2 = s2.C;
+    }
+    nd.k = static_cast<int>(n.get_int("k", 1));
+    nd.stride = static_cast<int>(n.get_int("stride", 1));
+    nd.pad = static_cast<int>(n.get_int("pad", 0));
+    nd.cout = static_cast<int>(n.at("cout").as_int("cout"));
+    if (nd.k != 1 && nd.k != 3 && nd.k != 7) fail("conv.k must be 1, 3 or 7");
+    if (nd.stride < 1 || nd.stride > 4 || nd.pad < 0 || nd.pad >= nd.k + 1) fail("conv: bad stride / pad");
+    if (nd.cout < 1 || nd.cout > 65536) fail("conv.cout out of range");
+    if (nd.src2 >= 0 && (nd.k != 1 || nd.cin1 % 8 || nd.cin2 % 8))
+      fail("conv.src2 (channel concat) needs k == 1 and channel counts divisible by 8");
+    nd.Ho = (nd.H + 2 * nd.pad - nd.k) / nd.stride + 1;
+    nd.Wo = (nd.W + 2 * nd.pad - nd.k) / nd.stride + 1;
+    if (nd.Ho < 1 || nd.Wo < 1) fail("conv: output would be empty");
+    nd.act = act_of(n.get_str("act", "none"));
+    const int cin = nd.cin1 + nd.cin2;
+    const int K = nd.k * nd.k * cin;
+    const Json& w = n.at("w");
+    nd.w_off = w.at("off").as_int("w.off");
+    nd.w_ldk = w.get_int("ldk", K);
+    nd.w_k0 = w.get_int("k0", 0);
+    if (nd.w_k0 < 0 || nd.w_k0 + K > nd.w_ldk) fail("conv.w: column range [k0, k0+K) exceeds ldk");
+    const int esz = sp.dt == DType::BF16 ? 2 : 4;
+    need_bytes(nd.w_off, ((int64_t)(nd.cout - 1) * nd.w_ldk + nd.w_k0 + K) * esz, esz, "conv.w");
+    nd.scale_off = f32_vec(n, "scale", nd.cout);
+    nd.shift_off = f32_vec(n, "shift", nd.cout);
+    if (n.has("res") && !n.at("res").is_null()) {
+      nd.res = use(n.at("res"), "conv.res", nd.seq_pre);
+      const TensorInfo& r = sp.tensors[nd.res];
+      if (r.H != nd.Ho || r.W != nd.Wo || r.C != nd.cout) fail("conv.res: shape differs from the output");
+    }
+    if (sp.dt == DType::F32) {
+      if (nd.k != 1 || nd.H != 1 || nd.W != 1 || nd.src2 >= 0 || nd.res >= 0 || nd.scale_off >= 0 ||
+          nd.act == k::ACT_GELU)
+        fail("fp32 specs support only linear layers (k 1 on 1x1 rows, bias, ReLU)");
+      if (nd.w_k0 != 0 || nd.w_ldk != K) fail("fp32 linear weights must be dense [cout][cin]");
+    } else {
+      nd.tile = k::conv_pick_tile(max_batch * nd.Ho * nd.Wo, nd.cout);
+      nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, K, nd.tile.bn);
+    }
+    nd.dst = define(n.at("dst"), nd.Ho, nd.Wo, nd.cout, nd.seq_pre, "conv.dst");
+    return nd;
+  }
+
+  Node maxpool(const Json& n) {
+    Node nd;
+    nd.kind = NodeKind::MaxPool;
+    nd.seq_pre = nd.seq_post = sp.seq++;
+    if (sp.dt != DType::BF16) fail("maxpool needs a bf16 spec");
+    nd.src = use(n.at("src"), "maxpool.src", nd.seq_pre);
+    const TensorInfo s = sp.tensors[nd.src];
+    if (s.C % 8) fail("maxpool: channels must be a multiple of 8");
+    nd.H = s.H;
+    nd.W = s.W;
+    nd.Ho = (s.H + 2 - 3) / 2 + 1;
+    nd.Wo = (s.W + 2 - 3) / 2 + 1;
+    nd.dst = define(n.at("dst"), nd.Ho, nd.Wo, s.C, nd.seq_pre, "maxpool.dst");
+    return nd;
+  }
+
+  void head_channels(const TensorInfo& s, const char* what) {
+    if (sp.dt == DType::BF16) {
+      if (!is_pow2(s.C) || s.C < 8 || s.C > 2048)
+        fail(std::string(what) + ": pooled channels must be a power of two in [8, 2048]");
+    } else if (s.H * s.W != 1) {
+      fail(std::string(what) + ": fp32 heads read 1x1 rows");
+    }
+  }
+
+  void carry(const Json& n, const char* key, Node& nd, int old_space) {
+    if (!n.has(key)) return;
+    const Json& c = n.at(key);
+    for (size_t i = 0; i < c.size(); ++i) {
+      const Json& pr = c.at(i);
+      if (pr.size() != 2) fail(std::string(key) + ": entries are [old, new] pairs");
+      space = old_space;
+      int o = use(pr.at(0), key, nd.seq_pre);
+      space = next_space - 1;   // the new row space of the surviving rows
+      const TensorInfo ot = sp.tensors[o];
+      int nw = define(pr.at(1), ot.H, ot.W, ot.C, nd.seq_pre, key);
+      nd.pairs.push_back({o, nw});
+    }
+  }
+
+  Node exit_node(const Json& n) {
+    Node nd;
+    nd.kind = NodeKind::Exit;
+    nd.seq_pre = nd.seq_post = sp.seq++;
+    if (in_body) fail("exit inside a gate body is not supported");
+    nd.src = use(n.at("src"), "exit.src", nd.seq_pre);
+    const TensorInfo s = sp.tensors[nd.src];
+    head_channels(s, "exit");
+    nd.H = s.H;
+    nd.W = s.W;
+    nd.hc = s.C;
+    nd.ncls = static_cast<int>(n.at("ncls").as_int("ncls"));
+    if (nd.ncls != sp.n_out) fail("exit.ncls must equal n_out");
+    nd.h_w = f32_vec(n, "w", (int64_t)nd.ncls * s.C);
+    nd.h_b = f32_vec(n, "b", nd.ncls);
+    nd.h_T = f32_vec(n, "T", 1);
+    nd.final_ = n.get_bool("final", false);
+    if (nd.h_w < 0 || nd.h_b < 0) fail("exit: w and b are required");
+    if (!nd.final_ && nd.h_T < 0) fail("exit: a non-final exit needs its temperature T");
+    nd.tau = static_cast<float>(n.get_num("tau", 0.0));
+    nd.index = static_cast<int>(n.get_int("index", 0));   // -1: a classifier that records no exit
+    if (nd.index < -1) fail("exit.index must be >= -1");
+    nd.decision = sp.decisions++;
+    sp.max_head_c = std::max(sp.max_head_c, s.C);
+    sp.max_ncls = std::max(sp.max_ncls, nd.ncls);
+    if (!nd.final_) {
+      int old = space;
+      space = next_space++;
+      carry(n, "carry", nd, old);
+      space = next_space - 1;
+    } else {
+      if (n.has("carry") && n.at("carry").size()) fail("a final exit carries nothing");
+      space = next_space++;   // no rows remain
+    }
+    return nd;
+  }
+
+  Node gate_node(const Json& n, int max_batch) {
+    Node nd;
+    nd.kind = NodeKind::Gate;
+    nd.seq_pre = sp.seq++;
+    if (in_body) fail("nested gates are not supported");
+    if (sp.dt != DType::BF16) fail("gates need a bf16 spec");
+    nd.src = use(n.at("src"), "gate.src", nd.seq_pre);
+    const TensorInfo s = sp.tensors[nd.src];
+    head_channels(s, "gate");
+    nd.H = s.H;
+    nd.W = s.W;
+    nd.hc = s.C;
+    nd.h_w = f32_vec(n, "u", s.C);
+    nd.h_b = f32_vec(n, "v", 1);
+    if (nd.h_w < 0 || nd.h_b < 0) fail("gate: u and v are required");
+    nd.tau = static_cast<float>(n.get_num("threshold", 0.5));
+    nd.index = static_cast<int>(n.at("index").as_int("index"));
+    if (nd.index < 0 || nd.index > 63) fail("gate.index must be in [0, 63]");
+    nd.decision = sp.decisions++;
+    const int outer = space;
+    const int inner = next_space++;
+    const Json& g = n.at("gather");
+    for (size_t i = 0; i < g.size(); ++i) {
+      const Json& pr = g.at(i);
+      if (pr.size() != 2) fail("gate.gather entries are [outer, inner] pairs");
+      space = outer;
+      int o = use(pr.at(0), "gate.gather", nd.seq_pre);
+      space = inner;
+      const TensorInfo ot = sp.tensors[o];
+      nd.pairs.push_back({o, define(pr.at(1), ot.H, ot.W, ot.C, nd.seq_pre, "gate.gather")});
+    }
+    space = inner;
+    in_body = true;
+    const Json& body = n.at("body");
+    for (size_t i = 0; i < body.size(); ++i) nd.body.push_back(node(body.at(i), max_batch));
+    in_body = false;
+    nd.seq_post = sp.seq++;
+    const Json& sc = n.at("scatter");
+    for (size_t i = 0; i < sc.size(); ++i) {
+      const Json& pr = sc.at(i);
+      if (pr.size() != 2) fail("gate.scatter entries are [inner, outer] pairs");
+      space = inner;
+      int in = use(pr.at(0), "gate.scatter", nd.seq_post);
+      space = outer;
+      int out = use(pr.at(1), "gate.scatter", nd.seq_post);
+      const TensorInfo &a = sp.tensors[in], &b = sp.tensors[out];
+      if (a.H != b.H || a.W != b.W || a.C != b.C) fail("gate.scatter: shapes differ");
+      if (b.external) fail("gate.scatter: cannot write the caller's input");
+      nd.scatter.push_back({in, out});
+    }
+    space = outer;
+    return nd;
+  }
+
+  Node halt_node(const Json& n) {
+    Node nd;
+    nd.kind = NodeKind::Halt;
+    nd.seq_pre = nd.seq_post = sp.seq++;
+    if (in_body) fail("halt inside a gate body is not supported");
+    if (sp.dt != DType::BF16 || !sp.aux) fail("halt needs a bf16 spec with per-sample aux inputs");
+    nd.src = use(n.at("src"), "halt.src", nd.seq_pre);
+    const TensorInfo s = sp.tensors[nd.src];
+    if (s.H != 1 || s.W != 1 || s.C % 8) fail("halt.src must be a 1x1 row with channels divisible by 8");
+    nd.hc = s.C;
+    nd.h_w = f32_vec(n, "w", s.C);
+    if (nd.h_w < 0) fail("halt.w is required");
+    nd.tau = static_cast<float>(n.at("tau").as_num("tau"));
+    nd.index = static_cast<int>(n.at("step").as_int("step"));
+    nd.max_steps = static_cast<int>(n.at("max_steps").as_int("max_steps"));
+    if (nd.index < 1 || nd.index > nd.max_steps) fail("halt.step must be in [1, max_steps]");
+    nd.decision = sp.decisions++;
+    sp.any_halt = true;
+    const Json& pk = n.at("park");
+    if (pk.size() != 2) fail("halt.park is [src, parked]");
+    nd.park_src = use(pk.at(0), "halt.park", nd.seq_pre);
+    const std::string& pn = pk.at(1).as_str("halt.park");
+    if (names.count(pn)) {
+      nd.park_dst = names[pn];
+      const TensorInfo& pt = sp.tensors[nd.park_dst];
+      if (!pt.parked || pt.C != s.C) fail("halt.park: '" + pn + "' is not a parked tensor of this shape");
+      touch(nd.park_dst, nd.seq_pre);
+    } else {
+      nd.park_dst = define(pk.at(1), 1, 1, s.C, nd.seq_pre, "halt.park");
+      sp.tensors[nd.park_dst].parked = true;
+    }
+    int old = space;
+    space = next_space++;
+    carry(n, "carry", nd, old);
+    space = next_space - 1;
+    return nd;
+  }
+
+  Node output_node(const Json& n) {
+    Node nd;
+    nd.kind = NodeKind::Output;
+    nd.seq_pre = nd.seq_post = sp.seq++;
+    if (in_body) fail("output inside a gate body is not supported");
+    int t = lookup(n.at("src"), "output.src");
+    if (!sp.tensors[t].parked) fail("output.src must be a parked tensor");
+    touch(t, nd.seq_pre);
+    nd.src = t;
+    const TensorInfo s = sp.tensors[t];
+    nd.cin1 = s.C;
+    nd.cout = static_cast<int>(n.at("cout").as_int("cout"));
+    if (nd.cout != sp.n_out) fail("output.cout must equal n_out");
+    const Json& w = n.at("w");
+    nd.w_off = w.at("off").as_int("w.off");
+    nd.w_ldk = w.get_int("ldk", s.C);
+    nd.w_k0 = w.get_int("k0", 0);
+    if (nd.w_k0 < 0 || nd.w_k0 + s.C > nd.w_ldk) fail("output.w: column range exceeds ldk");
+    need_bytes(nd.w_off, ((int64_t)(nd.cout - 1) * nd.w_ldk + nd.w_k0 + s.C) * 2, 2, "output.w");
+    nd.shift_off = f32_vec(n, "bias", nd.cout);
+    nd.tile = k::conv_pick_tile(0, nd.cout);
+    nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, s.C, nd.tile.bn);
+    return nd;
+  }
+
+  Node node(const Json& n, int max_batch) {
+    const std::string& op = n.at("op").as_str("op");
+    ++sp.nodes_total;
+    if (op == "conv") return conv(n, max_batch);
+    if (op == "maxpool") return maxpool(n);
+    if (op == "exit") return exit_node(n);
+    if (op == "gate") return gate_node(n, max_batch);
+    if (op == "halt") return halt_node(n);
+    if (op == "output") return output_node(n);
+    fail("unknown node op '" + op + "'");
+  }
+};
+
+}  // namespace
+
+void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
+  *this = Spec();
+  Json j = Json::parse(json);
+  if (j.kind != Json::Object) throw SpecError("the spec must be a JSON object");
+  if (j.get_int("version", 1) != 1) throw SpecError("unsupported spec version");
+  const std::string dts = j.at("dtype").as_str("dtype");
+  if (dts == "bf16")
+    dt = DType::BF16;
+  else if (dts == "f32")
+    dt = DType::F32;
+  else
+    throw SpecError("dtype must be bf16 or f32");
+  n_out = static_cast<int>(j.at("n_out").as_int("n_out"));
+  if (n_out < 1 || n_out > 65536) throw SpecError("n_out out of range");
+  aux = j.get_bool("aux", false);
+  if (max_batch < 1 || max_batch > (1 << 24)) throw SpecError("max_batch must be in [1, 2^24]");
+
+  Builder b(*this, weights_bytes);
+  const Json& in = j.at("input");
+  const Json& shp = in.at("shape");
+  int H = 1, W = 1, C = 1;
+  if (shp.size() == 3) {
+    H = static_cast<int>(shp.at(0).as_int("shape"));
+    W = static_cast<int>(shp.at(1).as_int("shape"));
+    C = static_cast<int>(shp.at(2).as_int("shape"));
+  } else if (shp.size() == 1) {
+    C = static_cast<int>(shp.at(0).as_int("shape"));
+  } else {
+    throw SpecError("input.shape is [H, W, C] or [D]");
+  }
+  input = b.define(in.at("name"), H, W, C, seq++, "input");
+  tensors[input].external = true;
+  if (tensors[input].row_bytes(dt) % 16 != 0 && (dt == DType::F32 || C % 8 == 0))
+    ;  // rows are moved only for non-input tensors; nothing to check here
+  const Json& ns = j.at("nodes");
+  if (ns.kind != Json::Array || ns.size() == 0) throw SpecError("nodes must be a non-empty array");
+  for (size_t i = 0; i < ns.size(); ++i) nodes.push_back(b.node(ns.at(i), max_batch));
+
+  // every tensor that is moved between row groups must be a whole number of
+  // 16-byte vectors
+  for (const TensorInfo& t : tensors)
+    if (!t.external && t.row_bytes(dt) % 16 != 0)
+      throw SpecError("tensor '" + t.name + "': per-sample bytes must be a multiple of 16");
+
+  std::ostringstream os;
+  os << "nodes=" << nodes_total << " decisions=" << decisions << " tensors=" << tensors.size()
+     << " packed_weights=" << packed.size() << " n_out=" << n_out << " dtype=" << dts;
+  summary = os.str();
+}
+
+}  // namespace dycl

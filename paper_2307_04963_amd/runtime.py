@@ -1,0 +1,114 @@
+"""Python-side plan object over the C ABI (argument marshalling only).
+
+torch supplies device memory and the stream; every step of the run happens
+in libdycl.so.  ``Plan.run`` takes device tensors; ``run_numpy`` is a
+convenience for tests and tools that copies host arrays in and out.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import _lib
+from .lowering import lower_json
+
+check = _lib.check
+lib = _lib.lib
+
+
+class Plan:
+    def __init__(self, spec_json: str, blob: bytes, max_batch: int, device: int = 0):
+        self._h = C.c_void_p()
+        self._blob = C.create_string_buffer(blob, len(blob))
+        check(lib.dycl_plan_create(spec_json.encode(), C.cast(self._blob, C.c_void_p), len(blob), int(max_batch),
+                                   int(device), C.byref(self._h)))
+        self.device = device
+        self.max_batch = max_batch
+        info = self.info()
+        self.n_out = int(info["n_out"])
+        self.decisions = int(info["decisions"])
+        self.aux = bool(info["aux"])
+
+    @classmethod
+    def from_workload(cls, wl, max_batch: int, device: int = 0):
+        blob, man = wl.blob()
+        return cls(lower_json(wl.arch, man), blob, max_batch, device)
+
+    def close(self):
+        if self._h:
+            lib.dycl_plan_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def info(self) -> dict:
+        buf = (C.c_int64 * 8)()
+        n = check(lib.dycl_plan_info(self._h, buf, 8))
+        keys = ["n_out", "in_bytes", "decisions", "workspace_bytes", "weight_bytes", "max_batch", "aux", "nodes"]
+        return {k: int(buf[i]) for i, k in enumerate(keys[:n])}
+
+    def run(self, x: torch.Tensor, aux, logits: torch.Tensor, records: torch.Tensor, stream=None):
+        """x, aux, logits (fp32 [B, n_out]) and records (int32 [B, 4]) are device tensors."""
+        B = x.shape[0]
+        if stream is None:
+            stream = torch.cuda.current_stream(x.device)
+        check(lib.dycl_run(self._h, C.c_void_p(x.data_ptr()), int(B),
+                           C.c_void_p(aux.data_ptr()) if aux is not None else None,
+                           C.c_void_p(logits.data_ptr()), C.c_void_p(records.data_ptr()),
+                           C.c_void_p(stream.cuda_stream)))
+
+    def counts(self):
+        buf = (C.c_int32 * (2 * max(1, self.decisions)))()
+        d = check(lib.dycl_last_counts(self._h, buf, 2 * max(1, self.decisions)))
+        return [(int(buf[2 * i]), int(buf[2 * i + 1])) for i in range(d)]
+
+    def profile(self, on: bool):
+        check(lib.dycl_profile_enable(self._h, 1 if on else 0))
+
+    def profile_read(self) -> dict:
+        rows = (C.c_double * (4 * 16))()
+        n = check(lib.dycl_profile_read(self._h, rows, 16))
+        out = {}
+        for c in range(n):
+            name = lib.dycl_profile_class(c).decode()
+            out[name] = {"launches": rows[4 * c], "ms": rows[4 * c + 1], "flops": rows[4 * c + 2],
+                         "bytes": rows[4 * c + 3]}
+        return out
+
+
+def decode_records(rec: np.ndarray):
+    """int32 [B, 4] -> (exit_index, iterations, skip_mask)."""
+    rec = np.ascontiguousarray(rec, dtype=np.int32)
+    exit_index = rec[:, 0].copy()
+    iterations = rec[:, 1].copy()
+    skip = rec[:, 2:4].copy().view(np.uint64).reshape(-1)
+    return exit_index, iterations, skip
+
+
+def device_inputs(wl, x: np.ndarray, aux, device="cuda"):
+    if x.dtype == np.uint16:
+        xt = torch.from_numpy(x.view(np.int16).copy()).view(torch.bfloat16).to(device)
+    else:
+        xt = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(device)
+    at = torch.from_numpy(np.ascontiguousarray(aux, dtype=np.float32)).to(device) if aux is not None else None
+    return xt, at
+
+
+def run_numpy(plan: Plan, wl, x: np.ndarray, aux=None, device="cuda"):
+    """Run host arrays through the plan; returns a dict like the oracle's."""
+    B = x.shape[0]
+    xt, at = device_inputs(wl, x, aux, device)
+    logits = torch.full((max(B, 1), plan.n_out), float("nan"), dtype=torch.float32, device=device)
+    rec = torch.zeros((max(B, 1), 4), dtype=torch.int32, device=device)
+    plan.run(xt, at, logits, rec)
+    torch.cuda.synchronize()
+    ex, it, sk = decode_records(rec[:B].cpu().numpy())
+    return {"logits": logits[:B].cpu().numpy(), "exit_index": ex, "iterations": it, "skip_mask": sk,
+            "counts": plan.counts()}

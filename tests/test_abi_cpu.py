@@ -1,0 +1,93 @@
+"""C-ABI checks that need no GPU: the library loads, exports what the
+header declares, and rejects bad specs / sizes / pointers before any HIP
+call; the front-end lowers every workload to a spec the host-side
+validator accepts with the expected HCFG shape."""
+
+import ctypes as C
+import json
+import os
+import re
+
+import pytest
+
+from paper_2307_04963_amd import _lib, lowering
+from workloads import configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+lib = _lib.lib
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "dycl.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(dycl_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_match_header():
+    names = _declared()
+    assert names == sorted(_lib.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _check(spec, blob_bytes, max_batch=8):
+    buf = C.create_string_buffer(512)
+    rc = lib.dycl_spec_check(spec.encode() if isinstance(spec, str) else spec, blob_bytes, max_batch, buf, 512)
+    return rc, (buf.value.decode() if rc == 0 else _lib.last_error())
+
+
+@pytest.mark.parametrize("name", configs.NAMES)
+def test_every_workload_spec_validates(name):
+    wl = configs.build(name)
+    blob, man = wl.blob()
+    spec = lowering.lower(wl.arch, man)
+    rc, msg = _check(json.dumps(spec), len(blob), configs.DEFAULT_BATCH[name])
+    assert rc == 0, msg
+    decisions = int(re.search(r"decisions=(\d+)", msg).group(1))
+    want = {"mlp_exit": 3, "resnet18_exit": 4, "skipnet38": 19, "resnet50_exit": 4, "act_loop": 16}[name]
+    assert decisions == want
+    # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
+    if name == "act_loop":
+        assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
+
+
+def _mlp_spec():
+    wl = configs.build("mlp_exit")
+    blob, man = wl.blob()
+    return lowering.lower(wl.arch, man), len(blob)
+
+
+def test_error_paths_before_any_hip_call():
+    spec, nb = _mlp_spec()
+    assert _check("{not json", nb)[0] == -2
+    assert _check(json.dumps(spec), nb - 4096)[0] == -3           # blob too small
+    assert _check(json.dumps(spec), nb, max_batch=0)[0] == -4
+    bad = json.loads(json.dumps(spec))
+    bad["nodes"][0]["src"] = "nope"
+    rc, msg = _check(json.dumps(bad), nb)
+    assert rc == -2 and "unknown tensor" in msg
+    # a tensor from before an exit, used after it without being carried
+    bad = json.loads(json.dumps(spec))
+    bad["nodes"][2]["src"] = bad["nodes"][0]["dst"]
+    rc, msg = _check(json.dumps(bad), nb)
+    assert rc == -2 and "carry" in msg
+    bad = json.loads(json.dumps(spec))
+    bad["nodes"][0]["k"] = 5
+    assert _check(json.dumps(bad), nb)[0] == -2
+    assert lib.dycl_spec_check(None, 0, 1, None, 0) == -1
+
+
+def test_plan_create_rejects_bad_arguments_without_gpu():
+    spec, nb = _mlp_spec()
+    out = C.c_void_p()
+    blob = C.create_string_buffer(nb)
+    assert lib.dycl_plan_create(None, blob, nb, 8, 0, C.byref(out)) == -1
+    assert lib.dycl_plan_create(json.dumps(spec).encode(), blob, nb, 0, 0, C.byref(out)) == -4
+    assert lib.dycl_plan_create(b"[]", blob, nb, 8, 0, C.byref(out)) == -2
+    assert out.value is None
+    assert lib.dycl_run(None, None, 1, None, None, None, None) == -1
+    assert lib.dycl_last_counts(None, None, 0) == -1
+    assert lib.dycl_plan_info(None, None, 0) == -1
+    lib.dycl_plan_destroy(None)
+    assert lib.dycl_profile_class(99) == b""
+    assert lib.dycl_profile_class(0) == b"conv_bf16_mfma"
