@@ -34,6 +34,11 @@ class Record(C.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2307_04963_amd.build` (needs hipcc)")
+    # torch carries its own HIP runtime under the same soname
+    # (libamdhip64.so.7); loading torch first makes libdycl.so bind to that
+    # one, so the process has a single runtime and torch's device pointers
+    # and streams are valid in the library.
+    import torch  # noqa: F401
     lib = C.CDLL(LIB_PATH)
     vp, i32, i64p = C.c_void_p, C.c_int, C.POINTER(C.c_int64)
     lib.dycl_plan_create.argtypes = [C.c_char_p, vp, C.c_size_t, i32, i32, C.POINTER(vp)]
