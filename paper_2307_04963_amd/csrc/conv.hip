@@ -4,17 +4,26 @@
 // code (Sec. 5.3); its convolutions and linear layers are dense
 // contractions:
 //   y[m, co] = sum_{kh, kw, ci} x[img, oh*s - p + kh, ow*s - p + kw, ci] * w[co, kh, kw, ci]
-// with m = (img, oh, ow) over the rows that are active in this branch.
-// As a GEMM: M = rows * Ho * Wo, N = Cout, K = kh * kw * Cin; NHWC keeps
-// the Cin run of one tap contiguous, so A is gathered in 16-byte vectors.
+// with m = (img, oh, ow) running over the rows active in this branch.
+// As a GEMM: M = rows * Ho * Wo, N = Cout, K = kh * kw * Cin.  NHWC keeps
+// the Cin run of one tap contiguous, so A is gathered in 16-byte vectors
+// straight from the activation tensor (no im2col buffer).
 //
-// Each 256-thread workgroup computes a BM x BN tile with four wave64s in a
-// WM x WN grid, each wave accumulating 32x32 blocks with
-// v_mfma_f32_32x32x16_bf16 (fp32 accumulate).  K advances 32 at a time
-// through double-buffered LDS (rows padded by 16 bytes so the 16 lanes of
-// a ds_read_b128 phase hit distinct banks).  The epilogue applies the
-// folded BatchNorm scale / shift (or bias), the residual, ReLU or exact
-// GELU, and rounds to bf16 (nearest even) or stores fp32.
+// Workgroup: 64*WM*WN threads computing a BM x BN tile; wave (wm, wn)
+// accumulates a (BM/WM) x (BN/WN) block with v_mfma_f32_32x32x16_bf16
+// (fp32 accumulate).  K advances 64 per step: the next step's A/B vectors
+// are loaded into registers while the current step's MFMAs run from LDS
+// (rows padded by 16 bytes: the lanes of each ds_read_b128 phase hit
+// distinct banks).  LDS use (<= 55 KB) and registers leave room for two
+// workgroups per CU, whose barrier phases interleave.
+//
+// Tiles are visited in an XCD-aware order: the dispatcher deals workgroups
+// round-robin over the 8 XCDs, so consecutive tile indices (the N tiles of
+// one M tile, which share their A rows) are given to workgroups of the same
+// XCD and its L2.
+//
+// Epilogue: folded BatchNorm scale/shift (or bias), residual, ReLU or exact
+// GELU, then round-to-nearest-even bf16 or an fp32 store.
 #include "kernels.hpp"
 
 namespace dycl {
@@ -29,12 +38,14 @@ struct ConvP {
   int cin1, cin2;
   int H, W, cin, Ho, Wo, cout, stride, pad;
   int M, K, Kp, cin_log2;
+  int mt, nt;
   const uint16_t* w;
   const float* scale;
   const float* shift;
   const uint16_t* res;
   void* dst;
   int act, out_f32;
+  const uint16_t* zeros;   // >= 16 zero bytes: the source of padding taps
 };
 
 __device__ __forceinline__ uint16_t f2bf(float f) {
@@ -52,100 +63,125 @@ __device__ __forceinline__ float apply_act(float v, int act) {
   return v;
 }
 
-template <int BM, int BN, int WM, int WN, int KS, bool SCALAR>
-__global__ __launch_bounds__(256) void conv_igemm_kernel(ConvP p) {
-  constexpr int BK = kBK, LDK = BK + 8;
-  constexpr int VPR = BK / 8;       // 16-byte vectors per tile row
-  constexpr int RPP = 256 / VPR;    // tile rows covered by one load pass
+template <int BM, int BN, int WM, int WN, int KS, bool SCALAR, int BK = 64, int STAGES = 1>
+__global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
+  constexpr int NT = 64 * WM * WN;
+  constexpr int LDK = BK + 8;
+  constexpr int VPR = BK / 8;        // 16-byte vectors per tile row
+  constexpr int RPP = NT / VPR;      // tile rows per load pass
   constexpr int PA = (BM + RPP - 1) / RPP;
   constexpr int PB = (BN + RPP - 1) / RPP;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  static_assert(TM >= 1 && TN >= 1, "wave tile below 32x32");
+  static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be 32x32 blocks");
 
-  __shared__ __align__(16) uint16_t As[2][BM * LDK];
-  __shared__ __align__(16) uint16_t Bs[2][BN * LDK];
+  __shared__ __align__(16) uint16_t As[STAGES][BM * LDK];
+  __shared__ __align__(16) uint16_t Bs[STAGES][BN * LDK];
+
+  // XCD-aware tile order (bijective on [0, mt*nt))
+  const int T = p.mt * p.nt;
+  const int T8 = (T >> 3) << 3;
+  const int wg = blockIdx.x;
+  const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (wg >> 3) : wg;
+  const int mtile = t / p.nt;
+  const int m0 = mtile * BM, n0 = (t - mtile * p.nt) * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
   const int chunk = tid % VPR, rsub = tid / VPR;
   const int HoWo = p.Ho * p.Wo;
 
-  int a_img[PA], a_ih0[PA], a_iw0[PA];
-  bool a_ok[PA];
+  // per A row: pixel index of the window origin and its (ih0, iw0); rows
+  // past M get an origin far outside the image, so every tap reads zero
+  int a_pix[PA], a_ih[PA], a_iw[PA];
 #pragma unroll
   for (int i = 0; i < PA; ++i) {
-    const int row = rsub + i * RPP;
-    const int m = m0 + row;
-    a_ok[i] = row < BM && m < p.M;
-    int img = 0, oh = 0, ow = 0;
-    if (a_ok[i]) {
-      img = m / HoWo;
+    const int m = m0 + rsub + i * RPP;
+    if (m < p.M) {
+      const int img = m / HoWo;
       const int rem = m - img * HoWo;
-      oh = rem / p.Wo;
-      ow = rem - oh * p.Wo;
+      const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
+      a_ih[i] = oh * p.stride - p.pad;
+      a_iw[i] = ow * p.stride - p.pad;
+      a_pix[i] = (img * p.H + a_ih[i]) * p.W + a_iw[i];
+    } else {
+      a_ih[i] = -0x4000;
+      a_iw[i] = -0x4000;
+      a_pix[i] = 0;
     }
-    a_img[i] = img;
-    a_ih0[i] = oh * p.stride - p.pad;
-    a_iw0[i] = ow * p.stride - p.pad;
   }
 
   uint4 ra[PA], rb[PB];
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  auto load_tile = [&](int kt) {
+
+  auto load_tile = [&](int kt) __attribute__((always_inline)) {
     const int kidx = kt * BK + chunk * 8;
-#pragma unroll
-    for (int i = 0; i < PA; ++i) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (a_ok[i]) {
-        if constexpr (!SCALAR) {
-          if (kidx < p.K) {
-            int tap = 0, ci = kidx;
-            if constexpr (KS != 1) {
-              tap = kidx >> p.cin_log2;
-              ci = kidx & (p.cin - 1);
-            }
-            const int kh = tap / KS, kw = tap - (tap / KS) * KS;
-            const int ih = a_ih0[i] + kh, iw = a_iw0[i] + kw;
-            if ((unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W) {
-              const size_t pix = ((size_t)a_img[i] * p.H + ih) * p.W + iw;
-              const uint16_t* ptr =
-                  ci < p.cin1 ? p.src + pix * p.cin1 + ci : p.src2 + pix * p.cin2 + (ci - p.cin1);
-              v = *reinterpret_cast<const uint4*>(ptr);
-            }
-          }
-        } else {
-          uint16_t e[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            e[j] = 0;
-            const int kk = kidx + j;
-            if (kk < p.K) {
-              const int tap = kk / p.cin;
-              const int ci = kk - tap * p.cin;
-              const int kh = tap / KS, kw = tap - (tap / KS) * KS;
-              const int ih = a_ih0[i] + kh, iw = a_iw0[i] + kw;
-              if ((unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W)
-                e[j] = p.src[(((size_t)a_img[i] * p.H + ih) * p.W + iw) * p.cin + ci];
-            }
-          }
-          v.x = e[0] | (uint32_t(e[1]) << 16);
-          v.y = e[2] | (uint32_t(e[3]) << 16);
-          v.z = e[4] | (uint32_t(e[5]) << 16);
-          v.w = e[6] | (uint32_t(e[7]) << 16);
-        }
+    if constexpr (!SCALAR) {
+      int tap = 0, ci = kidx;
+      if constexpr (KS != 1) {
+        tap = kidx >> p.cin_log2;
+        ci = kidx & (p.cin - 1);
       }
-      ra[i] = v;
+      const int kh = tap / KS, kw = tap - (tap / KS) * KS;
+      const bool kok = kidx < p.K;
+      const uint16_t* sp = p.src;
+      int cs = p.cin1, co = ci;
+      if (ci >= p.cin1) {
+        sp = p.src2;
+        cs = p.cin2;
+        co = ci - p.cin1;
+      }
+      const int doff = kh * p.W + kw;
+#pragma unroll
+      for (int i = 0; i < PA; ++i) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        const int ih = a_ih[i] + kh, iw = a_iw[i] + kw;
+        if (kok && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W && rsub + i * RPP < BM)
+          v = *reinterpret_cast<const uint4*>(sp + (size_t)(a_pix[i] + doff) * cs + co);
+        ra[i] = v;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < PA; ++i) {
+        uint16_t e[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          e[j] = 0;
+          const int kk = kidx + j;
+          if (kk < p.K && rsub + i * RPP < BM) {
+            const int tap = kk / p.cin;
+            const int ci = kk - tap * p.cin;
+            const int kh = tap / KS, kw = tap - (tap / KS) * KS;
+            const int ih = a_ih[i] + kh, iw = a_iw[i] + kw;
+            if ((unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W)
+              e[j] = p.src[(size_t)(a_pix[i] + kh * p.W + kw) * p.cin + ci];
+          }
+        }
+        ra[i].x = e[0] | (uint32_t(e[1]) << 16);
+        ra[i].y = e[2] | (uint32_t(e[3]) << 16);
+        ra[i].z = e[4] | (uint32_t(e[5]) << 16);
+        ra[i].w = e[6] | (uint32_t(e[7]) << 16);
+      }
     }
 #pragma unroll
     for (int i = 0; i < PB; ++i) {
+      // written on every path: a register array assigned only under a
+      // divergent branch is kept in scratch memory by the compiler
       const int row = rsub + i * RPP;
-      if (row < BN) rb[i] = *reinterpret_cast<const uint4*>(p.w + (size_t)(n0 + row) * p.Kp + kidx);
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (BN % RPP == 0 || row < BN) v = *reinterpret_cast<const uint4*>(p.w + (size_t)(n0 + row) * p.Kp + kidx);
+      rb[i] = v;
     }
   };
 
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < PA; ++i) {
       const int row = rsub + i * RPP;
@@ -158,51 +194,58 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvP p) {
     }
   };
 
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-
-  const int nk = p.Kp / BK;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load_tile(kt + 1);
+  auto compute = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
       bf16x8 af[TM], bfr[TN];
       const int koff = s * 16 + (lane >> 5) * 8;
 #pragma unroll
       for (int a = 0; a < TM; ++a)
-        af[a] = *reinterpret_cast<const bf16x8*>(&As[cur][(wm * WTM + a * 32 + (lane & 31)) * LDK + koff]);
+        af[a] = *reinterpret_cast<const bf16x8*>(&As[buf][(wm * WTM + a * 32 + (lane & 31)) * LDK + koff]);
 #pragma unroll
       for (int b = 0; b < TN; ++b)
-        bfr[b] = *reinterpret_cast<const bf16x8*>(&Bs[cur][(wn * WTN + b * 32 + (lane & 31)) * LDK + koff]);
+        bfr[b] = *reinterpret_cast<const bf16x8*>(&Bs[buf][(wn * WTN + b * 32 + (lane & 31)) * LDK + koff]);
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
         for (int b = 0; b < TN; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_tile(cur ^ 1);
+  };
+
+  const int nk = p.Kp / BK;
+  load_tile(0);
+  if constexpr (STAGES == 1) {
+    // one LDS buffer: store, barrier, prefetch the next step, compute, barrier
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt > 0) __syncthreads();    // every wave is done reading the previous step
+      store_tile(0);
+      __syncthreads();
+      if (kt + 1 < nk) load_tile(kt + 1);
+      compute(0);
+    }
+  } else {
+    // two LDS buffers: one barrier per step
+    store_tile(0);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + 1 < nk) load_tile(kt + 1);
+      compute(kt & 1);
+      if (kt + 1 < nk) store_tile((kt + 1) & 1);
+      __syncthreads();
+    }
   }
 
   // epilogue: lane owns column (lane & 31) of each 32x32 block, rows
   // 8*(r/4) + 4*(lane/32) + r%4
 #pragma unroll
-  for (int a = 0; a < TM; ++a) {
+  for (int b = 0; b < TN; ++b) {
+    const int col = n0 + wn * WTN + b * 32 + (lane & 31);
+    if (col >= p.cout) continue;
+    const float sc = p.scale ? p.scale[col] : 1.0f;
+    const float sh = p.shift ? p.shift[col] : 0.0f;
 #pragma unroll
-    for (int b = 0; b < TN; ++b) {
-      const int col = n0 + wn * WTN + b * 32 + (lane & 31);
-      if (col >= p.cout) continue;
-      const float sc = p.scale ? p.scale[col] : 1.0f;
-      const float sh = p.shift ? p.shift[col] : 0.0f;
+    for (int a = 0; a < TM; ++a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * WTM + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -220,33 +263,297 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvP p) {
   }
 }
 
-ConvTile conv_pick_tile(int /*M*/, int cout) {
-  if (cout >= 128) return {128, 128};
-  if (cout >= 64) return {128, 64};
-  return {128, 32};
+
+// ------------------------------------------------- direct-to-LDS kernel ----
+// Same contraction, with gfx950's global_load_lds_dwordx4: each lane's 16
+// bytes go straight from global memory to LDS at (wave base + 16 * lane), so
+// tiles need no staging registers and no ds_write.  The LDS row of a tile is
+// 128 bytes (64 bf16 of K); its eight 16-byte chunks are stored XOR-swizzled
+// (physical chunk = logical ^ ((row >> 1) & 7)), which makes the 16 lanes of
+// every ds_read_b128 phase of the MFMA operand reads hit 16 distinct bank
+// groups.  The swizzle is applied on the global side: each lane picks the
+// global chunk that belongs at its fixed LDS slot.  Padding taps and rows
+// past M read a zero buffer.  Two LDS stages, one barrier per K step: the
+// loads of step k+1 are in flight while step k's MFMAs run.
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+
+// Wait until at most N vector-memory operations of this thread are still in
+// flight (loads complete in order, so every older one - the tile about to be
+// read - has landed), then barrier.  Inline asm with a memory clobber keeps
+// the compiler from moving LDS reads across it and from widening the wait.
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+template <int BM, int BN, int WM, int WN, int KS, int NS = 2>
+__global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
+  constexpr int NT = 64 * WM * WN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128, STAGE = A_BYTES + B_BYTES;
+  constexpr int JA = BM * 8 / NT, JB = BN * 8 / NT;
+  constexpr int EPW = WTN + 4;                        // epilogue row stride (floats)
+  constexpr int EPI = (NT / 64) * 32 * EPW * 4;
+  constexpr int SMEM = NS * STAGE > EPI ? NS * STAGE : EPI;
+  static_assert(NS >= 2 && NS <= 4, "2 to 4 LDS stages");
+  static_assert(BM * 8 % NT == 0 && BN * 8 % NT == 0 && JB >= 1, "tile rows must fill whole load passes");
+  static_assert(NT % 128 == 0, "swizzle assumes NT a multiple of 128");
+  static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be 32x32 blocks");
+
+  __shared__ __align__(16) char smem[SMEM];
+
+  const int T = p.mt * p.nt;
+  const int T8 = (T >> 3) << 3;
+  const int wg = blockIdx.x;
+  const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (wg >> 3) : wg;
+  const int mtile = t / p.nt;
+  const int m0 = mtile * BM, n0 = (t - mtile * p.nt) * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int lchunk = (tid & 7) ^ ((tid >> 4) & 7);   // logical K chunk this thread loads
+  const int rbase = tid >> 3;                        // + j * NT / 8
+  const int HoWo = p.Ho * p.Wo;
+
+  int a_pix[JA], a_ih[JA], a_iw[JA];
+#pragma unroll
+  for (int j = 0; j < JA; ++j) {
+    const int m = m0 + rbase + j * (NT / 8);
+    if (m < p.M) {
+      const int img = m / HoWo;
+      const int rem = m - img * HoWo;
+      const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
+      a_ih[j] = oh * p.stride - p.pad;
+      a_iw[j] = ow * p.stride - p.pad;
+      a_pix[j] = (img * p.H + a_ih[j]) * p.W + a_iw[j];
+    } else {
+      a_ih[j] = -0x4000;
+      a_iw[j] = -0x4000;
+      a_pix[j] = 0;
+    }
+  }
+  const uint16_t* wrow = p.w + (size_t)(n0 + rbase) * p.Kp + lchunk * 8;
+
+  auto issue = [&](int kt, int stage) __attribute__((always_inline)) {
+    char* sb = smem + stage * STAGE;
+    const int kidx = kt * 64 + lchunk * 8;
+    int tap = 0, ci = kidx;
+    if constexpr (KS != 1) {
+      tap = kidx >> p.cin_log2;
+      ci = kidx & (p.cin - 1);
+    }
+    const int kh = tap / KS, kw = tap - (tap / KS) * KS;
+    const bool kok = kidx < p.K;
+    const uint16_t* sp = p.src;
+    int cs = p.cin1, co = ci;
+    if (ci >= p.cin1) {
+      sp = p.src2;
+      cs = p.cin2;
+      co = ci - p.cin1;
+    }
+    const int doff = kh * p.W + kw;
+#pragma unroll
+    for (int j = 0; j < JA; ++j) {
+      const int ih = a_ih[j] + kh, iw = a_iw[j] + kw;
+      const bool ok = kok && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
+      const uint16_t* g = ok ? sp + (size_t)(a_pix[j] + doff) * cs + co : p.zeros;
+      __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(sb + (j * NT + wave * 64) * 16), 16, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const uint16_t* g = wrow + (size_t)j * (NT / 8) * p.Kp + kt * 64;
+      __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(sb + A_BYTES + (j * NT + wave * 64) * 16), 16,
+                                       0, 0);
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  const int lsw = (lane >> 1) & 7;
+  // operands of K sub-step s+1 are read from LDS while sub-step s's MFMAs run
+  auto compute = [&](int stage) __attribute__((always_inline)) {
+    const char* sa = smem + stage * STAGE + (wm * WTM + (lane & 31)) * 128;
+    const char* sbp = smem + stage * STAGE + A_BYTES + (wn * WTN + (lane & 31)) * 128;
+    bf16x8 af[2][TM], bfr[2][TN];
+    auto fetch = [&](int s, int slot) __attribute__((always_inline)) {
+      const int phys = ((2 * s + (lane >> 5)) ^ lsw) * 16;
+#pragma unroll
+      for (int a = 0; a < TM; ++a) af[slot][a] = *reinterpret_cast<const bf16x8*>(sa + a * 32 * 128 + phys);
+#pragma unroll
+      for (int b = 0; b < TN; ++b) bfr[slot][b] = *reinterpret_cast<const bf16x8*>(sbp + b * 32 * 128 + phys);
+    };
+    fetch(0, 0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s + 1 < 4) fetch(s + 1, (s + 1) & 1);
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][a], bfr[s & 1][b], acc[a][b], 0, 0, 0);
+    }
+  };
+
+  // NS-stage pipeline: the loads of step kt+NS-1 are issued while step kt
+  // is computed; the stage they fill was read in step kt-1, which every wave
+  // finished before the barrier of step kt
+  const int nk = p.Kp / 64;
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i)
+    if (i < nk) issue(i, i);
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + NS - 2 < nk)
+      wait_vm_barrier<(NS - 2) * (JA + JB)>();   // steps kt+1 .. kt+NS-2 may stay in flight
+    else
+      wait_vm_barrier<0>();
+    if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
+    compute(kt % NS);
+  }
+
+  // epilogue through LDS: each wave stages 32 x WTN fp32 values (scale and
+  // shift applied), then every lane finishes 8 consecutive channels of a row
+  // (residual, activation, rounding) and writes them with one 16-byte store
+  __syncthreads();
+  float* ep = reinterpret_cast<float*>(smem) + wave * 32 * EPW;
+  float sc[TN], sh[TN];
+#pragma unroll
+  for (int b = 0; b < TN; ++b) {
+    const int col = n0 + wn * WTN + b * 32 + (lane & 31);
+    sc[b] = (p.scale && col < p.cout) ? p.scale[col] : 1.0f;
+    sh[b] = (p.shift && col < p.cout) ? p.shift[col] : 0.0f;
+  }
+#pragma unroll
+  for (int a = 0; a < TM; ++a) {
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EPW + b * 32 + (lane & 31)] = fmaf(acc[a][b][r], sc[b], sh[b]);
+    __syncthreads();
+    constexpr int G = WTN / 8;           // 8-channel groups per row
+#pragma unroll
+    for (int v = 0; v < 32 * G / 64; ++v) {
+      const int idx = v * 64 + lane;
+      const int rl = idx / G, g = idx - (idx / G) * G;
+      const int row = m0 + wm * WTM + a * 32 + rl;
+      const int col = n0 + wn * WTN + g * 8;
+      if (row < p.M && col < p.cout) {
+        const float4 lo = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8);
+        const float4 hi = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8 + 4);
+        float vv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const size_t o = (size_t)row * p.cout + col;
+        if (p.res) {
+          const uint4 rv = *reinterpret_cast<const uint4*>(p.res + o);
+          const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            vv[2 * q] += __uint_as_float(rw[q] << 16);
+            vv[2 * q + 1] += __uint_as_float(rw[q] & 0xffff0000u);
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) vv[q] = apply_act(vv[q], p.act);
+        if (p.out_f32) {
+          float* d = static_cast<float*>(p.dst) + o;
+          *reinterpret_cast<float4*>(d) = make_float4(vv[0], vv[1], vv[2], vv[3]);
+          *reinterpret_cast<float4*>(d + 4) = make_float4(vv[4], vv[5], vv[6], vv[7]);
+        } else {
+          uint4 ov;
+          ov.x = f2bf(vv[0]) | (uint32_t(f2bf(vv[1])) << 16);
+          ov.y = f2bf(vv[2]) | (uint32_t(f2bf(vv[3])) << 16);
+          ov.z = f2bf(vv[4]) | (uint32_t(f2bf(vv[5])) << 16);
+          ov.w = f2bf(vv[6]) | (uint32_t(f2bf(vv[7])) << 16);
+          *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.dst) + o) = ov;
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------- launch ----
+
+namespace {
+
+struct TileCfg {
+  int bm, bn, wm, wn;
+};
+
+// register-staged kernel (element-gathering stems, unaligned outputs)
+constexpr TileCfg kWide[] = {{128, 128, 2, 2}, {128, 64, 2, 2}, {64, 64, 2, 2}};
+constexpr TileCfg kMid[] = {{128, 64, 2, 2}, {64, 64, 2, 2}};
+constexpr TileCfg kNarrow[] = {{128, 32, 4, 1}, {64, 32, 2, 1}};
+
+long tiles_of(const TileCfg& c, int M, int cout) {
+  return (long)((M + c.bm - 1) / c.bm) * ((cout + c.bn - 1) / c.bn);
+}
+
+template <size_t N>
+TileCfg choose(const TileCfg (&cs)[N], int M, int cout) {
+  for (size_t i = 0; i < N; ++i)
+    if (tiles_of(cs[i], M, cout) >= 512) return cs[i];
+  return cs[N - 1];
+}
+
+template <int BM, int BN, int WM, int WN, int KS, bool SC>
+void go(const ConvP& p, hipStream_t s) {
+  hipLaunchKernelGGL((conv_kernel<BM, BN, WM, WN, KS, SC, 64, 1>), dim3(p.mt * p.nt), dim3(64 * WM * WN), 0, s, p);
+}
+
+template <int KS>
+void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
+  switch (c.bm * 1000 + c.bn) {
+    case 128128: go<128, 128, 2, 2, KS, false>(p, s); break;
+    case 128064: go<128, 64, 2, 2, KS, false>(p, s); break;
+    case 64064: go<64, 64, 2, 2, KS, false>(p, s); break;
+    case 128032: go<128, 32, 4, 1, KS, false>(p, s); break;
+    default: go<64, 32, 2, 1, KS, false>(p, s); break;
+  }
+}
+
+// direct-to-LDS kernel: the largest tile that still gives the chip enough
+// workgroups (measured on the layer shapes of the workloads)
+TileCfg choose_lds(int M, int cout) {
+  const TileCfg c256{256, 256, 4, 2}, c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2},
+      c32{128, 32, 4, 1};
+  if (cout < 64) return c32;
+  if (cout >= 256 && tiles_of(c256, M, cout) >= 512) return c256;
+  if (cout >= 128 && tiles_of(c128, M, cout) >= 384) return c128;
+  if (tiles_of(c12864, M, cout) >= 512) return c12864;
+  return c64;
 }
 
 template <int BM, int BN, int WM, int WN, int KS>
-static void launch_sc(dim3 grid, bool scalar, const ConvP& p, hipStream_t s) {
-  if (scalar)
-    hipLaunchKernelGGL((conv_igemm_kernel<BM, BN, WM, WN, KS, true>), grid, dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL((conv_igemm_kernel<BM, BN, WM, WN, KS, false>), grid, dim3(256), 0, s, p);
+void go_lds(const ConvP& p, hipStream_t s) {
+  hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), dim3(p.mt * p.nt), dim3(64 * WM * WN), 0, s, p);
 }
 
-template <int BM, int BN, int WM, int WN>
-static void launch_ks(const ConvArgs& a, const ConvP& p, hipStream_t s) {
-  dim3 grid((p.M + BM - 1) / BM, (a.cout + BN - 1) / BN);
-  // 16-byte A vectors need Cin % 8 == 0, and a power-of-two Cin when the
-  // tap index is split off with a shift; anything else gathers by element
-  const bool pow2 = (a.cin & (a.cin - 1)) == 0;
-  const bool scalar = (a.cin % 8) != 0 || (a.k != 1 && !pow2);
-  if (a.k == 1)
-    launch_sc<BM, BN, WM, WN, 1>(grid, scalar, p, s);
-  else if (a.k == 3)
-    launch_sc<BM, BN, WM, WN, 3>(grid, scalar, p, s);
-  else
-    launch_sc<BM, BN, WM, WN, 7>(grid, scalar, p, s);
+template <int KS>
+void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s) {
+  switch (c.bm * 1000 + c.bn) {
+    case 256256: go_lds<256, 256, 4, 2, KS>(p, s); break;
+    case 128128: go_lds<128, 128, 2, 2, KS>(p, s); break;
+    case 128064: go_lds<128, 64, 2, 2, KS>(p, s); break;
+    case 64064: go_lds<64, 64, 2, 2, KS>(p, s); break;
+    default: go_lds<128, 32, 4, 1, KS>(p, s); break;
+  }
+}
+
+}  // namespace
+
+int conv_cout_pad(int cout) {
+  if (cout >= 256) return (cout + 255) / 256 * 256;
+  if (cout >= 128) return (cout + 127) / 128 * 128;
+  if (cout >= 64) return (cout + 63) / 64 * 64;
+  return (cout + 31) / 32 * 32;
 }
 
 void conv_bf16(const ConvArgs& a, hipStream_t s) {
@@ -276,12 +583,53 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.dst = a.dst;
   p.act = a.act;
   p.out_f32 = a.out_f32;
-  if (a.tile.bn == 128)
-    launch_ks<128, 128, 2, 2>(a, p, s);
-  else if (a.tile.bn == 64)
-    launch_ks<128, 64, 2, 2>(a, p, s);
+  p.zeros = a.zeros;
+
+  // 16-byte A vectors need Cin % 8 == 0, and a power-of-two Cin when the tap
+  // index is split off with a shift; anything else gathers element by element
+  const bool pow2 = (a.cin & (a.cin - 1)) == 0;
+  const bool scalar = (a.cin % 8) != 0 || (a.k != 1 && !pow2);
+  if (scalar) {
+    const TileCfg c = a.cout >= 64 ? TileCfg{128, 64, 2, 2} : TileCfg{128, 32, 4, 1};
+    p.mt = (p.M + c.bm - 1) / c.bm;
+    p.nt = (a.cout + c.bn - 1) / c.bn;
+    if (c.bn == 64) {
+      if (a.k == 7) go<128, 64, 2, 2, 7, true>(p, s);
+      else if (a.k == 3) go<128, 64, 2, 2, 3, true>(p, s);
+      else go<128, 64, 2, 2, 1, true>(p, s);
+    } else {
+      if (a.k == 7) go<128, 32, 4, 1, 7, true>(p, s);
+      else if (a.k == 3) go<128, 32, 4, 1, 3, true>(p, s);
+      else go<128, 32, 4, 1, 1, true>(p, s);
+    }
+    return;
+  }
+  // the direct-to-LDS kernel stores 8 channels per 16-byte vector
+  const bool vec_out = a.cout % 8 == 0 && (reinterpret_cast<uintptr_t>(a.dst) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
+  if (vec_out) {
+    const TileCfg c = choose_lds(p.M, a.cout);
+    p.mt = (p.M + c.bm - 1) / c.bm;
+    p.nt = (a.cout + c.bn - 1) / c.bn;
+    if (a.k == 1)
+      dispatch_lds<1>(c, p, s);
+    else if (a.k == 3)
+      dispatch_lds<3>(c, p, s);
+    else
+      dispatch_lds<7>(c, p, s);
+    return;
+  }
+  const TileCfg c = a.cout >= 128 ? choose(kWide, p.M, a.cout)
+                    : a.cout >= 64 ? choose(kMid, p.M, a.cout)
+                                   : choose(kNarrow, p.M, a.cout);
+  p.mt = (p.M + c.bm - 1) / c.bm;
+  p.nt = (a.cout + c.bn - 1) / c.bn;
+  if (a.k == 1)
+    dispatch_staged<1>(c, p, s);
+  else if (a.k == 3)
+    dispatch_staged<3>(c, p, s);
   else
-    launch_ks<128, 32, 4, 1>(a, p, s);
+    dispatch_staged<7>(c, p, s);
 }
 
 }  // namespace k

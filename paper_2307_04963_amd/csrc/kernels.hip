@@ -168,6 +168,75 @@ void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int
                      logits, n_out, rec);
 }
 
+// ----------------------------------------------------- fused exit head ----
+// One workgroup per row: pooled features g (GAP of a bf16 [HW, C] row, or
+// the fp32 row itself), head logits z = W g + b from the transposed head
+// weights Wt [C][ncls] (coalesced over classes), then the decision of the
+// exit: p = max softmax(z / T), leave when p >= tau (or always when final).
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void exit_head_kernel(const void* __restrict__ x, int HW, int C,
+                                                        const float* __restrict__ Wt, const float* __restrict__ bias,
+                                                        int ncls, const float* __restrict__ Tp, float tau,
+                                                        int final_, int head, const int32_t* __restrict__ orig,
+                                                        uint8_t* flags, float* __restrict__ logits, int n_out,
+                                                        dycl_record* rec) {
+  __shared__ float part[2048];
+  __shared__ float g[2048];
+  __shared__ float z[1024];
+  __shared__ float red[8];
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if constexpr (BF16) {
+    row_channel_sums(static_cast<const uint16_t*>(x) + (size_t)r * HW * C, HW, C, g, part);
+    const float inv = 1.0f / static_cast<float>(HW);
+    for (int c = tid; c < C; c += 256) g[c] *= inv;
+  } else {
+    for (int c = tid; c < C; c += 256) g[c] = static_cast<const float*>(x)[(size_t)r * C + c];
+  }
+  __syncthreads();
+  float m = -INFINITY;
+  for (int j = tid; j < ncls; j += 256) {
+    float acc = 0.f;
+    for (int c = 0; c < C; ++c) acc = fmaf(Wt[(size_t)c * ncls + j], g[c], acc);
+    acc += bias[j];
+    z[j] = acc;
+    m = fmaxf(m, acc);
+  }
+  bool ex = final_ != 0;
+  if (!ex) {
+    m = wave_max(m);
+    if (lane == 0) red[wave] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float T = *Tp;
+    float sum = 0.f;
+    for (int j = tid; j < ncls; j += 256) sum += expf((z[j] - m) / T);
+    sum = wave_sum(sum);
+    __syncthreads();
+    if (lane == 0) red[4 + wave] = sum;
+    __syncthreads();
+    sum = red[4] + red[5] + red[6] + red[7];
+    ex = (1.0f / sum) >= tau;
+  }
+  if (ex) {
+    const int o = orig ? orig[r] : r;
+    for (int j = tid; j < ncls; j += 256) logits[(size_t)o * n_out + j] = z[j];
+    if (tid == 0 && head >= 0) rec[o].exit_index = head;
+  }
+  if (tid == 0) flags[r] = ex ? 1 : 0;
+}
+
+void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* Wt, const float* bias, int ncls,
+               const float* T, float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits,
+               int n_out, dycl_record* rec, hipStream_t s) {
+  if (bf16)
+    hipLaunchKernelGGL(exit_head_kernel<true>, dim3(n), dim3(256), 0, s, x, HW, C, Wt, bias, ncls, T, tau, final_,
+                       head, orig, flags, logits, n_out, rec);
+  else
+    hipLaunchKernelGGL(exit_head_kernel<false>, dim3(n), dim3(256), 0, s, x, HW, C, Wt, bias, ncls, T, tau, final_,
+                       head, orig, flags, logits, n_out, rec);
+}
+
 // ---------------------------------------------------------------- gate ----
 
 __global__ __launch_bounds__(256) void gate_kernel(const uint16_t* __restrict__ x, int HW, int C,
@@ -371,6 +440,28 @@ void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y,
   const size_t total = static_cast<size_t>(n) * Ho * Wo * (C / 8);
   hipLaunchKernelGGL(maxpool_kernel, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, x, H, W, C,
                      Ho, Wo, y, total);
+}
+
+// ---------------------------------------------------- stem input padding ----
+
+__global__ __launch_bounds__(256) void pad_channels_kernel(const uint16_t* __restrict__ x, size_t pixels, int cin,
+                                                           uint16_t* __restrict__ y) {
+  const size_t p = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (p >= pixels) return;
+  uint16_t e[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int c = 0; c < cin && c < 8; ++c) e[c] = x[p * cin + c];
+  uint4 o;
+  o.x = e[0] | (uint32_t(e[1]) << 16);
+  o.y = e[2] | (uint32_t(e[3]) << 16);
+  o.z = e[4] | (uint32_t(e[5]) << 16);
+  o.w = e[6] | (uint32_t(e[7]) << 16);
+  *reinterpret_cast<uint4*>(y + p * 8) = o;
+}
+
+void pad_channels_bf16(const uint16_t* x, size_t pixels, int cin, int cout, uint16_t* y, hipStream_t s) {
+  (void)cout;   // always 8
+  hipLaunchKernelGGL(pad_channels_kernel, dim3(static_cast<unsigned>((pixels + 255) / 256)), dim3(256), 0, s, x,
+                     pixels, cin, y);
 }
 
 // --------------------------------------------------------------- small ----

@@ -15,14 +15,11 @@ namespace k {
 
 enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_GELU = 2 };
 
-// Tile shape of the implicit-GEMM convolution (rows = output pixels,
-// columns = output channels).  The packed weights are padded to a multiple
-// of bn rows and kBK columns.
-struct ConvTile {
-  int bm, bn;
-};
-constexpr int kBK = 32;
-ConvTile conv_pick_tile(int M, int cout);
+// The implicit-GEMM convolution picks its tile at launch from the active
+// row count.  Packed weights are [conv_cout_pad(cout)][Kp] with Kp a
+// multiple of kBK, zero-filled, so that every tile width divides the rows.
+constexpr int kBK = 64;
+int conv_cout_pad(int cout);
 
 struct ConvArgs {
   const uint16_t* src;   // [n, H, W, cin1] bf16 NHWC
@@ -31,13 +28,13 @@ struct ConvArgs {
   int n, H, W, cin, Ho, Wo, cout, k, stride, pad;
   const uint16_t* w;     // packed [cout_pad][Kp] bf16, K order (kh, kw, ci)
   int Kp;
-  ConvTile tile;
   const float* scale;    // [cout] or null (1)
   const float* shift;    // [cout] or null (0)
   const uint16_t* res;   // [n, Ho, Wo, cout] bf16 or null
   int act;
   void* dst;             // [n, Ho, Wo, cout] bf16, or fp32 when out_f32
   int out_f32;
+  const uint16_t* zeros; // >= 16 zero bytes on the device (padding taps)
 };
 void conv_bf16(const ConvArgs& a, hipStream_t s);
 
@@ -53,6 +50,13 @@ void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, hipStream_t s);
 // their original position.
 void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int final_, int head,
                  const int32_t* orig, uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s);
+
+// Fused exit head for small heads (C <= 2048, ncls <= 1024): pooling, head
+// linear from transposed weights Wt [C][ncls], and the exit decision, one
+// workgroup per row.  Same outputs as gap_bf16 + linear_f32 + exit_decide.
+void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* Wt, const float* bias, int ncls,
+               const float* T, float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits,
+               int n_out, dycl_record* rec, hipStream_t s);
 
 // Gate: q = sigmoid(u . GAP(x) + v); flag = q > thr (execute); skipped rows set
 // bit `gate` of their record.
@@ -74,6 +78,9 @@ void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, in
 // r < n; row_bytes is a multiple of 16.
 void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,
                hipStream_t s);
+
+// y[p, c] = c < cin ? x[p, c] : 0 for every pixel p, c < cout (cout == 8)
+void pad_channels_bf16(const uint16_t* x, size_t pixels, int cin, int cout, uint16_t* y, hipStream_t s);
 
 void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s);
 void init_records(dycl_record* rec, int n, hipStream_t s);

@@ -102,13 +102,30 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     std::vector<uint16_t> h(static_cast<size_t>(q.cout_pad) * q.Kp, 0);
     for (int co = 0; co < q.cout; ++co) {
       const uint8_t* row = hb + q.w_off + (static_cast<size_t>(co) * q.w_ldk + q.w_k0) * 2;
-      std::memcpy(&h[static_cast<size_t>(co) * q.Kp], row, static_cast<size_t>(q.K) * 2);
+      for (int t = 0; t < q.taps; ++t)
+        std::memcpy(&h[static_cast<size_t>(co) * q.Kp + static_cast<size_t>(t) * q.cin_pack],
+                    row + static_cast<size_t>(t) * q.cin_src * 2, static_cast<size_t>(q.cin_src) * 2);
     }
     void* ptr = nullptr;
     if (hipMalloc(&ptr, h.size() * 2) != hipSuccess) throw OomError("packed weights: hipMalloc failed");
     q.dev = static_cast<uint16_t*>(ptr);
     p->weight_bytes += h.size() * 2;
     hip_check(hipMemcpy(q.dev, h.data(), h.size() * 2, hipMemcpyHostToDevice), "packed weights upload");
+  }
+
+  // transposed weights of the fused exit heads
+  p->head_t.assign(sp.n_head_t, nullptr);
+  for (const Node& nd : sp.nodes) {
+    if (nd.kind != NodeKind::Exit || nd.head_t < 0) continue;
+    std::vector<float> wt(static_cast<size_t>(nd.hc) * nd.ncls);
+    const float* w = reinterpret_cast<const float*>(hb + nd.h_w);
+    for (int j = 0; j < nd.ncls; ++j)
+      for (int c = 0; c < nd.hc; ++c) wt[static_cast<size_t>(c) * nd.ncls + j] = w[static_cast<size_t>(j) * nd.hc + c];
+    void* ptr = nullptr;
+    if (hipMalloc(&ptr, wt.size() * 4) != hipSuccess) throw OomError("head weights: hipMalloc failed");
+    p->head_t[nd.head_t] = static_cast<float*>(ptr);
+    p->weight_bytes += wt.size() * 4;
+    hip_check(hipMemcpy(ptr, wt.data(), wt.size() * 4, hipMemcpyHostToDevice), "head weights upload");
   }
 
   assign_buffers(p, p->max_batch);
@@ -125,6 +142,12 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
   p->d_G = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_head_c, "pooled features");
   p->d_Z = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_ncls, "head logits");
   p->d_S = dev_alloc<float>(p, B, "halting sums");
+  p->d_zeros = dev_alloc<uint16_t>(p, 128, "zero page");
+  if (sp.pad_input_c) {
+    const TensorInfo& in = sp.tensors[sp.input];
+    p->d_xpad = dev_alloc<uint16_t>(p, static_cast<size_t>(B) * in.H * in.W * sp.pad_input_c, "padded input");
+  }
+  hip_check(hipMemset(p->d_zeros, 0, 256), "zero page");
   {
     void* ptr = nullptr;
     hip_check(hipHostMalloc(&ptr, sizeof(int32_t) * 2 * std::max(1, sp.decisions), hipHostMallocDefault),
@@ -153,10 +176,13 @@ void plan_free(dycl_plan* p) {
   p->ev_free.clear();
   for (Packed& q : p->spec.packed)
     if (q.dev) hipFree(q.dev);
+  for (float* h : p->head_t)
+    if (h) hipFree(h);
   for (void* b : p->buffers)
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
-                     p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S};
+                     p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S, p->d_zeros,
+                     p->d_xpad};
   for (void* s : singles)
     if (s) hipFree(s);
   if (p->h_counts) hipHostFree(p->h_counts);
@@ -241,14 +267,14 @@ struct Run {
       return;
     }
     k::ConvArgs a;
-    a.src = static_cast<const uint16_t*>(tp[nd.src]);
+    a.src = nd.pad_in ? p->d_xpad : static_cast<const uint16_t*>(tp[nd.src]);
     a.src2 = nd.src2 >= 0 ? static_cast<const uint16_t*>(tp[nd.src2]) : nullptr;
-    a.cin1 = nd.cin1;
+    a.cin1 = nd.pad_in ? sp.pad_input_c : nd.cin1;
     a.cin2 = nd.cin2;
     a.n = n;
     a.H = nd.H;
     a.W = nd.W;
-    a.cin = cin;
+    a.cin = nd.pad_in ? sp.pad_input_c : cin;
     a.Ho = nd.Ho;
     a.Wo = nd.Wo;
     a.cout = nd.cout;
@@ -257,13 +283,13 @@ struct Run {
     a.pad = nd.pad;
     a.w = q->dev;
     a.Kp = q->Kp;
-    a.tile = nd.tile;
     a.scale = f32(nd.scale_off);
     a.shift = f32(nd.shift_off);
     a.res = nd.res >= 0 ? static_cast<const uint16_t*>(tp[nd.res]) : nullptr;
     a.act = nd.act;
     a.dst = tp[nd.dst];
     a.out_f32 = 0;
+    a.zeros = p->d_zeros;
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
                                 static_cast<double>(nd.cout) * nd.k * nd.k * cin);
     launch(P_CONV, flops, bytes, [&] { k::conv_bf16(a, s); });
@@ -289,19 +315,28 @@ struct Run {
           if (n <= 0) break;
           const int HW = nd.H * nd.W;
           const float* G = static_cast<const float*>(tp[nd.src]);
-          if (sp.dt == DType::BF16) {
+          const double esz = sp.dt == DType::BF16 ? 2.0 : 4.0;
+          if (nd.head_t >= 0) {
+            launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, esz * n * HW * nd.hc + 4.0 * nd.ncls * (nd.hc + 1), [&] {
+              k::exit_head(tp[nd.src], sp.dt == DType::BF16, n, HW, nd.hc, p->head_t[nd.head_t], f32(nd.h_b),
+                           nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags, logits,
+                           sp.n_out, rec, s);
+            });
+          } else if (sp.dt == DType::BF16) {
             launch(P_HEAD, 0, 2.0 * n * HW * nd.hc + 4.0 * n * nd.hc, [&] {
               k::gap_bf16(static_cast<const uint16_t*>(tp[nd.src]), n, HW, nd.hc, p->d_G, s);
             });
             G = p->d_G;
           }
-          launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, 4.0 * (n * (nd.hc + nd.ncls) + nd.ncls * nd.hc), [&] {
-            k::linear_f32(G, n, nd.hc, f32(nd.h_w), f32(nd.h_b), nd.ncls, k::ACT_NONE, p->d_Z, s);
-          });
-          launch(P_HEAD, 0, 4.0 * n * nd.ncls * 2, [&] {
-            k::exit_decide(p->d_Z, n, nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags,
-                           logits, sp.n_out, rec, s);
-          });
+          if (nd.head_t < 0) {
+            launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, 4.0 * (n * (nd.hc + nd.ncls) + nd.ncls * nd.hc), [&] {
+              k::linear_f32(G, n, nd.hc, f32(nd.h_w), f32(nd.h_b), nd.ncls, k::ACT_NONE, p->d_Z, s);
+            });
+            launch(P_HEAD, 0, 4.0 * n * nd.ncls * 2, [&] {
+              k::exit_decide(p->d_Z, n, nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags,
+                             logits, sp.n_out, rec, s);
+            });
+          }
           if (nd.final_) {
             p->h_counts[2 * nd.decision] = n;
             p->h_counts[2 * nd.decision + 1] = 0;
@@ -371,13 +406,13 @@ struct Run {
           a.pad = 0;
           a.w = q.dev;
           a.Kp = q.Kp;
-          a.tile = nd.tile;
           a.scale = nullptr;
           a.shift = f32(nd.shift_off);
           a.res = nullptr;
           a.act = k::ACT_NONE;
           a.dst = logits;
           a.out_f32 = 1;
+          a.zeros = p->d_zeros;
           const double flops = 2.0 * B * nd.cout * nd.cin1;
           launch(P_CONV, flops, 2.0 * B * nd.cin1 + 4.0 * B * nd.cout + 2.0 * nd.cout * nd.cin1,
                  [&] { k::conv_bf16(a, s); });
@@ -410,6 +445,13 @@ void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logit
   r.orig = p->d_iota;
   r.launch(P_MISC, 0, 16.0 * B, [&] { k::init_records(rec, B, s); });
   if (sp.any_halt) r.launch(P_MISC, 0, 4.0 * B, [&] { k::fill_f32(p->d_S, 0.f, B, s); });
+  if (sp.pad_input_c) {
+    const TensorInfo& in = sp.tensors[sp.input];
+    const size_t pix = static_cast<size_t>(B) * in.H * in.W;
+    r.launch(P_MISC, 0, pix * 2.0 * (in.C + sp.pad_input_c), [&] {
+      k::pad_channels_bf16(static_cast<const uint16_t*>(x), pix, in.C, sp.pad_input_c, p->d_xpad, s);
+    });
+  }
   int n = B;
   r.exec(sp.nodes, n);
 }

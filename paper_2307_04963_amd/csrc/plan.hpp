@@ -51,10 +51,11 @@ struct Node {
   int64_t w_off = -1, w_ldk = 0, w_k0 = 0;   // weight tensor byte offset, row length, first column
   int64_t scale_off = -1, shift_off = -1;    // fp32 [cout] byte offsets (or -1)
   int packed = -1;                           // index of packed bf16 weights
-  k::ConvTile tile{128, 128};
+  bool pad_in = false;                       // reads the input padded to 8 channels
   // heads: exit W [ncls][C], b [ncls], T [1]; gate u [C], v [1]; halt w [C]
   int64_t h_w = -1, h_b = -1, h_T = -1;
   int ncls = 0, hc = 0;
+  int head_t = -1;      // index of the transposed head weights (fused exit head), or -1
   float tau = 0.f;
   bool final_ = false;
   int index = 0;        // exit head / gate / loop step
@@ -69,6 +70,9 @@ struct Node {
 struct Packed {
   int64_t w_off, w_ldk, w_k0;
   int cout, K, cout_pad, Kp;
+  // taps x cin_src weights per output channel in the blob, stored as
+  // taps x cin_pack (zero-filled) when the input channels are padded
+  int taps = 1, cin_src = 0, cin_pack = 0;
   uint16_t* dev = nullptr;
 };
 
@@ -91,6 +95,8 @@ struct Spec {
   bool any_halt = false;
   int max_head_c = 8, max_ncls = 8;
   int nodes_total = 0;
+  int pad_input_c = 0;
+  int n_head_t = 0;      // exit heads that use the fused kernel   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
 
   void parse(const std::string& json, size_t weights_bytes, int max_batch);
@@ -117,6 +123,9 @@ struct dycl_plan {
   float* d_G = nullptr;          // [max_batch, max_head_c]
   float* d_Z = nullptr;          // [max_batch, max_ncls]
   float* d_S = nullptr;          // [max_batch]
+  uint16_t* d_zeros = nullptr;   // 256 zero bytes: source of convolution padding taps
+  uint16_t* d_xpad = nullptr;    // input padded to 8 channels (stems with Cin < 8)
+  std::vector<float*> head_t;    // transposed exit-head weights [C][ncls]
   size_t workspace_bytes = 0, weight_bytes = 0;
   // profiling
   bool profile = false;

@@ -86,10 +86,13 @@ struct Builder {
     return off;
   }
 
-  int pack_index(int64_t off, int64_t ldk, int64_t k0, int cout, int K, int bn) {
+  int pack_index(int64_t off, int64_t ldk, int64_t k0, int cout, int K, int taps = 1, int cin_src = 0,
+                 int cin_pack = 0) {
+    if (cin_src == 0) cin_src = cin_pack = K;   // one run of K values
     for (size_t i = 0; i < sp.packed.size(); ++i) {
       const Packed& q = sp.packed[i];
-      if (q.w_off == off && q.w_ldk == ldk && q.w_k0 == k0 && q.cout == cout && q.K == K && q.cout_pad % bn == 0)
+      if (q.w_off == off && q.w_ldk == ldk && q.w_k0 == k0 && q.cout == cout && q.K == taps * cin_pack &&
+          q.cin_src == cin_src && q.cin_pack == cin_pack)
         return static_cast<int>(i);
     }
     Packed q;
@@ -97,9 +100,12 @@ struct Builder {
     q.w_ldk = ldk;
     q.w_k0 = k0;
     q.cout = cout;
-    q.K = K;
-    q.cout_pad = (cout + bn - 1) / bn * bn;
-    q.Kp = (K + k::kBK - 1) / k::kBK * k::kBK;
+    q.K = taps * cin_pack;
+    q.taps = taps;
+    q.cin_src = cin_src;
+    q.cin_pack = cin_pack;
+    q.cout_pad = k::conv_cout_pad(cout);
+    q.Kp = (q.K + k::kBK - 1) / k::kBK * k::kBK;
     sp.packed.push_back(q);
     return static_cast<int>(sp.packed.size()) - 1;
   }
@@ -153,9 +159,15 @@ struct Builder {
           nd.act == k::ACT_GELU)
         fail("fp32 specs support only linear layers (k 1 on 1x1 rows, bias, ReLU)");
       if (nd.w_k0 != 0 || nd.w_ldk != K) fail("fp32 linear weights must be dense [cout][cin]");
+    } else if (sp.tensors[nd.src].external && nd.src2 < 0 && nd.cin1 < 8) {
+      // a stem on a narrow input: the input is zero-padded to 8 channels once
+      // per run and the weights likewise, so the stem runs on 16-byte
+      // vectors (the padded products are exact zeros)
+      nd.pad_in = true;
+      sp.pad_input_c = 8;
+      nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, K, nd.k * nd.k, nd.cin1, 8);
     } else {
-      nd.tile = k::conv_pick_tile(max_batch * nd.Ho * nd.Wo, nd.cout);
-      nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, K, nd.tile.bn);
+      nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, K);
     }
     nd.dst = define(n.at("dst"), nd.Ho, nd.Wo, nd.cout, nd.seq_pre, "conv.dst");
     return nd;
@@ -226,6 +238,8 @@ struct Builder {
     nd.decision = sp.decisions++;
     sp.max_head_c = std::max(sp.max_head_c, s.C);
     sp.max_ncls = std::max(sp.max_ncls, nd.ncls);
+    // small heads (weights streamed from L2 once per row) use the fused kernel
+    if (nd.ncls <= 1024 && static_cast<int64_t>(s.C) * nd.ncls <= (int64_t(1) << 18)) nd.head_t = sp.n_head_t++;
     if (!nd.final_) {
       int old = space;
       space = next_space++;
@@ -350,8 +364,7 @@ struct Builder {
     if (nd.w_k0 < 0 || nd.w_k0 + s.C > nd.w_ldk) fail("output.w: column range exceeds ldk");
     need_bytes(nd.w_off, ((int64_t)(nd.cout - 1) * nd.w_ldk + nd.w_k0 + s.C) * 2, 2, "output.w");
     nd.shift_off = f32_vec(n, "bias", nd.cout);
-    nd.tile = k::conv_pick_tile(0, nd.cout);
-    nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, s.C, nd.tile.bn);
+    nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, s.C);
     return nd;
   }
 
@@ -409,10 +422,14 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   for (size_t i = 0; i < ns.size(); ++i) nodes.push_back(b.node(ns.at(i), max_batch));
 
   // every tensor that is moved between row groups must be a whole number of
-  // 16-byte vectors
-  for (const TensorInfo& t : tensors)
+  // 16-byte vectors, and a whole batch of it must be indexable with 32-bit
+  // pixel offsets
+  for (const TensorInfo& t : tensors) {
     if (!t.external && t.row_bytes(dt) % 16 != 0)
       throw SpecError("tensor '" + t.name + "': per-sample bytes must be a multiple of 16");
+    if (static_cast<int64_t>(max_batch) * t.H * t.W * t.C >= (int64_t(1) << 31))
+      throw SpecError("tensor '" + t.name + "': max_batch rows exceed 2^31 elements");
+  }
 
   std::ostringstream os;
   os << "nodes=" << nodes_total << " decisions=" << decisions << " tensors=" << tensors.size()
