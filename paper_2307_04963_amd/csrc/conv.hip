@@ -297,7 +297,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   constexpr int EPW = WTN + 4;                        // epilogue row stride (floats)
   constexpr int EPI = (NT / 64) * 32 * EPW * 4;
   constexpr int SMEM = NS * STAGE > EPI ? NS * STAGE : EPI;
-  static_assert(NS >= 2 && NS <= 4, "2 to 4 LDS stages");
+  static_assert(NS >= 1 && NS <= 4, "1 to 4 LDS stages (1: a single K step only)");
   static_assert(BM * 8 % NT == 0 && BN * 8 % NT == 0 && JB >= 1, "tile rows must fill whole load passes");
   static_assert(NT % 128 == 0, "swizzle assumes NT a multiple of 128");
   static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be 32x32 blocks");
@@ -409,13 +409,21 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
     if (i < nk) issue(i, i);
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + NS - 2 < nk)
-      wait_vm_barrier<(NS - 2) * (JA + JB)>();   // steps kt+1 .. kt+NS-2 may stay in flight
-    else
-      wait_vm_barrier<0>();
-    if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
-    compute(kt % NS);
+  if constexpr (NS == 1) {
+    // one K step (Kp == 64): no pipeline, a small LDS footprint, more
+    // workgroups per CU for these memory-bound layers
+    issue(0, 0);
+    wait_vm_barrier<0>();
+    compute(0);
+  } else {
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + NS - 2 < nk)
+        wait_vm_barrier<(NS - 2) * (JA + JB)>();   // steps kt+1 .. kt+NS-2 may stay in flight
+      else
+        wait_vm_barrier<0>();
+      if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
+      compute(kt % NS);
+    }
   }
 
   // epilogue through LDS: each wave stages 32 x WTN fp32 values (scale and
@@ -521,10 +529,11 @@ void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
 
 // direct-to-LDS kernel: the largest tile that still gives the chip enough
 // workgroups (measured on the layer shapes of the workloads)
-TileCfg choose_lds(int M, int cout) {
+TileCfg choose_lds(int M, int cout, int Kp) {
   const TileCfg c256{256, 256, 4, 2}, c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2},
       c32{128, 32, 4, 1};
   if (cout < 64) return c32;
+  if (Kp <= 64) return cout >= 128 ? c128 : c12864;   // one K step: memory-bound, small tiles
   if (cout >= 256 && tiles_of(c256, M, cout) >= 512) return c256;
   if (cout >= 128 && tiles_of(c128, M, cout) >= 384) return c128;
   if (tiles_of(c12864, M, cout) >= 512) return c12864;
@@ -533,7 +542,10 @@ TileCfg choose_lds(int M, int cout) {
 
 template <int BM, int BN, int WM, int WN, int KS>
 void go_lds(const ConvP& p, hipStream_t s) {
-  hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), dim3(p.mt * p.nt), dim3(64 * WM * WN), 0, s, p);
+  if (p.Kp == 64)
+    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), dim3(p.mt * p.nt), dim3(64 * WM * WN), 0, s, p);
+  else
+    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), dim3(p.mt * p.nt), dim3(64 * WM * WN), 0, s, p);
 }
 
 template <int KS>
@@ -608,7 +620,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   const bool vec_out = a.cout % 8 == 0 && (reinterpret_cast<uintptr_t>(a.dst) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
   if (vec_out) {
-    const TileCfg c = choose_lds(p.M, a.cout);
+    const TileCfg c = choose_lds(p.M, a.cout, p.Kp);
     p.mt = (p.M + c.bm - 1) / c.bm;
     p.nt = (a.cout + c.bn - 1) / c.bn;
     if (a.k == 1)

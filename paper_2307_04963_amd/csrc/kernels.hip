@@ -135,6 +135,64 @@ void linear_f32(const float* X, int n, int K, const float* W, const float* bias,
   hipLaunchKernelGGL(linear_f32_kernel, grid, dim3(256), 0, s, X, n, K, W, bias, N, act, Y);
 }
 
+// ------------------------------------------------------- skinny linear ----
+// Y[m, j] = act(b[j] + sum_k X[m, k] Wt[k, j]) with the weights transposed
+// (Wt [K][N]): a workgroup owns R rows x 64 columns; its NW waves take the
+// K range interleaved (wave w: k = w, w + NW, ...) so that every lane keeps
+// many independent loads in flight, and the partial sums meet in LDS.  The
+// weight reads are coalesced over columns and shared by the R rows.
+
+template <int R, int NW>
+__global__ __launch_bounds__(64 * NW) void linear_t_kernel(const float* __restrict__ X, int n, int K,
+                                                           const float* __restrict__ Wt,
+                                                           const float* __restrict__ bias, int N, int act,
+                                                           float* __restrict__ Y) {
+  __shared__ float red[NW][R][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = blockIdx.y * 64 + lane, m0 = blockIdx.x * R;
+  const int cc = col < N ? col : N - 1;
+  const float* xr[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) xr[r] = X + (size_t)(m0 + r < n ? m0 + r : n - 1) * K;
+  float acc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[r] = 0.f;
+#pragma unroll 4
+  for (int k = w; k < K; k += NW) {
+    const float wv = Wt[(size_t)k * N + cc];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = fmaf(xr[r][k], wv, acc[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) red[w][r][lane] = acc[r];
+  __syncthreads();
+  if (w == 0 && col < N) {
+    const float b = bias ? bias[col] : 0.f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (m0 + r >= n) break;
+      float v = 0.f;
+#pragma unroll
+      for (int q = 0; q < NW; ++q) v += red[q][r][lane];
+      v += b;
+      if (act == ACT_RELU) v = v > 0.f ? v : 0.f;
+      Y[(size_t)(m0 + r) * N + col] = v;
+    }
+  }
+}
+
+void linear_t_f32(const float* X, int n, int K, const float* Wt, const float* bias, int N, int act, float* Y,
+                  hipStream_t s) {
+  const int gy = (N + 63) / 64;
+  // rows per workgroup: as many as keep >= 256 workgroups in flight
+  if ((long)((n + 7) / 8) * gy >= 256)
+    hipLaunchKernelGGL((linear_t_kernel<8, 8>), dim3((n + 7) / 8, gy), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y);
+  else if ((long)((n + 3) / 4) * gy >= 128)
+    hipLaunchKernelGGL((linear_t_kernel<4, 8>), dim3((n + 3) / 4, gy), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y);
+  else
+    hipLaunchKernelGGL((linear_t_kernel<1, 8>), dim3(n, gy), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y);
+}
+
 // --------------------------------------------------------- exit decide ----
 
 __global__ __launch_bounds__(64) void exit_decide_kernel(const float* __restrict__ Z, int ncls,
@@ -386,6 +444,33 @@ __global__ __launch_bounds__(256) void move_rows_kernel(uint4* __restrict__ dst,
     const size_t v = v0 + static_cast<size_t>(j) * 256;
     if (v < vpr) dp[v] = sp[v];
   }
+}
+
+// several tensors moved with the same index list in one launch (blockIdx.z
+// selects the tensor)
+__global__ __launch_bounds__(256) void move_rows_multi_kernel(MoveSet set, const int32_t* __restrict__ dst_idx,
+                                                              const int32_t* __restrict__ src_idx) {
+  const int t = blockIdx.z;
+  const size_t vpr = set.vpr[t];
+  const size_t v0 = static_cast<size_t>(blockIdx.y) * 1024 + threadIdx.x;
+  if (v0 >= vpr) return;
+  const int r = blockIdx.x;
+  const size_t d = dst_idx ? static_cast<size_t>(dst_idx[r]) : static_cast<size_t>(r);
+  const size_t sr = src_idx ? static_cast<size_t>(src_idx[r]) : static_cast<size_t>(r);
+  const uint4* sp = static_cast<const uint4*>(set.src[t]) + sr * vpr;
+  uint4* dp = static_cast<uint4*>(set.dst[t]) + d * vpr;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const size_t v = v0 + static_cast<size_t>(j) * 256;
+    if (v < vpr) dp[v] = sp[v];
+  }
+}
+
+void move_rows_multi(const MoveSet& set, const int32_t* dst_idx, const int32_t* src_idx, int n, hipStream_t s) {
+  size_t maxv = 0;
+  for (int t = 0; t < set.count; ++t) maxv = set.vpr[t] > maxv ? set.vpr[t] : maxv;
+  dim3 grid(n, static_cast<unsigned>((maxv + 1023) / 1024), set.count);
+  hipLaunchKernelGGL(move_rows_multi_kernel, grid, dim3(256), 0, s, set, dst_idx, src_idx);
 }
 
 void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,

@@ -38,6 +38,11 @@ struct ConvArgs {
 };
 void conv_bf16(const ConvArgs& a, hipStream_t s);
 
+// Y[m, j] = act(sum_k X[m, k] Wt[k, j] + bias[j]), fp32, weights transposed;
+// for few rows (MLP layers, exit heads)
+void linear_t_f32(const float* X, int n, int K, const float* Wt, const float* bias, int N, int act, float* Y,
+                  hipStream_t s);
+
 // Y[m, j] = act(sum_k X[m, k] W[j, k] + bias[j]), fp32
 void linear_f32(const float* X, int n, int K, const float* W, const float* bias, int N, int act, float* Y,
                 hipStream_t s);
@@ -81,6 +86,15 @@ void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t
 
 // y[p, c] = c < cin ? x[p, c] : 0 for every pixel p, c < cout (cout == 8)
 void pad_channels_bf16(const uint16_t* x, size_t pixels, int cin, int cout, uint16_t* y, hipStream_t s);
+
+// up to 4 tensors moved with one index list in one launch
+struct MoveSet {
+  int count;
+  void* dst[4];
+  const void* src[4];
+  size_t vpr[4];   // 16-byte vectors per row
+};
+void move_rows_multi(const MoveSet& set, const int32_t* dst_idx, const int32_t* src_idx, int n, hipStream_t s);
 
 void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s);
 void init_records(dycl_record* rec, int n, hipStream_t s);

@@ -113,14 +113,17 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     hip_check(hipMemcpy(q.dev, h.data(), h.size() * 2, hipMemcpyHostToDevice), "packed weights upload");
   }
 
-  // transposed weights of the fused exit heads
+  // fp32 weight matrices [rows][cols] kept transposed ([cols][rows]): exit
+  // heads and fp32 linear layers
   p->head_t.assign(sp.n_head_t, nullptr);
   for (const Node& nd : sp.nodes) {
-    if (nd.kind != NodeKind::Exit || nd.head_t < 0) continue;
-    std::vector<float> wt(static_cast<size_t>(nd.hc) * nd.ncls);
-    const float* w = reinterpret_cast<const float*>(hb + nd.h_w);
-    for (int j = 0; j < nd.ncls; ++j)
-      for (int c = 0; c < nd.hc; ++c) wt[static_cast<size_t>(c) * nd.ncls + j] = w[static_cast<size_t>(j) * nd.hc + c];
+    if (nd.head_t < 0) continue;
+    const bool ex = nd.kind == NodeKind::Exit;
+    const int rows = ex ? nd.ncls : nd.cout, cols = ex ? nd.hc : nd.cin1;
+    std::vector<float> wt(static_cast<size_t>(rows) * cols);
+    const float* w = reinterpret_cast<const float*>(hb + (ex ? nd.h_w : nd.w_off));
+    for (int j = 0; j < rows; ++j)
+      for (int c = 0; c < cols; ++c) wt[static_cast<size_t>(c) * rows + j] = w[static_cast<size_t>(j) * cols + c];
     void* ptr = nullptr;
     if (hipMalloc(&ptr, wt.size() * 4) != hipSuccess) throw OomError("head weights: hipMalloc failed");
     p->head_t[nd.head_t] = static_cast<float*>(ptr);
@@ -252,6 +255,27 @@ struct Run {
     launch(cls, 0, 2.0 * rb * n + 4.0 * n, [&] { k::move_rows(dst, didx, src, sidx, rb, n, s); });
   }
 
+  // every (from, to) tensor pair moved with the same index lists (row r of
+  // `to` at didx[r] <- row sidx[r] of `from`; null = identity), four per launch
+  void move_pairs(const std::vector<std::pair<int, int>>& pairs, const int32_t* didx, const int32_t* sidx, int n) {
+    if (n <= 0 || pairs.empty()) return;
+    const Spec& sp = p->spec;
+    for (size_t i = 0; i < pairs.size(); i += 4) {
+      k::MoveSet set{};
+      double bytes = 0;
+      for (size_t j = i; j < pairs.size() && j < i + 4; ++j) {
+        const int from = pairs[j].first, to = pairs[j].second;
+        const size_t rb = sp.tensors[from].row_bytes(sp.dt);
+        set.src[set.count] = tp[from];
+        set.dst[set.count] = tp[to];
+        set.vpr[set.count] = rb / 16;
+        ++set.count;
+        bytes += 2.0 * rb * n + 4.0 * n;
+      }
+      launch(P_MOVE, 0, bytes, [&] { k::move_rows_multi(set, didx, sidx, n, s); });
+    }
+  }
+
   void conv(const Node& nd, int n) {
     const Spec& sp = p->spec;
     const Packed* q = nd.packed >= 0 ? &sp.packed[nd.packed] : nullptr;
@@ -261,8 +285,8 @@ struct Run {
     if (sp.dt == DType::F32) {
       const double bytes = 4.0 * (static_cast<double>(n) * (cin + nd.cout) + static_cast<double>(nd.cout) * cin);
       launch(P_LINEAR32, flops, bytes, [&] {
-        k::linear_f32(static_cast<const float*>(tp[nd.src]), n, cin, f32(nd.w_off), f32(nd.shift_off), nd.cout,
-                      nd.act, static_cast<float*>(tp[nd.dst]), s);
+        k::linear_t_f32(static_cast<const float*>(tp[nd.src]), n, cin, p->head_t[nd.head_t], f32(nd.shift_off),
+                        nd.cout, nd.act, static_cast<float*>(tp[nd.dst]), s);
       });
       return;
     }
@@ -316,7 +340,7 @@ struct Run {
           const int HW = nd.H * nd.W;
           const float* G = static_cast<const float*>(tp[nd.src]);
           const double esz = sp.dt == DType::BF16 ? 2.0 : 4.0;
-          if (nd.head_t >= 0) {
+          if (nd.fused) {
             launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, esz * n * HW * nd.hc + 4.0 * nd.ncls * (nd.hc + 1), [&] {
               k::exit_head(tp[nd.src], sp.dt == DType::BF16, n, HW, nd.hc, p->head_t[nd.head_t], f32(nd.h_b),
                            nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags, logits,
@@ -328,9 +352,9 @@ struct Run {
             });
             G = p->d_G;
           }
-          if (nd.head_t < 0) {
+          if (!nd.fused) {
             launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, 4.0 * (n * (nd.hc + nd.ncls) + nd.ncls * nd.hc), [&] {
-              k::linear_f32(G, n, nd.hc, f32(nd.h_w), f32(nd.h_b), nd.ncls, k::ACT_NONE, p->d_Z, s);
+              k::linear_t_f32(G, n, nd.hc, p->head_t[nd.head_t], f32(nd.h_b), nd.ncls, k::ACT_NONE, p->d_Z, s);
             });
             launch(P_HEAD, 0, 4.0 * n * nd.ncls * 2, [&] {
               k::exit_decide(p->d_Z, n, nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags,
@@ -346,8 +370,7 @@ struct Run {
           int32_t* next = p->d_orig[orig_next];
           compact(n, nd.decision, next);
           const int stay = p->h_counts[2 * nd.decision + 1];
-          for (auto& pr : nd.pairs)
-            move(P_MOVE, tp[pr.second], nullptr, tp[pr.first], p->d_idx0, sp.tensors[pr.first].row_bytes(sp.dt), stay);
+          move_pairs(nd.pairs, nullptr, p->d_idx0, stay);
           orig = next;
           orig_next ^= 1;
           n = stay;
@@ -363,12 +386,10 @@ struct Run {
           compact(n, nd.decision, p->d_org0);
           int ne = p->h_counts[2 * nd.decision];
           if (ne > 0) {
-            for (auto& pr : nd.pairs)
-              move(P_MOVE, tp[pr.second], nullptr, tp[pr.first], p->d_idx1, sp.tensors[pr.first].row_bytes(sp.dt), ne);
+            move_pairs(nd.pairs, nullptr, p->d_idx1, ne);     // gather the executing rows
             int nb = ne;
             exec(nd.body, nb);
-            for (auto& pr : nd.scatter)
-              move(P_MOVE, tp[pr.second], p->d_idx1, tp[pr.first], nullptr, sp.tensors[pr.first].row_bytes(sp.dt), ne);
+            move_pairs(nd.scatter, p->d_idx1, nullptr, ne);   // scatter the block outputs back
           }
           break;
         }
@@ -383,8 +404,7 @@ struct Run {
           const int nh = p->h_counts[2 * nd.decision], stay = p->h_counts[2 * nd.decision + 1];
           move(P_MOVE, tp[nd.park_dst], p->d_org1, tp[nd.park_src], p->d_idx1,
                sp.tensors[nd.park_src].row_bytes(sp.dt), nh);
-          for (auto& pr : nd.pairs)
-            move(P_MOVE, tp[pr.second], nullptr, tp[pr.first], p->d_idx0, sp.tensors[pr.first].row_bytes(sp.dt), stay);
+          move_pairs(nd.pairs, nullptr, p->d_idx0, stay);
           orig = next;
           orig_next ^= 1;
           n = stay;

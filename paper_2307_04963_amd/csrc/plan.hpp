@@ -55,7 +55,8 @@ struct Node {
   // heads: exit W [ncls][C], b [ncls], T [1]; gate u [C], v [1]; halt w [C]
   int64_t h_w = -1, h_b = -1, h_T = -1;
   int ncls = 0, hc = 0;
-  int head_t = -1;      // index of the transposed head weights (fused exit head), or -1
+  int head_t = -1;      // index of the transposed fp32 weights (exit heads, fp32 linear layers), or -1
+  bool fused = false;   // exit head small enough for the one-kernel path
   float tau = 0.f;
   bool final_ = false;
   int index = 0;        // exit head / gate / loop step
@@ -96,7 +97,7 @@ struct Spec {
   int max_head_c = 8, max_ncls = 8;
   int nodes_total = 0;
   int pad_input_c = 0;
-  int n_head_t = 0;      // exit heads that use the fused kernel   // > 0: the input is zero-padded to this many channels for the stem
+  int n_head_t = 0;      // fp32 weight matrices kept transposed on the device   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
 
   void parse(const std::string& json, size_t weights_bytes, int max_batch);
@@ -125,7 +126,7 @@ struct dycl_plan {
   float* d_S = nullptr;          // [max_batch]
   uint16_t* d_zeros = nullptr;   // 256 zero bytes: source of convolution padding taps
   uint16_t* d_xpad = nullptr;    // input padded to 8 channels (stems with Cin < 8)
-  std::vector<float*> head_t;    // transposed exit-head weights [C][ncls]
+  std::vector<float*> head_t;    // transposed fp32 weights: exit heads [C][ncls], fp32 linears [cin][cout]
   size_t workspace_bytes = 0, weight_bytes = 0;
   // profiling
   bool profile = false;

@@ -159,6 +159,7 @@ struct Builder {
           nd.act == k::ACT_GELU)
         fail("fp32 specs support only linear layers (k 1 on 1x1 rows, bias, ReLU)");
       if (nd.w_k0 != 0 || nd.w_ldk != K) fail("fp32 linear weights must be dense [cout][cin]");
+      nd.head_t = sp.n_head_t++;   // kept transposed on the device
     } else if (sp.tensors[nd.src].external && nd.src2 < 0 && nd.cin1 < 8) {
       // a stem on a narrow input: the input is zero-padded to 8 channels once
       // per run and the weights likewise, so the stem runs on 16-byte
@@ -238,8 +239,10 @@ struct Builder {
     nd.decision = sp.decisions++;
     sp.max_head_c = std::max(sp.max_head_c, s.C);
     sp.max_ncls = std::max(sp.max_ncls, nd.ncls);
-    // small heads (weights streamed from L2 once per row) use the fused kernel
-    if (nd.ncls <= 1024 && static_cast<int64_t>(s.C) * nd.ncls <= (int64_t(1) << 18)) nd.head_t = sp.n_head_t++;
+    // the head weights live transposed on the device; small heads (weights
+    // streamed from L2 once per row) run as one fused kernel
+    nd.head_t = sp.n_head_t++;
+    nd.fused = nd.ncls <= 1024 && static_cast<int64_t>(s.C) * nd.ncls <= (int64_t(1) << 16);
     if (!nd.final_) {
       int old = space;
       space = next_space++;
