@@ -19,6 +19,8 @@ STATUS = {0: "DYCL_OK", -1: "DYCL_E_INVALID", -2: "DYCL_E_SPEC", -3: "DYCL_E_WEI
 # every symbol include/dycl.h declares
 EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_last_counts", "dycl_plan_info", "dycl_profile_enable",
            "dycl_profile_read", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
+# every symbol include/dycl_ops.h declares
+OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_move_rows"]
 
 
 class DyclError(RuntimeError):
@@ -61,6 +63,12 @@ def _load():
     lib.dycl_plan_destroy.restype = None
     lib.dycl_last_error.argtypes = []
     lib.dycl_last_error.restype = C.c_char_p
+    lib.dycl_op_compact_workspace.argtypes = [C.c_int64]
+    lib.dycl_op_compact_workspace.restype = C.c_size_t
+    lib.dycl_op_compact.argtypes = [vp, vp, C.c_int64, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
+    lib.dycl_op_compact.restype = i32
+    lib.dycl_op_move_rows.argtypes = [vp, vp, vp, vp, C.c_size_t, C.c_int64, vp]
+    lib.dycl_op_move_rows.restype = i32
     return lib
 
 

@@ -169,3 +169,75 @@ void dycl_plan_destroy(dycl_plan* plan) {
 const char* dycl_last_error(void) { return g_err.c_str(); }
 
 }  // extern "C"
+
+// ------------------------------------------------------------ routing ops ---
+
+#include "../../include/dycl_ops.h"
+
+extern "C" {
+
+size_t dycl_op_compact_workspace(int64_t n) {
+  if (n <= 0) return 0;
+  return n <= 16384 ? 0 : dycl::k::compact_workspace(static_cast<size_t>(n));
+}
+
+int dycl_op_compact(const uint8_t* flags, const int32_t* orig, int64_t n, int32_t* idx1, int32_t* org1,
+                    int32_t* idx0, int32_t* org0, int32_t* counts, void* workspace, size_t workspace_bytes,
+                    void* hip_stream) {
+  if (n < 0 || n >= (int64_t(1) << 31)) return fail(DYCL_E_INVALID, "dycl_op_compact: n outside [0, 2^31)");
+  if (!counts) return fail(DYCL_E_INVALID, "dycl_op_compact: null counts");
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (n == 0) {
+    return guarded([&] {
+      const int32_t z[2] = {0, 0};
+      if (hipMemcpyAsync(counts, z, sizeof(z), hipMemcpyHostToDevice, s) != hipSuccess ||
+          hipStreamSynchronize(s) != hipSuccess)
+        throw dycl::HipError("dycl_op_compact: clearing counts failed");
+      return DYCL_OK;
+    });
+  }
+  if (!flags || !idx1 || !idx0) return fail(DYCL_E_INVALID, "dycl_op_compact: null flags or index output");
+  if (reinterpret_cast<uintptr_t>(flags) & 15) return fail(DYCL_E_INVALID, "dycl_op_compact: flags must be 16-byte aligned");
+  const size_t need = dycl_op_compact_workspace(n);
+  if (need && (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 7)))
+    return fail(DYCL_E_INVALID, "dycl_op_compact: workspace missing, too small or misaligned (need " +
+                                    std::to_string(need) + " bytes)");
+  return guarded([&] {
+    if (n <= 16384) {
+      // single workgroup; it always writes both id lists
+      if (!org1 || !org0) {
+        if (!workspace || workspace_bytes < 8 * static_cast<size_t>(n))
+          throw std::invalid_argument(
+              "dycl_op_compact: for n <= 16384 pass org1 and org0, or 8*n bytes of workspace to receive them");
+        int32_t* w = static_cast<int32_t*>(workspace);
+        dycl::k::compact(flags, orig, static_cast<int>(n), idx1, org1 ? org1 : w, idx0, org0 ? org0 : w + n, counts,
+                         s);
+      } else {
+        dycl::k::compact(flags, orig, static_cast<int>(n), idx1, org1, idx0, org0, counts, s);
+      }
+    } else {
+      dycl::k::compact_large(flags, orig, static_cast<size_t>(n), idx1, org1, idx0, org0, counts, workspace, s);
+    }
+    if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_compact: launch failed");
+    return DYCL_OK;
+  });
+}
+
+int dycl_op_move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes,
+                      int64_t n, void* hip_stream) {
+  if (n < 0 || n >= (int64_t(1) << 31)) return fail(DYCL_E_INVALID, "dycl_op_move_rows: n outside [0, 2^31)");
+  if (n == 0) return DYCL_OK;
+  if (!dst || !src) return fail(DYCL_E_INVALID, "dycl_op_move_rows: null dst or src");
+  if (row_bytes == 0 || row_bytes % 16 || (reinterpret_cast<uintptr_t>(dst) & 15) ||
+      (reinterpret_cast<uintptr_t>(src) & 15))
+    return fail(DYCL_E_INVALID, "dycl_op_move_rows: row_bytes must be a positive multiple of 16, buffers 16-byte aligned");
+  if (row_bytes / 16 > (size_t(65535) * 1024))
+    return fail(DYCL_E_INVALID, "dycl_op_move_rows: rows longer than 1 GiB are not supported");
+  return guarded([&] {
+    dycl::k::move_rows(dst, dst_idx, src, src_idx, row_bytes, static_cast<int>(n), static_cast<hipStream_t>(hip_stream));
+    if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_move_rows: launch failed");
+    return DYCL_OK;
+  });
+}
+
+}  // extern "C"

@@ -428,6 +428,128 @@ void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, in
   hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, flags, orig, n, idx1, org1, idx0, org0, counts);
 }
 
+// ------------------------------------------------- large-n compaction ----
+// Reduce-then-scan over blocks of 4096 flags: (1) every block counts its
+// set flags, (2) one workgroup turns the counts into per-block output
+// offsets, (3) every block ranks its flags again (16 per thread, loaded as
+// one 16-byte vector; wave prefix sums by shuffles, waves combined through
+// LDS) and writes both lists.  Order is preserved (stable partition).
+
+constexpr int kCompactBlock = 4096;
+
+__device__ __forceinline__ int flag_count16(const uint8_t* __restrict__ f, size_t i0, size_t n, uint8_t v[16]) {
+  if (i0 + 16 <= n) {
+    const uint4 q = *reinterpret_cast<const uint4*>(f + i0);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v[j] = (w[j >> 2] >> (8 * (j & 3))) & 0xff;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v[j] = (i0 + j < n) ? f[i0 + j] : 0;
+  }
+  int c = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) c += v[j] != 0;
+  return c;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+__global__ __launch_bounds__(256) void compact_count_kernel(const uint8_t* __restrict__ flags, size_t n,
+                                                            int32_t* __restrict__ bcount) {
+  __shared__ int ws[4];
+  uint8_t v[16];
+  const size_t i0 = static_cast<size_t>(blockIdx.x) * kCompactBlock + threadIdx.x * 16;
+  int c = i0 < n ? flag_count16(flags, i0, n, v) : 0;
+  c = wave_incl_scan(c);
+  if ((threadIdx.x & 63) == 63) ws[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) bcount[blockIdx.x] = ws[0] + ws[1] + ws[2] + ws[3];
+}
+
+__global__ __launch_bounds__(1024) void compact_scan_kernel(const int32_t* __restrict__ bcount, int nb, size_t n,
+                                                            int64_t* __restrict__ boff, int32_t* counts) {
+  __shared__ int64_t ws[16];
+  __shared__ int64_t carry;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  for (int b0 = 0; b0 < nb; b0 += 1024) {
+    const int b = b0 + threadIdx.x;
+    const int c = b < nb ? bcount[b] : 0;
+    int x = wave_incl_scan(c);
+    if ((threadIdx.x & 63) == 63) ws[threadIdx.x >> 6] = x;
+    __syncthreads();
+    int64_t before = carry;
+    for (int w = 0; w < (int)(threadIdx.x >> 6); ++w) before += ws[w];
+    if (b < nb) boff[b] = before + x - c;     // ones before block b
+    __syncthreads();
+    if (threadIdx.x == 1023) carry = before + x;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    counts[0] = static_cast<int32_t>(carry);
+    counts[1] = static_cast<int32_t>(static_cast<int64_t>(n) - carry);
+  }
+}
+
+__global__ __launch_bounds__(256) void compact_write_kernel(const uint8_t* __restrict__ flags,
+                                                            const int32_t* __restrict__ orig, size_t n,
+                                                            const int64_t* __restrict__ boff, int32_t* idx1,
+                                                            int32_t* org1, int32_t* idx0, int32_t* org0) {
+  __shared__ int ws[4];
+  uint8_t v[16];
+  const size_t blk0 = static_cast<size_t>(blockIdx.x) * kCompactBlock;
+  const size_t i0 = blk0 + threadIdx.x * 16;
+  const int c = i0 < n ? flag_count16(flags, i0, n, v) : 0;
+  const int x = wave_incl_scan(c);
+  if ((threadIdx.x & 63) == 63) ws[threadIdx.x >> 6] = x;
+  __syncthreads();
+  int before = x - c;
+  for (int w = 0; w < (int)(threadIdx.x >> 6); ++w) before += ws[w];
+  const int64_t ones_before_blk = boff[blockIdx.x];
+  int64_t o1 = ones_before_blk + before;                               // next slot for a set flag
+  int64_t o0 = static_cast<int64_t>(i0) - ones_before_blk - before;    // next slot for a clear one
+  if (i0 >= n) return;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const size_t i = i0 + j;
+    if (i >= n) break;
+    const int32_t id = orig ? orig[i] : static_cast<int32_t>(i);
+    if (v[j]) {
+      idx1[o1] = static_cast<int32_t>(i);
+      if (org1) org1[o1] = id;
+      ++o1;
+    } else {
+      idx0[o0] = static_cast<int32_t>(i);
+      if (org0) org0[o0] = id;
+      ++o0;
+    }
+  }
+}
+
+size_t compact_workspace(size_t n) {
+  const size_t nb = (n + kCompactBlock - 1) / kCompactBlock;
+  return nb * (sizeof(int32_t) + sizeof(int64_t)) + 256;
+}
+
+void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t* idx1, int32_t* org1, int32_t* idx0,
+                   int32_t* org0, int32_t* counts, void* workspace, hipStream_t s) {
+  const int nb = static_cast<int>((n + kCompactBlock - 1) / kCompactBlock);
+  int64_t* boff = static_cast<int64_t*>(workspace);
+  int32_t* bcount = reinterpret_cast<int32_t*>(boff + nb);
+  hipLaunchKernelGGL(compact_count_kernel, dim3(nb), dim3(256), 0, s, flags, n, bcount);
+  hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, s, bcount, nb, n, boff, counts);
+  hipLaunchKernelGGL(compact_write_kernel, dim3(nb), dim3(256), 0, s, flags, orig, n, boff, idx1, org1, idx0, org0);
+}
+
 // ------------------------------------------------------------ row moves ---
 
 __global__ __launch_bounds__(256) void move_rows_kernel(uint4* __restrict__ dst, const int32_t* __restrict__ dst_idx,

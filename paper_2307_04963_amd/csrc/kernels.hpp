@@ -79,6 +79,13 @@ void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux
 void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, int32_t* org1, int32_t* idx0,
              int32_t* org0, int32_t* counts, hipStream_t s);
 
+// The same partition for large n (reduce-then-scan over 4096-flag blocks);
+// org1 / org0 may be null.  workspace: compact_workspace(n) bytes, 8-byte
+// aligned.  n < 2^31.
+size_t compact_workspace(size_t n);
+void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t* idx1, int32_t* org1, int32_t* idx0,
+                   int32_t* org0, int32_t* counts, void* workspace, hipStream_t s);
+
 // dst row (dst_idx ? dst_idx[r] : r) = src row (src_idx ? src_idx[r] : r),
 // r < n; row_bytes is a multiple of 16.
 void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,

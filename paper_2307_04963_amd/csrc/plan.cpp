@@ -146,6 +146,7 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
   p->d_Z = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_ncls, "head logits");
   p->d_S = dev_alloc<float>(p, B, "halting sums");
   p->d_zeros = dev_alloc<uint16_t>(p, 128, "zero page");
+  if (B > 16384) p->d_cws = dev_alloc<uint8_t>(p, k::compact_workspace(B), "compaction workspace");
   if (sp.pad_input_c) {
     const TensorInfo& in = sp.tensors[sp.input];
     p->d_xpad = dev_alloc<uint16_t>(p, static_cast<size_t>(B) * in.H * in.W * sp.pad_input_c, "padded input");
@@ -185,7 +186,7 @@ void plan_free(dycl_plan* p) {
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
                      p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S, p->d_zeros,
-                     p->d_xpad};
+                     p->d_xpad, p->d_cws};
   for (void* s : singles)
     if (s) hipFree(s);
   if (p->h_counts) hipHostFree(p->h_counts);
@@ -244,8 +245,11 @@ struct Run {
   void compact(int n, int d, int32_t* org0) {
     const Spec& sp = p->spec;
     (void)sp;
-    launch(P_COMPACT, 0, n * (1.0 + 16.0), [&] {
-      k::compact(p->d_flags, orig, n, p->d_idx1, p->d_org1, p->d_idx0, org0, p->d_counts + 2 * d, s);
+    launch(P_COMPACT, 0, n * (1.0 + 4.0 + 16.0), [&] {
+      if (n <= 16384)
+        k::compact(p->d_flags, orig, n, p->d_idx1, p->d_org1, p->d_idx0, org0, p->d_counts + 2 * d, s);
+      else
+        k::compact_large(p->d_flags, orig, n, p->d_idx1, p->d_org1, p->d_idx0, org0, p->d_counts + 2 * d, p->d_cws, s);
     });
     read_counts(d);
   }

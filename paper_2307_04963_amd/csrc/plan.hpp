@@ -124,6 +124,7 @@ struct dycl_plan {
   float* d_G = nullptr;          // [max_batch, max_head_c]
   float* d_Z = nullptr;          // [max_batch, max_ncls]
   float* d_S = nullptr;          // [max_batch]
+  void* d_cws = nullptr;         // workspace of the large-n compaction (max_batch > 16384)
   uint16_t* d_zeros = nullptr;   // 256 zero bytes: source of convolution padding taps
   uint16_t* d_xpad = nullptr;    // input padded to 8 channels (stems with Cin < 8)
   std::vector<float*> head_t;    // transposed fp32 weights: exit heads [C][ncls], fp32 linears [cin][cout]

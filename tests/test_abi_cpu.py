@@ -17,17 +17,30 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 lib = _lib.lib
 
 
-def _declared():
-    with open(os.path.join(ROOT, "include", "dycl.h")) as f:
+def _declared(header):
+    with open(os.path.join(ROOT, "include", header)) as f:
         text = f.read()
-    return sorted(set(re.findall(r"\b(dycl_[a-z_]+)\s*\(", text)))
+    # function declarations only (return type at the start of the line)
+    return sorted(set(re.findall(r"^(?:int|size_t|void|const char\s*\*)\s*(dycl_[a-z_]+)\s*\(", text, re.M)))
 
 
-def test_exports_match_header():
-    names = _declared()
-    assert names == sorted(_lib.EXPORTS)
-    for n in names:
-        assert hasattr(lib, n), n
+def test_exports_match_headers():
+    for header, exported in (("dycl.h", _lib.EXPORTS), ("dycl_ops.h", _lib.OPS_EXPORTS)):
+        names = _declared(header)
+        assert names == sorted(exported), header
+        for n in names:
+            assert hasattr(lib, n), n
+
+
+def test_ops_reject_bad_arguments_without_gpu():
+    assert lib.dycl_op_compact_workspace(0) == 0
+    assert lib.dycl_op_compact_workspace(100) == 0
+    assert lib.dycl_op_compact_workspace(1 << 20) > (1 << 20) // 4096 * 12
+    assert lib.dycl_op_compact(None, None, -1, None, None, None, None, None, None, 0, None) == -1
+    assert lib.dycl_op_compact(None, None, 5, None, None, None, None, None, None, 0, None) == -1
+    assert lib.dycl_op_move_rows(None, None, None, None, 16, 3, None) == -1
+    assert lib.dycl_op_move_rows(C.c_void_p(16), None, C.c_void_p(32), None, 24, 3, None) == -1   # row_bytes % 16
+    assert lib.dycl_op_move_rows(None, None, None, None, 16, 0, None) == 0
 
 
 def _check(spec, blob_bytes, max_batch=8):
