@@ -51,6 +51,74 @@ def cpu_baseline(wl, seconds: float):
             "sample": f"{n} samples of {wl.name} run one by one (float64 accumulation, bf16 storage), {el:.1f} s"}
 
 
+def hbm_kernels(stream, reps: int = 10):
+    """Routing primitives at sizes where HBM bandwidth is the bound, timed
+    with HIP events on `stream`: the large-n compaction of 2^26 flags (set
+    with probability 1/2, with original ids) and the gather of ResNet-50
+    stage-1 activation rows (56x56x256 bf16 = 1.5 MiB per sample)."""
+    import ctypes as C
+    import numpy as np
+    import torch
+    from paper_2307_04963_amd import _lib
+    L = _lib.lib
+    out = {}
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    n = 1 << 26
+    g = torch.Generator(device="cuda").manual_seed(3)
+    flags = (torch.rand(n, device="cuda", generator=g) < 0.5).to(torch.uint8)
+    orig = torch.randperm(n, device="cuda", generator=g).to(torch.int32)
+    outs = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in range(4)]
+    counts = torch.empty(2, dtype=torch.int32, device="cuda")
+    wsb = L.dycl_op_compact_workspace(n)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    args = [C.c_void_p(flags.data_ptr()), C.c_void_p(orig.data_ptr()), n] + [C.c_void_p(t.data_ptr()) for t in outs]
+    args += [C.c_void_p(counts.data_ptr()), C.c_void_p(ws.data_ptr()), wsb, C.c_void_p(stream.cuda_stream)]
+    _lib.check(L.dycl_op_compact(*args))
+    a, b = ev(), ev()
+    a.record(stream)
+    for _ in range(reps):
+        _lib.check(L.dycl_op_compact(*args))
+    b.record(stream)
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / reps
+    nbytes = n * (1 + 4 + 8)      # flags, ids in; one index and one id out per element
+    out["compaction_2^26"] = {"us": us, "algorithmic_bytes": nbytes, "gbs": nbytes / (us * 1e-6) / 1e9,
+                              "frac": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+    del flags, orig, outs, ws
+
+    row, rows, total = 56 * 56 * 256 * 2, 182, 256
+    src = torch.empty(total * row // 2, dtype=torch.int16, device="cuda")
+    dst = torch.empty(rows * row // 2, dtype=torch.int16, device="cuda")
+    idx = torch.from_numpy(np.sort(np.random.default_rng(5).choice(total, rows, replace=False)).astype(np.int32)).cuda()
+    args = [C.c_void_p(dst.data_ptr()), None, C.c_void_p(src.data_ptr()), C.c_void_p(idx.data_ptr()), row, rows,
+            C.c_void_p(stream.cuda_stream)]
+    _lib.check(L.dycl_op_move_rows(*args))
+    a.record(stream)
+    for _ in range(reps):
+        _lib.check(L.dycl_op_move_rows(*args))
+    b.record(stream)
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / reps
+    nbytes = 2 * row * rows + 4 * rows
+    out["gather_rows_1.5MiB"] = {"us": us, "rows": rows, "row_bytes": row, "algorithmic_bytes": nbytes,
+                                 "gbs": nbytes / (us * 1e-6) / 1e9, "frac": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+    return out
+
+
+def copy_probe():
+    """A plain 1 GiB device copy (torch's copy kernel), three times: the
+    reference for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    a = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": 2 * a.numel(), "copies": 3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -60,7 +128,12 @@ def main():
     ap.add_argument("--batch", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-hbm-kernels", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true", help="only run the counter-scaling copy")
     args = ap.parse_args()
+    if args.copy_probe:
+        copy_probe()
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
               "(samples are independent, so a multi-GPU run would shard the batch; not built)", file=sys.stderr)
@@ -134,9 +207,12 @@ def main():
                      "avg_launch_ms": conv_ms, "avg_launch_flops": conv_flops},
         "kernels": kernels,
     }
+    plan.close()
+    del xt, at, logits, rec
+    if not args.no_hbm_kernels:
+        out["hbm_kernels"] = hbm_kernels(stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
-    plan.close()
     print(json.dumps(out), flush=True)
 
 

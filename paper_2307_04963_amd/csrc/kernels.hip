@@ -504,34 +504,79 @@ __global__ __launch_bounds__(256) void compact_write_kernel(const uint8_t* __res
                                                             const int32_t* __restrict__ orig, size_t n,
                                                             const int64_t* __restrict__ boff, int32_t* idx1,
                                                             int32_t* org1, int32_t* idx0, int32_t* org0) {
-  __shared__ int ws[4];
-  uint8_t v[16];
+  // 4 rounds of 1024 consecutive flags, 4 per lane (one 32-bit load): the
+  // lanes' counts are prefix-summed by shuffles within the wave and through
+  // LDS across the 4 waves; each lane then writes its elements to
+  // consecutive slots, so a wave fills one contiguous run of each list
+  __shared__ int wc1[4], wc0[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t blk0 = static_cast<size_t>(blockIdx.x) * kCompactBlock;
-  const size_t i0 = blk0 + threadIdx.x * 16;
-  const int c = i0 < n ? flag_count16(flags, i0, n, v) : 0;
-  const int x = wave_incl_scan(c);
-  if ((threadIdx.x & 63) == 63) ws[threadIdx.x >> 6] = x;
-  __syncthreads();
-  int before = x - c;
-  for (int w = 0; w < (int)(threadIdx.x >> 6); ++w) before += ws[w];
-  const int64_t ones_before_blk = boff[blockIdx.x];
-  int64_t o1 = ones_before_blk + before;                               // next slot for a set flag
-  int64_t o0 = static_cast<int64_t>(i0) - ones_before_blk - before;    // next slot for a clear one
-  if (i0 >= n) return;
+  int64_t base1 = boff[blockIdx.x];
+  int64_t base0 = static_cast<int64_t>(blk0) - base1;
+  for (int rd = 0; rd < kCompactBlock / 1024; ++rd) {
+    const size_t e = blk0 + static_cast<size_t>(rd) * 1024 + static_cast<size_t>(tid) * 4;
+    uint8_t v[4] = {0, 0, 0, 0};
+    int nv = 0;
+    if (e + 4 <= n) {
+      const uint32_t w = *reinterpret_cast<const uint32_t*>(flags + e);
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    const size_t i = i0 + j;
-    if (i >= n) break;
-    const int32_t id = orig ? orig[i] : static_cast<int32_t>(i);
-    if (v[j]) {
-      idx1[o1] = static_cast<int32_t>(i);
-      if (org1) org1[o1] = id;
-      ++o1;
+      for (int j = 0; j < 4; ++j) v[j] = (w >> (8 * j)) & 0xff;
+      nv = 4;
     } else {
-      idx0[o0] = static_cast<int32_t>(i);
-      if (org0) org0[o0] = id;
-      ++o0;
+      for (int j = 0; j < 4; ++j)
+        if (e + j < n) {
+          v[j] = flags[e + j];
+          ++nv;
+        }
     }
+    int c1 = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c1 += (j < nv && v[j] != 0);
+    const int c0 = nv - c1;
+    const int s1 = wave_incl_scan(c1), s0 = wave_incl_scan(c0);
+    if (lane == 63) {
+      wc1[wave] = s1;
+      wc0[wave] = s0;
+    }
+    __syncthreads();
+    int64_t o1 = base1 + s1 - c1, o0 = base0 + s0 - c0;
+    int t1 = 0, t0 = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (w < wave) {
+        o1 += wc1[w];
+        o0 += wc0[w];
+      }
+      t1 += wc1[w];
+      t0 += wc0[w];
+    }
+    int32_t id[4];
+    if (orig && nv == 4) {
+      const int4 q = *reinterpret_cast<const int4*>(orig + e);
+      id[0] = q.x;
+      id[1] = q.y;
+      id[2] = q.z;
+      id[3] = q.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) id[j] = j < nv ? (orig ? orig[e + j] : static_cast<int32_t>(e + j)) : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j >= nv) break;
+      if (v[j]) {
+        idx1[o1] = static_cast<int32_t>(e + j);
+        if (org1) org1[o1] = id[j];
+        ++o1;
+      } else {
+        idx0[o0] = static_cast<int32_t>(e + j);
+        if (org0) org0[o0] = id[j];
+        ++o0;
+      }
+    }
+    base1 += t1;
+    base0 += t0;
+    __syncthreads();
   }
 }
 
