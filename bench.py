@@ -33,6 +33,28 @@ PEAK_HBM_GBS = 8000.0
 PEAK_F32_TFLOPS = 157.3
 
 
+def measured_traffic(workload: str, batch: int):
+    """HBM bytes per conv launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), or None when there is
+    none for this workload or the conv kernel source changed since the
+    counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"conv_bf16_mfma__{workload}_b{batch}__traffic.md")
+    if not os.path.exists(path):
+        return None, "no counter summary for this workload"
+    kv = {}
+    for line in open(path):
+        if " = " in line:
+            k, v = line.strip().split(" = ", 1)
+            kv[k] = v
+    src = os.path.join(ROOT, kv.get("kernel_source", ""))
+    if not os.path.isfile(src):
+        return None, "kernel source named by the summary is missing"
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != kv.get("kernel_source_sha256"):
+        return None, "conv kernel changed since the counters were taken"
+    return float(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
+
+
 def cpu_baseline(wl, seconds: float):
     import numpy as np
     import torch
@@ -185,6 +207,7 @@ def main():
                    "gbs": (v["bytes"] / (v["ms"] * 1e-3) / 1e9) if v["ms"] else 0.0}
                for k, v in prof.items() if v["launches"]}
 
+    traffic, traffic_src = measured_traffic(args.workload, B)
     out = {
         "metric": METRIC,
         "value": B / (ms * 1e-3),
@@ -203,7 +226,9 @@ def main():
                    "branch_counts": counts, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "conv_bf16_mfma (implicit-GEMM conv / linear)",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+                     "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
+                     "algorithmic_bytes_per_launch": conv["bytes"] / max(conv["launches"], 1),
                      "avg_launch_ms": conv_ms, "avg_launch_flops": conv_flops},
         "kernels": kernels,
     }
