@@ -54,6 +54,36 @@ int dycl_op_compact(const uint8_t* flags, const int32_t* orig, int64_t n, int32_
 int dycl_op_move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes,
                       int64_t n, void* hip_stream);
 
+/*
+ * A sub-network convolution on its own (Sec. 5.3: sub-DNN nodes are
+ * conditional-free tensor code; here, one conv layer with its folded
+ * BatchNorm, residual and activation), on the kernels dycl_run uses:
+ *   y[i, oh, ow, co] = act(scale[co] * sum_{kh, kw, ci} x[i, oh*stride - pad + kh, ow*stride - pad + kw, ci]
+ *                                                   * w[co, kh, kw, ci]
+ *                          + shift[co] + res[i, oh, ow, co])
+ * bf16 storage, float32 accumulation, one round-to-nearest-even to bf16 at
+ * the end.  Ho = (H + 2 pad - k) / stride + 1, likewise Wo.
+ *
+ * dycl_op_conv_packed_bytes  size of the packed weight layout (0 if the
+ *                            shape is invalid).
+ * dycl_op_conv_pack          host to host: w [cout][k][k][cin] bf16 into the
+ *                            packed layout (zero-padded rows and K); both
+ *                            pointers are host memory.
+ * dycl_op_conv               device pointers: x [n][H][W][cin] bf16,
+ *                            packed (uploaded result of dycl_op_conv_pack),
+ *                            scale / shift [cout] float32 or NULL (1 / 0),
+ *                            res [n][Ho][Wo][cout] bf16 or NULL, y the same
+ *                            shape as res.  act: 0 none, 1 ReLU, 2 exact GELU.
+ *                            k in {1, 3, 7}; n >= 0 (0 does nothing); every
+ *                            tensor below 2^31 elements.  Work is queued on
+ *                            hip_stream.
+ */
+size_t dycl_op_conv_packed_bytes(int cout, int k, int cin);
+int dycl_op_conv_pack(const uint16_t* w, int cout, int k, int cin, uint16_t* packed, size_t packed_bytes);
+int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed, int cout, int k, int stride,
+                 int pad, const float* scale, const float* shift, const uint16_t* res, int act, uint16_t* y,
+                 void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

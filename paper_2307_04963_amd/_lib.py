@@ -20,7 +20,8 @@ STATUS = {0: "DYCL_OK", -1: "DYCL_E_INVALID", -2: "DYCL_E_SPEC", -3: "DYCL_E_WEI
 EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_last_counts", "dycl_plan_info", "dycl_profile_enable",
            "dycl_profile_read", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
 # every symbol include/dycl_ops.h declares
-OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_move_rows"]
+OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_move_rows", "dycl_op_conv_packed_bytes",
+               "dycl_op_conv_pack", "dycl_op_conv"]
 
 
 class DyclError(RuntimeError):
@@ -69,6 +70,12 @@ def _load():
     lib.dycl_op_compact.restype = i32
     lib.dycl_op_move_rows.argtypes = [vp, vp, vp, vp, C.c_size_t, C.c_int64, vp]
     lib.dycl_op_move_rows.restype = i32
+    lib.dycl_op_conv_packed_bytes.argtypes = [i32, i32, i32]
+    lib.dycl_op_conv_packed_bytes.restype = C.c_size_t
+    lib.dycl_op_conv_pack.argtypes = [vp, i32, i32, i32, vp, C.c_size_t]
+    lib.dycl_op_conv_pack.restype = i32
+    lib.dycl_op_conv.argtypes = [vp, i32, i32, i32, i32, vp, i32, i32, i32, i32, vp, vp, vp, i32, vp, vp]
+    lib.dycl_op_conv.restype = i32
     return lib
 
 

@@ -240,4 +240,75 @@ int dycl_op_move_rows(void* dst, const int32_t* dst_idx, const void* src, const 
   });
 }
 
+size_t dycl_op_conv_packed_bytes(int cout, int k, int cin) {
+  if (cout < 1 || cin < 1 || (k != 1 && k != 3 && k != 7) || cout > (1 << 20) || cin > (1 << 20)) return 0;
+  const size_t K = static_cast<size_t>(k) * k * cin;
+  const size_t Kp = (K + dycl::k::kBK - 1) / dycl::k::kBK * dycl::k::kBK;
+  return static_cast<size_t>(dycl::k::conv_cout_pad(cout)) * Kp * 2;
+}
+
+int dycl_op_conv_pack(const uint16_t* w, int cout, int k, int cin, uint16_t* packed, size_t packed_bytes) {
+  const size_t need = dycl_op_conv_packed_bytes(cout, k, cin);
+  if (!need) return fail(DYCL_E_INVALID, "dycl_op_conv_pack: need cout, cin >= 1 and k in {1, 3, 7}");
+  if (!w || !packed) return fail(DYCL_E_INVALID, "dycl_op_conv_pack: null weights or output");
+  if (packed_bytes < need)
+    return fail(DYCL_E_INVALID, "dycl_op_conv_pack: output too small (need " + std::to_string(need) + " bytes)");
+  const size_t K = static_cast<size_t>(k) * k * cin;
+  const size_t Kp = need / 2 / dycl::k::conv_cout_pad(cout);
+  std::memset(packed, 0, need);
+  for (int co = 0; co < cout; ++co) std::memcpy(packed + co * Kp, w + co * K, K * 2);
+  return DYCL_OK;
+}
+
+int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed, int cout, int k, int stride,
+                 int pad, const float* scale, const float* shift, const uint16_t* res, int act, uint16_t* y,
+                 void* hip_stream) {
+  if (n < 0) return fail(DYCL_E_INVALID, "dycl_op_conv: n < 0");
+  if (!dycl_op_conv_packed_bytes(cout, k, cin))
+    return fail(DYCL_E_INVALID, "dycl_op_conv: need cout, cin >= 1 and k in {1, 3, 7}");
+  if (H < 1 || W < 1 || stride < 1 || pad < 0 || pad >= k || act < 0 || act > 2)
+    return fail(DYCL_E_INVALID, "dycl_op_conv: need H, W, stride >= 1, 0 <= pad < k, act in {0, 1, 2}");
+  const long Ho = (static_cast<long>(H) + 2 * pad - k) / stride + 1, Wo = (static_cast<long>(W) + 2 * pad - k) / stride + 1;
+  if (H + 2 * pad < k || W + 2 * pad < k) return fail(DYCL_E_INVALID, "dycl_op_conv: kernel larger than the padded input");
+  const long lim = 1L << 31;
+  if (static_cast<long>(n) * H * W * cin >= lim || static_cast<long>(n) * Ho * Wo * cout >= lim)
+    return fail(DYCL_E_INVALID, "dycl_op_conv: a tensor reaches 2^31 elements");
+  if (n == 0) return DYCL_OK;
+  if (!x || !packed || !y) return fail(DYCL_E_INVALID, "dycl_op_conv: null x, packed weights or y");
+  if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(packed) | reinterpret_cast<uintptr_t>(y) |
+       reinterpret_cast<uintptr_t>(res)) & 15)
+    return fail(DYCL_E_INVALID, "dycl_op_conv: x, packed, y and res must be 16-byte aligned");
+  return guarded([&] {
+    const uint16_t* zeros = dycl::k::zero_page();
+    if (!zeros) throw dycl::HipError("dycl_op_conv: zero page unavailable");
+    dycl::k::ConvArgs a;
+    a.src = x;
+    a.src2 = nullptr;
+    a.cin1 = cin;
+    a.cin2 = 0;
+    a.n = n;
+    a.H = H;
+    a.W = W;
+    a.cin = cin;
+    a.Ho = static_cast<int>(Ho);
+    a.Wo = static_cast<int>(Wo);
+    a.cout = cout;
+    a.k = k;
+    a.stride = stride;
+    a.pad = pad;
+    a.w = packed;
+    a.Kp = static_cast<int>(dycl_op_conv_packed_bytes(cout, k, cin) / 2 / dycl::k::conv_cout_pad(cout));
+    a.scale = scale;
+    a.shift = shift;
+    a.res = res;
+    a.act = act;
+    a.dst = y;
+    a.out_f32 = 0;
+    a.zeros = zeros;
+    dycl::k::conv_bf16(a, static_cast<hipStream_t>(hip_stream));
+    if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_conv: launch failed");
+    return DYCL_OK;
+  });
+}
+
 }  // extern "C"

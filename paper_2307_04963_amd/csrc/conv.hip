@@ -30,6 +30,7 @@ namespace dycl {
 namespace k {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 struct ConvP {
@@ -487,6 +488,259 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   }
 }
 
+// --------------------------------- 3x3 conv, halo tiles, resident weights ----
+// For 3x3 / stride 1 / pad 1 layers with 64 input and 64 output channels.
+// A persistent workgroup walks a contiguous range of 128 x 64 output tiles;
+// a tile is R whole output rows of one image (or G whole images when an
+// image is smaller than the tile).  The tile's input patch - its rows plus
+// one halo row above and below, one zero column left and right - is staged
+// in LDS once and the nine taps read shifted windows of it, so each input
+// pixel crosses L2 -> LDS about (R + 2) / R times instead of nine.
+//
+// Eight waves in three roles, one barrier per tile:
+//  * four compute waves (2 x 2 over the tile, 64 x 32 each) hold their
+//    weights in registers for the whole kernel (36 B fragments per lane:
+//    9 taps x 4 K sub-steps of one output column), run the 36 MFMA K steps
+//    on the current patch and write the finished bf16 tile (scale / shift,
+//    residual, activation, rounding) to an LDS staging buffer;
+//  * two loader waves copy the next tile's patch and residual rows from
+//    global memory straight into LDS and, before the barrier, wait for them;
+//  * two store waves copy the previous tile's staging buffer to global
+//    memory with 16-byte stores and never wait for them.
+// The memory counter of gfx9 counts loads and stores together; with loads
+// and stores in different waves, the one wait per tile covers loads issued
+// a whole tile earlier and nothing else.
+//
+// Patch pixels are stored 144 bytes apart (eight 16-byte K chunks and one
+// unused slot): the 16 lanes of a ds_read_b128 phase, 16 consecutive
+// pixels, fall on 16 distinct bank groups, and a tap's window is a constant
+// byte offset from the lane's base address.
+struct Conv3P {
+  const uint16_t* src;
+  const uint16_t* w;      // [64][576] packed, K = tap * 64 + ci
+  const float* scale;
+  const float* shift;
+  const uint16_t* res;
+  uint16_t* dst;
+  const uint16_t* zeros;
+  int n, H, W, cout, act;
+  int RS, segs, PW, NP;    // rows per patch segment, segments, patch width, patch pixels
+  int tiles, tpi;          // tiles; tiles per image (row mode) or 0 (image mode)
+};
+
+constexpr int kW3Patch = 256;                      // patch pixels per buffer
+constexpr int kW3PB = kW3Patch * 144;              // 36864 B per patch buffer
+constexpr int kW3RB = 128 * 128;                   // 16384 B: a tile of residual / output rows
+constexpr int kW3Lds = 2 * kW3PB + 4 * kW3RB + 512;  // 139776 B (+ scale / shift)
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ __forceinline__ void all_barrier() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <int ACT, bool RES>
+__global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
+  constexpr int NL = 128;                          // loader / store threads
+  constexpr int JP = kW3Patch * 9 / NL;            // 18 patch load passes
+  __shared__ __align__(16) char smem[kW3Lds];
+  char* const pbuf = smem;                         // [2][256 px][144 B]
+  char* const rbuf = smem + 2 * kW3PB;             // [2][128 rows][128 B] residual
+  char* const sbuf = rbuf + 2 * kW3RB;             // [2][128 rows][128 B] finished bf16 tile
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int HW = p.H * p.W;
+  const int t_begin = static_cast<int>((static_cast<long>(p.tiles) * blockIdx.x) / gridDim.x);
+  const int t_end = static_cast<int>((static_cast<long>(p.tiles) * (blockIdx.x + 1)) / gridDim.x);
+  if (t_begin >= t_end) return;
+
+  auto tile_geom = [&](int t, int& img, int& oh0, int& m0, int& lim) __attribute__((always_inline)) {
+    if (p.tpi) {
+      img = t / p.tpi;
+      oh0 = (t - img * p.tpi) * p.RS;
+      m0 = img * HW + oh0 * p.W;
+      lim = min(p.RS, p.H - oh0) * p.W;
+    } else {
+      img = t * p.segs;
+      oh0 = 0;
+      m0 = img * HW;
+      lim = min(p.segs, p.n - img) * HW;
+    }
+  };
+  // 16-byte chunk position of (row, logical chunk) in a residual / staging
+  // row of 128 bytes: XOR with (row >> 1) & 7, so that 16 consecutive rows
+  // at one logical chunk fall on 16 distinct bank groups
+  auto rsw = [](int row, int c) { return c ^ ((row >> 1) & 7); };
+
+  if (wave >= 6) {
+    // ---------------- store waves: tile t - 1 while tile t is computed ----
+    const int st = tid - 6 * 64;
+    for (int t = t_begin; t <= t_end; ++t) {
+      lds_barrier();
+      if (t == t_begin) continue;
+      int img, oh0, m0, lim;
+      tile_geom(t - 1, img, oh0, m0, lim);
+      const char* sb = sbuf + ((t - 1 - t_begin) & 1) * kW3RB;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int u = k * NL + st, row = u >> 3, pos = u & 7;
+        if (row < lim) {
+          const uint4 v = *reinterpret_cast<const uint4*>(sb + row * 128 + pos * 16);
+          *reinterpret_cast<uint4*>(p.dst + (size_t)(m0 + row) * 64 + rsw(row, pos) * 8) = v;
+        }
+      }
+    }
+    return;
+  }
+
+  if (wave >= 4) {
+    // ---------------- loader waves: tile t + 1 while tile t is computed ----
+    const int ld = tid - 4 * 64, lw = wave - 4;
+    // tile-invariant geometry of this thread's patch slots, packed: bits
+    // 0-7 row + 1, 8-15 column + 1, 16-23 segment, 24 no data (past the
+    // patch, or the unused slot of a pixel), 25-27 K chunk
+    int qg[JP];
+#pragma unroll
+    for (int j = 0; j < JP; ++j) {
+      const int u = j * NL + ld, q = u / 9, ch = u - (u / 9) * 9;
+      const int segpix = (p.RS + 2) * p.PW;
+      const int sg = q / segpix, rem = q - sg * segpix;
+      const int pr = rem / p.PW, pc = rem - (rem / p.PW) * p.PW;
+      const bool data = q < p.NP && ch < 8;
+      qg[j] = data ? (pr | (pc << 8) | (sg << 16) | (ch << 25)) : (1 << 24);
+    }
+    for (int t = t_begin; t <= t_end; ++t) {
+      if (t < t_end) {
+        const int buf = (t - t_begin) & 1;
+        int img, oh0, m0, lim;
+        tile_geom(t, img, oh0, m0, lim);
+        char* pb = pbuf + buf * kW3PB;
+#pragma unroll
+        for (int j = 0; j < JP; ++j) {
+          const int v = qg[j];
+          const int im = img + ((v >> 16) & 0xff), ih = oh0 + (v & 0xff) - 1, iw = ((v >> 8) & 0xff) - 1;
+          const bool ok =
+              !(v & (1 << 24)) && im < p.n && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
+          const uint16_t* g = ok ? p.src + ((size_t)(im * p.H + ih) * p.W + iw) * 64 + ((v >> 25) & 7) * 8 : p.zeros;
+          __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(pb + (j * NL + lw * 64) * 16), 16, 0, 0);
+        }
+        if (RES) {
+          char* rb = rbuf + buf * kW3RB;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const int u = k * NL + ld, row = u >> 3, pos = u & 7;
+            const uint16_t* g = row < lim ? p.res + (size_t)(m0 + row) * 64 + rsw(row, pos) * 8 : p.zeros;
+            __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(rb + (k * NL + lw * 64) * 16), 16, 0, 0);
+          }
+        }
+      }
+      all_barrier();                      // tile t is in LDS for the compute waves
+    }
+    return;
+  }
+
+  // ---------------- compute waves: tile t ----------------
+  // MFMA operands: A = weights (32 output channels of this wave), B = patch
+  // pixels, so a lane's results are 4 consecutive channels of one pixel per
+  // group: channels wn*32 + 8q + 4*hi .. +3, q = 0..3, of pixel (lane & 31)
+  const int wm = wave >> 1, wn = wave & 1, hi = lane >> 5;
+  const int co_l = wn * 32 + (lane & 31);
+  bf16x8 bw[36];
+#pragma unroll
+  for (int k = 0; k < 36; ++k)
+    bw[k] = *reinterpret_cast<const bf16x8*>(p.w + (size_t)co_l * 576 + (k >> 2) * 64 + (2 * (k & 3) + hi) * 8);
+  // scale / shift of the 64 channels, in LDS after the staging buffers
+  float* const ssl = reinterpret_cast<float*>(sbuf + 2 * kW3RB);
+  if (tid < 64) ssl[tid] = p.scale ? p.scale[tid] : 1.0f;
+  else if (tid < 128) ssl[tid] = p.shift ? p.shift[tid - 64] : 0.0f;
+  int pix0[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int i = wm * 64 + a * 32 + (lane & 31);
+    const int sg = i / (p.RS * p.W), r = (i / p.W) - sg * p.RS, c = i - (i / p.W) * p.W;
+    pix0[a] = sg < p.segs ? (sg * (p.RS + 2) + r) * p.PW + c : 0;
+  }
+  // a compiler-visible wait: the fragments are resident before the loop,
+  // so no memory wait is placed inside it
+  __builtin_amdgcn_s_waitcnt(0);
+
+  lds_barrier();                          // the loaders' first tile
+  for (int t = t_begin; t < t_end; ++t) {
+    const int buf = (t - t_begin) & 1;
+    f32x16 acc[2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][r] = 0.f;
+    // lane base addresses of the three tap rows; the tap column and the K
+    // chunk are constant offsets
+    const char* ab[2][3];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int dy = 0; dy < 3; ++dy) ab[a][dy] = pbuf + buf * kW3PB + (pix0[a] + dy * p.PW) * 144 + hi * 16;
+    bf16x8 af[2][2][2];                   // [slot][step of the pair][a]
+    auto fetch = [&](int g, int slot) __attribute__((always_inline)) {
+      const int tap = g >> 1, dy = tap / 3, dx = tap % 3;
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          af[slot][j][a] = *reinterpret_cast<const bf16x8*>(ab[a][dy] + dx * 144 + (2 * (2 * (g & 1) + j)) * 16);
+    };
+    fetch(0, 0);
+#pragma unroll
+    for (int g = 0; g < 18; ++g) {
+      if (g + 1 < 18) fetch(g + 1, (g + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+          acc[a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[2 * g + j], af[g & 1][j][a], acc[a], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // epilogue into this tile's staging buffer (the store waves finished its
+    // previous contents, tile t - 2, before the last barrier): 8 bytes =
+    // 4 channels per group.  All LDS reads of a step are issued before any
+    // is used, so their latencies overlap.
+    const char* rb = rbuf + buf * kW3RB;
+    char* sb = sbuf + buf * kW3RB;
+    float4 sc[4], sh[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      sc[q] = *reinterpret_cast<const float4*>(ssl + wn * 32 + 8 * q + 4 * hi);
+      sh[q] = *reinterpret_cast<const float4*>(ssl + 64 + wn * 32 + 8 * q + 4 * hi);
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int px = wm * 64 + a * 32 + (lane & 31);
+      int off[4];
+      uint2 rr[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        off[q] = px * 128 + (rsw(px, wn * 4 + q) << 4) + hi * 8;
+        if (RES) rr[q] = *reinterpret_cast<const uint2*>(rb + off[q]);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4] = {fmaf(acc[a][4 * q], sc[q].x, sh[q].x), fmaf(acc[a][4 * q + 1], sc[q].y, sh[q].y),
+                      fmaf(acc[a][4 * q + 2], sc[q].z, sh[q].z), fmaf(acc[a][4 * q + 3], sc[q].w, sh[q].w)};
+        if (RES) {
+          v[0] += __uint_as_float(rr[q].x << 16);
+          v[1] += __uint_as_float(rr[q].x & 0xffff0000u);
+          v[2] += __uint_as_float(rr[q].y << 16);
+          v[3] += __uint_as_float(rr[q].y & 0xffff0000u);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = apply_act(v[e], ACT);
+        bf16x2 lo = {(__bf16)v[0], (__bf16)v[1]}, hv = {(__bf16)v[2], (__bf16)v[3]};
+        *reinterpret_cast<uint2*>(sb + off[q]) =
+            make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hv));
+      }
+    }
+    lds_barrier();                        // staging written; the next tile has landed
+  }
+}
+
 // ------------------------------------------------------------- launch ----
 
 namespace {
@@ -559,7 +813,73 @@ void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s) {
   }
 }
 
+// the weights-resident 3x3 kernel, if the layer and its geometry fit it
+bool conv3_wres(const ConvArgs& a, hipStream_t s) {
+  if (a.k != 3 || a.stride != 1 || a.pad != 1 || a.cin != 64 || a.cout != 64 || a.src2 || a.Kp != 576 || a.out_f32)
+    return false;
+  if (a.Ho != a.H || a.Wo != a.W || a.W > 128 || a.n <= 0) return false;
+  Conv3P p;
+  const int HW = a.H * a.W;
+  if (HW > 128) {             // row mode: R whole rows of one image per tile
+    p.RS = 128 / a.W;
+    p.segs = 1;
+    p.tpi = (a.H + p.RS - 1) / p.RS;
+    p.tiles = a.n * p.tpi;
+  } else {                    // image mode: G whole images per tile
+    p.RS = a.H;
+    p.segs = 128 / HW;
+    p.tpi = 0;
+    p.tiles = (a.n + p.segs - 1) / p.segs;
+  }
+  p.PW = a.W + 2;
+  p.NP = p.segs * (p.RS + 2) * p.PW;
+  if (p.NP > kW3Patch) return false;
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+  if (!cus[dev] && hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return false;
+  p.src = a.src;
+  p.w = a.w;
+  p.scale = a.scale;
+  p.shift = a.shift;
+  p.res = a.res;
+  p.dst = static_cast<uint16_t*>(a.dst);
+  p.zeros = a.zeros;
+  p.n = a.n;
+  p.H = a.H;
+  p.W = a.W;
+  p.cout = a.cout;
+  p.act = a.act;
+  const int grid = p.tiles < cus[dev] ? p.tiles : cus[dev];
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(512), 0, s, p); };
+  if (p.res) {
+    if (p.act == ACT_RELU) go(conv3_wres_kernel<ACT_RELU, true>);
+    else if (p.act == ACT_GELU) go(conv3_wres_kernel<ACT_GELU, true>);
+    else go(conv3_wres_kernel<ACT_NONE, true>);
+  } else {
+    if (p.act == ACT_RELU) go(conv3_wres_kernel<ACT_RELU, false>);
+    else if (p.act == ACT_GELU) go(conv3_wres_kernel<ACT_GELU, false>);
+    else go(conv3_wres_kernel<ACT_NONE, false>);
+  }
+  return true;
+}
+
 }  // namespace
+
+__device__ __align__(16) uint16_t g_zero_page[64];   // zero-initialised device memory
+
+const uint16_t* zero_page() {
+  static const uint16_t* addr[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_zero_page)) != hipSuccess) return nullptr;
+    addr[dev] = static_cast<const uint16_t*>(ptr);
+  }
+  return addr[dev];
+}
 
 int conv_cout_pad(int cout) {
   if (cout >= 256) return (cout + 255) / 256 * 256;
@@ -619,6 +939,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   // the direct-to-LDS kernel stores 8 channels per 16-byte vector
   const bool vec_out = a.cout % 8 == 0 && (reinterpret_cast<uintptr_t>(a.dst) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
+  if (vec_out && conv3_wres(a, s)) return;
   if (vec_out) {
     const TileCfg c = choose_lds(p.M, a.cout, p.Kp);
     p.mt = (p.M + c.bm - 1) / c.bm;

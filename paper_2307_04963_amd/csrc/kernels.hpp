@@ -38,6 +38,10 @@ struct ConvArgs {
 };
 void conv_bf16(const ConvArgs& a, hipStream_t s);
 
+// 128 zero bytes in device memory of the current device (the source of the
+// convolutions' padding taps), or null if the symbol cannot be resolved
+const uint16_t* zero_page();
+
 // Y[m, j] = act(sum_k X[m, k] Wt[k, j] + bias[j]), fp32, weights transposed;
 // for few rows (MLP layers, exit heads)
 void linear_t_f32(const float* X, int n, int K, const float* Wt, const float* bias, int N, int act, float* Y,

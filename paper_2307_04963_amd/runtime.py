@@ -112,3 +112,31 @@ def run_numpy(plan: Plan, wl, x: np.ndarray, aux=None, device="cuda"):
     ex, it, sk = decode_records(rec[:B].cpu().numpy())
     return {"logits": logits[:B].cpu().numpy(), "exit_index": ex, "iterations": it, "skip_mask": sk,
             "counts": plan.counts()}
+
+
+def pack_conv_weights(w_bits: np.ndarray) -> np.ndarray:
+    """Packed kernel layout (dycl_op_conv_pack) of bf16 weights given as
+    uint16 bits [cout][k][k][cin]; returns uint16 host array."""
+    cout, k, _, cin = w_bits.shape
+    nbytes = lib.dycl_op_conv_packed_bytes(cout, k, cin)
+    if nbytes == 0:
+        raise ValueError(f"unsupported conv shape {w_bits.shape}")
+    w = np.ascontiguousarray(w_bits, dtype=np.uint16)
+    out = np.zeros(nbytes // 2, dtype=np.uint16)
+    check(lib.dycl_op_conv_pack(w.ctypes.data, cout, k, cin, out.ctypes.data, nbytes))
+    return out
+
+
+def conv(x: torch.Tensor, packed: torch.Tensor, cout: int, k: int, stride: int, pad: int, scale=None, shift=None,
+         res=None, act: int = 0, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """dycl_op_conv on device tensors: x [n, H, W, cin] bf16, packed weights
+    on the device (int16 / uint16 storage), optional float32 scale / shift
+    [cout] and bf16 residual; returns y [n, Ho, Wo, cout] bf16."""
+    n, H, W, cin = x.shape
+    Ho, Wo = (H + 2 * pad - k) // stride + 1, (W + 2 * pad - k) // stride + 1
+    y = out if out is not None else torch.empty((n, Ho, Wo, cout), dtype=torch.bfloat16, device=x.device)
+    s = stream if stream is not None else torch.cuda.current_stream(x.device)
+    ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+    check(lib.dycl_op_conv(x.data_ptr(), n, H, W, cin, packed.data_ptr(), cout, k, stride, pad, ptr(scale), ptr(shift),
+                         ptr(res), act, y.data_ptr(), s.cuda_stream))
+    return y

@@ -104,3 +104,41 @@ def test_plan_create_rejects_bad_arguments_without_gpu():
     lib.dycl_plan_destroy(None)
     assert lib.dycl_profile_class(99) == b""
     assert lib.dycl_profile_class(0) == b"conv_bf16_mfma"
+
+
+def test_conv_pack_and_validation():
+    """dycl_op_conv_pack lays out [cout_pad][Kp] with zero padding; the conv
+    entry point rejects bad arguments before touching the device."""
+    import ctypes as C
+
+    import numpy as np
+    from paper_2307_04963_amd import _lib
+    lib = _lib.lib
+    assert lib.dycl_op_conv_packed_bytes(64, 3, 64) == 64 * 576 * 2
+    assert lib.dycl_op_conv_packed_bytes(24, 3, 3) == 32 * 64 * 2        # K 27 -> 64, Cout 24 -> 32
+    assert lib.dycl_op_conv_packed_bytes(300, 1, 100) == 512 * 128 * 2   # Cout >= 256 pads to 256s
+    assert lib.dycl_op_conv_packed_bytes(64, 5, 64) == 0
+    assert lib.dycl_op_conv_packed_bytes(0, 3, 64) == 0
+    rng = np.random.default_rng(0)
+    w = rng.integers(0, 65535, (24, 3, 3, 3), dtype=np.uint16)
+    nb = lib.dycl_op_conv_packed_bytes(24, 3, 3)
+    out = np.full(nb // 2, 7, np.uint16)
+    assert lib.dycl_op_conv_pack(w.ctypes.data, 24, 3, 3, out.ctypes.data, nb) == 0
+    ref = np.zeros((32, 64), np.uint16)
+    ref[:24, :27] = w.reshape(24, 27)
+    assert (out.reshape(32, 64) == ref).all()
+    assert lib.dycl_op_conv_pack(w.ctypes.data, 24, 3, 3, out.ctypes.data, nb - 2) == -1
+    assert lib.dycl_op_conv_pack(None, 24, 3, 3, out.ctypes.data, nb) == -1
+    p16 = C.c_void_p(256)
+    args = lambda **kw: [kw.get("x", p16), kw.get("n", 2), 8, 8, 64, kw.get("w", p16), 64, kw.get("k", 3),  # noqa: E731
+                         kw.get("s", 1), kw.get("pad", 1), None, None, kw.get("res"), kw.get("act", 1),
+                         kw.get("y", p16), None]
+    assert lib.dycl_op_conv(*args(n=-1)) == -1
+    assert lib.dycl_op_conv(*args(k=5)) == -1
+    assert lib.dycl_op_conv(*args(pad=3)) == -1
+    assert lib.dycl_op_conv(*args(act=3)) == -1
+    assert lib.dycl_op_conv(*args(x=None)) == -1
+    assert lib.dycl_op_conv(*args(y=C.c_void_p(258))) == -1               # misaligned
+    assert lib.dycl_op_conv(*args(res=C.c_void_p(264))) == -1
+    assert "aligned" in _lib.last_error()
+    assert lib.dycl_op_conv(*args(n=0)) == 0                              # nothing to do

@@ -1,0 +1,113 @@
+"""Sub-network convolution kernels through dycl_op_conv, element by element
+against the oracle's convolution (float64, bf16 inputs), at every geometry
+the launcher distinguishes: the halo-tiled kernel with register-resident
+weights (64 -> 64 channels, 3x3, stride 1: row tiles, partial row tiles,
+whole-image tiles with a ragged last tile, several tiles per workgroup), the
+direct-to-LDS implicit GEMM (1x1, 3x3, strided) and the element-gathering
+kernel (3-channel stems, Cout not a multiple of 8).
+
+Bound per element: the fp32 accumulation error (K terms, gamma_K * sum |x w|)
+scaled by |scale|, the fp32 epilogue roundings, and half a bf16 ulp of the
+final rounding."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dycl_oracle as O
+from workloads.configs import bf16_bits_to_f32, to_bf16_bits
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # n, H, W, cin, cout, k, stride, pad, residual, act
+    (3, 32, 32, 64, 64, 3, 1, 1, True, 1),      # row tiles (4 rows of 32)
+    (80, 32, 32, 64, 64, 3, 1, 1, True, 1),     # 640 tiles: several per workgroup
+    (5, 8, 8, 64, 64, 3, 1, 1, False, 1),       # two images per tile, ragged last tile
+    (1500, 8, 8, 64, 64, 3, 1, 1, True, 0),     # 750 image tiles
+    (3, 56, 56, 64, 64, 3, 1, 1, True, 1),      # 112-row tiles (2 rows of 56)
+    (9, 4, 4, 64, 64, 3, 1, 1, False, 2),       # eight images per tile, GELU
+    (40, 14, 14, 64, 64, 3, 1, 1, True, 1),     # 9-row tiles, 5-row remainder
+    (2, 9, 9, 64, 64, 3, 1, 1, False, 0),       # one 81-pixel image per tile
+    (3, 7, 7, 64, 64, 3, 1, 1, True, 1),
+    (4, 16, 16, 128, 128, 3, 1, 1, True, 1),    # implicit GEMM
+    (4, 16, 16, 64, 128, 3, 2, 1, False, 1),    # strided
+    (4, 16, 16, 128, 256, 1, 1, 0, False, 0),   # 1x1
+    (6, 8, 8, 256, 512, 3, 1, 1, True, 1),
+    (3, 20, 20, 3, 64, 7, 2, 3, False, 1),      # 3-channel stem, element gathers
+    (5, 12, 12, 16, 32, 3, 1, 1, False, 1),
+    (5, 12, 12, 64, 24, 3, 1, 1, True, 2),      # Cout not a multiple of 8
+]
+
+
+def _bits(a):
+    return torch.from_numpy(to_bf16_bits(np.asarray(a, np.float32)).view(np.int16).copy())
+
+
+def _case(n, H, W, cin, cout, k, stride, pad, residual, act, seed):
+    from paper_2307_04963_amd import runtime
+    rng = np.random.default_rng(seed)
+    x = bf16_bits_to_f32(to_bf16_bits(rng.standard_normal((n, H, W, cin)).astype(np.float32)))
+    bound = np.sqrt(6.0 / (k * k * cin))
+    w = bf16_bits_to_f32(to_bf16_bits(rng.uniform(-bound, bound, (cout, k, k, cin)).astype(np.float32)))
+    sc = rng.uniform(0.5, 1.5, cout).astype(np.float32)
+    sh = rng.uniform(-0.3, 0.3, cout).astype(np.float32)
+    Ho, Wo = (H + 2 * pad - k) // stride + 1, (W + 2 * pad - k) // stride + 1
+    r = bf16_bits_to_f32(to_bf16_bits(rng.standard_normal((n, Ho, Wo, cout)).astype(np.float32))) if residual else None
+    packed = torch.from_numpy(runtime.pack_conv_weights(to_bf16_bits(w)).view(np.int16)).cuda()
+    xt = _bits(x).cuda().view(torch.bfloat16)
+    rt = _bits(r).cuda().view(torch.bfloat16) if residual else None
+    y = runtime.conv(xt, packed, cout, k, stride, pad, torch.from_numpy(sc).cuda(), torch.from_numpy(sh).cuda(), rt, act)
+    torch.cuda.synchronize()
+    got = bf16_bits_to_f32(y.cpu().view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
+
+    # reference on every image of small batches, on 8 spread images of large ones
+    imgs = np.arange(n) if n <= 16 else np.unique(np.linspace(0, n - 1, 8).astype(int))
+    wt = torch.from_numpy(w.astype(np.float64)).permute(0, 3, 1, 2)
+    K = k * k * cin
+    gamma = K * 2.0 ** -24 / (1 - K * 2.0 ** -24)
+    lip = 1.13 if act == 2 else 1.0
+    for i in imgs:
+        xi = torch.from_numpy(x[i].astype(np.float64)).permute(2, 0, 1)
+        acc = O.conv2d(xi, wt, stride, pad).permute(1, 2, 0).numpy()
+        mag = O.conv2d(xi.abs(), wt.abs(), stride, pad).permute(1, 2, 0).numpy()
+        v = acc * sc + sh + (r[i] if residual else 0.0)
+        if act == 1:
+            v = np.maximum(v, 0.0)
+        elif act == 2:
+            v = O.gelu(torch.from_numpy(v)).numpy()
+        tol = (2.0 ** -8 * 1.001 * np.abs(v) +
+               lip * (gamma * mag * np.abs(sc) + 2.0 ** -22 * (np.abs(acc * sc) + np.abs(sh) + (np.abs(r[i]) if residual else 0))))
+        err = np.abs(got[i] - v)
+        bad = np.argwhere(err > tol)
+        assert bad.size == 0, (f"image {i}: {len(bad)} elements out of bound, first {tuple(bad[0])}: "
+                               f"got {got[i][tuple(bad[0])]} ref {v[tuple(bad[0])]}")
+    return got
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "n{}_{}x{}_{}to{}_k{}s{}".format(*c[:7]))
+def test_conv_op(case):
+    _case(*case, seed=hash(case) % (2 ** 31))
+
+
+def test_conv_op_full_stage1_shape():
+    """The first-stage layer of the ResNet-18 early-exit network at the
+    benchmark batch (1024 x 32 x 32 x 64 -> 64, residual, ReLU), 8 images
+    checked element by element."""
+    _case(1024, 32, 32, 64, 64, 3, 1, 1, True, 1, seed=7)
+
+
+def test_conv_op_repeat_is_deterministic():
+    """Two launches on the same inputs give the same bits (no race between
+    the deferred writes and the next tile's staging)."""
+    from paper_2307_04963_amd import runtime
+    rng = np.random.default_rng(3)
+    n, H, W = 300, 32, 32
+    x = _bits(rng.standard_normal((n, H, W, 64))).cuda().view(torch.bfloat16)
+    w = to_bf16_bits(rng.uniform(-0.06, 0.06, (64, 3, 3, 64)).astype(np.float32))
+    packed = torch.from_numpy(runtime.pack_conv_weights(w).view(np.int16)).cuda()
+    res = _bits(rng.standard_normal((n, H, W, 64))).cuda().view(torch.bfloat16)
+    a = runtime.conv(x, packed, 64, 3, 1, 1, None, None, res, 1)
+    b = runtime.conv(x, packed, 64, 3, 1, 1, None, None, res, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
