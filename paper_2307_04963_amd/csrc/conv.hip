@@ -528,7 +528,7 @@ struct Conv3P {
   int tiles, tpi;          // tiles; tiles per image (row mode) or 0 (image mode)
 };
 
-constexpr int kW3Patch = 256;                      // patch pixels per buffer
+constexpr int kW3Patch = 256;                      // patch pixels per buffer (= kHP)
 constexpr int kW3PB = kW3Patch * 144;              // 36864 B per patch buffer
 constexpr int kW3RB = 128 * 128;                   // 16384 B: a tile of residual / output rows
 constexpr int kW3Lds = 2 * kW3PB + 4 * kW3RB + 512;  // 139776 B (+ scale / shift)
@@ -741,6 +741,347 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
   }
 }
 
+// ------------------------------ 3x3 conv, halo tiles, streamed weights ----
+// For 3x3 / stride 1 / pad 1 layers with Cin and Cout multiples of 64.  A
+// persistent workgroup walks a contiguous range of work units, a unit being
+// one BM-pixel output tile (128 or 256; the row / image geometry of the
+// kernel above) times BN output channels.  The K loop runs over 64-channel chunks and,
+// inside a chunk, the nine taps: one step = one tap of one chunk = 64 of K.
+//  * the input patch of a chunk (the tile's pixels plus the one-pixel halo,
+//    144 bytes per pixel) is staged in LDS once and read by all nine taps;
+//    it is double-buffered, and the next chunk's patch is requested at the
+//    first step of the current chunk, nine steps before it is needed;
+//  * the weights of a step (BN rows x 128 bytes, XOR-swizzled) stream
+//    through NS LDS stages, NS - 1 steps ahead of the MFMAs.
+// Eight waves, one barrier per step: four compute waves (2 x 2, each
+// BM/2 pixels x BN/2 channels: 4 or 2 MFMA blocks of 32 pixels by BN/64
+// blocks of 32 channels) touch global memory only in the epilogue;
+// two weight loader waves and two patch loader waves issue every load
+// straight into LDS.  Each loader role waits only for its own loads (the memory counter
+// completes in order, so one role's slow loads never hold up the other's):
+// the weight loaders for step g's weights, issued NS - 1 steps earlier; the
+// patch loaders, at a chunk start, for that chunk's patch.
+//
+// MFMA operands: A = weights (32 output channels), B = patch pixels, so a
+// lane's results are 4 consecutive channels of one pixel per group and the
+// epilogue writes 8-byte pieces of NHWC rows directly; scale and shift of
+// every output channel are kept in LDS.
+struct Conv3HP {
+  const uint16_t* src;
+  const uint16_t* w;       // [cout_pad][Kp] packed, K = tap * cin + ci
+  const float* scale;
+  const float* shift;
+  const uint16_t* res;
+  uint16_t* dst;
+  const uint16_t* zeros;
+  int n, H, W, cin, cout, Kp;
+  int RS, segs, PW, NP, tpi;
+  int ntiles, units, nch;  // output channel tiles, units, 64-channel chunks
+};
+
+constexpr int kHP = 256;                           // patch pixels per buffer of 128-pixel tiles
+constexpr int kHMaxC = 512;                        // output channels whose scale / shift fit LDS
+// patch loads per patch-loader thread and chunk (128 threads x 16 bytes),
+// and patch capacity in pixels, by tile height
+constexpr int halo_jp(int bm) { return bm == 128 ? 18 : 24; }
+constexpr int halo_cap(int bm) { return halo_jp(bm) * 128 / 9; }
+
+template <int BM, int BN, int WA, int ACT, bool RES, int kHNS>
+__global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3HP p) {
+  constexpr int CW = BM / (16 * WA);               // compute waves (BM / (32 WA) x 2)
+  constexpr int JW = BN / 16;                      // weight loads per weight-loader thread and step
+  constexpr int JP = halo_jp(BM);                  // patch loads per patch-loader thread and chunk
+  constexpr int kHPB = JP * 128 * 16;              // patch buffer bytes
+  constexpr int WSTAGE = BN * 128;
+  constexpr int TB = BN / 64;                      // 32-channel blocks per compute wave
+  static_assert(kHNS >= 3 && (kHNS - 3) * JW < 64, "stage count");
+  __shared__ __align__(16) char smem[kHNS * WSTAGE + 2 * kHPB + 2 * kHMaxC * 4];
+  char* const wbuf = smem;
+  char* const pbuf = smem + kHNS * WSTAGE;
+  float* const ssl = reinterpret_cast<float*>(pbuf + 2 * kHPB);   // [scale | shift]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int HW = p.H * p.W;
+  const int u_begin = static_cast<int>((static_cast<long>(p.units) * blockIdx.x) / gridDim.x);
+  const int u_end = static_cast<int>((static_cast<long>(p.units) * (blockIdx.x + 1)) / gridDim.x);
+  if (u_begin >= u_end) return;
+  const int S = 9 * p.nch;                         // steps per unit
+  const int T = (u_end - u_begin) * S;             // steps of this workgroup
+
+  // unit -> (pixel tile, channel tile); consecutive units share the pixel tile
+  auto unit_geom = [&](int u, int& img, int& oh0, int& m0, int& lim, int& n0) __attribute__((always_inline)) {
+    const int mt = u / p.ntiles;
+    n0 = (u - mt * p.ntiles) * BN;
+    if (p.tpi) {
+      img = mt / p.tpi;
+      oh0 = (mt - img * p.tpi) * p.RS;
+      m0 = img * HW + oh0 * p.W;
+      lim = min(p.RS, p.H - oh0) * p.W;
+    } else {
+      img = mt * p.segs;
+      oh0 = 0;
+      m0 = img * HW;
+      lim = min(p.segs, p.n - img) * HW;
+    }
+  };
+
+  if (wave >= CW + 2) {
+    // ---------------- patch loader waves ----------------
+    // Slot i of this thread (LDS slot i * 128 + lt: pixel q = slot / 9, K
+    // chunk slot % 9) holds, relative to the tile's first pixel (img, oh0,
+    // 0): the element offset, the patch row (for the ih bounds check), the
+    // image (image mode) and whether it can hold data at all (not the unused
+    // ninth slot, not past the patch, not a zero column).
+    const int lt = tid - (CW + 2) * 64, lw = wave - (CW + 2);
+    int rel[JP], tag[JP];
+#pragma unroll
+    for (int i = 0; i < JP; ++i) {
+      const int u = i * 128 + lt, q = u / 9, ch = u - (u / 9) * 9;
+      const int segpix = (p.RS + 2) * p.PW;
+      const int sg = q / segpix, rem = q - sg * segpix;
+      const int pr = rem / p.PW, pc = rem - (rem / p.PW) * p.PW;
+      const bool data = q < p.NP && ch < 8 && pc >= 1 && pc <= p.W;
+      rel[i] = ((sg * p.H + pr - 1) * p.W + pc - 1) * p.cin + ch * 8;
+      tag[i] = data ? (pr | (sg << 8)) : -1;
+    }
+    // chunk iterator: (unit, chunk) of the next patch to request, and its
+    // tile origin
+    int pu = u_begin, pc_ = 0, img = 0, oh0 = 0;
+    auto set_tile = [&]() __attribute__((always_inline)) {
+      int m0, lim, n0;
+      if (pu < u_end) unit_geom(pu, img, oh0, m0, lim, n0);
+    };
+    set_tile();
+    // loads k0 .. k1-1 of the patch of chunk sequence number cs
+    auto issue_patch = [&](int cs, int k0, int k1) __attribute__((always_inline)) {
+      const bool real = pu < u_end;
+      const uint16_t* base = p.src + ((size_t)(img * p.H + oh0) * p.W) * p.cin + pc_ * 64;
+      char* pb = pbuf + (cs & 1) * kHPB;
+#pragma unroll
+      for (int i = 0; i < JP; ++i) {
+        if (i < k0 || i >= k1) continue;
+        const int t = tag[i];
+        const int ih = oh0 + (t & 0xff) - 1, im = img + (t >> 8);
+        const bool ok = real && t >= 0 && (unsigned)ih < (unsigned)p.H && im < p.n;
+        const uint16_t* g = ok ? base + rel[i] : p.zeros;
+        __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(pb + (i * 128 + lw * 64) * 16), 16, 0, 0);
+      }
+    };
+    auto next_chunk = [&]() __attribute__((always_inline)) {
+      if (++pc_ == p.nch) {
+        pc_ = 0;
+        ++pu;
+        set_tile();
+      }
+    };
+    issue_patch(0, 0, JP);
+    next_chunk();
+    // chunk q + 1 is requested in six pieces over the first six steps of
+    // chunk q and must have landed before the barrier of step 9q + 8 (whose
+    // compute waves prefetch the first operands of step 9(q + 1))
+    // iteration k precedes the barrier that starts compute step k (steps k
+    // and k + 1 must be resident), k = 0 .. T
+    int r = 0;
+    for (int k = 0; k <= T; ++k) {
+      if (k == 0 || r == 8)
+        wait_vm_barrier<0>();
+      else
+        asm volatile("s_barrier" ::: "memory");
+      if (r < 6) {
+        const int cs = k / 9 + 1;
+        if (r == 0) issue_patch(cs, 0, JP / 6);
+        else if (r == 1) issue_patch(cs, JP / 6, 2 * JP / 6);
+        else if (r == 2) issue_patch(cs, 2 * JP / 6, 3 * JP / 6);
+        else if (r == 3) issue_patch(cs, 3 * JP / 6, 4 * JP / 6);
+        else if (r == 4) issue_patch(cs, 4 * JP / 6, 5 * JP / 6);
+        else {
+          issue_patch(cs, 5 * JP / 6, JP);
+          next_chunk();
+        }
+      }
+      if (++r == 9) r = 0;
+    }
+    wait_vm_barrier<0>();                          // the last (placeholder) chunk, before the workgroup ends
+    return;
+  }
+
+  if (wave >= CW) {
+    // ---------------- weight loader waves ----------------
+    const int lt = tid - CW * 64, lw = wave - CW;
+    // this thread's slots of a stage: row (k * 128 + lt) / 8 and the
+    // swizzled K chunk that belongs at its LDS position
+    int wofs[JW];
+#pragma unroll
+    for (int k = 0; k < JW; ++k) {
+      const int u = k * 128 + lt, row = u >> 3, pos = u & 7;
+      wofs[k] = row * p.Kp + ((pos ^ ((row >> 1) & 7)) * 8);
+    }
+    // step iterator of the next weights to request: unit, its channel
+    // tile, chunk and tap (K offset tap * cin + chunk * 64)
+    int wu = u_begin, wnt = u_begin % p.ntiles, wc = 0, wt = 0, ws_i = 0;
+    auto issue_weights = [&]() __attribute__((always_inline)) {
+      const bool real = wu < u_end;
+      const uint16_t* base = p.w + (size_t)wnt * BN * p.Kp + wt * p.cin + wc * 64;
+      char* ws = wbuf + ws_i * WSTAGE;
+#pragma unroll
+      for (int k = 0; k < JW; ++k) {
+        const uint16_t* g = real ? base + wofs[k] : p.zeros;
+        __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(ws + (k * 128 + lw * 64) * 16), 16, 0, 0);
+      }
+      if (++ws_i == kHNS) ws_i = 0;
+      if (++wt == 9) {
+        wt = 0;
+        if (++wc == p.nch) {
+          wc = 0;
+          ++wu;
+          if (++wnt == p.ntiles) wnt = 0;
+        }
+      }
+    };
+    for (int k = 0; k < kHNS - 1; ++k) issue_weights();
+    // iteration k precedes the barrier that starts compute step k: steps k
+    // and k + 1 must be resident (step k + 1's first operands are read
+    // during step k), i.e. everything up to step k + 1's weights, issued
+    // NS - 2 iterations ago
+    for (int k = 0; k <= T; ++k) {
+      wait_vm_barrier<(kHNS - 3) * JW>();
+      issue_weights();                             // step k + NS - 1, into the stage of step k - 1
+    }
+    wait_vm_barrier<0>();
+    return;
+  }
+
+  // ---------------- compute waves ----------------
+  for (int c = tid; c < p.cout; c += CW * 64) {
+    ssl[c] = p.scale ? p.scale[c] : 1.0f;
+    ssl[kHMaxC + c] = p.shift ? p.shift[c] : 0.0f;
+  }
+  const int wm = wave >> 1, wn = wave & 1, hi = lane >> 5;
+  int pix0[WA];
+#pragma unroll
+  for (int a = 0; a < WA; ++a) {
+    const int i = wm * (32 * WA) + a * 32 + (lane & 31);
+    const int sg = i / (p.RS * p.W), r = (i / p.W) - sg * p.RS, c = i - (i / p.W) * p.W;
+    pix0[a] = sg < p.segs ? (sg * (p.RS + 2) + r) * p.PW + c : 0;
+  }
+  int wrow[TB];
+#pragma unroll
+  for (int b = 0; b < TB; ++b) wrow[b] = wn * (BN / 2) + b * 32 + (lane & 31);
+
+  f32x16 acc[TB][WA];
+#pragma unroll
+  for (int b = 0; b < TB; ++b)
+#pragma unroll
+    for (int a = 0; a < WA; ++a)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[b][a][r] = 0.f;
+
+  // fragment addresses of a step: weight stage and patch window
+  auto step_ptrs = [&](int st_, int pbi_, int tap_, const char*& ws_, const char*& pb_) __attribute__((always_inline)) {
+    const int dy = tap_ / 3, dx = tap_ - (tap_ / 3) * 3;
+    ws_ = wbuf + st_ * WSTAGE;
+    pb_ = pbuf + pbi_ * kHPB + (dy * p.PW + dx) * 144 + hi * 16;
+  };
+  bf16x8 wf[2][TB], pf[2][WA];
+  auto fetch = [&](const char* ws_, const char* pb_, int s, int slot) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < TB; ++b)
+      wf[slot][b] = *reinterpret_cast<const bf16x8*>(ws_ + wrow[b] * 128 + (((2 * s + hi) ^ ((wrow[b] >> 1) & 7)) << 4));
+#pragma unroll
+    for (int a = 0; a < WA; ++a) pf[slot][a] = *reinterpret_cast<const bf16x8*>(pb_ + pix0[a] * 144 + s * 32);
+  };
+  int tap = 0, jc = 0, cu = u_begin, st = 0, pbi = 0;   // tap, step in unit, unit, stage, patch buffer
+  // the barrier of step g also guarantees step g + 1's data, so the first
+  // operands of step g + 1 are read before it
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");   // scale / shift; steps 0 and 1
+  const char* ws;
+  const char* pb;
+  step_ptrs(0, 0, 0, ws, pb);
+  fetch(ws, pb, 0, 0);
+  for (int g = 0; g < T; ++g) {
+    const bool unit_end = jc == S - 1;
+    // the next step's stage / patch buffer / tap
+    int st1 = st + 1 == kHNS ? 0 : st + 1, tap1 = tap + 1, pbi1 = pbi;
+    if (tap1 == 9) {
+      tap1 = 0;
+      pbi1 ^= 1;
+    }
+    const char* ws1;
+    const char* pb1;
+    step_ptrs(st1, pbi1, tap1, ws1, pb1);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s + 1 < 4)
+        fetch(ws, pb, s + 1, (s + 1) & 1);
+      else if (g + 1 < T)
+        fetch(ws1, pb1, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int b = 0; b < TB; ++b)
+#pragma unroll
+        for (int a = 0; a < WA; ++a)
+          acc[b][a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s & 1][b], pf[s & 1][a], acc[b][a], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    st = st1;
+    tap = tap1;
+    pbi = pbi1;
+    ws = ws1;
+    pb = pb1;
+    if (++jc == S) jc = 0;
+
+    if (unit_end) {
+      // unit done: epilogue straight to global memory, 8 bytes per group
+      int img, oh0, m0, lim, n0;
+      unit_geom(cu++, img, oh0, m0, lim, n0);
+#pragma unroll
+      for (int a = 0; a < WA; ++a) {
+        const int px = wm * (32 * WA) + a * 32 + (lane & 31);
+        const bool live = px < lim;
+        const size_t rowo = (size_t)(m0 + (live ? px : 0)) * p.cout;
+        uint2 rr[TB][4];
+        if (RES && live) {
+#pragma unroll
+          for (int b = 0; b < TB; ++b)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              rr[b][q] = *reinterpret_cast<const uint2*>(p.res + rowo + n0 + wn * (BN / 2) + b * 32 + 8 * q + 4 * hi);
+        }
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int c0 = n0 + wn * (BN / 2) + b * 32 + 8 * q + 4 * hi;
+            const float4 sc = *reinterpret_cast<const float4*>(ssl + c0);
+            const float4 sh = *reinterpret_cast<const float4*>(ssl + kHMaxC + c0);
+            float v[4] = {fmaf(acc[b][a][4 * q], sc.x, sh.x), fmaf(acc[b][a][4 * q + 1], sc.y, sh.y),
+                          fmaf(acc[b][a][4 * q + 2], sc.z, sh.z), fmaf(acc[b][a][4 * q + 3], sc.w, sh.w)};
+            if (RES) {
+              v[0] += __uint_as_float(rr[b][q].x << 16);
+              v[1] += __uint_as_float(rr[b][q].x & 0xffff0000u);
+              v[2] += __uint_as_float(rr[b][q].y << 16);
+              v[3] += __uint_as_float(rr[b][q].y & 0xffff0000u);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = apply_act(v[e], ACT);
+            bf16x2 lo = {(__bf16)v[0], (__bf16)v[1]}, hv = {(__bf16)v[2], (__bf16)v[3]};
+            if (live)
+              *reinterpret_cast<uint2*>(p.dst + rowo + c0) =
+                  make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hv));
+          }
+      }
+#pragma unroll
+      for (int b = 0; b < TB; ++b)
+#pragma unroll
+        for (int a = 0; a < WA; ++a)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[b][a][r] = 0.f;
+    }
+    // this step's LDS reads are done; step g + 2's data is ready after it
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+}
+
 // ------------------------------------------------------------- launch ----
 
 namespace {
@@ -813,32 +1154,55 @@ void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s) {
   }
 }
 
-// the weights-resident 3x3 kernel, if the layer and its geometry fit it
-bool conv3_wres(const ConvArgs& a, hipStream_t s) {
-  if (a.k != 3 || a.stride != 1 || a.pad != 1 || a.cin != 64 || a.cout != 64 || a.src2 || a.Kp != 576 || a.out_f32)
-    return false;
-  if (a.Ho != a.H || a.Wo != a.W || a.W > 128 || a.n <= 0) return false;
-  Conv3P p;
-  const int HW = a.H * a.W;
-  if (HW > 128) {             // row mode: R whole rows of one image per tile
-    p.RS = 128 / a.W;
-    p.segs = 1;
-    p.tpi = (a.H + p.RS - 1) / p.RS;
-    p.tiles = a.n * p.tpi;
-  } else {                    // image mode: G whole images per tile
-    p.RS = a.H;
-    p.segs = 128 / HW;
-    p.tpi = 0;
-    p.tiles = (a.n + p.segs - 1) / p.segs;
+// Tile geometry of the halo kernels: BM-pixel tiles of R whole rows of one
+// image, or of G whole images; the patch (tile rows + halo) must fit `cap`
+// pixels.
+struct HaloGeom {
+  int RS, segs, tpi, PW, NP, mtiles;
+};
+
+bool halo_geom(int n, int H, int W, int bm, int cap, HaloGeom& g) {
+  if (W > bm || n <= 0) return false;
+  const int HW = H * W;
+  if (HW > bm) {
+    g.RS = bm / W;
+    g.segs = 1;
+    g.tpi = (H + g.RS - 1) / g.RS;
+    g.mtiles = n * g.tpi;
+  } else {
+    g.RS = H;
+    g.segs = bm / HW;
+    while (g.segs > 1 && g.segs * (H + 2) * (W + 2) > cap) --g.segs;
+    g.tpi = 0;
+    g.mtiles = (n + g.segs - 1) / g.segs;
   }
-  p.PW = a.W + 2;
-  p.NP = p.segs * (p.RS + 2) * p.PW;
-  if (p.NP > kW3Patch) return false;
+  g.PW = W + 2;
+  g.NP = g.segs * (g.RS + 2) * g.PW;
+  return g.NP <= cap;
+}
+
+int cu_count() {
   static int cus[64] = {0};
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
   if (!cus[dev] && hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    return false;
+    cus[dev] = 0;
+  return cus[dev];
+}
+
+bool is_halo_layer(const ConvArgs& a) {
+  return a.k == 3 && a.stride == 1 && a.pad == 1 && !a.src2 && !a.out_f32 && a.Ho == a.H && a.Wo == a.W &&
+         a.cin % 64 == 0 && a.cout % 64 == 0 && a.Kp == 9 * a.cin &&
+         !((reinterpret_cast<uintptr_t>(a.scale) | reinterpret_cast<uintptr_t>(a.shift)) & 15);
+}
+
+// the weights-resident 3x3 kernel (64 -> 64 channels)
+bool conv3_wres(const ConvArgs& a, hipStream_t s) {
+  HaloGeom g;
+  if (!is_halo_layer(a) || a.cin != 64 || a.cout != 64 || !halo_geom(a.n, a.H, a.W, 128, kHP, g)) return false;
+  const int cus = cu_count();
+  if (!cus) return false;
+  Conv3P p;
   p.src = a.src;
   p.w = a.w;
   p.scale = a.scale;
@@ -851,7 +1215,13 @@ bool conv3_wres(const ConvArgs& a, hipStream_t s) {
   p.W = a.W;
   p.cout = a.cout;
   p.act = a.act;
-  const int grid = p.tiles < cus[dev] ? p.tiles : cus[dev];
+  p.RS = g.RS;
+  p.segs = g.segs;
+  p.tpi = g.tpi;
+  p.PW = g.PW;
+  p.NP = g.NP;
+  p.tiles = g.mtiles;
+  const int grid = p.tiles < cus ? p.tiles : cus;
   auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(512), 0, s, p); };
   if (p.res) {
     if (p.act == ACT_RELU) go(conv3_wres_kernel<ACT_RELU, true>);
@@ -862,6 +1232,77 @@ bool conv3_wres(const ConvArgs& a, hipStream_t s) {
     else if (p.act == ACT_GELU) go(conv3_wres_kernel<ACT_GELU, false>);
     else go(conv3_wres_kernel<ACT_NONE, false>);
   }
+  return true;
+}
+
+// the streamed-weights 3x3 kernel (Cin, Cout multiples of 64): 256-pixel
+// tiles when they are at least 3/4 used and give every CU work, else 128
+bool conv3_halo(const ConvArgs& a, hipStream_t s) {
+  if (!is_halo_layer(a) || a.cout > kHMaxC) return false;
+  // images so small that the halo more than doubles the patch (4 x 4: 36
+  // pixels for 16) go to the implicit GEMM, which is faster there
+  if (a.H * a.W <= 128 && 2 * a.H * a.W < (a.H + 2) * (a.W + 2)) return false;
+  const int cus = cu_count();
+  if (!cus) return false;
+  HaloGeom g;
+  int bm = 256;
+  if (!halo_geom(a.n, a.H, a.W, 256, halo_cap(256), g) ||
+      4L * a.n * a.H * a.W < 3L * 256 * g.mtiles || (long)g.mtiles * (a.cout / 128) < cus) {
+    bm = 128;
+    if (!halo_geom(a.n, a.H, a.W, 128, halo_cap(128), g)) return false;
+  }
+  const int bn = (a.cout % 128 == 0 && conv_cout_pad(a.cout) % 128 == 0 && (long)g.mtiles * (a.cout / 128) >= cus)
+                     ? 128 : 64;
+  Conv3HP p;
+  p.src = a.src;
+  p.w = a.w;
+  p.scale = a.scale;
+  p.shift = a.shift;
+  p.res = a.res;
+  p.dst = static_cast<uint16_t*>(a.dst);
+  p.zeros = a.zeros;
+  p.n = a.n;
+  p.H = a.H;
+  p.W = a.W;
+  p.cin = a.cin;
+  p.cout = a.cout;
+  p.Kp = a.Kp;
+  p.RS = g.RS;
+  p.segs = g.segs;
+  p.tpi = g.tpi;
+  p.PW = g.PW;
+  p.NP = g.NP;
+  p.ntiles = a.cout / bn;
+  p.units = g.mtiles * p.ntiles;
+  p.nch = a.cin / 64;
+  const int grid = p.units < cus ? p.units : cus;
+  // four compute waves: 128 x 64 (pixels x channels) each for 256-pixel
+  // tiles, 64 x BN/2 for 128-pixel tiles; plus four loader waves
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(512), 0, s, p); };
+#define DYCL_H(BM, BN, NS)                                                              \
+  if (p.res) {                                                                          \
+    if (a.act == ACT_RELU) go(conv3h_kernel<BM, BN, BM / 64, ACT_RELU, true, NS>);      \
+    else if (a.act == ACT_GELU) go(conv3h_kernel<BM, BN, BM / 64, ACT_GELU, true, NS>); \
+    else go(conv3h_kernel<BM, BN, BM / 64, ACT_NONE, true, NS>);                        \
+  } else {                                                                              \
+    if (a.act == ACT_RELU) go(conv3h_kernel<BM, BN, BM / 64, ACT_RELU, false, NS>);     \
+    else if (a.act == ACT_GELU) go(conv3h_kernel<BM, BN, BM / 64, ACT_GELU, false, NS>); \
+    else go(conv3h_kernel<BM, BN, BM / 64, ACT_NONE, false, NS>);                       \
+  }
+  if (bm == 256) {
+    if (bn == 128) {
+      DYCL_H(256, 128, 3)
+    } else {
+      DYCL_H(256, 64, 6)
+    }
+  } else {
+    if (bn == 128) {
+      DYCL_H(128, 128, 5)
+    } else {
+      DYCL_H(128, 64, 8)
+    }
+  }
+#undef DYCL_H
   return true;
 }
 
@@ -939,7 +1380,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   // the direct-to-LDS kernel stores 8 channels per 16-byte vector
   const bool vec_out = a.cout % 8 == 0 && (reinterpret_cast<uintptr_t>(a.dst) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
-  if (vec_out && conv3_wres(a, s)) return;
+  if (vec_out && (conv3_wres(a, s) || conv3_halo(a, s))) return;
   if (vec_out) {
     const TileCfg c = choose_lds(p.M, a.cout, p.Kp);
     p.mt = (p.M + c.bm - 1) / c.bm;

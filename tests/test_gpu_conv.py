@@ -30,7 +30,14 @@ CASES = [
     (40, 14, 14, 64, 64, 3, 1, 1, True, 1),     # 9-row tiles, 5-row remainder
     (2, 9, 9, 64, 64, 3, 1, 1, False, 0),       # one 81-pixel image per tile
     (3, 7, 7, 64, 64, 3, 1, 1, True, 1),
-    (4, 16, 16, 128, 128, 3, 1, 1, True, 1),    # implicit GEMM
+    (4, 16, 16, 128, 128, 3, 1, 1, True, 1),    # halo tiles, streamed weights
+    (300, 16, 16, 128, 128, 3, 1, 1, True, 1),  # 600 units: several per workgroup
+    (9, 4, 4, 512, 512, 3, 1, 1, True, 1),      # 7 images per tile (patch capacity)
+    (3, 7, 7, 512, 512, 3, 1, 1, False, 0),
+    (2, 14, 14, 256, 256, 3, 1, 1, True, 1),    # 9-row tiles, 5-row remainder
+    (2, 28, 28, 128, 128, 3, 1, 1, False, 2),
+    (5, 8, 8, 128, 64, 3, 1, 1, True, 1),       # 64-channel output tiles
+    (40, 8, 8, 256, 256, 3, 1, 1, False, 1),
     (4, 16, 16, 64, 128, 3, 2, 1, False, 1),    # strided
     (4, 16, 16, 128, 256, 1, 1, 0, False, 0),   # 1x1
     (6, 8, 8, 256, 512, 3, 1, 1, True, 1),
@@ -95,6 +102,13 @@ def test_conv_op_full_stage1_shape():
     benchmark batch (1024 x 32 x 32 x 64 -> 64, residual, ReLU), 8 images
     checked element by element."""
     _case(1024, 32, 32, 64, 64, 3, 1, 1, True, 1, seed=7)
+
+
+def test_conv_op_full_stage2_shape():
+    """A second-stage layer of the ResNet-18 early-exit network at the rows
+    that reach it in the benchmark (774 x 16 x 16 x 128 -> 128, residual,
+    ReLU), 8 images checked element by element."""
+    _case(774, 16, 16, 128, 128, 3, 1, 1, True, 1, seed=8)
 
 
 def test_conv_op_repeat_is_deterministic():
