@@ -54,6 +54,13 @@ def build(verbose: bool = False) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    # every symbol of the library's own namespace must be defined (a kernel
+    # template whose host-side stub was not emitted links fine and fails at load)
+    nm = subprocess.run(["nm", "-u", "-C", tmp], capture_output=True, text=True)
+    missing = [ln.strip() for ln in nm.stdout.splitlines() if "dycl::" in ln]
+    if missing:
+        os.remove(tmp)
+        raise RuntimeError("undefined symbols in the library:\n" + "\n".join(missing[:20]))
     os.replace(tmp, OUT)
     if verbose:
         print("built", OUT, flush=True)

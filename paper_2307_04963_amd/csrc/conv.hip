@@ -741,6 +741,14 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
   }
 }
 
+// 16 bytes per lane from a raw buffer straight into LDS at `lds` + 16 * lane:
+// the buffer spans `bytes` from `base`, and a load at or past its end (an
+// offset of 2^31 or more included) writes zeros instead of reading memory.
+__device__ __forceinline__ void buffer_load_lds16(const void* base, uint32_t bytes, uint32_t offset, lds_void_ptr lds) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, offset, 0, 0, 0);
+}
+
 // ------------------------------ 3x3 conv, halo tiles, streamed weights ----
 // For 3x3 / stride 1 / pad 1 layers with Cin and Cout multiples of 64.  A
 // persistent workgroup walks a contiguous range of work units, a unit being
@@ -801,6 +809,7 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
   float* const ssl = reinterpret_cast<float*>(pbuf + 2 * kHPB);   // [scale | shift]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);   // the same, known wave-uniform
   const int HW = p.H * p.W;
   const int u_begin = static_cast<int>((static_cast<long>(p.units) * blockIdx.x) / gridDim.x);
   const int u_end = static_cast<int>((static_cast<long>(p.units) * (blockIdx.x + 1)) / gridDim.x);
@@ -825,62 +834,68 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
     }
   };
 
-  if (wave >= CW + 2) {
+  if (wv >= CW + 2) {
     // ---------------- patch loader waves ----------------
-    // Slot i of this thread (LDS slot i * 128 + lt: pixel q = slot / 9, K
-    // chunk slot % 9) holds, relative to the tile's first pixel (img, oh0,
-    // 0): the element offset, the patch row (for the ih bounds check), the
-    // image (image mode) and whether it can hold data at all (not the unused
-    // ninth slot, not past the patch, not a zero column).
-    const int lt = tid - (CW + 2) * 64, lw = wave - (CW + 2);
-    int rel[JP], tag[JP];
+    // Buffer loads straight into LDS.  A chunk's loads use one buffer
+    // resource spanning the tile's image(s) from the chunk's first channel;
+    // a load outside it returns zeros, which is the convolution's padding:
+    // a slot's byte offset is taken relative to the tile's first output row
+    // (row mode: plus oh0 rows, so the halo row above image row 0 wraps to
+    // a huge offset, and rows past the image exceed the resource), and slots
+    // that can never hold data (zero columns, the unused ninth slot, past
+    // the patch, the halo rows of image mode) get an offset above 2^31.
+    const int lt = tid - (CW + 2) * 64, lw = wv - (CW + 2);
+    const int rowb = p.W * p.cin * 2, imgb = p.H * rowb;
+    uint32_t vofs[JP];
 #pragma unroll
     for (int i = 0; i < JP; ++i) {
       const int u = i * 128 + lt, q = u / 9, ch = u - (u / 9) * 9;
       const int segpix = (p.RS + 2) * p.PW;
       const int sg = q / segpix, rem = q - sg * segpix;
       const int pr = rem / p.PW, pc = rem - (rem / p.PW) * p.PW;
-      const bool data = q < p.NP && ch < 8 && pc >= 1 && pc <= p.W;
-      rel[i] = ((sg * p.H + pr - 1) * p.W + pc - 1) * p.cin + ch * 8;
-      tag[i] = data ? (pr | (sg << 8)) : -1;
+      bool data = q < p.NP && ch < 8 && pc >= 1 && pc <= p.W;
+      if (!p.tpi) data = data && pr >= 1 && pr <= p.H;
+      vofs[i] = data ? static_cast<uint32_t>(sg * imgb + (pr - 1) * rowb + (pc - 1) * p.cin * 2 + ch * 16) : 0xC0000000u;
     }
-    // chunk iterator: (unit, chunk) of the next patch to request, and its
-    // tile origin
-    int pu = u_begin, pc_ = 0, img = 0, oh0 = 0;
-    auto set_tile = [&]() __attribute__((always_inline)) {
-      int m0, lim, n0;
-      if (pu < u_end) unit_geom(pu, img, oh0, m0, lim, n0);
+    // chunk iterator: (unit, chunk) of the next patch to request
+    int pu = u_begin, pc_ = 0;
+    const uint16_t* rbase = p.src;                 // the chunk's buffer: base and size
+    uint32_t rbytes = 0;
+    uint32_t tofs = 0;                             // row mode: oh0 rows, in bytes
+    auto set_chunk = [&]() __attribute__((always_inline)) {
+      int img = 0, oh0 = 0, nimg = 0;
+      if (pu < u_end) {
+        int m0, lim, n0;
+        unit_geom(pu, img, oh0, m0, lim, n0);
+        nimg = p.tpi ? 1 : min(p.segs, p.n - img);
+      }
+      rbase = p.src + (size_t)img * p.H * p.W * p.cin + pc_ * 64;
+      rbytes = nimg ? nimg * imgb - pc_ * 128 : 0;
+      tofs = static_cast<uint32_t>(oh0) * rowb;
     };
-    set_tile();
+    set_chunk();
     // loads k0 .. k1-1 of the patch of chunk sequence number cs
     auto issue_patch = [&](int cs, int k0, int k1) __attribute__((always_inline)) {
-      const bool real = pu < u_end;
-      const uint16_t* base = p.src + ((size_t)(img * p.H + oh0) * p.W) * p.cin + pc_ * 64;
       char* pb = pbuf + (cs & 1) * kHPB;
 #pragma unroll
       for (int i = 0; i < JP; ++i) {
         if (i < k0 || i >= k1) continue;
-        const int t = tag[i];
-        const int ih = oh0 + (t & 0xff) - 1, im = img + (t >> 8);
-        const bool ok = real && t >= 0 && (unsigned)ih < (unsigned)p.H && im < p.n;
-        const uint16_t* g = ok ? base + rel[i] : p.zeros;
-        __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(pb + (i * 128 + lw * 64) * 16), 16, 0, 0);
+        buffer_load_lds16(rbase, rbytes, vofs[i] + tofs, (lds_void_ptr)(pb + (i * 128 + lw * 64) * 16));
       }
     };
     auto next_chunk = [&]() __attribute__((always_inline)) {
       if (++pc_ == p.nch) {
         pc_ = 0;
         ++pu;
-        set_tile();
       }
+      set_chunk();
     };
     issue_patch(0, 0, JP);
     next_chunk();
     // chunk q + 1 is requested in six pieces over the first six steps of
     // chunk q and must have landed before the barrier of step 9q + 8 (whose
-    // compute waves prefetch the first operands of step 9(q + 1))
-    // iteration k precedes the barrier that starts compute step k (steps k
-    // and k + 1 must be resident), k = 0 .. T
+    // compute waves prefetch the first operands of step 9(q + 1)).
+    // Iteration k precedes the barrier that starts compute step k, k = 0..T.
     int r = 0;
     for (int k = 0; k <= T; ++k) {
       if (k == 0 || r == 8)
@@ -905,29 +920,28 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
     return;
   }
 
-  if (wave >= CW) {
+  if (wv >= CW) {
     // ---------------- weight loader waves ----------------
-    const int lt = tid - CW * 64, lw = wave - CW;
-    // this thread's slots of a stage: row (k * 128 + lt) / 8 and the
-    // swizzled K chunk that belongs at its LDS position
-    int wofs[JW];
+    // one buffer resource per step (its weights: BN rows from the step's K
+    // offset); each thread's slots are constant byte offsets from it
+    const int lt = tid - CW * 64, lw = wv - CW;
+    uint32_t wofs[JW];
 #pragma unroll
     for (int k = 0; k < JW; ++k) {
       const int u = k * 128 + lt, row = u >> 3, pos = u & 7;
-      wofs[k] = row * p.Kp + ((pos ^ ((row >> 1) & 7)) * 8);
+      wofs[k] = static_cast<uint32_t>(row * p.Kp + ((pos ^ ((row >> 1) & 7)) * 8)) * 2;
     }
+    const uint32_t wbytes = static_cast<uint32_t>(p.ntiles * BN) * p.Kp * 2;
     // step iterator of the next weights to request: unit, its channel
     // tile, chunk and tap (K offset tap * cin + chunk * 64)
     int wu = u_begin, wnt = u_begin % p.ntiles, wc = 0, wt = 0, ws_i = 0;
     auto issue_weights = [&]() __attribute__((always_inline)) {
-      const bool real = wu < u_end;
-      const uint16_t* base = p.w + (size_t)wnt * BN * p.Kp + wt * p.cin + wc * 64;
+      const uint32_t e0 = static_cast<uint32_t>(wnt * BN) * p.Kp + wt * p.cin + wc * 64;
+      const uint32_t wb = wu < u_end ? wbytes - e0 * 2 : 0;
       char* ws = wbuf + ws_i * WSTAGE;
 #pragma unroll
-      for (int k = 0; k < JW; ++k) {
-        const uint16_t* g = real ? base + wofs[k] : p.zeros;
-        __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(ws + (k * 128 + lw * 64) * 16), 16, 0, 0);
-      }
+      for (int k = 0; k < JW; ++k)
+        buffer_load_lds16(p.w + e0, wb, wofs[k], (lds_void_ptr)(ws + (k * 128 + lw * 64) * 16));
       if (++ws_i == kHNS) ws_i = 0;
       if (++wt == 9) {
         wt = 0;
