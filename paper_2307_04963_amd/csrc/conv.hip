@@ -488,6 +488,23 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   }
 }
 
+// 16 bytes per lane from a raw buffer straight into LDS at `lds` + 16 * lane:
+// the buffer spans `bytes` from `base`, and a load at or past its end (an
+// offset of 2^31 or more included) writes zeros instead of reading memory.
+__device__ __forceinline__ void buffer_load_lds16(const void* base, uint32_t bytes, uint32_t offset, lds_void_ptr lds) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, offset, 0, 0, 0);
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16 bytes per lane to a raw buffer of `bytes` from `base`; a store at or
+// past its end is dropped.
+__device__ __forceinline__ void buffer_store16(void* base, uint32_t bytes, uint32_t offset, u32x4 v) {
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, 0x00020000);
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, offset, 0, 0);
+}
+
 // --------------------------------- 3x3 conv, halo tiles, resident weights ----
 // For 3x3 / stride 1 / pad 1 layers with 64 input and 64 output channels.
 // A persistent workgroup walks a contiguous range of 128 x 64 output tiles;
@@ -569,8 +586,11 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
   // at one logical chunk fall on 16 distinct bank groups
   auto rsw = [](int row, int c) { return c ^ ((row >> 1) & 7); };
 
-  if (wave >= 6) {
+  const int wv = __builtin_amdgcn_readfirstlane(wave);   // the same, known wave-uniform
+  if (wv >= 6) {
     // ---------------- store waves: tile t - 1 while tile t is computed ----
+    // buffer stores: the tile's rows from m0, at most lim of them (stores
+    // to later rows fall outside the buffer and are dropped)
     const int st = tid - 6 * 64;
     for (int t = t_begin; t <= t_end; ++t) {
       lds_barrier();
@@ -578,56 +598,59 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
       int img, oh0, m0, lim;
       tile_geom(t - 1, img, oh0, m0, lim);
       const char* sb = sbuf + ((t - 1 - t_begin) & 1) * kW3RB;
+      uint16_t* const dbase = p.dst + (size_t)m0 * 64;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int u = k * NL + st, row = u >> 3, pos = u & 7;
-        if (row < lim) {
-          const uint4 v = *reinterpret_cast<const uint4*>(sb + row * 128 + pos * 16);
-          *reinterpret_cast<uint4*>(p.dst + (size_t)(m0 + row) * 64 + rsw(row, pos) * 8) = v;
-        }
+        const u32x4 v = *reinterpret_cast<const u32x4*>(sb + u * 16);
+        buffer_store16(dbase, static_cast<uint32_t>(lim) * 128, row * 128 + rsw(row, pos) * 16, v);
       }
     }
     return;
   }
 
-  if (wave >= 4) {
+  if (wv >= 4) {
     // ---------------- loader waves: tile t + 1 while tile t is computed ----
-    const int ld = tid - 4 * 64, lw = wave - 4;
-    // tile-invariant geometry of this thread's patch slots, packed: bits
-    // 0-7 row + 1, 8-15 column + 1, 16-23 segment, 24 no data (past the
-    // patch, or the unused slot of a pixel), 25-27 K chunk
-    int qg[JP];
+    // Buffer loads straight into LDS.  The patch's buffer spans the tile's
+    // image(s); a slot's byte offset is relative to the tile's first output
+    // row (row mode: plus oh0 rows, so the halo row above image row 0 wraps
+    // to a huge offset and rows past the image exceed the buffer), and
+    // slots that never hold data (zero columns, the unused ninth slot, past
+    // the patch, image-mode halo rows) get an offset above 2^31: all read as
+    // zeros, the convolution's padding.
+    const int ld = tid - 4 * 64, lw = wv - 4;
+    const int rowb = p.W * 128, imgb = p.H * rowb;
+    uint32_t vofs[JP];
 #pragma unroll
     for (int j = 0; j < JP; ++j) {
       const int u = j * NL + ld, q = u / 9, ch = u - (u / 9) * 9;
       const int segpix = (p.RS + 2) * p.PW;
       const int sg = q / segpix, rem = q - sg * segpix;
       const int pr = rem / p.PW, pc = rem - (rem / p.PW) * p.PW;
-      const bool data = q < p.NP && ch < 8;
-      qg[j] = data ? (pr | (pc << 8) | (sg << 16) | (ch << 25)) : (1 << 24);
+      bool data = q < p.NP && ch < 8 && pc >= 1 && pc <= p.W;
+      if (!p.tpi) data = data && pr >= 1 && pr <= p.H;
+      vofs[j] = data ? static_cast<uint32_t>(sg * imgb + (pr - 1) * rowb + (pc - 1) * 128 + ch * 16) : 0xC0000000u;
     }
     for (int t = t_begin; t <= t_end; ++t) {
       if (t < t_end) {
         const int buf = (t - t_begin) & 1;
         int img, oh0, m0, lim;
         tile_geom(t, img, oh0, m0, lim);
+        const int nimg = p.tpi ? 1 : min(p.segs, p.n - img);
+        const uint16_t* pbase = p.src + (size_t)img * p.H * p.W * 64;
+        const uint32_t pbytes = static_cast<uint32_t>(nimg) * imgb, tofs = static_cast<uint32_t>(oh0) * rowb;
         char* pb = pbuf + buf * kW3PB;
 #pragma unroll
-        for (int j = 0; j < JP; ++j) {
-          const int v = qg[j];
-          const int im = img + ((v >> 16) & 0xff), ih = oh0 + (v & 0xff) - 1, iw = ((v >> 8) & 0xff) - 1;
-          const bool ok =
-              !(v & (1 << 24)) && im < p.n && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
-          const uint16_t* g = ok ? p.src + ((size_t)(im * p.H + ih) * p.W + iw) * 64 + ((v >> 25) & 7) * 8 : p.zeros;
-          __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(pb + (j * NL + lw * 64) * 16), 16, 0, 0);
-        }
+        for (int j = 0; j < JP; ++j)
+          buffer_load_lds16(pbase, pbytes, vofs[j] + tofs, (lds_void_ptr)(pb + (j * NL + lw * 64) * 16));
         if (RES) {
           char* rb = rbuf + buf * kW3RB;
+          const uint16_t* rbase = p.res + (size_t)m0 * 64;
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
             const int u = k * NL + ld, row = u >> 3, pos = u & 7;
-            const uint16_t* g = row < lim ? p.res + (size_t)(m0 + row) * 64 + rsw(row, pos) * 8 : p.zeros;
-            __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(rb + (k * NL + lw * 64) * 16), 16, 0, 0);
+            buffer_load_lds16(rbase, static_cast<uint32_t>(lim) * 128, row * 128 + rsw(row, pos) * 16,
+                              (lds_void_ptr)(rb + (k * NL + lw * 64) * 16));
           }
         }
       }
@@ -739,14 +762,6 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
     }
     lds_barrier();                        // staging written; the next tile has landed
   }
-}
-
-// 16 bytes per lane from a raw buffer straight into LDS at `lds` + 16 * lane:
-// the buffer spans `bytes` from `base`, and a load at or past its end (an
-// offset of 2^31 or more included) writes zeros instead of reading memory.
-__device__ __forceinline__ void buffer_load_lds16(const void* base, uint32_t bytes, uint32_t offset, lds_void_ptr lds) {
-  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, offset, 0, 0, 0);
 }
 
 // ------------------------------ 3x3 conv, halo tiles, streamed weights ----
