@@ -233,66 +233,111 @@ void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int
 // exit: p = max softmax(z / T), leave when p >= tau (or always when final).
 
 template <bool BF16>
-__global__ __launch_bounds__(256) void exit_head_kernel(const void* __restrict__ x, int HW, int C,
-                                                        const float* __restrict__ Wt, const float* __restrict__ bias,
+__global__ __launch_bounds__(256) void exit_head_kernel(const void* __restrict__ x, int n, int R, int HW, int C,
+                                                        const float* __restrict__ W, const float* __restrict__ bias,
                                                         int ncls, const float* __restrict__ Tp, float tau,
                                                         int final_, int head, const int32_t* __restrict__ orig,
                                                         uint8_t* flags, float* __restrict__ logits, int n_out,
                                                         dycl_record* rec) {
-  __shared__ float part[2048];
-  __shared__ float g[2048];
-  __shared__ float z[1024];
-  __shared__ float red[8];
-  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if constexpr (BF16) {
-    row_channel_sums(static_cast<const uint16_t*>(x) + (size_t)r * HW * C, HW, C, g, part);
-    const float inv = 1.0f / static_cast<float>(HW);
-    for (int c = tid; c < C; c += 256) g[c] *= inv;
-  } else {
-    for (int c = tid; c < C; c += 256) g[c] = static_cast<const float*>(x)[(size_t)r * C + c];
+  // R rows per workgroup: pooled features g [R][C] and logits z [R][ncls]
+  // in LDS; the head weights W [ncls][C] are read once per workgroup
+  constexpr int RMAX = 8;
+  extern __shared__ float dyn[];   // part [2048] | g [R][C] | z [R][ncls]
+  float* const part = dyn;
+  float* const g = dyn + 2048;
+  float* const z = g + R * C;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r0 = blockIdx.x * R, nr = min(R, n - r0);
+  for (int i = 0; i < nr; ++i) {
+    float* gi = g + i * C;
+    if constexpr (BF16) {
+      row_channel_sums(static_cast<const uint16_t*>(x) + (size_t)(r0 + i) * HW * C, HW, C, gi, part);
+      const float inv = 1.0f / static_cast<float>(HW);
+      for (int c = tid; c < C; c += 256) gi[c] *= inv;
+    } else {
+      for (int c = tid; c < C; c += 256) gi[c] = static_cast<const float*>(x)[(size_t)(r0 + i) * C + c];
+    }
   }
   __syncthreads();
-  float m = -INFINITY;
-  for (int j = tid; j < ncls; j += 256) {
-    float acc = 0.f;
-    for (int c = 0; c < C; ++c) acc = fmaf(Wt[(size_t)c * ncls + j], g[c], acc);
-    acc += bias[j];
-    z[j] = acc;
-    m = fmaxf(m, acc);
+
+  // z[i][j] = bias[j] + sum_c W[j][c] g[i][c]: four lanes per class, each
+  // taking every fourth 16-byte piece of the weight row (independent loads),
+  // combined by lane shuffles
+  const int q = tid & 3, jl = tid >> 2, C4 = C >> 2;
+  for (int j0 = 0; j0 < ncls; j0 += 64) {
+    const int j = j0 + jl;
+    float acc[RMAX];
+#pragma unroll
+    for (int i = 0; i < RMAX; ++i) acc[i] = 0.f;
+    if (j < ncls) {
+      const float4* wr = reinterpret_cast<const float4*>(W + (size_t)j * C);
+#pragma unroll 4
+      for (int f = q; f < C4; f += 4) {
+        const float4 w = wr[f];
+#pragma unroll
+        for (int i = 0; i < RMAX; ++i) {
+          if (i < nr) {
+            const float4 gv = *reinterpret_cast<const float4*>(g + i * C + 4 * f);
+            acc[i] = fmaf(w.x, gv.x, fmaf(w.y, gv.y, fmaf(w.z, gv.z, fmaf(w.w, gv.w, acc[i]))));
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < RMAX; ++i) {
+      acc[i] += __shfl_xor(acc[i], 1);
+      acc[i] += __shfl_xor(acc[i], 2);
+    }
+    if (q == 0 && j < ncls) {
+      const float bj = bias[j];
+#pragma unroll
+      for (int i = 0; i < RMAX; ++i)
+        if (i < nr) z[i * ncls + j] = acc[i] + bj;
+    }
   }
-  bool ex = final_ != 0;
-  if (!ex) {
-    m = wave_max(m);
-    if (lane == 0) red[wave] = m;
-    __syncthreads();
-    m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    const float T = *Tp;
-    float sum = 0.f;
-    for (int j = tid; j < ncls; j += 256) sum += expf((z[j] - m) / T);
-    sum = wave_sum(sum);
-    __syncthreads();
-    if (lane == 0) red[4 + wave] = sum;
-    __syncthreads();
-    sum = red[4] + red[5] + red[6] + red[7];
-    ex = (1.0f / sum) >= tau;
+  __syncthreads();
+
+  // decision per row, one wave each: max softmax probability 1 / sum exp((z - max) / T)
+  for (int i = wave; i < nr; i += 4) {
+    const int r = r0 + i;
+    const float* zi = z + i * ncls;
+    bool ex = final_ != 0;
+    if (!ex) {
+      float m = -INFINITY;
+      for (int j = lane; j < ncls; j += 64) m = fmaxf(m, zi[j]);
+      m = wave_max(m);
+      const float T = *Tp;
+      float sum = 0.f;
+      for (int j = lane; j < ncls; j += 64) sum += expf((zi[j] - m) / T);
+      sum = wave_sum(sum);
+      ex = (1.0f / sum) >= tau;
+    }
+    if (ex) {
+      const int o = orig ? orig[r] : r;
+      for (int j = lane; j < ncls; j += 64) logits[(size_t)o * n_out + j] = zi[j];
+      if (lane == 0 && head >= 0) rec[o].exit_index = head;
+    }
+    if (lane == 0) flags[r] = ex ? 1 : 0;
   }
-  if (ex) {
-    const int o = orig ? orig[r] : r;
-    for (int j = tid; j < ncls; j += 256) logits[(size_t)o * n_out + j] = z[j];
-    if (tid == 0 && head >= 0) rec[o].exit_index = head;
-  }
-  if (tid == 0) flags[r] = ex ? 1 : 0;
 }
 
-void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* Wt, const float* bias, int ncls,
+void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* W, const float* bias, int ncls,
                const float* T, float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits,
                int n_out, dycl_record* rec, hipStream_t s) {
+  // rows per workgroup: one where pooling dominates (a row's pooling reads
+  // HW * C elements, its linear C * ncls weights); else enough rows to share
+  // the weights, keeping a workgroup for every CU, at most 8, within LDS
+  int R = HW >= ncls ? 1 : n / 256;
+  R = R < 1 ? 1 : (R > 8 ? 8 : R);
+  while (R > 1 && (R * C > 8 * 2048 || R * ncls > 8 * 1024)) --R;
+  const int grid = (n + R - 1) / R;
+  const size_t lds = (2048 + static_cast<size_t>(R) * (C + ncls)) * sizeof(float);
   if (bf16)
-    hipLaunchKernelGGL(exit_head_kernel<true>, dim3(n), dim3(256), 0, s, x, HW, C, Wt, bias, ncls, T, tau, final_,
-                       head, orig, flags, logits, n_out, rec);
+    hipLaunchKernelGGL(exit_head_kernel<true>, dim3(grid), dim3(256), lds, s, x, n, R, HW, C, W, bias, ncls, T, tau,
+                       final_, head, orig, flags, logits, n_out, rec);
   else
-    hipLaunchKernelGGL(exit_head_kernel<false>, dim3(n), dim3(256), 0, s, x, HW, C, Wt, bias, ncls, T, tau, final_,
-                       head, orig, flags, logits, n_out, rec);
+    hipLaunchKernelGGL(exit_head_kernel<false>, dim3(grid), dim3(256), lds, s, x, n, R, HW, C, W, bias, ncls, T, tau,
+                       final_, head, orig, flags, logits, n_out, rec);
 }
 
 // ---------------------------------------------------------------- gate ----

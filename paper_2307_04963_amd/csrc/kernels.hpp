@@ -60,10 +60,11 @@ void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, hipStream_t s);
 void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int final_, int head,
                  const int32_t* orig, uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s);
 
-// Fused exit head for small heads (C <= 2048, ncls <= 1024): pooling, head
-// linear from transposed weights Wt [C][ncls], and the exit decision, one
-// workgroup per row.  Same outputs as gap_bf16 + linear_f32 + exit_decide.
-void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* Wt, const float* bias, int ncls,
+// Fused exit head for small heads (C <= 2048 and a multiple of 4, ncls <=
+// 1024): pooling, head linear on the weights as stored W [ncls][C] (16-byte
+// aligned rows), and the exit decision, up to 8 rows per workgroup.  Same
+// outputs as gap_bf16 + linear_t_f32 + exit_decide.
+void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* W, const float* bias, int ncls,
                const float* T, float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits,
                int n_out, dycl_record* rec, hipStream_t s);
 

@@ -346,7 +346,7 @@ struct Run {
           const double esz = sp.dt == DType::BF16 ? 2.0 : 4.0;
           if (nd.fused) {
             launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, esz * n * HW * nd.hc + 4.0 * nd.ncls * (nd.hc + 1), [&] {
-              k::exit_head(tp[nd.src], sp.dt == DType::BF16, n, HW, nd.hc, p->head_t[nd.head_t], f32(nd.h_b),
+              k::exit_head(tp[nd.src], sp.dt == DType::BF16, n, HW, nd.hc, f32(nd.h_w), f32(nd.h_b),
                            nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags, logits,
                            sp.n_out, rec, s);
             });

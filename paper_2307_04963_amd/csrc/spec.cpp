@@ -239,10 +239,12 @@ struct Builder {
     nd.decision = sp.decisions++;
     sp.max_head_c = std::max(sp.max_head_c, s.C);
     sp.max_ncls = std::max(sp.max_ncls, nd.ncls);
-    // the head weights live transposed on the device; small heads (weights
-    // streamed from L2 once per row) run as one fused kernel
+    // small heads run as one fused kernel (pooling, linear on the weights
+    // as stored [ncls][C], decision); the others pool, then multiply by a
+    // transposed copy of the weights
     nd.head_t = sp.n_head_t++;
-    nd.fused = nd.ncls <= 1024 && static_cast<int64_t>(s.C) * nd.ncls <= (int64_t(1) << 16);
+    nd.fused = nd.ncls <= 1024 && s.C <= 2048 && s.C % 4 == 0 &&
+               static_cast<int64_t>(s.C) * nd.ncls <= (int64_t(1) << 16);
     if (!nd.final_) {
       int old = space;
       space = next_space++;
