@@ -506,7 +506,8 @@ __device__ __forceinline__ void buffer_store16(void* base, uint32_t bytes, uint3
 }
 
 // --------------------------------- 3x3 conv, halo tiles, resident weights ----
-// For 3x3 / stride 1 / pad 1 layers with 64 input and 64 output channels.
+// For 3x3 / stride 1 / pad 1 layers with 64 input and 64 output channels,
+// and for stems with 8 (padded) input channels and 64 output channels.
 // A persistent workgroup walks a contiguous range of 128 x 64 output tiles;
 // a tile is R whole output rows of one image (or G whole images when an
 // image is smaller than the tile).  The tile's input patch - its rows plus
@@ -531,10 +532,13 @@ __device__ __forceinline__ void buffer_store16(void* base, uint32_t bytes, uint3
 // Patch pixels are stored 144 bytes apart (eight 16-byte K chunks and one
 // unused slot): the 16 lanes of a ds_read_b128 phase, 16 consecutive
 // pixels, fall on 16 distinct bank groups, and a tap's window is a constant
-// byte offset from the lane's base address.
+// byte offset from the lane's base address.  With 8 input channels a pixel
+// is one 16-byte K chunk (stored densely), a K sub-step of 16 spans two
+// taps - tap 2s in lanes 0-31, 2s + 1 in lanes 32-63 - and nine taps take
+// five sub-steps (the tenth tap's weights are zero).
 struct Conv3P {
   const uint16_t* src;
-  const uint16_t* w;      // [64][576] packed, K = tap * 64 + ci
+  const uint16_t* w;      // [64][Kp] packed, K = tap * cin + ci (Kp = 576, or 128 for 8 channels)
   const float* scale;
   const float* shift;
   const uint16_t* res;
@@ -546,18 +550,23 @@ struct Conv3P {
 };
 
 constexpr int kW3Patch = 256;                      // patch pixels per buffer (= kHP)
-constexpr int kW3PB = kW3Patch * 144;              // 36864 B per patch buffer
 constexpr int kW3RB = 128 * 128;                   // 16384 B: a tile of residual / output rows
-constexpr int kW3Lds = 2 * kW3PB + 4 * kW3RB + 512;  // 139776 B (+ scale / shift)
+// patch bytes per pixel and per buffer, by input channels
+constexpr int w3_pxb(int cin) { return cin == 8 ? 16 : 144; }
+constexpr int w3_pb(int cin) { return kW3Patch * w3_pxb(cin); }
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 __device__ __forceinline__ void all_barrier() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int ACT, bool RES>
+template <int CIN, int ACT, bool RES>
 __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
   constexpr int NL = 128;                          // loader / store threads
-  constexpr int JP = kW3Patch * 9 / NL;            // 18 patch load passes
-  __shared__ __align__(16) char smem[kW3Lds];
+  constexpr int PXB = w3_pxb(CIN), kW3PB = w3_pb(CIN);
+  constexpr int SLOTS = PXB / 16;                  // 16-byte slots per patch pixel (9 or 1)
+  constexpr int JP = kW3Patch * SLOTS / NL;        // patch loads per loader thread (18 or 2)
+  constexpr int KP = CIN == 8 ? 128 : 576;         // packed row length
+  constexpr int NS = CIN == 8 ? 5 : 36;            // K sub-steps of 16
+  __shared__ __align__(16) char smem[2 * kW3PB + 4 * kW3RB + 512];
   char* const pbuf = smem;                         // [2][256 px][144 B]
   char* const rbuf = smem + 2 * kW3PB;             // [2][128 rows][128 B] residual
   char* const sbuf = rbuf + 2 * kW3RB;             // [2][128 rows][128 B] finished bf16 tile
@@ -619,17 +628,17 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
     // the patch, image-mode halo rows) get an offset above 2^31: all read as
     // zeros, the convolution's padding.
     const int ld = tid - 4 * 64, lw = wv - 4;
-    const int rowb = p.W * 128, imgb = p.H * rowb;
+    const int rowb = p.W * CIN * 2, imgb = p.H * rowb;
     uint32_t vofs[JP];
 #pragma unroll
     for (int j = 0; j < JP; ++j) {
-      const int u = j * NL + ld, q = u / 9, ch = u - (u / 9) * 9;
+      const int u = j * NL + ld, q = u / SLOTS, ch = u - (u / SLOTS) * SLOTS;
       const int segpix = (p.RS + 2) * p.PW;
       const int sg = q / segpix, rem = q - sg * segpix;
       const int pr = rem / p.PW, pc = rem - (rem / p.PW) * p.PW;
       bool data = q < p.NP && ch < 8 && pc >= 1 && pc <= p.W;
       if (!p.tpi) data = data && pr >= 1 && pr <= p.H;
-      vofs[j] = data ? static_cast<uint32_t>(sg * imgb + (pr - 1) * rowb + (pc - 1) * 128 + ch * 16) : 0xC0000000u;
+      vofs[j] = data ? static_cast<uint32_t>(sg * imgb + (pr - 1) * rowb + (pc - 1) * CIN * 2 + ch * 16) : 0xC0000000u;
     }
     for (int t = t_begin; t <= t_end; ++t) {
       if (t < t_end) {
@@ -637,7 +646,7 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
         int img, oh0, m0, lim;
         tile_geom(t, img, oh0, m0, lim);
         const int nimg = p.tpi ? 1 : min(p.segs, p.n - img);
-        const uint16_t* pbase = p.src + (size_t)img * p.H * p.W * 64;
+        const uint16_t* pbase = p.src + (size_t)img * p.H * p.W * CIN;
         const uint32_t pbytes = static_cast<uint32_t>(nimg) * imgb, tofs = static_cast<uint32_t>(oh0) * rowb;
         char* pb = pbuf + buf * kW3PB;
 #pragma unroll
@@ -665,10 +674,12 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
   // group: channels wn*32 + 8q + 4*hi .. +3, q = 0..3, of pixel (lane & 31)
   const int wm = wave >> 1, wn = wave & 1, hi = lane >> 5;
   const int co_l = wn * 32 + (lane & 31);
-  bf16x8 bw[36];
+  // B fragments: sub-step k covers K 16k .. 16k + 15 (64 channels: tap k/4,
+  // channels 16 (k%4) ..; 8 channels: taps 2k, 2k + 1); this lane's half
+  bf16x8 bw[NS];
 #pragma unroll
-  for (int k = 0; k < 36; ++k)
-    bw[k] = *reinterpret_cast<const bf16x8*>(p.w + (size_t)co_l * 576 + (k >> 2) * 64 + (2 * (k & 3) + hi) * 8);
+  for (int k = 0; k < NS; ++k)
+    bw[k] = *reinterpret_cast<const bf16x8*>(p.w + (size_t)co_l * KP + 16 * k + 8 * hi);
   // scale / shift of the 64 channels, in LDS after the staging buffers
   float* const ssl = reinterpret_cast<float*>(sbuf + 2 * kW3RB);
   if (tid < 64) ssl[tid] = p.scale ? p.scale[tid] : 1.0f;
@@ -692,33 +703,48 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
     for (int a = 0; a < 2; ++a)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][r] = 0.f;
-    // lane base addresses of the three tap rows; the tap column and the K
-    // chunk are constant offsets
-    const char* ab[2][3];
+    if constexpr (CIN == 8) {
+      // sub-step k: this lane's tap 2k + hi (the tenth tap has zero weights)
+      const char* pcur = pbuf + buf * kW3PB;
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+      for (int k = 0; k < NS; ++k) {
+        const int tap = 2 * k + hi < 9 ? 2 * k + hi : 0;
+        const int toff = (tap / 3) * p.PW + (tap % 3);
+        bf16x8 af[2];
 #pragma unroll
-      for (int dy = 0; dy < 3; ++dy) ab[a][dy] = pbuf + buf * kW3PB + (pix0[a] + dy * p.PW) * 144 + hi * 16;
-    bf16x8 af[2][2][2];                   // [slot][step of the pair][a]
-    auto fetch = [&](int g, int slot) __attribute__((always_inline)) {
-      const int tap = g >> 1, dy = tap / 3, dx = tap % 3;
+        for (int a = 0; a < 2; ++a) af[a] = *reinterpret_cast<const bf16x8*>(pcur + (pix0[a] + toff) * 16);
+#pragma unroll
+        for (int a = 0; a < 2; ++a) acc[a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[k], af[a], acc[a], 0, 0, 0);
+      }
+    } else {
+      // lane base addresses of the three tap rows; the tap column and the K
+      // chunk are constant offsets
+      const char* ab[2][3];
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          af[slot][j][a] = *reinterpret_cast<const bf16x8*>(ab[a][dy] + dx * 144 + (2 * (2 * (g & 1) + j)) * 16);
-    };
-    fetch(0, 0);
-#pragma unroll
-    for (int g = 0; g < 18; ++g) {
-      if (g + 1 < 18) fetch(g + 1, (g + 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
+        for (int dy = 0; dy < 3; ++dy) ab[a][dy] = pbuf + buf * kW3PB + (pix0[a] + dy * p.PW) * 144 + hi * 16;
+      bf16x8 af[2][2][2];                   // [slot][step of the pair][a]
+      auto fetch = [&](int g, int slot) __attribute__((always_inline)) {
+        const int tap = g >> 1, dy = tap / 3, dx = tap % 3;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
-          acc[a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[2 * g + j], af[g & 1][j][a], acc[a], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            af[slot][j][a] = *reinterpret_cast<const bf16x8*>(ab[a][dy] + dx * 144 + (2 * (2 * (g & 1) + j)) * 16);
+      };
+      fetch(0, 0);
+#pragma unroll
+      for (int g = 0; g < 18; ++g) {
+        if (g + 1 < 18) fetch(g + 1, (g + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+            acc[a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[2 * g + j], af[g & 1][j][a], acc[a], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
 
     // epilogue into this tile's staging buffer (the store waves finished its
@@ -1228,7 +1254,11 @@ bool is_halo_layer(const ConvArgs& a) {
 // the weights-resident 3x3 kernel (64 -> 64 channels)
 bool conv3_wres(const ConvArgs& a, hipStream_t s) {
   HaloGeom g;
-  if (!is_halo_layer(a) || a.cin != 64 || a.cout != 64 || !halo_geom(a.n, a.H, a.W, 128, kHP, g)) return false;
+  const bool stem = a.cin == 8 && a.Kp == 128 && a.k == 3 && a.stride == 1 && a.pad == 1 && !a.src2 && !a.out_f32 &&
+                    a.Ho == a.H && a.Wo == a.W &&
+                    !((reinterpret_cast<uintptr_t>(a.scale) | reinterpret_cast<uintptr_t>(a.shift)) & 15);
+  if (!(stem || (is_halo_layer(a) && a.cin == 64)) || a.cout != 64 || !halo_geom(a.n, a.H, a.W, 128, kHP, g))
+    return false;
   const int cus = cu_count();
   if (!cus) return false;
   Conv3P p;
@@ -1252,15 +1282,22 @@ bool conv3_wres(const ConvArgs& a, hipStream_t s) {
   p.tiles = g.mtiles;
   const int grid = p.tiles < cus ? p.tiles : cus;
   auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(512), 0, s, p); };
-  if (p.res) {
-    if (p.act == ACT_RELU) go(conv3_wres_kernel<ACT_RELU, true>);
-    else if (p.act == ACT_GELU) go(conv3_wres_kernel<ACT_GELU, true>);
-    else go(conv3_wres_kernel<ACT_NONE, true>);
-  } else {
-    if (p.act == ACT_RELU) go(conv3_wres_kernel<ACT_RELU, false>);
-    else if (p.act == ACT_GELU) go(conv3_wres_kernel<ACT_GELU, false>);
-    else go(conv3_wres_kernel<ACT_NONE, false>);
+#define DYCL_W(CIN)                                                     \
+  if (p.res) {                                                          \
+    if (p.act == ACT_RELU) go(conv3_wres_kernel<CIN, ACT_RELU, true>);  \
+    else if (p.act == ACT_GELU) go(conv3_wres_kernel<CIN, ACT_GELU, true>); \
+    else go(conv3_wres_kernel<CIN, ACT_NONE, true>);                    \
+  } else {                                                              \
+    if (p.act == ACT_RELU) go(conv3_wres_kernel<CIN, ACT_RELU, false>); \
+    else if (p.act == ACT_GELU) go(conv3_wres_kernel<CIN, ACT_GELU, false>); \
+    else go(conv3_wres_kernel<CIN, ACT_NONE, false>);                   \
   }
+  if (stem) {
+    DYCL_W(8)
+  } else {
+    DYCL_W(64)
+  }
+#undef DYCL_W
   return true;
 }
 

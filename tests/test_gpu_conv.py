@@ -41,6 +41,9 @@ CASES = [
     (4, 16, 16, 64, 128, 3, 2, 1, False, 1),    # strided
     (4, 16, 16, 128, 256, 1, 1, 0, False, 0),   # 1x1
     (6, 8, 8, 256, 512, 3, 1, 1, True, 1),
+    (3, 32, 32, 8, 64, 3, 1, 1, False, 1),      # 8-channel stem, weights in registers
+    (300, 32, 32, 8, 64, 3, 1, 1, True, 1),     # several tiles per workgroup
+    (5, 8, 8, 8, 64, 3, 1, 1, False, 2),        # image tiles, ragged
     (3, 20, 20, 3, 64, 7, 2, 3, False, 1),      # 3-channel stem, element gathers
     (5, 12, 12, 16, 32, 3, 1, 1, False, 1),
     (5, 12, 12, 64, 24, 3, 1, 1, True, 2),      # Cout not a multiple of 8
