@@ -27,29 +27,49 @@ __device__ __forceinline__ float wave_max(float v) {
 
 // Sum over HW of one row [HW, C] (bf16) into per-channel floats in `red`
 // (shared, C floats).  256 threads; C is a power of two >= 8 and <= 2048.
-__device__ void row_channel_sums(const uint16_t* __restrict__ x, int HW, int C, float* red, float* part) {
+// Channel sums of positions [p0, p1) of one NHWC bf16 row: red[c], fp32.
+// 256 threads: each takes 16-byte vectors of one channel group at every
+// PG-th position, four positions in flight; partial sums meet in `part`.
+__device__ void row_channel_sums(const uint16_t* __restrict__ x, int p0, int p1, int C, float* red, float* part) {
   const int tid = threadIdx.x;
   const int C8 = C >> 3;              // 16-byte vectors per position
   const int PG = 256 / C8 > 0 ? 256 / C8 : 1;
   const int cv = tid % C8, pg = tid / C8;
-  float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float s[4][8] = {};
   if (pg < PG) {
-    for (int pos = pg; pos < HW; pos += PG) {
+    int pos = p0 + pg;
+    for (; pos + 3 * PG < p1; pos += 4 * PG) {
+      uint4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(x + (size_t)(pos + u * PG) * C + cv * 8);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        s[u][0] += __uint_as_float(v[u].x << 16);
+        s[u][1] += __uint_as_float(v[u].x & 0xffff0000u);
+        s[u][2] += __uint_as_float(v[u].y << 16);
+        s[u][3] += __uint_as_float(v[u].y & 0xffff0000u);
+        s[u][4] += __uint_as_float(v[u].z << 16);
+        s[u][5] += __uint_as_float(v[u].z & 0xffff0000u);
+        s[u][6] += __uint_as_float(v[u].w << 16);
+        s[u][7] += __uint_as_float(v[u].w & 0xffff0000u);
+      }
+    }
+    for (; pos < p1; pos += PG) {
       const uint4 v = *reinterpret_cast<const uint4*>(x + (size_t)pos * C + cv * 8);
-      s[0] += __uint_as_float(v.x << 16);
-      s[1] += __uint_as_float(v.x & 0xffff0000u);
-      s[2] += __uint_as_float(v.y << 16);
-      s[3] += __uint_as_float(v.y & 0xffff0000u);
-      s[4] += __uint_as_float(v.z << 16);
-      s[5] += __uint_as_float(v.z & 0xffff0000u);
-      s[6] += __uint_as_float(v.w << 16);
-      s[7] += __uint_as_float(v.w & 0xffff0000u);
+      s[0][0] += __uint_as_float(v.x << 16);
+      s[0][1] += __uint_as_float(v.x & 0xffff0000u);
+      s[0][2] += __uint_as_float(v.y << 16);
+      s[0][3] += __uint_as_float(v.y & 0xffff0000u);
+      s[0][4] += __uint_as_float(v.z << 16);
+      s[0][5] += __uint_as_float(v.z & 0xffff0000u);
+      s[0][6] += __uint_as_float(v.w << 16);
+      s[0][7] += __uint_as_float(v.w & 0xffff0000u);
     }
   }
   // part: [PG][C]
   if (pg < PG) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) part[pg * C + cv * 8 + j] = s[j];
+    for (int j = 0; j < 8; ++j) part[pg * C + cv * 8 + j] = (s[0][j] + s[1][j]) + (s[2][j] + s[3][j]);
   }
   __syncthreads();
   for (int c = tid; c < C; c += 256) {
@@ -68,13 +88,47 @@ __global__ __launch_bounds__(256) void gap_kernel(const uint16_t* __restrict__ x
   __shared__ float part[2048];
   __shared__ float red[2048];
   const int r = blockIdx.x;
-  row_channel_sums(x + (size_t)r * HW * C, HW, C, red, part);
+  row_channel_sums(x + (size_t)r * HW * C, 0, HW, C, red, part);
   const float inv = 1.0f / static_cast<float>(HW);
   for (int c = threadIdx.x; c < C; c += 256) G[(size_t)r * C + c] = red[c] * inv;
 }
 
-void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, hipStream_t s) {
-  hipLaunchKernelGGL(gap_kernel, dim3(n), dim3(256), 0, s, x, HW, C, G);
+// a large row's positions split over S workgroups: partial sums
+// P[split][row][C], then a fixed-order sum per (row, channel)
+__global__ __launch_bounds__(256) void gap_split_kernel(const uint16_t* __restrict__ x, int n, int HW, int C, int S,
+                                                        float* __restrict__ P) {
+  __shared__ float part[2048];
+  __shared__ float red[2048];
+  const int r = blockIdx.x / S, sp = blockIdx.x - (blockIdx.x / S) * S;
+  const int p0 = static_cast<int>(static_cast<long>(HW) * sp / S), p1 = static_cast<int>(static_cast<long>(HW) * (sp + 1) / S);
+  row_channel_sums(x + (size_t)r * HW * C, p0, p1, C, red, part);
+  for (int c = threadIdx.x; c < C; c += 256) P[((size_t)sp * n + r) * C + c] = red[c];
+}
+
+__global__ void gap_merge_kernel(const float* __restrict__ P, int n, int HW, int C, int S, float* __restrict__ G) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= static_cast<size_t>(n) * C) return;
+  float t = 0.f;
+  for (int sp = 0; sp < S; ++sp) t += P[(size_t)sp * n * C + i];
+  G[i] = t * (1.0f / static_cast<float>(HW));
+}
+
+int gap_splits(int n, int HW) {
+  int S = (2048 + n - 1) / n;        // about 2048 workgroups
+  if (S > HW / 64) S = HW / 64;      // at least 64 positions each
+  return S < 1 ? 1 : (S > kGapMaxSplit ? kGapMaxSplit : S);
+}
+
+void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, float* P, hipStream_t s) {
+  const int S = P ? gap_splits(n, HW) : 1;
+  if (S == 1) {
+    hipLaunchKernelGGL(gap_kernel, dim3(n), dim3(256), 0, s, x, HW, C, G);
+    return;
+  }
+  hipLaunchKernelGGL(gap_split_kernel, dim3(n * S), dim3(256), 0, s, x, n, HW, C, S, P);
+  const size_t total = static_cast<size_t>(n) * C;
+  hipLaunchKernelGGL(gap_merge_kernel, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, P, n, HW, C, S,
+                     G);
 }
 
 // -------------------------------------------------------------- linear ----
@@ -251,7 +305,7 @@ __global__ __launch_bounds__(256) void exit_head_kernel(const void* __restrict__
   for (int i = 0; i < nr; ++i) {
     float* gi = g + i * C;
     if constexpr (BF16) {
-      row_channel_sums(static_cast<const uint16_t*>(x) + (size_t)(r0 + i) * HW * C, HW, C, gi, part);
+      row_channel_sums(static_cast<const uint16_t*>(x) + (size_t)(r0 + i) * HW * C, 0, HW, C, gi, part);
       const float inv = 1.0f / static_cast<float>(HW);
       for (int c = tid; c < C; c += 256) gi[c] *= inv;
     } else {
@@ -350,7 +404,7 @@ __global__ __launch_bounds__(256) void gate_kernel(const uint16_t* __restrict__ 
   __shared__ float red[2048];
   __shared__ float wsum[4];
   const int r = blockIdx.x;
-  row_channel_sums(x + (size_t)r * HW * C, HW, C, red, part);
+  row_channel_sums(x + (size_t)r * HW * C, 0, HW, C, red, part);
   const float inv = 1.0f / static_cast<float>(HW);
   float d = 0.f;
   for (int c = threadIdx.x; c < C; c += 256) d = fmaf(u[c], red[c] * inv, d);

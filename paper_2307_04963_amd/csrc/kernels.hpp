@@ -51,8 +51,11 @@ void linear_t_f32(const float* X, int n, int K, const float* Wt, const float* bi
 void linear_f32(const float* X, int n, int K, const float* W, const float* bias, int N, int act, float* Y,
                 hipStream_t s);
 
-// G[r, c] = sum_{hw} x[r, hw, c] / HW
-void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, hipStream_t s);
+// G[r, c] = sum_{hw} x[r, hw, c] / HW.  With a workspace P of
+// kGapMaxSplit * n * C floats, long rows are split over several workgroups
+// (partial sums, then a fixed-order merge); P may be null.
+constexpr int kGapMaxSplit = 16;
+void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, float* P, hipStream_t s);
 
 // Exit decision from head logits Z [n, ncls]: p = max softmax(Z / T); rows
 // with p >= tau (or all rows when final) write their logits and exit index at

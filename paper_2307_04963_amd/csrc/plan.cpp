@@ -143,6 +143,11 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
   p->d_iota = dev_alloc<int32_t>(p, B, "iota");
   p->d_counts = dev_alloc<int32_t>(p, 2 * std::max(1, sp.decisions), "counts");
   p->d_G = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_head_c, "pooled features");
+  bool split_pool = false;   // a bf16 head pooled outside the fused kernel
+  for (const Node& nd : sp.nodes)
+    if (nd.kind == NodeKind::Exit && !nd.fused && sp.dt == DType::BF16) split_pool = true;
+  if (split_pool)
+    p->d_Gpart = dev_alloc<float>(p, static_cast<size_t>(k::kGapMaxSplit) * B * sp.max_head_c, "pooling partials");
   p->d_Z = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_ncls, "head logits");
   p->d_S = dev_alloc<float>(p, B, "halting sums");
   p->d_zeros = dev_alloc<uint16_t>(p, 128, "zero page");
@@ -186,7 +191,7 @@ void plan_free(dycl_plan* p) {
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
                      p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S, p->d_zeros,
-                     p->d_xpad, p->d_cws};
+                     p->d_xpad, p->d_cws, p->d_Gpart};
   for (void* s : singles)
     if (s) hipFree(s);
   if (p->h_counts) hipHostFree(p->h_counts);
@@ -352,7 +357,7 @@ struct Run {
             });
           } else if (sp.dt == DType::BF16) {
             launch(P_HEAD, 0, 2.0 * n * HW * nd.hc + 4.0 * n * nd.hc, [&] {
-              k::gap_bf16(static_cast<const uint16_t*>(tp[nd.src]), n, HW, nd.hc, p->d_G, s);
+              k::gap_bf16(static_cast<const uint16_t*>(tp[nd.src]), n, HW, nd.hc, p->d_G, p->d_Gpart, s);
             });
             G = p->d_G;
           }
