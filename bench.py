@@ -55,11 +55,26 @@ def measured_traffic(workload: str, batch: int):
     return float(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
 
-def cpu_baseline(wl, seconds: float):
-    import numpy as np
-    import torch
+def _cpu_info():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    smt = None
+    try:
+        smt = open("/sys/devices/system/cpu/smt/active").read().strip() == "1"
+    except OSError:
+        pass
+    return model, os.cpu_count(), smt
+
+
+def _time_oracle(wl, acc: str, seconds: float):
     from oracle import dycl_oracle as O
-    o = O.from_workload(wl)
+    o = O.from_workload(wl, acc)
     x, aux = wl.inputs_f32(64)
     n, t0 = 0, time.perf_counter()
     while True:
@@ -68,9 +83,21 @@ def cpu_baseline(wl, seconds: float):
         el = time.perf_counter() - t0
         if (el >= seconds and n >= 2) or el >= 4 * seconds:
             break
-    _ = np
-    return {"value": n / el, "unit": "samples/s", "cores": torch.get_num_threads(), "kind": "oracle",
-            "sample": f"{n} samples of {wl.name} run one by one (float64 accumulation, bf16 storage), {el:.1f} s"}
+    return n, el
+
+
+def cpu_baseline(wl, seconds: float):
+    """The oracle (per-sample interpreter, torch CPU ops) timed on this
+    host: float64 accumulation (the reference) and float32."""
+    import torch
+    n64, el64 = _time_oracle(wl, "f64", seconds)
+    n32, el32 = _time_oracle(wl, "f32", seconds / 2)
+    model, ncpu, smt = _cpu_info()
+    return {"value": n64 / el64, "unit": "samples/s", "cores": torch.get_num_threads(), "kind": "oracle",
+            "sample": f"{n64} samples of {wl.name} (the first 64 of the batch, cycled) run one by one with float64 "
+                      f"accumulation and bf16 storage, {el64:.1f} s",
+            "acc32_value": n32 / el32, "acc32_sample": f"{n32} samples, {el32:.1f} s",
+            "cpu_model": model, "logical_cpus": ncpu, "smt_active": smt}
 
 
 def hbm_kernels(stream, reps: int = 10):
