@@ -7,7 +7,13 @@ HBM before the timed region; the plan (weights, workspace) is built before.
 
 Prints one JSON line:
   value        samples/s over exactly --steps timed steps (HIP events on the
-               run's stream, bracketed by device synchronisation);
+               run's stream, bracketed by device synchronisation) in the
+               host mode --host-mode;
+  host_modes   the same --steps timed in each host mode: sync (branch counts
+               read back at every decision point), device (counts stay on the
+               device, count-guarded launches) and graph (device mode
+               replayed from a captured HIP graph), with the host-module cost
+               per decision point that the device modes remove;
   roofline     the dominant kernel class (the MFMA convolutions), timed per
                launch with HIP events in a second, profiled pass of the same
                steps: algorithmic FLOPs of the executed rows / kernel time,
@@ -179,6 +185,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm-kernels", action="store_true")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-scaling copy")
+    ap.add_argument("--host-mode", default="device", choices=["sync", "device", "graph"],
+                    help="host mode of the headline value (all three are timed)")
     args = ap.parse_args()
     if args.copy_probe:
         copy_probe()
@@ -201,22 +209,37 @@ def main():
     rec = torch.empty((B, 4), dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
 
-    for _ in range(args.warmup):
-        plan.run(xt, at, logits, rec, stream)
-    torch.cuda.synchronize()
+    def timed(mode):
+        plan.set_host_mode(mode)
+        for _ in range(args.warmup):
+            plan.run(xt, at, logits, rec, stream)
+        torch.cuda.synchronize()
+        # timed region: exactly --steps steps
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            plan.run(xt, at, logits, rec, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        return e0.elapsed_time(e1) / args.steps, wall * 1e3 / args.steps, plan.counts()
 
-    # timed region: exactly --steps steps
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        plan.run(xt, at, logits, rec, stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    ms = e0.elapsed_time(e1) / args.steps
-    counts = plan.counts()
+    modes = {}
+    for mode in [m for m in ("sync", "device", "graph") if m != args.host_mode] + [args.host_mode]:
+        modes[mode] = timed(mode)
+    ms, wall_ms, counts = modes[args.host_mode]
+    assert all(m[2] == counts for m in modes.values()), "host modes disagree on the branch counts"
+    plan.set_host_mode("sync")
+    decisions = sum(1 for a, b in counts if a + b > 0)
+    host_modes = {m: {"ms_per_step": v[0], "wall_ms_per_step": v[1], "samples_per_s": B / (v[0] * 1e-3)}
+                  for m, v in modes.items()}
+    host_modes["decision_points_reached"] = decisions
+    host_modes["us_per_decision_sync_minus_device"] = (
+        (modes["sync"][0] - modes["device"][0]) * 1e3 / decisions if decisions else None)
+    host_modes["us_per_decision_sync_minus_graph"] = (
+        (modes["sync"][0] - modes["graph"][0]) * 1e3 / decisions if decisions else None)
 
     # profiled pass: per-launch HIP events around every kernel on the run's stream
     plan.profile(True)
@@ -243,14 +266,15 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
-        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "wall_ms_per_step": wall_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.arch["dtype"],
         "data": "synthetic (seeded N(0,1) inputs, seeded random-init weights, calibrated BN/heads)",
         "config": {"workload": args.workload, "batch": B, "input": list(wl.arch["input"]),
-                   "branch_counts": counts, "parallelism": "single GPU"},
+                   "branch_counts": counts, "host_mode": args.host_mode, "parallelism": "single GPU"},
+        "host_modes": host_modes,
         "roofline": {"bound": "mfma", "kernel": "conv_bf16_mfma (implicit-GEMM conv / linear)",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,

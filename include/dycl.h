@@ -89,26 +89,56 @@ int dycl_plan_create(const char* spec_json, const void* weights, size_t weights_
  *   logits_dev  device fp32 [batch, n_out], written in the original sample
  *               order.
  *   records_dev device dycl_record [batch], original order.
- * The host code waits only for the per-decision branch counts; when the call
- * returns, the remaining work may still be queued on the stream.  Results are
- * valid after the stream is synchronised.
+ * In the default host mode (DYCL_HOST_SYNC) the host code waits only for the
+ * per-decision branch counts; in the device modes it waits for nothing (see
+ * dycl_plan_set_host_mode).  When the call returns, the remaining work may
+ * still be queued on the stream.  Results are valid after the stream is
+ * synchronised.
  */
 int dycl_run(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev, float* logits_dev,
              dycl_record* records_dev, void* hip_stream);
+
+/*
+ * How the host module learns the branch counts (Sec. 5: the host program
+ * keeps the conditionals and calls the compiled sub-DNNs; Sec. 4, Challenge
+ * 2 and Sec. 6.4, Table 4: host-device transfers that compute nothing are
+ * overhead worth removing).
+ *   DYCL_HOST_SYNC    after each decision point the host reads the two branch
+ *                     counts back and launches the next kernels on exactly
+ *                     that many rows (one wait per decision point).
+ *   DYCL_HOST_DEVICE  the counts stay on the device: every later kernel is
+ *                     launched for the largest possible row count (the rows
+ *                     that reached the decision) and reads the live count
+ *                     when it starts; surplus workgroups leave at once.  The
+ *                     host never waits inside dycl_run.
+ *   DYCL_HOST_GRAPH   DYCL_HOST_DEVICE with the whole run captured once into
+ *                     a HIP graph and replayed by later runs with the same
+ *                     batch size and the same x / aux / logits / records
+ *                     pointers (any change re-captures).  While profiling is
+ *                     enabled, runs are launched without the graph.
+ * Results are identical in every mode.  Returns the previous mode, or
+ * DYCL_E_INVALID for an unknown mode.  Not to be called while a run of the
+ * plan is being enqueued.
+ */
+typedef enum { DYCL_HOST_SYNC = 0, DYCL_HOST_DEVICE = 1, DYCL_HOST_GRAPH = 2 } dycl_host_mode;
+int dycl_plan_set_host_mode(dycl_plan* plan, int mode);
 
 /*
  * Branch counts of the last dycl_run: for decision point d (in program
  * order, loop steps unrolled) counts[2d] = samples that took the "true"
  * branch (exit / execute / halt) and counts[2d+1] = the others; decisions
  * the batch never reached read 0.  Writes min(n, 2 * decisions) entries and
- * returns the number of decision points.
+ * returns the number of decision points.  After a run in a device mode the
+ * counts are read from the device, which first synchronises that run's
+ * stream.
  */
 int dycl_last_counts(const dycl_plan* plan, int32_t* counts, int n);
 
 /*
  * Plan facts, info[0..n): 0 n_out, 1 input bytes per sample, 2 decision
  * points, 3 device workspace bytes, 4 device weight bytes, 5 max_batch,
- * 6 aux required (0/1), 7 number of nodes.  Returns the number written.
+ * 6 aux required (0/1), 7 number of nodes, 8 host mode, 9 graph captures
+ * so far.  Returns the number written.
  */
 int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n);
 
@@ -119,7 +149,9 @@ int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n);
  * dycl_profile_read fills up to `cap` rows of
  *   { launches, total_ms, flops, bytes }  (4 doubles per row)
  * for the classes named by dycl_profile_class(i) and returns the number of
- * classes.  Reading synchronises the plan's last stream.
+ * classes.  Reading synchronises the plan's last stream.  In the device host
+ * modes the host does not know the live row counts, and the work is counted
+ * for the rows each kernel was launched for (an upper bound).
  */
 int dycl_profile_enable(dycl_plan* plan, int on);
 int dycl_profile_read(dycl_plan* plan, double* rows, int cap);

@@ -86,12 +86,26 @@ int dycl_run(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev
   });
 }
 
+int dycl_plan_set_host_mode(dycl_plan* plan, int mode) {
+  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_plan_set_host_mode: invalid plan handle");
+  if (mode != DYCL_HOST_SYNC && mode != DYCL_HOST_DEVICE && mode != DYCL_HOST_GRAPH)
+    return fail(DYCL_E_INVALID, "dycl_plan_set_host_mode: unknown mode " + std::to_string(mode));
+  const int prev = plan->mode;
+  const int rc = guarded([&] {
+    dycl::plan_set_mode(plan, mode);
+    return DYCL_OK;
+  });
+  return rc == DYCL_OK ? prev : rc;
+}
+
 int dycl_last_counts(const dycl_plan* plan, int32_t* counts, int n) {
   if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_last_counts: invalid plan handle");
   if (n < 0 || (n > 0 && !counts)) return fail(DYCL_E_INVALID, "dycl_last_counts: bad buffer");
-  const int total = 2 * plan->spec.decisions;
-  for (int i = 0; i < n && i < total; ++i) counts[i] = plan->h_counts[i];
-  return plan->spec.decisions;
+  const int rc = guarded([&] {
+    dycl::plan_read_counts(plan, counts, n);
+    return DYCL_OK;
+  });
+  return rc == DYCL_OK ? plan->spec.decisions : rc;
 }
 
 int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n) {
@@ -99,16 +113,18 @@ int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n) {
   if (n < 0 || (n > 0 && !info)) return fail(DYCL_E_INVALID, "dycl_plan_info: bad buffer");
   const dycl::Spec& sp = plan->spec;
   const dycl::TensorInfo& in = sp.tensors[sp.input];
-  const int64_t v[8] = {sp.n_out,
-                        static_cast<int64_t>(in.row_bytes(sp.dt)),
-                        sp.decisions,
-                        static_cast<int64_t>(plan->workspace_bytes),
-                        static_cast<int64_t>(plan->weight_bytes),
-                        plan->max_batch,
-                        sp.aux ? 1 : 0,
-                        sp.nodes_total};
+  const int64_t v[10] = {sp.n_out,
+                         static_cast<int64_t>(in.row_bytes(sp.dt)),
+                         sp.decisions,
+                         static_cast<int64_t>(plan->workspace_bytes),
+                         static_cast<int64_t>(plan->weight_bytes),
+                         plan->max_batch,
+                         sp.aux ? 1 : 0,
+                         sp.nodes_total,
+                         plan->mode,
+                         plan->graph_captures};
   int w = 0;
-  for (; w < n && w < 8; ++w) info[w] = v[w];
+  for (; w < n && w < 10; ++w) info[w] = v[w];
   return w;
 }
 

@@ -40,6 +40,8 @@ struct ConvP {
   int H, W, cin, Ho, Wo, cout, stride, pad;
   int M, K, Kp, cin_log2;
   int mt, nt;
+  const int32_t* nc;       // device count of live images (<= nmax) or null
+  int nmax;                // images the grid is sized for
   const uint16_t* w;
   const float* scale;
   const float* shift;
@@ -80,9 +82,13 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
   __shared__ __align__(16) uint16_t Bs[STAGES][BN * LDK];
 
   // XCD-aware tile order (bijective on [0, mt*nt))
-  const int T = p.mt * p.nt;
+  // with a device count, only the tiles of the live images exist: the
+  // grid was sized for nmax images and the surplus workgroups leave
+  const int M = p.nc ? min(*p.nc, p.nmax) * p.Ho * p.Wo : p.M;
+  const int T = (p.nc ? (M + BM - 1) / BM : p.mt) * p.nt;
   const int T8 = (T >> 3) << 3;
   const int wg = blockIdx.x;
+  if (wg >= T) return;
   const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (wg >> 3) : wg;
   const int mtile = t / p.nt;
   const int m0 = mtile * BM, n0 = (t - mtile * p.nt) * BN;
@@ -98,7 +104,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
 #pragma unroll
   for (int i = 0; i < PA; ++i) {
     const int m = m0 + rsub + i * RPP;
-    if (m < p.M) {
+    if (m < M) {
       const int img = m / HoWo;
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
@@ -250,7 +256,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * WTM + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row >= p.M) continue;
+        if (row >= M) continue;
         const size_t o = (size_t)row * p.cout + col;
         float v = fmaf(acc[a][b][r], sc, sh);
         if (p.res) v += bf2f(p.res[o]);
@@ -305,9 +311,13 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
 
   __shared__ __align__(16) char smem[SMEM];
 
-  const int T = p.mt * p.nt;
+  // with a device count, only the tiles of the live images exist: the
+  // grid was sized for nmax images and the surplus workgroups leave
+  const int M = p.nc ? min(*p.nc, p.nmax) * p.Ho * p.Wo : p.M;
+  const int T = (p.nc ? (M + BM - 1) / BM : p.mt) * p.nt;
   const int T8 = (T >> 3) << 3;
   const int wg = blockIdx.x;
+  if (wg >= T) return;
   const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (wg >> 3) : wg;
   const int mtile = t / p.nt;
   const int m0 = mtile * BM, n0 = (t - mtile * p.nt) * BN;
@@ -322,7 +332,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
 #pragma unroll
   for (int j = 0; j < JA; ++j) {
     const int m = m0 + rbase + j * (NT / 8);
-    if (m < p.M) {
+    if (m < M) {
       const int img = m / HoWo;
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
@@ -454,7 +464,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
       const int rl = idx / G, g = idx - (idx / G) * G;
       const int row = m0 + wm * WTM + a * 32 + rl;
       const int col = n0 + wn * WTN + g * 8;
-      if (row < p.M && col < p.cout) {
+      if (row < M && col < p.cout) {
         const float4 lo = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8);
         const float4 hi = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8 + 4);
         float vv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
@@ -547,6 +557,7 @@ struct Conv3P {
   int n, H, W, cout, act;
   int RS, segs, PW, NP;    // rows per patch segment, segments, patch width, patch pixels
   int tiles, tpi;          // tiles; tiles per image (row mode) or 0 (image mode)
+  const int32_t* nc;       // device count of live images (<= n) or null
 };
 
 constexpr int kW3Patch = 256;                      // patch pixels per buffer (= kHP)
@@ -573,8 +584,12 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int HW = p.H * p.W;
-  const int t_begin = static_cast<int>((static_cast<long>(p.tiles) * blockIdx.x) / gridDim.x);
-  const int t_end = static_cast<int>((static_cast<long>(p.tiles) * (blockIdx.x + 1)) / gridDim.x);
+  // with a device count the live tiles are dealt over the grid (sized for
+  // n images); workgroups left without a tile leave
+  const int n = p.nc ? min(*p.nc, p.n) : p.n;
+  const int tiles = p.nc ? (p.tpi ? n * p.tpi : (n + p.segs - 1) / p.segs) : p.tiles;
+  const int t_begin = static_cast<int>((static_cast<long>(tiles) * blockIdx.x) / gridDim.x);
+  const int t_end = static_cast<int>((static_cast<long>(tiles) * (blockIdx.x + 1)) / gridDim.x);
   if (t_begin >= t_end) return;
 
   auto tile_geom = [&](int t, int& img, int& oh0, int& m0, int& lim) __attribute__((always_inline)) {
@@ -587,7 +602,7 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
       img = t * p.segs;
       oh0 = 0;
       m0 = img * HW;
-      lim = min(p.segs, p.n - img) * HW;
+      lim = min(p.segs, n - img) * HW;
     }
   };
   // 16-byte chunk position of (row, logical chunk) in a residual / staging
@@ -645,7 +660,7 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
         const int buf = (t - t_begin) & 1;
         int img, oh0, m0, lim;
         tile_geom(t, img, oh0, m0, lim);
-        const int nimg = p.tpi ? 1 : min(p.segs, p.n - img);
+        const int nimg = p.tpi ? 1 : min(p.segs, n - img);
         const uint16_t* pbase = p.src + (size_t)img * p.H * p.W * CIN;
         const uint32_t pbytes = static_cast<uint32_t>(nimg) * imgb, tofs = static_cast<uint32_t>(oh0) * rowb;
         char* pb = pbuf + buf * kW3PB;
@@ -826,6 +841,7 @@ struct Conv3HP {
   int n, H, W, cin, cout, Kp;
   int RS, segs, PW, NP, tpi;
   int ntiles, units, nch;  // output channel tiles, units, 64-channel chunks
+  const int32_t* nc;       // device count of live images (<= n) or null
 };
 
 constexpr int kHP = 256;                           // patch pixels per buffer of 128-pixel tiles
@@ -852,8 +868,10 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wv = __builtin_amdgcn_readfirstlane(wave);   // the same, known wave-uniform
   const int HW = p.H * p.W;
-  const int u_begin = static_cast<int>((static_cast<long>(p.units) * blockIdx.x) / gridDim.x);
-  const int u_end = static_cast<int>((static_cast<long>(p.units) * (blockIdx.x + 1)) / gridDim.x);
+  const int n = p.nc ? min(*p.nc, p.n) : p.n;
+  const int units = p.nc ? (p.tpi ? n * p.tpi : (n + p.segs - 1) / p.segs) * p.ntiles : p.units;
+  const int u_begin = static_cast<int>((static_cast<long>(units) * blockIdx.x) / gridDim.x);
+  const int u_end = static_cast<int>((static_cast<long>(units) * (blockIdx.x + 1)) / gridDim.x);
   if (u_begin >= u_end) return;
   const int S = 9 * p.nch;                         // steps per unit
   const int T = (u_end - u_begin) * S;             // steps of this workgroup
@@ -871,7 +889,7 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
       img = mt * p.segs;
       oh0 = 0;
       m0 = img * HW;
-      lim = min(p.segs, p.n - img) * HW;
+      lim = min(p.segs, n - img) * HW;
     }
   };
 
@@ -908,7 +926,7 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
       if (pu < u_end) {
         int m0, lim, n0;
         unit_geom(pu, img, oh0, m0, lim, n0);
-        nimg = p.tpi ? 1 : min(p.segs, p.n - img);
+        nimg = p.tpi ? 1 : min(p.segs, n - img);
       }
       rbase = p.src + (size_t)img * p.H * p.W * p.cin + pc_ * 64;
       rbytes = nimg ? nimg * imgb - pc_ * 128 : 0;
@@ -1280,6 +1298,7 @@ bool conv3_wres(const ConvArgs& a, hipStream_t s) {
   p.PW = g.PW;
   p.NP = g.NP;
   p.tiles = g.mtiles;
+  p.nc = a.ncount;
   const int grid = p.tiles < cus ? p.tiles : cus;
   auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(512), 0, s, p); };
 #define DYCL_W(CIN)                                                     \
@@ -1310,15 +1329,19 @@ bool conv3_halo(const ConvArgs& a, hipStream_t s) {
   if (a.H * a.W <= 128 && 2 * a.H * a.W < (a.H + 2) * (a.W + 2)) return false;
   const int cus = cu_count();
   if (!cus) return false;
+  // the tile shape follows the expected live images; the geometry (and the
+  // grid) is then laid out for all n
+  const int nh = a.nhint > 0 && a.nhint < a.n ? a.nhint : a.n;
   HaloGeom g;
   int bm = 256;
-  if (!halo_geom(a.n, a.H, a.W, 256, halo_cap(256), g) ||
-      4L * a.n * a.H * a.W < 3L * 256 * g.mtiles || (long)g.mtiles * (a.cout / 128) < cus) {
+  if (!halo_geom(nh, a.H, a.W, 256, halo_cap(256), g) ||
+      4L * nh * a.H * a.W < 3L * 256 * g.mtiles || (long)g.mtiles * (a.cout / 128) < cus) {
     bm = 128;
-    if (!halo_geom(a.n, a.H, a.W, 128, halo_cap(128), g)) return false;
+    if (!halo_geom(nh, a.H, a.W, 128, halo_cap(128), g)) return false;
   }
   const int bn = (a.cout % 128 == 0 && conv_cout_pad(a.cout) % 128 == 0 && (long)g.mtiles * (a.cout / 128) >= cus)
                      ? 128 : 64;
+  if (!halo_geom(a.n, a.H, a.W, bm, halo_cap(bm), g)) return false;
   Conv3HP p;
   p.src = a.src;
   p.w = a.w;
@@ -1341,6 +1364,7 @@ bool conv3_halo(const ConvArgs& a, hipStream_t s) {
   p.ntiles = a.cout / bn;
   p.units = g.mtiles * p.ntiles;
   p.nch = a.cin / 64;
+  p.nc = a.ncount;
   const int grid = p.units < cus ? p.units : cus;
   // four compute waves: 128 x 64 (pixels x channels) each for 256-pixel
   // tiles, 64 x BN/2 for 128-pixel tiles; plus four loader waves
@@ -1423,6 +1447,8 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.act = a.act;
   p.out_f32 = a.out_f32;
   p.zeros = a.zeros;
+  p.nc = a.ncount;
+  p.nmax = a.n;
 
   // 16-byte A vectors need Cin % 8 == 0, and a power-of-two Cin when the tap
   // index is split off with a shift; anything else gathers element by element
@@ -1443,12 +1469,14 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
     }
     return;
   }
+  // tile shapes follow the expected live rows (the grid covers all n)
+  const int Mh = (a.nhint > 0 && a.nhint < a.n ? a.nhint : a.n) * a.Ho * a.Wo;
   // the direct-to-LDS kernel stores 8 channels per 16-byte vector
   const bool vec_out = a.cout % 8 == 0 && (reinterpret_cast<uintptr_t>(a.dst) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
   if (vec_out && (conv3_wres(a, s) || conv3_halo(a, s))) return;
   if (vec_out) {
-    const TileCfg c = choose_lds(p.M, a.cout, p.Kp);
+    const TileCfg c = choose_lds(Mh, a.cout, p.Kp);
     p.mt = (p.M + c.bm - 1) / c.bm;
     p.nt = (a.cout + c.bn - 1) / c.bn;
     if (a.k == 1)
@@ -1459,9 +1487,9 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
       dispatch_lds<7>(c, p, s);
     return;
   }
-  const TileCfg c = a.cout >= 128 ? choose(kWide, p.M, a.cout)
-                    : a.cout >= 64 ? choose(kMid, p.M, a.cout)
-                                   : choose(kNarrow, p.M, a.cout);
+  const TileCfg c = a.cout >= 128 ? choose(kWide, Mh, a.cout)
+                    : a.cout >= 64 ? choose(kMid, Mh, a.cout)
+                                   : choose(kNarrow, Mh, a.cout);
   p.mt = (p.M + c.bm - 1) / c.bm;
   p.nt = (a.cout + c.bn - 1) / c.bn;
   if (a.k == 1)

@@ -13,6 +13,10 @@ namespace {
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
 
+// live rows: the device count when there is one (never above the n the
+// launch was sized for), else n
+__device__ __forceinline__ int live(const int32_t* nc, int n) { return nc ? min(*nc, n) : n; }
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -84,10 +88,12 @@ __device__ void row_channel_sums(const uint16_t* __restrict__ x, int p0, int p1,
 
 // ----------------------------------------------------------------- GAP ----
 
-__global__ __launch_bounds__(256) void gap_kernel(const uint16_t* __restrict__ x, int HW, int C, float* G) {
+__global__ __launch_bounds__(256) void gap_kernel(const uint16_t* __restrict__ x, int HW, int C, float* G,
+                                                  const int32_t* nc, int n) {
   __shared__ float part[2048];
   __shared__ float red[2048];
   const int r = blockIdx.x;
+  if (r >= live(nc, n)) return;
   row_channel_sums(x + (size_t)r * HW * C, 0, HW, C, red, part);
   const float inv = 1.0f / static_cast<float>(HW);
   for (int c = threadIdx.x; c < C; c += 256) G[(size_t)r * C + c] = red[c] * inv;
@@ -96,39 +102,43 @@ __global__ __launch_bounds__(256) void gap_kernel(const uint16_t* __restrict__ x
 // a large row's positions split over S workgroups: partial sums
 // P[split][row][C], then a fixed-order sum per (row, channel)
 __global__ __launch_bounds__(256) void gap_split_kernel(const uint16_t* __restrict__ x, int n, int HW, int C, int S,
-                                                        float* __restrict__ P) {
+                                                        float* __restrict__ P, const int32_t* nc) {
   __shared__ float part[2048];
   __shared__ float red[2048];
   const int r = blockIdx.x / S, sp = blockIdx.x - (blockIdx.x / S) * S;
+  if (r >= live(nc, n)) return;
   const int p0 = static_cast<int>(static_cast<long>(HW) * sp / S), p1 = static_cast<int>(static_cast<long>(HW) * (sp + 1) / S);
   row_channel_sums(x + (size_t)r * HW * C, p0, p1, C, red, part);
   for (int c = threadIdx.x; c < C; c += 256) P[((size_t)sp * n + r) * C + c] = red[c];
 }
 
-__global__ void gap_merge_kernel(const float* __restrict__ P, int n, int HW, int C, int S, float* __restrict__ G) {
+__global__ void gap_merge_kernel(const float* __restrict__ P, int n, int HW, int C, int S, float* __restrict__ G,
+                                 const int32_t* nc) {
+  // P is laid out for n rows; only the live ones are summed
   const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= static_cast<size_t>(n) * C) return;
+  if (i >= static_cast<size_t>(live(nc, n)) * C) return;
   float t = 0.f;
   for (int sp = 0; sp < S; ++sp) t += P[(size_t)sp * n * C + i];
   G[i] = t * (1.0f / static_cast<float>(HW));
 }
 
-int gap_splits(int n, int HW) {
-  int S = (2048 + n - 1) / n;        // about 2048 workgroups
-  if (S > HW / 64) S = HW / 64;      // at least 64 positions each
+// splits of a row: a function of HW alone (about 256 positions each), so a
+// row's sum has the same rounding whatever the row count of the launch
+int gap_splits(int HW) {
+  const int S = HW / 256;
   return S < 1 ? 1 : (S > kGapMaxSplit ? kGapMaxSplit : S);
 }
 
-void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, float* P, hipStream_t s) {
-  const int S = P ? gap_splits(n, HW) : 1;
+void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, float* P, hipStream_t s, const int32_t* nc) {
+  const int S = P ? gap_splits(HW) : 1;
   if (S == 1) {
-    hipLaunchKernelGGL(gap_kernel, dim3(n), dim3(256), 0, s, x, HW, C, G);
+    hipLaunchKernelGGL(gap_kernel, dim3(n), dim3(256), 0, s, x, HW, C, G, nc, n);
     return;
   }
-  hipLaunchKernelGGL(gap_split_kernel, dim3(n * S), dim3(256), 0, s, x, n, HW, C, S, P);
+  hipLaunchKernelGGL(gap_split_kernel, dim3(n * S), dim3(256), 0, s, x, n, HW, C, S, P, nc);
   const size_t total = static_cast<size_t>(n) * C;
   hipLaunchKernelGGL(gap_merge_kernel, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, P, n, HW, C, S,
-                     G);
+                     G, nc);
 }
 
 // -------------------------------------------------------------- linear ----
@@ -200,10 +210,16 @@ template <int R, int NW>
 __global__ __launch_bounds__(64 * NW) void linear_t_kernel(const float* __restrict__ X, int n, int K,
                                                            const float* __restrict__ Wt,
                                                            const float* __restrict__ bias, int N, int act,
-                                                           float* __restrict__ Y) {
+                                                           float* __restrict__ Y, const int32_t* nc) {
   __shared__ float red[NW][R][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int col = blockIdx.y * 64 + lane, m0 = blockIdx.x * R;
+  // workgroup = row group * gy + column block: the workgroups of live rows
+  // are dispatched first and the surplus ones (device counts) last
+  const int gy = (N + 63) / 64;
+  const int rg = blockIdx.x / gy;
+  const int col = (blockIdx.x - rg * gy) * 64 + lane, m0 = rg * R;
+  n = live(nc, n);
+  if (m0 >= n) return;
   const int cc = col < N ? col : N - 1;
   const float* xr[R];
 #pragma unroll
@@ -236,15 +252,16 @@ __global__ __launch_bounds__(64 * NW) void linear_t_kernel(const float* __restri
 }
 
 void linear_t_f32(const float* X, int n, int K, const float* Wt, const float* bias, int N, int act, float* Y,
-                  hipStream_t s) {
+                  hipStream_t s, const int32_t* nc, int nhint) {
   const int gy = (N + 63) / 64;
+  const int nh = nhint > 0 && nhint < n ? nhint : n;
   // rows per workgroup: as many as keep >= 256 workgroups in flight
-  if ((long)((n + 7) / 8) * gy >= 256)
-    hipLaunchKernelGGL((linear_t_kernel<8, 8>), dim3((n + 7) / 8, gy), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y);
-  else if ((long)((n + 3) / 4) * gy >= 128)
-    hipLaunchKernelGGL((linear_t_kernel<4, 8>), dim3((n + 3) / 4, gy), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y);
+  if ((long)((nh + 7) / 8) * gy >= 256)
+    hipLaunchKernelGGL((linear_t_kernel<8, 8>), dim3(gy * ((n + 7) / 8)), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y, nc);
+  else if ((long)((nh + 3) / 4) * gy >= 128)
+    hipLaunchKernelGGL((linear_t_kernel<4, 8>), dim3(gy * ((n + 3) / 4)), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y, nc);
   else
-    hipLaunchKernelGGL((linear_t_kernel<1, 8>), dim3(n, gy), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y);
+    hipLaunchKernelGGL((linear_t_kernel<1, 8>), dim3(gy * (n)), dim3(512), 0, s, X, n, K, Wt, bias, N, act, Y, nc);
 }
 
 // --------------------------------------------------------- exit decide ----
@@ -252,8 +269,10 @@ void linear_t_f32(const float* X, int n, int K, const float* Wt, const float* bi
 __global__ __launch_bounds__(64) void exit_decide_kernel(const float* __restrict__ Z, int ncls,
                                                          const float* __restrict__ Tp, float tau, int final_, int head,
                                                          const int32_t* __restrict__ orig, uint8_t* flags,
-                                                         float* __restrict__ logits, int n_out, dycl_record* rec) {
+                                                         float* __restrict__ logits, int n_out, dycl_record* rec,
+                                                         const int32_t* nc, int n) {
   const int r = blockIdx.x, lane = threadIdx.x;
+  if (r >= live(nc, n)) return;
   const float* z = Z + (size_t)r * ncls;
   bool ex = final_ != 0;
   if (!ex) {
@@ -275,9 +294,9 @@ __global__ __launch_bounds__(64) void exit_decide_kernel(const float* __restrict
 }
 
 void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int final_, int head, const int32_t* orig,
-                 uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s) {
+                 uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s, const int32_t* nc) {
   hipLaunchKernelGGL(exit_decide_kernel, dim3(n), dim3(64), 0, s, Z, ncls, T, tau, final_, head, orig, flags,
-                     logits, n_out, rec);
+                     logits, n_out, rec, nc, n);
 }
 
 // ----------------------------------------------------- fused exit head ----
@@ -292,7 +311,7 @@ __global__ __launch_bounds__(256) void exit_head_kernel(const void* __restrict__
                                                         int ncls, const float* __restrict__ Tp, float tau,
                                                         int final_, int head, const int32_t* __restrict__ orig,
                                                         uint8_t* flags, float* __restrict__ logits, int n_out,
-                                                        dycl_record* rec) {
+                                                        dycl_record* rec, const int32_t* nc) {
   // R rows per workgroup: pooled features g [R][C] and logits z [R][ncls]
   // in LDS; the head weights W [ncls][C] are read once per workgroup
   constexpr int RMAX = 8;
@@ -301,7 +320,9 @@ __global__ __launch_bounds__(256) void exit_head_kernel(const void* __restrict__
   float* const g = dyn + 2048;
   float* const z = g + R * C;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  n = live(nc, n);
   const int r0 = blockIdx.x * R, nr = min(R, n - r0);
+  if (nr <= 0) return;
   for (int i = 0; i < nr; ++i) {
     float* gi = g + i * C;
     if constexpr (BF16) {
@@ -377,21 +398,22 @@ __global__ __launch_bounds__(256) void exit_head_kernel(const void* __restrict__
 
 void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* W, const float* bias, int ncls,
                const float* T, float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits,
-               int n_out, dycl_record* rec, hipStream_t s) {
+               int n_out, dycl_record* rec, hipStream_t s, const int32_t* nc, int nhint) {
   // rows per workgroup: one where pooling dominates (a row's pooling reads
   // HW * C elements, its linear C * ncls weights); else enough rows to share
   // the weights, keeping a workgroup for every CU, at most 8, within LDS
-  int R = HW >= ncls ? 1 : n / 256;
+  const int nh = nhint > 0 && nhint < n ? nhint : n;
+  int R = HW >= ncls ? 1 : nh / 256;
   R = R < 1 ? 1 : (R > 8 ? 8 : R);
   while (R > 1 && (R * C > 8 * 2048 || R * ncls > 8 * 1024)) --R;
   const int grid = (n + R - 1) / R;
   const size_t lds = (2048 + static_cast<size_t>(R) * (C + ncls)) * sizeof(float);
   if (bf16)
     hipLaunchKernelGGL(exit_head_kernel<true>, dim3(grid), dim3(256), lds, s, x, n, R, HW, C, W, bias, ncls, T, tau,
-                       final_, head, orig, flags, logits, n_out, rec);
+                       final_, head, orig, flags, logits, n_out, rec, nc);
   else
     hipLaunchKernelGGL(exit_head_kernel<false>, dim3(grid), dim3(256), lds, s, x, n, R, HW, C, W, bias, ncls, T, tau,
-                       final_, head, orig, flags, logits, n_out, rec);
+                       final_, head, orig, flags, logits, n_out, rec, nc);
 }
 
 // ---------------------------------------------------------------- gate ----
@@ -399,11 +421,12 @@ void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* W, c
 __global__ __launch_bounds__(256) void gate_kernel(const uint16_t* __restrict__ x, int HW, int C,
                                                    const float* __restrict__ u, const float* __restrict__ v,
                                                    float thr, int gate, const int32_t* __restrict__ orig,
-                                                   uint8_t* flags, dycl_record* rec) {
+                                                   uint8_t* flags, dycl_record* rec, const int32_t* nc, int n) {
   __shared__ float part[2048];
   __shared__ float red[2048];
   __shared__ float wsum[4];
   const int r = blockIdx.x;
+  if (r >= live(nc, n)) return;
   row_channel_sums(x + (size_t)r * HW * C, 0, HW, C, red, part);
   const float inv = 1.0f / static_cast<float>(HW);
   float d = 0.f;
@@ -424,8 +447,8 @@ __global__ __launch_bounds__(256) void gate_kernel(const uint16_t* __restrict__ 
 }
 
 void gate_head(const uint16_t* x, int n, int HW, int C, const float* u, const float* v, float thr, int gate,
-               const int32_t* orig, uint8_t* flags, dycl_record* rec, hipStream_t s) {
-  hipLaunchKernelGGL(gate_kernel, dim3(n), dim3(256), 0, s, x, HW, C, u, v, thr, gate, orig, flags, rec);
+               const int32_t* orig, uint8_t* flags, dycl_record* rec, hipStream_t s, const int32_t* nc) {
+  hipLaunchKernelGGL(gate_kernel, dim3(n), dim3(256), 0, s, x, HW, C, u, v, thr, gate, orig, flags, rec, nc, n);
 }
 
 // ---------------------------------------------------------------- halt ----
@@ -433,8 +456,9 @@ void gate_head(const uint16_t* x, int n, int HW, int C, const float* u, const fl
 __global__ __launch_bounds__(64) void halt_kernel(const uint16_t* __restrict__ h, int C, const float* __restrict__ w,
                                                   const float* __restrict__ aux, const int32_t* __restrict__ orig,
                                                   float* S, int step, int max_steps, float tau, uint8_t* flags,
-                                                  dycl_record* rec) {
+                                                  dycl_record* rec, const int32_t* nc, int n) {
   const int r = blockIdx.x, lane = threadIdx.x;
+  if (r >= live(nc, n)) return;
   const uint16_t* row = h + (size_t)r * C;
   float d = 0.f;
   for (int c = lane * 8; c < C; c += 64 * 8) {
@@ -461,8 +485,10 @@ __global__ __launch_bounds__(64) void halt_kernel(const uint16_t* __restrict__ h
 }
 
 void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux, const int32_t* orig, float* S,
-               int step, int max_steps, float tau, uint8_t* flags, dycl_record* rec, hipStream_t s) {
-  hipLaunchKernelGGL(halt_kernel, dim3(n), dim3(64), 0, s, h, C, w, aux, orig, S, step, max_steps, tau, flags, rec);
+               int step, int max_steps, float tau, uint8_t* flags, dycl_record* rec, hipStream_t s,
+               const int32_t* nc) {
+  hipLaunchKernelGGL(halt_kernel, dim3(n), dim3(64), 0, s, h, C, w, aux, orig, S, step, max_steps, tau, flags, rec,
+                     nc, n);
 }
 
 // ---------------------------------------------------------- compaction ----
@@ -473,9 +499,11 @@ void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux
 
 __global__ __launch_bounds__(1024) void compact_kernel(const uint8_t* __restrict__ flags,
                                                        const int32_t* __restrict__ orig, int n, int32_t* idx1,
-                                                       int32_t* org1, int32_t* idx0, int32_t* org0, int32_t* counts) {
+                                                       int32_t* org1, int32_t* idx0, int32_t* org0, int32_t* counts,
+                                                       const int32_t* nc) {
   __shared__ int wc1[16], wc0[16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  n = live(nc, n);
   int base1 = 0, base0 = 0;
   for (int start = 0; start < n; start += 1024) {
     const int i = start + tid;
@@ -523,8 +551,8 @@ __global__ __launch_bounds__(1024) void compact_kernel(const uint8_t* __restrict
 }
 
 void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, int32_t* org1, int32_t* idx0,
-             int32_t* org0, int32_t* counts, hipStream_t s) {
-  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, flags, orig, n, idx1, org1, idx0, org0, counts);
+             int32_t* org0, int32_t* counts, hipStream_t s, const int32_t* nc) {
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, flags, orig, n, idx1, org1, idx0, org0, counts, nc);
 }
 
 // ------------------------------------------------- large-n compaction ----
@@ -563,8 +591,9 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
 }
 
 __global__ __launch_bounds__(256) void compact_count_kernel(const uint8_t* __restrict__ flags, size_t n,
-                                                            int32_t* __restrict__ bcount) {
+                                                            int32_t* __restrict__ bcount, const int32_t* nc) {
   __shared__ int ws[4];
+  if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
   uint8_t v[16];
   const size_t i0 = static_cast<size_t>(blockIdx.x) * kCompactBlock + threadIdx.x * 16;
   int c = i0 < n ? flag_count16(flags, i0, n, v) : 0;
@@ -575,9 +604,11 @@ __global__ __launch_bounds__(256) void compact_count_kernel(const uint8_t* __res
 }
 
 __global__ __launch_bounds__(1024) void compact_scan_kernel(const int32_t* __restrict__ bcount, int nb, size_t n,
-                                                            int64_t* __restrict__ boff, int32_t* counts) {
+                                                            int64_t* __restrict__ boff, int32_t* counts,
+                                                            const int32_t* nc) {
   __shared__ int64_t ws[16];
   __shared__ int64_t carry;
+  if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
   if (threadIdx.x == 0) carry = 0;
   __syncthreads();
   for (int b0 = 0; b0 < nb; b0 += 1024) {
@@ -602,7 +633,8 @@ __global__ __launch_bounds__(1024) void compact_scan_kernel(const int32_t* __res
 __global__ __launch_bounds__(256) void compact_write_kernel(const uint8_t* __restrict__ flags,
                                                             const int32_t* __restrict__ orig, size_t n,
                                                             const int64_t* __restrict__ boff, int32_t* idx1,
-                                                            int32_t* org1, int32_t* idx0, int32_t* org0) {
+                                                            int32_t* org1, int32_t* idx0, int32_t* org0,
+                                                            const int32_t* nc) {
   // 4 rounds of 1024 consecutive flags, 4 per lane (one 32-bit load): the
   // lanes' counts are prefix-summed by shuffles within the wave and through
   // LDS across the 4 waves; each lane then writes its elements to
@@ -610,6 +642,8 @@ __global__ __launch_bounds__(256) void compact_write_kernel(const uint8_t* __res
   __shared__ int wc1[4], wc0[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t blk0 = static_cast<size_t>(blockIdx.x) * kCompactBlock;
+  if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
+  if (blk0 >= n) return;
   int64_t base1 = boff[blockIdx.x];
   int64_t base0 = static_cast<int64_t>(blk0) - base1;
   for (int rd = 0; rd < kCompactBlock / 1024; ++rd) {
@@ -685,73 +719,95 @@ size_t compact_workspace(size_t n) {
 }
 
 void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t* idx1, int32_t* org1, int32_t* idx0,
-                   int32_t* org0, int32_t* counts, void* workspace, hipStream_t s) {
+                   int32_t* org0, int32_t* counts, void* workspace, hipStream_t s, const int32_t* nc) {
   const int nb = static_cast<int>((n + kCompactBlock - 1) / kCompactBlock);
   int64_t* boff = static_cast<int64_t*>(workspace);
   int32_t* bcount = reinterpret_cast<int32_t*>(boff + nb);
-  hipLaunchKernelGGL(compact_count_kernel, dim3(nb), dim3(256), 0, s, flags, n, bcount);
-  hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, s, bcount, nb, n, boff, counts);
-  hipLaunchKernelGGL(compact_write_kernel, dim3(nb), dim3(256), 0, s, flags, orig, n, boff, idx1, org1, idx0, org0);
+  hipLaunchKernelGGL(compact_count_kernel, dim3(nb), dim3(256), 0, s, flags, n, bcount, nc);
+  hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, s, bcount, nb, n, boff, counts, nc);
+  hipLaunchKernelGGL(compact_write_kernel, dim3(nb), dim3(256), 0, s, flags, orig, n, boff, idx1, org1, idx0, org0,
+                     nc);
 }
 
 // ------------------------------------------------------------ row moves ---
 
+// Work item w = row * chunks + chunk (chunk: 1024 16-byte vectors of a row),
+// taken by workgroups in a grid-stride loop over the live rows' items: the
+// first workgroups take the live rows, surplus ones (device counts) leave.
+constexpr size_t kMoveMaxGrid = size_t(1) << 20;
+
 __global__ __launch_bounds__(256) void move_rows_kernel(uint4* __restrict__ dst, const int32_t* __restrict__ dst_idx,
                                                         const uint4* __restrict__ src,
-                                                        const int32_t* __restrict__ src_idx, size_t vpr) {
-  const int r = blockIdx.x;
-  const size_t d = dst_idx ? static_cast<size_t>(dst_idx[r]) : static_cast<size_t>(r);
-  const size_t s = src_idx ? static_cast<size_t>(src_idx[r]) : static_cast<size_t>(r);
-  const uint4* sp = src + s * vpr;
-  uint4* dp = dst + d * vpr;
-  const size_t v0 = static_cast<size_t>(blockIdx.y) * 1024 + threadIdx.x;
+                                                        const int32_t* __restrict__ src_idx, size_t vpr,
+                                                        const int32_t* nc, int n) {
+  const size_t chunks = (vpr + 1023) / 1024;
+  const size_t items = chunks * static_cast<size_t>(live(nc, n));
+  for (size_t w = blockIdx.x; w < items; w += gridDim.x) {
+    const size_t r = w / chunks;
+    const size_t d = dst_idx ? static_cast<size_t>(dst_idx[r]) : r;
+    const size_t sr = src_idx ? static_cast<size_t>(src_idx[r]) : r;
+    const uint4* sp = src + sr * vpr;
+    uint4* dp = dst + d * vpr;
+    const size_t v0 = (w - r * chunks) * 1024 + threadIdx.x;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const size_t v = v0 + static_cast<size_t>(j) * 256;
-    if (v < vpr) dp[v] = sp[v];
+    for (int j = 0; j < 4; ++j) {
+      const size_t v = v0 + static_cast<size_t>(j) * 256;
+      if (v < vpr) dp[v] = sp[v];
+    }
   }
 }
 
-// several tensors moved with the same index list in one launch (blockIdx.z
-// selects the tensor)
+// several tensors moved with the same index lists in one launch: work item
+// w = (row * count + tensor) * chunks + chunk
 __global__ __launch_bounds__(256) void move_rows_multi_kernel(MoveSet set, const int32_t* __restrict__ dst_idx,
-                                                              const int32_t* __restrict__ src_idx) {
-  const int t = blockIdx.z;
-  const size_t vpr = set.vpr[t];
-  const size_t v0 = static_cast<size_t>(blockIdx.y) * 1024 + threadIdx.x;
-  if (v0 >= vpr) return;
-  const int r = blockIdx.x;
-  const size_t d = dst_idx ? static_cast<size_t>(dst_idx[r]) : static_cast<size_t>(r);
-  const size_t sr = src_idx ? static_cast<size_t>(src_idx[r]) : static_cast<size_t>(r);
-  const uint4* sp = static_cast<const uint4*>(set.src[t]) + sr * vpr;
-  uint4* dp = static_cast<uint4*>(set.dst[t]) + d * vpr;
+                                                              const int32_t* __restrict__ src_idx, int chunks,
+                                                              const int32_t* nc, int n) {
+  const size_t items = static_cast<size_t>(live(nc, n)) * set.count * chunks;
+  for (size_t w = blockIdx.x; w < items; w += gridDim.x) {
+    const size_t rt = w / chunks;
+    const size_t r = rt / set.count;
+    const int t = static_cast<int>(rt - r * set.count);
+    const size_t vpr = set.vpr[t];
+    const size_t v0 = (w - rt * chunks) * 1024 + threadIdx.x;
+    if (v0 >= vpr) continue;
+    const size_t d = dst_idx ? static_cast<size_t>(dst_idx[r]) : r;
+    const size_t sr = src_idx ? static_cast<size_t>(src_idx[r]) : r;
+    const uint4* sp = static_cast<const uint4*>(set.src[t]) + sr * vpr;
+    uint4* dp = static_cast<uint4*>(set.dst[t]) + d * vpr;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const size_t v = v0 + static_cast<size_t>(j) * 256;
-    if (v < vpr) dp[v] = sp[v];
+    for (int j = 0; j < 4; ++j) {
+      const size_t v = v0 + static_cast<size_t>(j) * 256;
+      if (v < vpr) dp[v] = sp[v];
+    }
   }
 }
 
-void move_rows_multi(const MoveSet& set, const int32_t* dst_idx, const int32_t* src_idx, int n, hipStream_t s) {
+void move_rows_multi(const MoveSet& set, const int32_t* dst_idx, const int32_t* src_idx, int n, hipStream_t s,
+                     const int32_t* nc) {
   size_t maxv = 0;
   for (int t = 0; t < set.count; ++t) maxv = set.vpr[t] > maxv ? set.vpr[t] : maxv;
-  dim3 grid(n, static_cast<unsigned>((maxv + 1023) / 1024), set.count);
-  hipLaunchKernelGGL(move_rows_multi_kernel, grid, dim3(256), 0, s, set, dst_idx, src_idx);
+  const int chunks = static_cast<int>((maxv + 1023) / 1024);
+  const size_t items = static_cast<size_t>(n) * set.count * chunks;
+  const dim3 grid(static_cast<unsigned>(items < kMoveMaxGrid ? items : kMoveMaxGrid));
+  hipLaunchKernelGGL(move_rows_multi_kernel, grid, dim3(256), 0, s, set, dst_idx, src_idx, chunks, nc, n);
 }
 
 void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,
-               hipStream_t s) {
+               hipStream_t s, const int32_t* nc) {
   const size_t vpr = row_bytes / 16;
-  dim3 grid(n, static_cast<unsigned>((vpr + 1023) / 1024));
+  const size_t items = (vpr + 1023) / 1024 * static_cast<size_t>(n);
+  const dim3 grid(static_cast<unsigned>(items < kMoveMaxGrid ? items : kMoveMaxGrid));
   hipLaunchKernelGGL(move_rows_kernel, grid, dim3(256), 0, s, static_cast<uint4*>(dst), dst_idx,
-                     static_cast<const uint4*>(src), src_idx, vpr);
+                     static_cast<const uint4*>(src), src_idx, vpr, nc, n);
 }
 
 // ------------------------------------------------------------- maxpool ----
 
 __global__ __launch_bounds__(256) void maxpool_kernel(const uint16_t* __restrict__ x, int H, int W, int C, int Ho,
-                                                      int Wo, uint16_t* __restrict__ y, size_t total) {
+                                                      int Wo, uint16_t* __restrict__ y, size_t total,
+                                                      const int32_t* nc, int n) {
   const size_t t = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;   // one 8-channel vector
+  if (nc) total = total / n * live(nc, n);   // the vectors of the live images
   if (t >= total) return;
   const int C8 = C >> 3;
   const int cv = static_cast<int>(t % C8);
@@ -786,11 +842,11 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const uint16_t* __restrict
   *reinterpret_cast<uint4*>(y + t * 8) = o;
 }
 
-void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s) {
+void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s, const int32_t* nc) {
   const int Ho = (H + 2 - 3) / 2 + 1, Wo = (W + 2 - 3) / 2 + 1;
   const size_t total = static_cast<size_t>(n) * Ho * Wo * (C / 8);
   hipLaunchKernelGGL(maxpool_kernel, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, x, H, W, C,
-                     Ho, Wo, y, total);
+                     Ho, Wo, y, total, nc, n);
 }
 
 // ---------------------------------------------------- stem input padding ----
@@ -816,6 +872,17 @@ void pad_channels_bf16(const uint16_t* x, size_t pixels, int cin, int cout, uint
 }
 
 // --------------------------------------------------------------- small ----
+
+__global__ void final_counts_kernel(const int32_t* nc, int n, int32_t* counts) {
+  if (threadIdx.x == 0) {
+    counts[0] = live(nc, n);
+    counts[1] = 0;
+  }
+}
+
+void final_counts(const int32_t* nc, int n, int32_t* counts, hipStream_t s) {
+  hipLaunchKernelGGL(final_counts_kernel, dim3(1), dim3(64), 0, s, nc, n, counts);
+}
 
 __global__ void init_records_kernel(dycl_record* rec, int n) {
   const int i = blockIdx.x * 256 + threadIdx.x;

@@ -1,6 +1,15 @@
 // Host-side launchers of the gfx950 kernels.  Every launcher checks nothing
 // about shapes: the plan builder validates them before any launch, and each
 // launcher is called only with n >= 1 rows.
+//
+// Row counts on the device: the launchers whose work scales with the row
+// count take `nc`, a device pointer to the live count.  With nc null the
+// kernels process n rows; otherwise the launch is sized for n rows (an
+// upper bound the host knows) and the kernels read the count when they
+// start and process min(*nc, n) rows (possibly none), so the host never has
+// to wait for a count to launch the next kernel.  `nhint`, where taken, is
+// the live count the host expects (0: n): it only picks the tile shape or
+// rows per workgroup, which change no result.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -35,6 +44,8 @@ struct ConvArgs {
   void* dst;             // [n, Ho, Wo, cout] bf16, or fp32 when out_f32
   int out_f32;
   const uint16_t* zeros; // >= 16 zero bytes on the device (padding taps)
+  const int32_t* ncount = nullptr;  // device count of live images (<= n) or null
+  int nhint = 0;                    // expected live images for the tile choice (0: n)
 };
 void conv_bf16(const ConvArgs& a, hipStream_t s);
 
@@ -45,7 +56,7 @@ const uint16_t* zero_page();
 // Y[m, j] = act(sum_k X[m, k] Wt[k, j] + bias[j]), fp32, weights transposed;
 // for few rows (MLP layers, exit heads)
 void linear_t_f32(const float* X, int n, int K, const float* Wt, const float* bias, int N, int act, float* Y,
-                  hipStream_t s);
+                  hipStream_t s, const int32_t* nc = nullptr, int nhint = 0);
 
 // Y[m, j] = act(sum_k X[m, k] W[j, k] + bias[j]), fp32
 void linear_f32(const float* X, int n, int K, const float* W, const float* bias, int N, int act, float* Y,
@@ -53,15 +64,18 @@ void linear_f32(const float* X, int n, int K, const float* W, const float* bias,
 
 // G[r, c] = sum_{hw} x[r, hw, c] / HW.  With a workspace P of
 // kGapMaxSplit * n * C floats, long rows are split over several workgroups
-// (partial sums, then a fixed-order merge); P may be null.
+// (partial sums, then a fixed-order merge; the split depends on HW only);
+// P may be null.
 constexpr int kGapMaxSplit = 16;
-void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, float* P, hipStream_t s);
+void gap_bf16(const uint16_t* x, int n, int HW, int C, float* G, float* P, hipStream_t s,
+              const int32_t* nc = nullptr);
 
 // Exit decision from head logits Z [n, ncls]: p = max softmax(Z / T); rows
 // with p >= tau (or all rows when final) write their logits and exit index at
 // their original position.
 void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int final_, int head,
-                 const int32_t* orig, uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s);
+                 const int32_t* orig, uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s,
+                 const int32_t* nc = nullptr);
 
 // Fused exit head for small heads (C <= 2048 and a multiple of 4, ncls <=
 // 1024): pooling, head linear on the weights as stored W [ncls][C] (16-byte
@@ -69,35 +83,36 @@ void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int
 // outputs as gap_bf16 + linear_t_f32 + exit_decide.
 void exit_head(const void* x, bool bf16, int n, int HW, int C, const float* W, const float* bias, int ncls,
                const float* T, float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits,
-               int n_out, dycl_record* rec, hipStream_t s);
+               int n_out, dycl_record* rec, hipStream_t s, const int32_t* nc = nullptr, int nhint = 0);
 
 // Gate: q = sigmoid(u . GAP(x) + v); flag = q > thr (execute); skipped rows set
 // bit `gate` of their record.
 void gate_head(const uint16_t* x, int n, int HW, int C, const float* u, const float* v, float thr, int gate,
-               const int32_t* orig, uint8_t* flags, dycl_record* rec, hipStream_t s);
+               const int32_t* orig, uint8_t* flags, dycl_record* rec, hipStream_t s, const int32_t* nc = nullptr);
 
 // Halting unit of step `step`: p = sigmoid(w . h + aux[orig]); S[orig] += p;
 // flag = S >= tau or step == max_steps (halt); halted rows record step.
 void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux, const int32_t* orig, float* S,
-               int step, int max_steps, float tau, uint8_t* flags, dycl_record* rec, hipStream_t s);
+               int step, int max_steps, float tau, uint8_t* flags, dycl_record* rec, hipStream_t s,
+               const int32_t* nc = nullptr);
 
 // Stable two-way partition of rows 0..n-1 by flag: idx1/org1 list the rows
 // (and their original ids) with flag != 0, idx0/org0 the others, in order;
 // counts[0] = |flag != 0|, counts[1] = the rest.
 void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, int32_t* org1, int32_t* idx0,
-             int32_t* org0, int32_t* counts, hipStream_t s);
+             int32_t* org0, int32_t* counts, hipStream_t s, const int32_t* nc = nullptr);
 
 // The same partition for large n (reduce-then-scan over 4096-flag blocks);
 // org1 / org0 may be null.  workspace: compact_workspace(n) bytes, 8-byte
 // aligned.  n < 2^31.
 size_t compact_workspace(size_t n);
 void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t* idx1, int32_t* org1, int32_t* idx0,
-                   int32_t* org0, int32_t* counts, void* workspace, hipStream_t s);
+                   int32_t* org0, int32_t* counts, void* workspace, hipStream_t s, const int32_t* nc = nullptr);
 
 // dst row (dst_idx ? dst_idx[r] : r) = src row (src_idx ? src_idx[r] : r),
 // r < n; row_bytes is a multiple of 16.
 void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,
-               hipStream_t s);
+               hipStream_t s, const int32_t* nc = nullptr);
 
 // y[p, c] = c < cin ? x[p, c] : 0 for every pixel p, c < cout (cout == 8)
 void pad_channels_bf16(const uint16_t* x, size_t pixels, int cin, int cout, uint16_t* y, hipStream_t s);
@@ -109,9 +124,14 @@ struct MoveSet {
   const void* src[4];
   size_t vpr[4];   // 16-byte vectors per row
 };
-void move_rows_multi(const MoveSet& set, const int32_t* dst_idx, const int32_t* src_idx, int n, hipStream_t s);
+void move_rows_multi(const MoveSet& set, const int32_t* dst_idx, const int32_t* src_idx, int n, hipStream_t s,
+                     const int32_t* nc = nullptr);
 
-void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s);
+void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y, hipStream_t s,
+                     const int32_t* nc = nullptr);
+// counts[0] = *nc (or n when nc is null), counts[1] = 0: the branch counts of
+// a final exit, which every row takes
+void final_counts(const int32_t* nc, int n, int32_t* counts, hipStream_t s);
 void init_records(dycl_record* rec, int n, hipStream_t s);
 void fill_f32(float* p, float v, int n, hipStream_t s);
 void iota_i32(int32_t* p, int n, hipStream_t s);

@@ -163,6 +163,12 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
               "hipHostMalloc");
     p->h_counts = static_cast<int32_t*>(ptr);
     std::memset(p->h_counts, 0, sizeof(int32_t) * 2 * std::max(1, sp.decisions));
+    ptr = nullptr;
+    hip_check(hipHostMalloc(&ptr, sizeof(int32_t) * 2 * std::max(1, sp.decisions), hipHostMallocDefault),
+              "hipHostMalloc");
+    p->h_hint_stage = static_cast<int32_t*>(ptr);
+    p->hint.assign(2 * std::max(1, sp.decisions), 0);
+    hip_check(hipEventCreateWithFlags(&p->hint_ev, hipEventDisableTiming), "hipEventCreate");
   }
   k::iota_i32(p->d_iota, B, nullptr);
   hip_check(hipGetLastError(), "iota launch");
@@ -183,6 +189,12 @@ void plan_free(dycl_plan* p) {
   }
   for (hipEvent_t e : p->ev_free) hipEventDestroy(e);
   p->ev_free.clear();
+  if (p->graph_exec) hipGraphExecDestroy(p->graph_exec);
+  if (p->graph) hipGraphDestroy(p->graph);
+  if (p->cap_stream) hipStreamDestroy(p->cap_stream);
+  p->graph_exec = nullptr;
+  p->graph = nullptr;
+  p->cap_stream = nullptr;
   for (Packed& q : p->spec.packed)
     if (q.dev) hipFree(q.dev);
   for (float* h : p->head_t)
@@ -195,11 +207,26 @@ void plan_free(dycl_plan* p) {
   for (void* s : singles)
     if (s) hipFree(s);
   if (p->h_counts) hipHostFree(p->h_counts);
+  if (p->hint_ev) hipEventSynchronize(p->hint_ev);
+  if (p->h_hint_stage) hipHostFree(p->h_hint_stage);
+  if (p->hint_ev) hipEventDestroy(p->hint_ev);
+  p->h_counts = nullptr;
+  p->h_hint_stage = nullptr;
+  p->hint_ev = nullptr;
 }
 
 // ------------------------------------------------------------------ run ---
 
 namespace {
+
+// The rows a node runs on: n rows exactly (nc null, sync mode), or at most n
+// rows whose live count the kernels read from nc (device modes); `hint` is
+// the live count expected (tile shapes only).
+struct Rows {
+  int n;
+  const int32_t* nc;
+  int hint;
+};
 
 struct Run {
   dycl_plan* p;
@@ -208,6 +235,7 @@ struct Run {
   float* logits;
   dycl_record* rec;
   int B;
+  bool device;               // counts stay on the device
   std::vector<void*> tp;     // tensor pointers
   const int32_t* orig;       // original ids of the current rows
   int orig_next = 0;         // which d_orig buffer the next compaction fills
@@ -240,34 +268,46 @@ struct Run {
 
   const float* f32(int64_t off) const { return off < 0 ? nullptr : reinterpret_cast<const float*>(p->d_blob + off); }
 
-  // wait for the branch counts of decision d (the only device->host read)
-  void read_counts(int d) {
-    hip_check(hipMemcpyAsync(p->h_counts + 2 * d, p->d_counts + 2 * d, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s),
+  // Partition the rows by flag at decision d.  Sync mode waits for the two
+  // counts (the only device->host read); device mode leaves them in
+  // d_counts and returns the rows of each branch as bounded by `r`.
+  void compact(Rows r, int d, int32_t* org0, Rows& ones, Rows& zeros) {
+    int32_t* cnt = p->d_counts + 2 * d;
+    launch(P_COMPACT, 0, r.n * (1.0 + 4.0 + 16.0), [&] {
+      if (r.n <= 16384)
+        k::compact(p->d_flags, orig, r.n, p->d_idx1, p->d_org1, p->d_idx0, org0, cnt, s, r.nc);
+      else
+        k::compact_large(p->d_flags, orig, r.n, p->d_idx1, p->d_org1, p->d_idx0, org0, cnt, p->d_cws, s, r.nc);
+    });
+    if (device) {
+      ones = {r.n, cnt, expected(2 * d, r.n)};
+      zeros = {r.n, cnt + 1, expected(2 * d + 1, r.n)};
+      return;
+    }
+    hip_check(hipMemcpyAsync(p->h_counts + 2 * d, cnt, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s),
               "count readback");
     hip_check(hipStreamSynchronize(s), "count readback sync");
+    ones = {p->h_counts[2 * d], nullptr, p->h_counts[2 * d]};
+    zeros = {p->h_counts[2 * d + 1], nullptr, p->h_counts[2 * d + 1]};
   }
 
-  void compact(int n, int d, int32_t* org0) {
-    const Spec& sp = p->spec;
-    (void)sp;
-    launch(P_COMPACT, 0, n * (1.0 + 4.0 + 16.0), [&] {
-      if (n <= 16384)
-        k::compact(p->d_flags, orig, n, p->d_idx1, p->d_org1, p->d_idx0, org0, p->d_counts + 2 * d, s);
-      else
-        k::compact_large(p->d_flags, orig, n, p->d_idx1, p->d_org1, p->d_idx0, org0, p->d_counts + 2 * d, p->d_cws, s);
-    });
-    read_counts(d);
+  // expected count of branch i: an earlier run's, scaled to this batch,
+  // within [1, bound]; the bound when there is none
+  int expected(int i, int bound) const {
+    if (!p->hint_B) return bound;
+    const long e = (static_cast<long>(p->hint[i]) * B + p->hint_B - 1) / p->hint_B;
+    return static_cast<int>(std::max(1L, std::min<long>(e, bound)));
   }
 
-  void move(int cls, void* dst, const int32_t* didx, const void* src, const int32_t* sidx, size_t rb, int n) {
-    if (n <= 0) return;
-    launch(cls, 0, 2.0 * rb * n + 4.0 * n, [&] { k::move_rows(dst, didx, src, sidx, rb, n, s); });
+  void move(int cls, void* dst, const int32_t* didx, const void* src, const int32_t* sidx, size_t rb, Rows r) {
+    if (r.n <= 0) return;
+    launch(cls, 0, 2.0 * rb * r.n + 4.0 * r.n, [&] { k::move_rows(dst, didx, src, sidx, rb, r.n, s, r.nc); });
   }
 
   // every (from, to) tensor pair moved with the same index lists (row r of
   // `to` at didx[r] <- row sidx[r] of `from`; null = identity), four per launch
-  void move_pairs(const std::vector<std::pair<int, int>>& pairs, const int32_t* didx, const int32_t* sidx, int n) {
-    if (n <= 0 || pairs.empty()) return;
+  void move_pairs(const std::vector<std::pair<int, int>>& pairs, const int32_t* didx, const int32_t* sidx, Rows r) {
+    if (r.n <= 0 || pairs.empty()) return;
     const Spec& sp = p->spec;
     for (size_t i = 0; i < pairs.size(); i += 4) {
       k::MoveSet set{};
@@ -279,14 +319,15 @@ struct Run {
         set.dst[set.count] = tp[to];
         set.vpr[set.count] = rb / 16;
         ++set.count;
-        bytes += 2.0 * rb * n + 4.0 * n;
+        bytes += 2.0 * rb * r.n + 4.0 * r.n;
       }
-      launch(P_MOVE, 0, bytes, [&] { k::move_rows_multi(set, didx, sidx, n, s); });
+      launch(P_MOVE, 0, bytes, [&] { k::move_rows_multi(set, didx, sidx, r.n, s, r.nc); });
     }
   }
 
-  void conv(const Node& nd, int n) {
+  void conv(const Node& nd, Rows r) {
     const Spec& sp = p->spec;
+    const int n = r.n;
     const Packed* q = nd.packed >= 0 ? &sp.packed[nd.packed] : nullptr;
     const int cin = nd.cin1 + nd.cin2;
     const double M = static_cast<double>(n) * nd.Ho * nd.Wo;
@@ -295,7 +336,7 @@ struct Run {
       const double bytes = 4.0 * (static_cast<double>(n) * (cin + nd.cout) + static_cast<double>(nd.cout) * cin);
       launch(P_LINEAR32, flops, bytes, [&] {
         k::linear_t_f32(static_cast<const float*>(tp[nd.src]), n, cin, p->head_t[nd.head_t], f32(nd.shift_off),
-                        nd.cout, nd.act, static_cast<float*>(tp[nd.dst]), s);
+                        nd.cout, nd.act, static_cast<float*>(tp[nd.dst]), s, r.nc, r.hint);
       });
       return;
     }
@@ -323,24 +364,27 @@ struct Run {
     a.dst = tp[nd.dst];
     a.out_f32 = 0;
     a.zeros = p->d_zeros;
+    a.ncount = r.nc;
+    a.nhint = r.hint;
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
                                 static_cast<double>(nd.cout) * nd.k * nd.k * cin);
     launch(P_CONV, flops, bytes, [&] { k::conv_bf16(a, s); });
   }
 
-  void exec(const std::vector<Node>& nodes, int& n) {
+  void exec(const std::vector<Node>& nodes, Rows& rows) {
     Spec& sp = p->spec;
     for (const Node& nd : nodes) {
+      const int n = rows.n;
       switch (nd.kind) {
         case NodeKind::Conv:
-          if (n > 0) conv(nd, n);
+          if (n > 0) conv(nd, rows);
           break;
         case NodeKind::MaxPool:
           if (n > 0) {
             const TensorInfo& t = sp.tensors[nd.src];
             launch(P_POOL, 0, 2.0 * n * (t.H * t.W + nd.Ho * nd.Wo) * t.C, [&] {
               k::maxpool3s2_bf16(static_cast<const uint16_t*>(tp[nd.src]), n, t.H, t.W, t.C,
-                                 static_cast<uint16_t*>(tp[nd.dst]), s);
+                                 static_cast<uint16_t*>(tp[nd.dst]), s, rows.nc);
             });
           }
           break;
@@ -353,36 +397,41 @@ struct Run {
             launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, esz * n * HW * nd.hc + 4.0 * nd.ncls * (nd.hc + 1), [&] {
               k::exit_head(tp[nd.src], sp.dt == DType::BF16, n, HW, nd.hc, f32(nd.h_w), f32(nd.h_b),
                            nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags, logits,
-                           sp.n_out, rec, s);
+                           sp.n_out, rec, s, rows.nc, rows.hint);
             });
           } else if (sp.dt == DType::BF16) {
             launch(P_HEAD, 0, 2.0 * n * HW * nd.hc + 4.0 * n * nd.hc, [&] {
-              k::gap_bf16(static_cast<const uint16_t*>(tp[nd.src]), n, HW, nd.hc, p->d_G, p->d_Gpart, s);
+              k::gap_bf16(static_cast<const uint16_t*>(tp[nd.src]), n, HW, nd.hc, p->d_G, p->d_Gpart, s, rows.nc);
             });
             G = p->d_G;
           }
           if (!nd.fused) {
             launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, 4.0 * (n * (nd.hc + nd.ncls) + nd.ncls * nd.hc), [&] {
-              k::linear_t_f32(G, n, nd.hc, p->head_t[nd.head_t], f32(nd.h_b), nd.ncls, k::ACT_NONE, p->d_Z, s);
+              k::linear_t_f32(G, n, nd.hc, p->head_t[nd.head_t], f32(nd.h_b), nd.ncls, k::ACT_NONE, p->d_Z, s,
+                              rows.nc, rows.hint);
             });
             launch(P_HEAD, 0, 4.0 * n * nd.ncls * 2, [&] {
               k::exit_decide(p->d_Z, n, nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags,
-                             logits, sp.n_out, rec, s);
+                             logits, sp.n_out, rec, s, rows.nc);
             });
           }
           if (nd.final_) {
-            p->h_counts[2 * nd.decision] = n;
-            p->h_counts[2 * nd.decision + 1] = 0;
-            n = 0;
+            if (device) {
+              launch(P_MISC, 0, 8.0, [&] { k::final_counts(rows.nc, n, p->d_counts + 2 * nd.decision, s); });
+            } else {
+              p->h_counts[2 * nd.decision] = n;
+              p->h_counts[2 * nd.decision + 1] = 0;
+            }
+            rows = {0, nullptr, 0};
             break;
           }
           int32_t* next = p->d_orig[orig_next];
-          compact(n, nd.decision, next);
-          const int stay = p->h_counts[2 * nd.decision + 1];
+          Rows gone, stay;
+          compact(rows, nd.decision, next, gone, stay);
           move_pairs(nd.pairs, nullptr, p->d_idx0, stay);
           orig = next;
           orig_next ^= 1;
-          n = stay;
+          rows = stay;
           break;
         }
         case NodeKind::Gate: {
@@ -390,15 +439,15 @@ struct Run {
           const int HW = nd.H * nd.W;
           launch(P_HEAD, 2.0 * n * nd.hc, 2.0 * n * HW * nd.hc, [&] {
             k::gate_head(static_cast<const uint16_t*>(tp[nd.src]), n, HW, nd.hc, f32(nd.h_w), f32(nd.h_b), nd.tau,
-                         nd.index, orig, p->d_flags, rec, s);
+                         nd.index, orig, p->d_flags, rec, s, rows.nc);
           });
-          compact(n, nd.decision, p->d_org0);
-          int ne = p->h_counts[2 * nd.decision];
-          if (ne > 0) {
-            move_pairs(nd.pairs, nullptr, p->d_idx1, ne);     // gather the executing rows
-            int nb = ne;
-            exec(nd.body, nb);
-            move_pairs(nd.scatter, p->d_idx1, nullptr, ne);   // scatter the block outputs back
+          Rows run, skip;
+          compact(rows, nd.decision, p->d_org0, run, skip);
+          if (run.n > 0) {
+            move_pairs(nd.pairs, nullptr, p->d_idx1, run);     // gather the executing rows
+            Rows body = run;
+            exec(nd.body, body);
+            move_pairs(nd.scatter, p->d_idx1, nullptr, run);   // scatter the block outputs back
           }
           break;
         }
@@ -406,17 +455,17 @@ struct Run {
           if (n <= 0) break;
           launch(P_HEAD, 2.0 * n * nd.hc, 2.0 * n * nd.hc, [&] {
             k::halt_head(static_cast<const uint16_t*>(tp[nd.src]), n, nd.hc, f32(nd.h_w), aux, orig, p->d_S, nd.index,
-                         nd.max_steps, nd.tau, p->d_flags, rec, s);
+                         nd.max_steps, nd.tau, p->d_flags, rec, s, rows.nc);
           });
           int32_t* next = p->d_orig[orig_next];
-          compact(n, nd.decision, next);
-          const int nh = p->h_counts[2 * nd.decision], stay = p->h_counts[2 * nd.decision + 1];
+          Rows halted, stay;
+          compact(rows, nd.decision, next, halted, stay);
           move(P_MOVE, tp[nd.park_dst], p->d_org1, tp[nd.park_src], p->d_idx1,
-               sp.tensors[nd.park_src].row_bytes(sp.dt), nh);
+               sp.tensors[nd.park_src].row_bytes(sp.dt), halted);
           move_pairs(nd.pairs, nullptr, p->d_idx0, stay);
           orig = next;
           orig_next ^= 1;
-          n = stay;
+          rows = stay;
           break;
         }
         case NodeKind::Output: {
@@ -442,6 +491,7 @@ struct Run {
           a.dst = logits;
           a.out_f32 = 1;
           a.zeros = p->d_zeros;
+          a.ncount = nullptr;
           const double flops = 2.0 * B * nd.cout * nd.cin1;
           launch(P_CONV, flops, 2.0 * B * nd.cin1 + 4.0 * B * nd.cout + 2.0 * nd.cout * nd.cin1,
                  [&] { k::conv_bf16(a, s); });
@@ -450,7 +500,35 @@ struct Run {
       }
     }
   }
+
+  // the whole run, enqueued on s
+  void all(const void* x) {
+    Spec& sp = p->spec;
+    tp.resize(sp.tensors.size());
+    for (size_t t = 0; t < sp.tensors.size(); ++t)
+      tp[t] = sp.tensors[t].external ? const_cast<void*>(x) : p->buffers[sp.tensors[t].buf];
+    orig = p->d_iota;
+    launch(P_MISC, 0, 16.0 * B, [&] { k::init_records(rec, B, s); });
+    if (sp.any_halt) launch(P_MISC, 0, 4.0 * B, [&] { k::fill_f32(p->d_S, 0.f, B, s); });
+    if (sp.pad_input_c) {
+      const TensorInfo& in = sp.tensors[sp.input];
+      const size_t pix = static_cast<size_t>(B) * in.H * in.W;
+      launch(P_MISC, 0, pix * 2.0 * (in.C + sp.pad_input_c), [&] {
+        k::pad_channels_bf16(static_cast<const uint16_t*>(x), pix, in.C, sp.pad_input_c, p->d_xpad, s);
+      });
+    }
+    Rows rows{B, nullptr, B};
+    exec(sp.nodes, rows);
+  }
 };
+
+void graph_reset(dycl_plan* p) {
+  if (p->graph_exec) hipGraphExecDestroy(p->graph_exec);
+  if (p->graph) hipGraphDestroy(p->graph);
+  p->graph_exec = nullptr;
+  p->graph = nullptr;
+  p->graph_key = dycl_plan::GraphKey{};
+}
 
 }  // namespace
 
@@ -459,30 +537,93 @@ void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logit
   Spec& sp = p->spec;
   hip_check(hipSetDevice(p->device), "hipSetDevice");
   p->last_stream = s;
-  std::memset(p->h_counts, 0, sizeof(int32_t) * 2 * std::max(1, sp.decisions));
   if (p->pending.size() > 8192) profile_flush(p);
   Run r;
   r.p = p;
-  r.s = s;
   r.aux = aux;
   r.logits = logits;
   r.rec = rec;
   r.B = B;
-  r.tp.resize(sp.tensors.size());
-  for (size_t t = 0; t < sp.tensors.size(); ++t)
-    r.tp[t] = sp.tensors[t].external ? const_cast<void*>(x) : p->buffers[sp.tensors[t].buf];
-  r.orig = p->d_iota;
-  r.launch(P_MISC, 0, 16.0 * B, [&] { k::init_records(rec, B, s); });
-  if (sp.any_halt) r.launch(P_MISC, 0, 4.0 * B, [&] { k::fill_f32(p->d_S, 0.f, B, s); });
-  if (sp.pad_input_c) {
-    const TensorInfo& in = sp.tensors[sp.input];
-    const size_t pix = static_cast<size_t>(B) * in.H * in.W;
-    r.launch(P_MISC, 0, pix * 2.0 * (in.C + sp.pad_input_c), [&] {
-      k::pad_channels_bf16(static_cast<const uint16_t*>(x), pix, in.C, sp.pad_input_c, p->d_xpad, s);
-    });
+  r.device = p->mode != DYCL_HOST_SYNC;
+  p->counts_on_device = r.device;
+  const size_t cbytes = sizeof(int32_t) * 2 * std::max(1, sp.decisions);
+  if (!r.device) {
+    std::memset(p->h_counts, 0, cbytes);
+    r.s = s;
+    r.all(x);
+    std::copy(p->h_counts, p->h_counts + 2 * std::max(1, sp.decisions), p->hint.begin());
+    p->hint_B = B;
+    return;
   }
-  int n = B;
-  r.exec(sp.nodes, n);
+  // the counts of an earlier device-mode run, if their copy has landed
+  if (p->hint_pending) {
+    const hipError_t q = hipEventQuery(p->hint_ev);
+    if (q == hipSuccess) {
+      std::copy(p->h_hint_stage, p->h_hint_stage + 2 * std::max(1, sp.decisions), p->hint.begin());
+      p->hint_B = p->hint_pending_B;
+      p->hint_pending = false;
+    } else if (q == hipErrorNotReady) {
+      hipGetLastError();   // not an error: the copy is still queued
+    } else {
+      hip_check(q, "hipEventQuery");
+    }
+  }
+  if (p->mode != DYCL_HOST_GRAPH || p->profile) {
+    r.s = s;
+    r.all(x);
+    if (!p->hint_pending) {
+      hip_check(hipMemcpyAsync(p->h_hint_stage, p->d_counts, cbytes, hipMemcpyDeviceToHost, s), "count copy");
+      hip_check(hipEventRecord(p->hint_ev, s), "hipEventRecord");
+      p->hint_pending = true;
+      p->hint_pending_B = B;
+    }
+    return;
+  }
+  const dycl_plan::GraphKey key{x, B, aux, logits, rec};
+  const dycl_plan::GraphKey& k0 = p->graph_key;
+  if (!p->graph_exec || k0.x != key.x || k0.B != key.B || k0.aux != key.aux || k0.logits != key.logits ||
+      k0.rec != key.rec) {
+    graph_reset(p);
+    if (!p->cap_stream) hip_check(hipStreamCreateWithFlags(&p->cap_stream, hipStreamNonBlocking), "hipStreamCreate");
+    // the capture stream only records: nothing runs on it
+    r.s = p->cap_stream;
+    hip_check(hipStreamBeginCapture(p->cap_stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+    try {
+      r.all(x);
+    } catch (...) {
+      hipGraph_t g = nullptr;
+      hipStreamEndCapture(p->cap_stream, &g);
+      if (g) hipGraphDestroy(g);
+      hipGetLastError();
+      throw;
+    }
+    hip_check(hipStreamEndCapture(p->cap_stream, &p->graph), "hipStreamEndCapture");
+    hip_check(hipGraphInstantiate(&p->graph_exec, p->graph, nullptr, nullptr, 0), "hipGraphInstantiate");
+    p->graph_key = key;
+    ++p->graph_captures;
+  }
+  hip_check(hipGraphLaunch(p->graph_exec, s), "hipGraphLaunch");
+}
+
+void plan_set_mode(dycl_plan* p, int mode) {
+  if (mode != p->mode) {
+    hip_check(hipSetDevice(p->device), "hipSetDevice");
+    graph_reset(p);
+  }
+  p->mode = mode;
+}
+
+void plan_read_counts(const dycl_plan* p, int32_t* out, int n) {
+  const int total = 2 * p->spec.decisions;
+  const int m = std::min(n, total);
+  if (m <= 0) return;
+  if (!p->counts_on_device) {
+    std::copy(p->h_counts, p->h_counts + m, out);
+    return;
+  }
+  hip_check(hipSetDevice(p->device), "hipSetDevice");
+  hip_check(hipStreamSynchronize(p->last_stream), "hipStreamSynchronize");
+  hip_check(hipMemcpy(out, p->d_counts, m * sizeof(int32_t), hipMemcpyDeviceToHost), "count read");
 }
 
 void profile_flush(dycl_plan* p) {

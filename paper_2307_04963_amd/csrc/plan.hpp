@@ -141,6 +141,30 @@ struct dycl_plan {
   std::vector<Pending> pending;
   dycl::ProfileRow prof[dycl::P_COUNT];
   hipStream_t last_stream = nullptr;
+  // host mode (dycl_host_mode) and the last run's: whether its branch
+  // counts are only in d_counts (device modes)
+  int mode = DYCL_HOST_SYNC;
+  bool counts_on_device = false;
+  // graph mode: the captured run, replayed while its key is unchanged
+  hipStream_t cap_stream = nullptr;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t graph_exec = nullptr;
+  struct GraphKey {
+    const void* x = nullptr;
+    int B = 0;
+    const float* aux = nullptr;
+    float* logits = nullptr;
+    dycl_record* rec = nullptr;
+  } graph_key;
+  long graph_captures = 0;
+  // device modes: the branch counts of an earlier run, copied back without a
+  // wait, as the expected live rows that pick tile shapes (never the grid)
+  std::vector<int32_t> hint;       // [2 * decisions]
+  int hint_B = 0;                  // batch those counts came from (0: none yet)
+  int32_t* h_hint_stage = nullptr; // pinned target of the asynchronous copy
+  hipEvent_t hint_ev = nullptr;
+  bool hint_pending = false;
+  int hint_pending_B = 0;
 };
 
 namespace dycl {
@@ -149,6 +173,10 @@ void plan_free(dycl_plan* p);
 void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logits, dycl_record* rec,
               hipStream_t s);
 void profile_flush(dycl_plan* p);
+// host mode (a dycl_host_mode value, already validated); drops a captured graph
+void plan_set_mode(dycl_plan* p, int mode);
+// the first min(n, 2 * decisions) branch counts of the last run
+void plan_read_counts(const dycl_plan* p, int32_t* out, int n);
 
 struct HipError : std::runtime_error {
   explicit HipError(const std::string& m) : std::runtime_error(m) {}

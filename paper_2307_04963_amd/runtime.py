@@ -19,6 +19,9 @@ check = _lib.check
 lib = _lib.lib
 
 
+HOST_MODES = {"sync": 0, "device": 1, "graph": 2}
+
+
 class Plan:
     def __init__(self, spec_json: str, blob: bytes, max_batch: int, device: int = 0):
         self._h = C.c_void_p()
@@ -49,10 +52,20 @@ class Plan:
             pass
 
     def info(self) -> dict:
-        buf = (C.c_int64 * 8)()
-        n = check(lib.dycl_plan_info(self._h, buf, 8))
-        keys = ["n_out", "in_bytes", "decisions", "workspace_bytes", "weight_bytes", "max_batch", "aux", "nodes"]
+        keys = ["n_out", "in_bytes", "decisions", "workspace_bytes", "weight_bytes", "max_batch", "aux", "nodes",
+                "host_mode", "graph_captures"]
+        buf = (C.c_int64 * len(keys))()
+        n = check(lib.dycl_plan_info(self._h, buf, len(keys)))
         return {k: int(buf[i]) for i, k in enumerate(keys[:n])}
+
+    def set_host_mode(self, mode: str) -> str:
+        """'sync' (read the branch counts back at each decision), 'device'
+        (counts stay on the device, count-guarded launches) or 'graph'
+        (device mode replayed from a captured HIP graph); returns the previous mode."""
+        if mode not in HOST_MODES:
+            raise ValueError(f"host mode must be one of {sorted(HOST_MODES)}")
+        prev = check(lib.dycl_plan_set_host_mode(self._h, HOST_MODES[mode]))
+        return {v: k for k, v in HOST_MODES.items()}[prev]
 
     def run(self, x: torch.Tensor, aux, logits: torch.Tensor, records: torch.Tensor, stream=None):
         """x, aux, logits (fp32 [B, n_out]) and records (int32 [B, 4]) are device tensors."""

@@ -100,6 +100,7 @@ def test_plan_create_rejects_bad_arguments_without_gpu():
     assert out.value is None
     assert lib.dycl_run(None, None, 1, None, None, None, None) == -1
     assert lib.dycl_last_counts(None, None, 0) == -1
+    assert lib.dycl_plan_set_host_mode(None, 1) == -1
     assert lib.dycl_plan_info(None, None, 0) == -1
     lib.dycl_plan_destroy(None)
     assert lib.dycl_profile_class(99) == b""
