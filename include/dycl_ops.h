@@ -69,20 +69,32 @@ int dycl_op_move_rows(void* dst, const int32_t* dst_idx, const void* src, const 
  * dycl_op_conv_pack          host to host: w [cout][k][k][cin] bf16 into the
  *                            packed layout (zero-padded rows and K); both
  *                            pointers are host memory.
+ * dycl_op_conv_workspace_bytes  device workspace that lets a layer with a
+ *                            deep K on few output pixels per image (Ho*Wo <=
+ *                            64, K = k*k*cin >= 4608, cout >= 256) split each
+ *                            output tile's K range over several workgroups;
+ *                            0 for every other shape.  The split depends on
+ *                            the shape alone, never on n.
  * dycl_op_conv               device pointers: x [n][H][W][cin] bf16,
  *                            packed (uploaded result of dycl_op_conv_pack),
  *                            scale / shift [cout] float32 or NULL (1 / 0),
  *                            res [n][Ho][Wo][cout] bf16 or NULL, y the same
  *                            shape as res.  act: 0 none, 1 ReLU, 2 exact GELU.
  *                            k in {1, 3, 7}; n >= 0 (0 does nothing); every
- *                            tensor below 2^31 elements.  Work is queued on
- *                            hip_stream.
+ *                            tensor below 2^31 elements.  workspace: NULL, or
+ *                            workspace_bytes >= dycl_op_conv_workspace_bytes
+ *                            of device memory, caller-owned, which the call
+ *                            overwrites (calls sharing one must not overlap);
+ *                            without it a split layer runs unsplit: the same
+ *                            sums, added in another order.  dycl_run always
+ *                            splits.  Work is queued on hip_stream.
  */
 size_t dycl_op_conv_packed_bytes(int cout, int k, int cin);
 int dycl_op_conv_pack(const uint16_t* w, int cout, int k, int cin, uint16_t* packed, size_t packed_bytes);
+size_t dycl_op_conv_workspace_bytes(int n, int H, int W, int cin, int cout, int k, int stride, int pad);
 int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed, int cout, int k, int stride,
                  int pad, const float* scale, const float* shift, const uint16_t* res, int act, uint16_t* y,
-                 void* hip_stream);
+                 void* workspace, size_t workspace_bytes, void* hip_stream);
 
 #ifdef __cplusplus
 }

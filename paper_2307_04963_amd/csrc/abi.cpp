@@ -276,9 +276,16 @@ int dycl_op_conv_pack(const uint16_t* w, int cout, int k, int cin, uint16_t* pac
   return DYCL_OK;
 }
 
+size_t dycl_op_conv_workspace_bytes(int n, int H, int W, int cin, int cout, int k, int stride, int pad) {
+  if (n < 1 || H < 1 || W < 1 || stride < 1 || pad < 0 || !dycl_op_conv_packed_bytes(cout, k, cin)) return 0;
+  if (H + 2 * pad < k || W + 2 * pad < k) return 0;
+  const int Ho = (H + 2 * pad - k) / stride + 1, Wo = (W + 2 * pad - k) / stride + 1;
+  return dycl::k::conv_ksplit_bytes(n, Ho, Wo, cout, k * k * cin, false);
+}
+
 int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed, int cout, int k, int stride,
                  int pad, const float* scale, const float* shift, const uint16_t* res, int act, uint16_t* y,
-                 void* hip_stream) {
+                 void* workspace, size_t workspace_bytes, void* hip_stream) {
   if (n < 0) return fail(DYCL_E_INVALID, "dycl_op_conv: n < 0");
   if (!dycl_op_conv_packed_bytes(cout, k, cin))
     return fail(DYCL_E_INVALID, "dycl_op_conv: need cout, cin >= 1 and k in {1, 3, 7}");
@@ -292,8 +299,8 @@ int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t
   if (n == 0) return DYCL_OK;
   if (!x || !packed || !y) return fail(DYCL_E_INVALID, "dycl_op_conv: null x, packed weights or y");
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(packed) | reinterpret_cast<uintptr_t>(y) |
-       reinterpret_cast<uintptr_t>(res)) & 15)
-    return fail(DYCL_E_INVALID, "dycl_op_conv: x, packed, y and res must be 16-byte aligned");
+       reinterpret_cast<uintptr_t>(res) | reinterpret_cast<uintptr_t>(workspace)) & 15)
+    return fail(DYCL_E_INVALID, "dycl_op_conv: x, packed, y, res and workspace must be 16-byte aligned");
   return guarded([&] {
     const uint16_t* zeros = dycl::k::zero_page();
     if (!zeros) throw dycl::HipError("dycl_op_conv: zero page unavailable");
@@ -321,6 +328,8 @@ int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t
     a.dst = y;
     a.out_f32 = 0;
     a.zeros = zeros;
+    a.splitws = static_cast<float*>(workspace);
+    a.splitws_bytes = workspace ? workspace_bytes : 0;
     dycl::k::conv_bf16(a, static_cast<hipStream_t>(hip_stream));
     if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_conv: launch failed");
     return DYCL_OK;

@@ -42,6 +42,8 @@ struct ConvP {
   int mt, nt;
   const int32_t* nc;       // device count of live images (<= nmax) or null
   int nmax;                // images the grid is sized for
+  int ksplit;              // K ranges per tile (conv_lds_kernel); > 1: fp32 partials to `part`
+  float* part;             // [ksplit][M][cout] partial sums (rows of the nmax images)
   const uint16_t* w;
   const float* scale;
   const float* shift;
@@ -312,12 +314,14 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   __shared__ __align__(16) char smem[SMEM];
 
   // with a device count, only the tiles of the live images exist: the
-  // grid was sized for nmax images and the surplus workgroups leave
+  // grid was sized for nmax images and the surplus workgroups leave.  With
+  // a K split, workgroup wg takes K range wg / T of tile wg % T.
   const int M = p.nc ? min(*p.nc, p.nmax) * p.Ho * p.Wo : p.M;
   const int T = (p.nc ? (M + BM - 1) / BM : p.mt) * p.nt;
   const int T8 = (T >> 3) << 3;
-  const int wg = blockIdx.x;
-  if (wg >= T) return;
+  if (static_cast<int>(blockIdx.x) >= T * p.ksplit) return;
+  const int split = blockIdx.x / T;
+  const int wg = blockIdx.x - split * T;
   const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (wg >> 3) : wg;
   const int mtile = t / p.nt;
   const int m0 = mtile * BM, n0 = (t - mtile * p.nt) * BN;
@@ -347,8 +351,14 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   }
   const uint16_t* wrow = p.w + (size_t)(n0 + rbase) * p.Kp + lchunk * 8;
 
+  // this workgroup's K steps: [kb, kb + nk) of the layer's Kp / 64
+  const int nk_all = p.Kp / 64;
+  const int kb = split * nk_all / p.ksplit;
+  const int nk = (split + 1) * nk_all / p.ksplit - kb;
+
   auto issue = [&](int kt, int stage) __attribute__((always_inline)) {
     char* sb = smem + stage * STAGE;
+    kt += kb;
     const int kidx = kt * 64 + lchunk * 8;
     int tap = 0, ci = kidx;
     if constexpr (KS != 1) {
@@ -416,7 +426,6 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   // NS-stage pipeline: the loads of step kt+NS-1 are issued while step kt
   // is computed; the stage they fill was read in step kt-1, which every wave
   // finished before the barrier of step kt
-  const int nk = p.Kp / 64;
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
     if (i < nk) issue(i, i);
@@ -443,11 +452,12 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   __syncthreads();
   float* ep = reinterpret_cast<float*>(smem) + wave * 32 * EPW;
   float sc[TN], sh[TN];
+  const bool partial = p.ksplit > 1;   // raw sums; the split reduction finishes them
 #pragma unroll
   for (int b = 0; b < TN; ++b) {
     const int col = n0 + wn * WTN + b * 32 + (lane & 31);
-    sc[b] = (p.scale && col < p.cout) ? p.scale[col] : 1.0f;
-    sh[b] = (p.shift && col < p.cout) ? p.shift[col] : 0.0f;
+    sc[b] = (!partial && p.scale && col < p.cout) ? p.scale[col] : 1.0f;
+    sh[b] = (!partial && p.shift && col < p.cout) ? p.shift[col] : 0.0f;
   }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
@@ -469,6 +479,12 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
         const float4 hi = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8 + 4);
         float vv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
         const size_t o = (size_t)row * p.cout + col;
+        if (partial) {
+          float* d = p.part + (size_t)split * p.M * p.cout + o;
+          *reinterpret_cast<float4*>(d) = lo;
+          *reinterpret_cast<float4*>(d + 4) = hi;
+          continue;
+        }
         if (p.res) {
           const uint4 rv = *reinterpret_cast<const uint4*>(p.res + o);
           const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
@@ -1155,6 +1171,53 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
   }
 }
 
+// ------------------------------------------------------- K-split sums ----
+// y[m, c..c+7] = finish(sum_s part[s][m][c..c+7]) with the splits added in
+// order s = 0, 1, ...: scale / shift, residual, activation, bf16 rounding,
+// as the single-range epilogue does.
+__global__ __launch_bounds__(256) void ksplit_finish_kernel(const float* __restrict__ part, int S, int Mb, int cout,
+                                                            const int32_t* nc, int nmax, int HoWo,
+                                                            const float* __restrict__ scale,
+                                                            const float* __restrict__ shift,
+                                                            const uint16_t* __restrict__ res, int act,
+                                                            uint16_t* __restrict__ dst) {
+  const int M = (nc ? min(*nc, nmax) : nmax) * HoWo;
+  const int C8 = cout >> 3;
+  const size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<size_t>(M) * C8) return;
+  const size_t row = i / C8;
+  const int c = static_cast<int>(i - row * C8) * 8;
+  const size_t o = row * cout + c;
+  const size_t stride = static_cast<size_t>(Mb) * cout;
+  float4 lo = *reinterpret_cast<const float4*>(part + o), hi = *reinterpret_cast<const float4*>(part + o + 4);
+  for (int sp = 1; sp < S; ++sp) {
+    const float4 a = *reinterpret_cast<const float4*>(part + sp * stride + o);
+    const float4 b = *reinterpret_cast<const float4*>(part + sp * stride + o + 4);
+    lo.x += a.x; lo.y += a.y; lo.z += a.z; lo.w += a.w;
+    hi.x += b.x; hi.y += b.y; hi.z += b.z; hi.w += b.w;
+  }
+  float vv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+  for (int q = 0; q < 8; ++q) vv[q] = fmaf(vv[q], scale ? scale[c + q] : 1.0f, shift ? shift[c + q] : 0.0f);
+  if (res) {
+    const uint4 rv = *reinterpret_cast<const uint4*>(res + o);
+    const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      vv[2 * q] += __uint_as_float(rw[q] << 16);
+      vv[2 * q + 1] += __uint_as_float(rw[q] & 0xffff0000u);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) vv[q] = apply_act(vv[q], act);
+  uint4 ov;
+  ov.x = f2bf(vv[0]) | (uint32_t(f2bf(vv[1])) << 16);
+  ov.y = f2bf(vv[2]) | (uint32_t(f2bf(vv[3])) << 16);
+  ov.z = f2bf(vv[4]) | (uint32_t(f2bf(vv[5])) << 16);
+  ov.w = f2bf(vv[6]) | (uint32_t(f2bf(vv[7])) << 16);
+  *reinterpret_cast<uint4*>(dst + o) = ov;
+}
+
 // ------------------------------------------------------------- launch ----
 
 namespace {
@@ -1208,22 +1271,32 @@ TileCfg choose_lds(int M, int cout, int Kp) {
   return c64;
 }
 
+#ifndef DYCL_DEEP_NS
+#define DYCL_DEEP_NS 2
+#endif
+#ifndef DYCL_DEEP_MIN_K
+#define DYCL_DEEP_MIN_K 8
+#endif
 template <int BM, int BN, int WM, int WN, int KS>
-void go_lds(const ConvP& p, hipStream_t s) {
+void go_lds(const ConvP& p, hipStream_t s, int S) {
+  constexpr int kDeep = (BM + BN) * 128 <= 32768 ? DYCL_DEEP_NS : 2;
+  const dim3 grid(p.mt * p.nt * S);
   if (p.Kp == 64)
-    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), dim3(p.mt * p.nt), dim3(64 * WM * WN), 0, s, p);
+    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
+  else if (kDeep > 2 && p.Kp >= 64 * DYCL_DEEP_MIN_K)
+    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, kDeep>), grid, dim3(64 * WM * WN), 0, s, p);
   else
-    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), dim3(p.mt * p.nt), dim3(64 * WM * WN), 0, s, p);
+    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), grid, dim3(64 * WM * WN), 0, s, p);
 }
 
 template <int KS>
-void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s) {
+void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s, int S = 1) {
   switch (c.bm * 1000 + c.bn) {
-    case 256256: go_lds<256, 256, 4, 2, KS>(p, s); break;
-    case 128128: go_lds<128, 128, 2, 2, KS>(p, s); break;
-    case 128064: go_lds<128, 64, 2, 2, KS>(p, s); break;
-    case 64064: go_lds<64, 64, 2, 2, KS>(p, s); break;
-    default: go_lds<128, 32, 4, 1, KS>(p, s); break;
+    case 256256: go_lds<256, 256, 4, 2, KS>(p, s, S); break;
+    case 128128: go_lds<128, 128, 2, 2, KS>(p, s, S); break;
+    case 128064: go_lds<128, 64, 2, 2, KS>(p, s, S); break;
+    case 64064: go_lds<64, 64, 2, 2, KS>(p, s, S); break;
+    default: go_lds<128, 32, 4, 1, KS>(p, s, S); break;
   }
 }
 
@@ -1412,6 +1485,13 @@ const uint16_t* zero_page() {
   return addr[dev];
 }
 
+int conv_ksplit(int Ho, int Wo, int cout, int K, bool out_f32) {
+  // measured: K = 4608 on 4x4 outputs gains from four ranges, K = 2304
+  // loses from two (the partial sums cost more than the idle CUs)
+  if (out_f32 || Ho * Wo > 64 || K < 4608 || cout < 256 || cout % 64) return 1;
+  return 4;
+}
+
 int conv_cout_pad(int cout) {
   if (cout >= 256) return (cout + 255) / 256 * 256;
   if (cout >= 128) return (cout + 127) / 128 * 128;
@@ -1449,6 +1529,8 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.zeros = a.zeros;
   p.nc = a.ncount;
   p.nmax = a.n;
+  p.ksplit = 1;
+  p.part = nullptr;
 
   // 16-byte A vectors need Cin % 8 == 0, and a power-of-two Cin when the tap
   // index is split off with a shift; anything else gathers element by element
@@ -1476,9 +1558,31 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
   if (vec_out && (conv3_wres(a, s) || conv3_halo(a, s))) return;
   if (vec_out) {
-    const TileCfg c = choose_lds(Mh, a.cout, p.Kp);
+    // deep K on few pixels per image: K ranges of one tile on several
+    // workgroups, fp32 partials summed in a fixed order by a second kernel
+    // (the split depends on the layer's shape only, never on n)
+    const int S = conv_ksplit(a.Ho, a.Wo, a.cout, p.K, a.out_f32 != 0);
+    const bool split = S > 1 && a.splitws &&
+                       a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
+    const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
+                            : choose_lds(Mh, a.cout, p.Kp);
     p.mt = (p.M + c.bm - 1) / c.bm;
     p.nt = (a.cout + c.bn - 1) / c.bn;
+    if (split) {
+      p.ksplit = S;
+      p.part = a.splitws;
+      if (a.k == 1)
+        dispatch_lds<1>(c, p, s, S);
+      else if (a.k == 3)
+        dispatch_lds<3>(c, p, s, S);
+      else
+        dispatch_lds<7>(c, p, s, S);
+      const size_t items = static_cast<size_t>(p.M) * (a.cout / 8);
+      hipLaunchKernelGGL(ksplit_finish_kernel, dim3(static_cast<unsigned>((items + 255) / 256)), dim3(256), 0, s,
+                         a.splitws, S, p.M, a.cout, a.ncount, a.n, a.Ho * a.Wo, a.scale, a.shift, a.res, a.act,
+                         static_cast<uint16_t*>(a.dst));
+      return;
+    }
     if (a.k == 1)
       dispatch_lds<1>(c, p, s);
     else if (a.k == 3)

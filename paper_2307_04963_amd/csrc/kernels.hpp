@@ -46,8 +46,20 @@ struct ConvArgs {
   const uint16_t* zeros; // >= 16 zero bytes on the device (padding taps)
   const int32_t* ncount = nullptr;  // device count of live images (<= n) or null
   int nhint = 0;                    // expected live images for the tile choice (0: n)
+  float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split
+  size_t splitws_bytes = 0;
 };
 void conv_bf16(const ConvArgs& a, hipStream_t s);
+
+// K ranges per output tile for the layer shape (1: none).  A split layer
+// needs conv_ksplit_bytes of workspace; without it the layer runs unsplit
+// (the same sums in another order).  Depends on the shape only, so every
+// row count takes the same rounding.
+int conv_ksplit(int Ho, int Wo, int cout, int K, bool out_f32);
+inline size_t conv_ksplit_bytes(int n, int Ho, int Wo, int cout, int K, bool out_f32) {
+  const int S = conv_ksplit(Ho, Wo, cout, K, out_f32);
+  return S > 1 ? static_cast<size_t>(S) * n * Ho * Wo * cout * sizeof(float) : 0;
+}
 
 // 128 zero bytes in device memory of the current device (the source of the
 // convolutions' padding taps), or null if the symbol cannot be resolved

@@ -11,6 +11,7 @@
 // residual block's output is its input (identity path) and is never copied;
 // records and counts are plain stores of the decision kernels.
 #include <algorithm>
+#include <functional>
 #include <cstring>
 
 #include "plan.hpp"
@@ -148,6 +149,22 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     if (nd.kind == NodeKind::Exit && !nd.fused && sp.dt == DType::BF16) split_pool = true;
   if (split_pool)
     p->d_Gpart = dev_alloc<float>(p, static_cast<size_t>(k::kGapMaxSplit) * B * sp.max_head_c, "pooling partials");
+  // K-split partial sums: the largest any bf16 conv layer needs at B rows
+  size_t split_bytes = 0;
+  std::function<void(const std::vector<Node>&)> walk = [&](const std::vector<Node>& nodes) {
+    for (const Node& nd : nodes) {
+      if (nd.kind == NodeKind::Conv && sp.dt == DType::BF16) {
+        const int K = nd.k * nd.k * (nd.pad_in ? sp.pad_input_c : nd.cin1 + nd.cin2);
+        split_bytes = std::max(split_bytes, k::conv_ksplit_bytes(B, nd.Ho, nd.Wo, nd.cout, K, false));
+      }
+      walk(nd.body);
+    }
+  };
+  walk(sp.nodes);
+  if (split_bytes) {
+    p->d_split = dev_alloc<float>(p, split_bytes / sizeof(float), "K-split partials");
+    p->split_bytes = split_bytes;
+  }
   p->d_Z = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_ncls, "head logits");
   p->d_S = dev_alloc<float>(p, B, "halting sums");
   p->d_zeros = dev_alloc<uint16_t>(p, 128, "zero page");
@@ -203,7 +220,7 @@ void plan_free(dycl_plan* p) {
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
                      p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S, p->d_zeros,
-                     p->d_xpad, p->d_cws, p->d_Gpart};
+                     p->d_xpad, p->d_cws, p->d_Gpart, p->d_split};
   for (void* s : singles)
     if (s) hipFree(s);
   if (p->h_counts) hipHostFree(p->h_counts);
@@ -366,6 +383,8 @@ struct Run {
     a.zeros = p->d_zeros;
     a.ncount = r.nc;
     a.nhint = r.hint;
+    a.splitws = p->d_split;
+    a.splitws_bytes = p->split_bytes;
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
                                 static_cast<double>(nd.cout) * nd.k * nd.k * cin);
     launch(P_CONV, flops, bytes, [&] { k::conv_bf16(a, s); });

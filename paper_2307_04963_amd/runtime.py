@@ -140,16 +140,26 @@ def pack_conv_weights(w_bits: np.ndarray) -> np.ndarray:
     return out
 
 
+def conv_workspace_bytes(n: int, H: int, W: int, cin: int, cout: int, k: int, stride: int, pad: int) -> int:
+    return int(lib.dycl_op_conv_workspace_bytes(n, H, W, cin, cout, k, stride, pad))
+
+
 def conv(x: torch.Tensor, packed: torch.Tensor, cout: int, k: int, stride: int, pad: int, scale=None, shift=None,
-         res=None, act: int = 0, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+         res=None, act: int = 0, out: torch.Tensor | None = None, stream=None, workspace="auto") -> torch.Tensor:
     """dycl_op_conv on device tensors: x [n, H, W, cin] bf16, packed weights
     on the device (int16 / uint16 storage), optional float32 scale / shift
-    [cout] and bf16 residual; returns y [n, Ho, Wo, cout] bf16."""
+    [cout] and bf16 residual; returns y [n, Ho, Wo, cout] bf16.  workspace:
+    "auto" allocates what a K-split layer needs (as dycl_run splits), None
+    runs it unsplit, or a device tensor."""
     n, H, W, cin = x.shape
     Ho, Wo = (H + 2 * pad - k) // stride + 1, (W + 2 * pad - k) // stride + 1
     y = out if out is not None else torch.empty((n, Ho, Wo, cout), dtype=torch.bfloat16, device=x.device)
     s = stream if stream is not None else torch.cuda.current_stream(x.device)
     ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+    if isinstance(workspace, str):
+        nb = conv_workspace_bytes(n, H, W, cin, cout, k, stride, pad)
+        workspace = torch.empty(nb, dtype=torch.uint8, device=x.device) if nb else None
+    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
     check(lib.dycl_op_conv(x.data_ptr(), n, H, W, cin, packed.data_ptr(), cout, k, stride, pad, ptr(scale), ptr(shift),
-                         ptr(res), act, y.data_ptr(), s.cuda_stream))
+                         ptr(res), act, y.data_ptr(), ptr(workspace), wsb, s.cuda_stream))
     return y

@@ -133,7 +133,7 @@ def test_conv_pack_and_validation():
     p16 = C.c_void_p(256)
     args = lambda **kw: [kw.get("x", p16), kw.get("n", 2), 8, 8, 64, kw.get("w", p16), 64, kw.get("k", 3),  # noqa: E731
                          kw.get("s", 1), kw.get("pad", 1), None, None, kw.get("res"), kw.get("act", 1),
-                         kw.get("y", p16), None]
+                         kw.get("y", p16), kw.get("ws"), kw.get("wsb", 0), None]
     assert lib.dycl_op_conv(*args(n=-1)) == -1
     assert lib.dycl_op_conv(*args(k=5)) == -1
     assert lib.dycl_op_conv(*args(pad=3)) == -1
@@ -142,4 +142,13 @@ def test_conv_pack_and_validation():
     assert lib.dycl_op_conv(*args(y=C.c_void_p(258))) == -1               # misaligned
     assert lib.dycl_op_conv(*args(res=C.c_void_p(264))) == -1
     assert "aligned" in _lib.last_error()
+    assert lib.dycl_op_conv(*args(ws=C.c_void_p(264), wsb=4096)) == -1   # misaligned workspace
     assert lib.dycl_op_conv(*args(n=0)) == 0                              # nothing to do
+    # K split workspace: deep K on few pixels only, sized by S * n * Ho * Wo * cout fp32
+    assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 512, 512, 3, 1, 1) == 4 * 255 * 16 * 512 * 4
+    assert lib.dycl_op_conv_workspace_bytes(255, 8, 8, 512, 512, 3, 2, 1) == 4 * 255 * 16 * 512 * 4
+    assert lib.dycl_op_conv_workspace_bytes(255, 8, 8, 256, 512, 3, 2, 1) == 0     # K = 2304
+    assert lib.dycl_op_conv_workspace_bytes(255, 16, 16, 512, 512, 3, 1, 1) == 0   # 256 pixels per image
+    assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 128, 512, 3, 1, 1) == 0     # K = 1152
+    assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 512, 128, 3, 1, 1) == 0     # cout < 256
+    assert lib.dycl_op_conv_workspace_bytes(0, 4, 4, 512, 512, 3, 1, 1) == 0

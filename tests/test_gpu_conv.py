@@ -3,8 +3,9 @@ against the oracle's convolution (float64, bf16 inputs), at every geometry
 the launcher distinguishes: the halo-tiled kernel with register-resident
 weights (64 -> 64 channels, 3x3, stride 1: row tiles, partial row tiles,
 whole-image tiles with a ragged last tile, several tiles per workgroup), the
-direct-to-LDS implicit GEMM (1x1, 3x3, strided) and the element-gathering
-kernel (3-channel stems, Cout not a multiple of 8).
+direct-to-LDS implicit GEMM (1x1, 3x3, strided; with the K range of each
+tile split over workgroups for deep K on few pixels, and without) and the
+element-gathering kernel (3-channel stems, Cout not a multiple of 8).
 
 Bound per element: the fp32 accumulation error (K terms, gamma_K * sum |x w|)
 scaled by |scale|, the fp32 epilogue roundings, and half a bf16 ulp of the
@@ -47,6 +48,11 @@ CASES = [
     (3, 20, 20, 3, 64, 7, 2, 3, False, 1),      # 3-channel stem, element gathers
     (5, 12, 12, 16, 32, 3, 1, 1, False, 1),
     (5, 12, 12, 64, 24, 3, 1, 1, True, 2),      # Cout not a multiple of 8
+    (37, 4, 4, 512, 512, 3, 1, 1, False, 1),    # K split in 4, ragged last row tile
+    (37, 8, 8, 512, 512, 3, 2, 1, True, 1),     # strided, K split in 4
+    (5, 4, 4, 512, 384, 3, 1, 1, True, 2),      # three 128-channel tiles, GELU
+    (11, 7, 7, 512, 256, 3, 2, 1, False, 0),    # 7x7 -> 4x4, K split in 4
+    (6, 4, 4, 4608, 256, 1, 1, 0, False, 1),    # 1x1 with K = 4608, split in 4
 ]
 
 
@@ -54,7 +60,7 @@ def _bits(a):
     return torch.from_numpy(to_bf16_bits(np.asarray(a, np.float32)).view(np.int16).copy())
 
 
-def _case(n, H, W, cin, cout, k, stride, pad, residual, act, seed):
+def _case(n, H, W, cin, cout, k, stride, pad, residual, act, seed, workspace="auto"):
     from paper_2307_04963_amd import runtime
     rng = np.random.default_rng(seed)
     x = bf16_bits_to_f32(to_bf16_bits(rng.standard_normal((n, H, W, cin)).astype(np.float32)))
@@ -67,7 +73,8 @@ def _case(n, H, W, cin, cout, k, stride, pad, residual, act, seed):
     packed = torch.from_numpy(runtime.pack_conv_weights(to_bf16_bits(w)).view(np.int16)).cuda()
     xt = _bits(x).cuda().view(torch.bfloat16)
     rt = _bits(r).cuda().view(torch.bfloat16) if residual else None
-    y = runtime.conv(xt, packed, cout, k, stride, pad, torch.from_numpy(sc).cuda(), torch.from_numpy(sh).cuda(), rt, act)
+    y = runtime.conv(xt, packed, cout, k, stride, pad, torch.from_numpy(sc).cuda(), torch.from_numpy(sh).cuda(), rt, act,
+                     workspace=workspace)
     torch.cuda.synchronize()
     got = bf16_bits_to_f32(y.cpu().view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
 
@@ -98,6 +105,26 @@ def _case(n, H, W, cin, cout, k, stride, pad, residual, act, seed):
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "n{}_{}x{}_{}to{}_k{}s{}".format(*c[:7]))
 def test_conv_op(case):
     _case(*case, seed=hash(case) % (2 ** 31))
+
+
+@pytest.mark.parametrize("case", [c for c in CASES if c[4] >= 256 and c[1] * c[2] <= 64], ids=str)
+def test_conv_op_unsplit_without_workspace(case):
+    # the same layers without a workspace: one K range per tile
+    _case(*case, seed=hash(case) % (2 ** 31), workspace=None)
+
+
+def test_conv_op_split_rows_are_independent():
+    # the first rows of a K-split batch alone give the same bits (the split
+    # depends on the layer shape, not on n)
+    from paper_2307_04963_amd import runtime
+    rng = np.random.default_rng(11)
+    x = _bits(rng.standard_normal((100, 4, 4, 512))).cuda().view(torch.bfloat16)
+    w = to_bf16_bits(rng.uniform(-0.02, 0.02, (512, 3, 3, 512)).astype(np.float32))
+    packed = torch.from_numpy(runtime.pack_conv_weights(w).view(np.int16)).cuda()
+    a = runtime.conv(x, packed, 512, 3, 1, 1, None, None, None, 1)
+    b = runtime.conv(x[:13].contiguous(), packed, 512, 3, 1, 1, None, None, None, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(a[:13].view(torch.int16), b.view(torch.int16))
 
 
 def test_conv_op_full_stage1_shape():
