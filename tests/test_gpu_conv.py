@@ -53,6 +53,13 @@ CASES = [
     (5, 4, 4, 512, 384, 3, 1, 1, True, 2),      # three 128-channel tiles, GELU
     (11, 7, 7, 512, 256, 3, 2, 1, False, 0),    # 7x7 -> 4x4, K split in 4
     (6, 4, 4, 4608, 256, 1, 1, 0, False, 1),    # 1x1 with K = 4608, split in 4
+    # deep K without a split: strided, deep 1x1, ragged channel tiles, many tiles
+    (7, 9, 9, 64, 96, 3, 2, 1, True, 1),        # half-used second channel tile
+    (3, 16, 16, 1024, 256, 1, 1, 0, True, 0),   # deep 1x1 with residual
+    (2, 14, 14, 256, 512, 3, 2, 1, False, 2),   # strided, GELU
+    (2000, 8, 8, 128, 256, 3, 2, 1, False, 1),  # 128-pixel tiles, several units per workgroup
+    (2500, 8, 8, 128, 256, 3, 2, 1, True, 1),   # 256-pixel tiles, several units per workgroup
+    (3, 6, 6, 600, 64, 1, 1, 0, False, 1),      # K = 600: the last step is partly padding
 ]
 
 
