@@ -174,6 +174,51 @@ def copy_probe():
     print(json.dumps({"copy_probe_bytes": 2 * a.numel(), "copies": 3}), flush=True)
 
 
+RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per HBM byte where the two bounds meet
+
+
+def layer_table(wl, plan, xt, at, logits, rec, stream, warmup):
+    """One profiled sync-mode step: each conv launch with its algorithmic
+    FLOPs and bytes (executed rows only) and its HIP-event time; the bound
+    is the layer's attainable rate min(peak, intensity x HBM peak)."""
+    import torch
+    from paper_2307_04963_amd.lowering import lower
+    blob, man = wl.blob()
+    names = []
+
+    def walk(nodes):
+        for nd in nodes:
+            if nd["op"] in ("conv", "output"):
+                names.append(nd.get("dst", "output"))
+            walk(nd.get("body", []))
+    walk(lower(wl.arch, man)["nodes"])
+    plan.set_host_mode("sync")
+    for _ in range(max(warmup, 1)):
+        plan.run(xt, at, logits, rec, stream)
+    plan.profile(True)
+    plan.run(xt, at, logits, rec, stream)
+    torch.cuda.synchronize()
+    launches = [r for r in plan.profile_launches() if r["class"] in ("conv_bf16_mfma", "linear_f32")]
+    plan.profile(False)
+    rows, cb_f, cb_t = [], 0.0, 0.0
+    for i, r in enumerate(launches):
+        inten = r["flops"] / r["bytes"] if r["bytes"] else 0.0
+        tf = r["flops"] / (r["ms"] * 1e-3) / 1e12 if r["ms"] else 0.0
+        attain = min(PEAK_BF16_TFLOPS, inten * PEAK_HBM_GBS / 1e3)
+        bound = "mfma" if inten >= RIDGE else "hbm"
+        if bound == "mfma":
+            cb_f += r["flops"]
+            cb_t += r["ms"]
+        rows.append({"layer": names[i] if i < len(names) else f"launch{i}", "us": round(r["ms"] * 1e3, 1),
+                     "gflop": round(r["flops"] / 1e9, 3), "mb": round(r["bytes"] / 1e6, 2),
+                     "flop_per_byte": round(inten, 1), "bound": bound, "tflops": round(tf, 1),
+                     "frac_peak": round(tf / PEAK_BF16_TFLOPS, 4), "frac_attainable": round(tf / attain, 4) if attain else None})
+    cb = cb_f / (cb_t * 1e-3) / 1e12 if cb_t else 0.0
+    return {"workload": wl.name, "batch": int(xt.shape[0]), "branch_counts": plan.counts(), "ridge_flop_per_byte": RIDGE,
+            "mfma_bound_layers": sum(r["bound"] == "mfma" for r in rows),
+            "mfma_bound_flop_weighted_tflops": cb, "mfma_bound_frac_peak": cb / PEAK_BF16_TFLOPS, "layers": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -185,6 +230,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm-kernels", action="store_true")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-scaling copy")
+    ap.add_argument("--layers", action="store_true",
+                    help="only the per-layer table: one profiled sync-mode step, every conv launch timed")
     ap.add_argument("--host-mode", default="device", choices=["sync", "device", "graph"],
                     help="host mode of the headline value (all three are timed)")
     args = ap.parse_args()
@@ -208,6 +255,10 @@ def main():
     logits = torch.empty((B, plan.n_out), dtype=torch.float32, device="cuda")
     rec = torch.empty((B, 4), dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
+
+    if args.layers:
+        print(json.dumps(layer_table(wl, plan, xt, at, logits, rec, stream, args.warmup)), flush=True)
+        return
 
     def timed(mode):
         plan.set_host_mode(mode)

@@ -158,6 +158,15 @@ int dycl_profile_read(dycl_plan* plan, double* rows, int cap);
 const char* dycl_profile_class(int i);
 
 /*
+ * Every launch of the last run made while profiling was enabled, in launch
+ * order: up to `cap` rows of { class index, ms, flops, bytes } (4 doubles),
+ * the same quantities dycl_profile_read sums.  Returns the number of
+ * launches of that run (which may exceed cap); synchronises like
+ * dycl_profile_read.
+ */
+int dycl_profile_launches(dycl_plan* plan, double* rows, int cap);
+
+/*
  * Host-only validation of a spec against a blob size and a batch bound (no
  * HIP call): parses, checks every reference and weight range, propagates
  * shapes, and writes a one-line summary into `summary` (may be NULL).

@@ -156,6 +156,21 @@ int dycl_profile_read(dycl_plan* plan, double* rows, int cap) {
   return dycl::P_COUNT;
 }
 
+int dycl_profile_launches(dycl_plan* plan, double* rows, int cap) {
+  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_profile_launches: invalid plan handle");
+  if (cap < 0 || (cap > 0 && !rows)) return fail(DYCL_E_INVALID, "dycl_profile_launches: bad buffer");
+  int rc = guarded([&] {
+    hipSetDevice(plan->device);
+    dycl::profile_flush(plan);
+    return DYCL_OK;
+  });
+  if (rc != DYCL_OK) return rc;
+  const size_t n = plan->last_run.size();
+  for (size_t i = 0; i < n && i < static_cast<size_t>(cap); ++i)
+    for (int j = 0; j < 4; ++j) rows[4 * i + j] = plan->last_run[i][j];
+  return static_cast<int>(n);
+}
+
 const char* dycl_profile_class(int i) {
   if (i < 0 || i >= dycl::P_COUNT) return "";
   return kClassNames[i];

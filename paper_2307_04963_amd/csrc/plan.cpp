@@ -557,6 +557,10 @@ void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logit
   hip_check(hipSetDevice(p->device), "hipSetDevice");
   p->last_stream = s;
   if (p->pending.size() > 8192) profile_flush(p);
+  if (p->profile) {
+    p->last_run.clear();
+    p->last_run_begin = p->pending.size();
+  }
   Run r;
   r.p = p;
   r.aux = aux;
@@ -646,7 +650,8 @@ void plan_read_counts(const dycl_plan* p, int32_t* out, int n) {
 }
 
 void profile_flush(dycl_plan* p) {
-  for (auto& e : p->pending) {
+  for (size_t i = 0; i < p->pending.size(); ++i) {
+    auto& e = p->pending[i];
     hip_check(hipEventSynchronize(e.b), "hipEventSynchronize");
     float ms = 0.f;
     hip_check(hipEventElapsedTime(&ms, e.a, e.b), "hipEventElapsedTime");
@@ -655,10 +660,12 @@ void profile_flush(dycl_plan* p) {
     row.ms += ms;
     row.flops += e.flops;
     row.bytes += e.bytes;
+    if (i >= p->last_run_begin) p->last_run.push_back({static_cast<double>(e.cls), ms, e.flops, e.bytes});
     p->ev_free.push_back(e.a);
     p->ev_free.push_back(e.b);
   }
   p->pending.clear();
+  p->last_run_begin = 0;
 }
 
 }  // namespace dycl

@@ -13,6 +13,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <array>
 #include <cstdint>
 #include <string>
 #include <utility>
@@ -142,6 +143,9 @@ struct dycl_plan {
   };
   std::vector<Pending> pending;
   dycl::ProfileRow prof[dycl::P_COUNT];
+  // launches of the last profiled run: {class, ms, flops, bytes}
+  std::vector<std::array<double, 4>> last_run;
+  size_t last_run_begin = 0;
   hipStream_t last_stream = nullptr;
   // host mode (dycl_host_mode) and the last run's: whether its branch
   // counts are only in d_counts (device modes)

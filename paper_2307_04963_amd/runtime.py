@@ -95,6 +95,14 @@ class Plan:
                          "bytes": rows[4 * c + 3]}
         return out
 
+    def profile_launches(self) -> list:
+        """Every launch of the last profiled run: class, ms, flops, bytes."""
+        n = check(lib.dycl_profile_launches(self._h, None, 0))
+        rows = (C.c_double * (4 * max(n, 1)))()
+        n = min(n, check(lib.dycl_profile_launches(self._h, rows, n)))
+        return [{"class": lib.dycl_profile_class(int(rows[4 * i])).decode(), "ms": rows[4 * i + 1],
+                 "flops": rows[4 * i + 2], "bytes": rows[4 * i + 3]} for i in range(n)]
+
 
 def decode_records(rec: np.ndarray):
     """int32 [B, 4] -> (exit_index, iterations, skip_mask)."""
