@@ -42,6 +42,7 @@ struct ConvP {
   int mt, nt;
   const int32_t* nc;       // device count of live images (<= nmax) or null
   int nmax;                // images the grid is sized for
+  const int32_t* rows;     // input image of output image i: rows[i] (a fused gather), or null: i
   int ksplit;              // K ranges per tile (conv_lds_kernel); > 1: fp32 partials to `part`
   float* part;             // [ksplit][M][cout] partial sums (rows of the nmax images)
   const uint16_t* w;
@@ -110,9 +111,10 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
       const int img = m / HoWo;
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
+      const int simg = p.rows ? p.rows[img] : img;
       a_ih[i] = oh * p.stride - p.pad;
       a_iw[i] = ow * p.stride - p.pad;
-      a_pix[i] = (img * p.H + a_ih[i]) * p.W + a_iw[i];
+      a_pix[i] = (simg * p.H + a_ih[i]) * p.W + a_iw[i];
     } else {
       a_ih[i] = -0x4000;
       a_iw[i] = -0x4000;
@@ -340,9 +342,10 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
       const int img = m / HoWo;
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
+      const int simg = p.rows ? p.rows[img] : img;
       a_ih[j] = oh * p.stride - p.pad;
       a_iw[j] = ow * p.stride - p.pad;
-      a_pix[j] = (img * p.H + a_ih[j]) * p.W + a_iw[j];
+      a_pix[j] = (simg * p.H + a_ih[j]) * p.W + a_iw[j];
     } else {
       a_ih[j] = -0x4000;
       a_iw[j] = -0x4000;
@@ -1531,6 +1534,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.nmax = a.n;
   p.ksplit = 1;
   p.part = nullptr;
+  p.rows = a.src_rows;
 
   // 16-byte A vectors need Cin % 8 == 0, and a power-of-two Cin when the tap
   // index is split off with a shift; anything else gathers element by element
@@ -1556,7 +1560,9 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   // the direct-to-LDS kernel stores 8 channels per 16-byte vector
   const bool vec_out = a.cout % 8 == 0 && (reinterpret_cast<uintptr_t>(a.dst) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
-  if (vec_out && (conv3_wres(a, s) || conv3_halo(a, s))) return;
+  // the halo kernels stage whole images from contiguous rows: a layer that
+  // reads its input through a row list takes the implicit GEMM
+  if (vec_out && !a.src_rows && (conv3_wres(a, s) || conv3_halo(a, s))) return;
   if (vec_out) {
     // deep K on few pixels per image: K ranges of one tile on several
     // workgroups, fp32 partials summed in a fixed order by a second kernel

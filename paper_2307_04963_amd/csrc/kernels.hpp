@@ -46,6 +46,7 @@ struct ConvArgs {
   const uint16_t* zeros; // >= 16 zero bytes on the device (padding taps)
   const int32_t* ncount = nullptr;  // device count of live images (<= n) or null
   int nhint = 0;                    // expected live images for the tile choice (0: n)
+  const int32_t* src_rows = nullptr; // image i of the input is image src_rows[i] of src (a fused gather), or null
   float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split
   size_t splitws_bytes = 0;
 };

@@ -40,7 +40,7 @@ void assign_buffers(dycl_plan* p, int max_batch) {
   Spec& sp = p->spec;
   std::vector<int> order;
   for (int i = 0; i < static_cast<int>(sp.tensors.size()); ++i)
-    if (!sp.tensors[i].external) order.push_back(i);
+    if (!sp.tensors[i].external && !sp.tensors[i].unused) order.push_back(i);
   std::sort(order.begin(), order.end(), [&](int a, int b) { return sp.tensors[a].first < sp.tensors[b].first; });
   std::vector<int> active;
   std::vector<bool> busy;
@@ -383,6 +383,7 @@ struct Run {
     a.zeros = p->d_zeros;
     a.ncount = r.nc;
     a.nhint = r.hint;
+    a.src_rows = nd.src_rows ? p->d_idx0 : nullptr;
     a.splitws = p->d_split;
     a.splitws_bytes = p->split_bytes;
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
@@ -525,7 +526,8 @@ struct Run {
     Spec& sp = p->spec;
     tp.resize(sp.tensors.size());
     for (size_t t = 0; t < sp.tensors.size(); ++t)
-      tp[t] = sp.tensors[t].external ? const_cast<void*>(x) : p->buffers[sp.tensors[t].buf];
+      tp[t] = sp.tensors[t].external ? const_cast<void*>(x)
+              : sp.tensors[t].unused ? nullptr : p->buffers[sp.tensors[t].buf];
     orig = p->d_iota;
     launch(P_MISC, 0, 16.0 * B, [&] { k::init_records(rec, B, s); });
     if (sp.any_halt) launch(P_MISC, 0, 4.0 * B, [&] { k::fill_f32(p->d_S, 0.f, B, s); });

@@ -34,6 +34,7 @@ struct TensorInfo {
   bool external = false;   // the caller's input
   bool parked = false;     // full batch, original sample order
   int first = -1, last = -1;   // liveness (node sequence numbers)
+  bool unused = false;     // never materialised (its readers go through a row list)
   int buf = -1;
   size_t row_bytes(DType dt) const { return (size_t)H * W * C * (dt == DType::BF16 ? 2 : 4); }
 };
@@ -53,6 +54,7 @@ struct Node {
   int64_t scale_off = -1, shift_off = -1;    // fp32 [cout] byte offsets (or -1)
   int packed = -1;                           // index of packed bf16 weights
   bool pad_in = false;                       // reads the input padded to 8 channels
+  bool src_rows = false;                     // reads src through the stay list of the last exit
   // heads: exit W [ncls][C], b [ncls], T [1]; gate u [C], v [1]; halt w [C]
   int64_t h_w = -1, h_b = -1, h_T = -1;
   int ncls = 0, hc = 0;
@@ -98,10 +100,12 @@ struct Spec {
   int max_head_c = 8, max_ncls = 8;
   int nodes_total = 0;
   int pad_input_c = 0;
+  int fused_gathers = 0;   // exit carries read in place through the row list
   int n_head_t = 0;      // fp32 weight matrices kept transposed on the device   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
 
   void parse(const std::string& json, size_t weights_bytes, int max_batch);
+  void fuse_exit_gathers();
 };
 
 }  // namespace dycl

@@ -388,6 +388,72 @@ struct Builder {
 
 }  // namespace
 
+namespace {
+
+// Every read of tensor t: the reading node, whether it is a conv's main
+// input, and the node's index among the top-level nodes (-1 inside a body).
+struct Use {
+  Node* node;
+  bool conv_src;
+  long top;
+};
+
+void uses_of(std::vector<Node>& nodes, int t, long top, std::vector<Use>& out) {
+  for (size_t i = 0; i < nodes.size(); ++i) {
+    Node& nd = nodes[i];
+    const long at = top < 0 ? static_cast<long>(i) : -1;
+    bool other = nd.src2 == t || nd.res == t || nd.park_src == t;
+    for (auto& pr : nd.pairs) other = other || pr.first == t;
+    for (auto& pr : nd.scatter) other = other || pr.first == t;
+    if (nd.src == t) out.push_back({&nd, nd.kind == NodeKind::Conv, at});
+    if (other) out.push_back({&nd, false, at});
+    uses_of(nd.body, t, 0, out);
+  }
+}
+
+bool is_decision(const Node& nd) {
+  return nd.kind == NodeKind::Exit || nd.kind == NodeKind::Gate || nd.kind == NodeKind::Halt;
+}
+
+}  // namespace
+
+// The gather of an exit's carried tensor fused into its readers (a row
+// gather is a copy that computes nothing): when every reader of the carried
+// copy is a bf16 convolution that takes it as its main input before the next
+// decision, the readers take the surviving rows of the original tensor
+// through the exit's stay list and the copy is never made.
+void Spec::fuse_exit_gathers() {
+  if (dt != DType::BF16) return;
+  for (size_t i = 0; i < nodes.size(); ++i) {
+    Node& ex = nodes[i];
+    if (ex.kind != NodeKind::Exit || ex.final_) continue;
+    size_t next = i + 1;
+    while (next < nodes.size() && !is_decision(nodes[next])) ++next;
+    for (size_t q = 0; q < ex.pairs.size();) {
+      const int from = ex.pairs[q].first, to = ex.pairs[q].second;
+      std::vector<Use> us;
+      uses_of(nodes, to, -1, us);
+      bool ok = !us.empty();
+      for (const Use& u : us)
+        ok = ok && u.conv_src && u.top > static_cast<long>(i) && u.top < static_cast<long>(next) && !u.node->pad_in &&
+             u.node->src2 < 0;
+      if (!ok) {
+        ++q;
+        continue;
+      }
+      for (const Use& u : us) {
+        u.node->src = from;
+        u.node->src_rows = true;
+        TensorInfo& f = tensors[from];
+        f.last = std::max(f.last, u.node->seq_pre);
+      }
+      tensors[to].unused = true;
+      ex.pairs.erase(ex.pairs.begin() + q);
+      ++fused_gathers;
+    }
+  }
+}
+
 void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   *this = Spec();
   Json j = Json::parse(json);
@@ -425,6 +491,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   const Json& ns = j.at("nodes");
   if (ns.kind != Json::Array || ns.size() == 0) throw SpecError("nodes must be a non-empty array");
   for (size_t i = 0; i < ns.size(); ++i) nodes.push_back(b.node(ns.at(i), max_batch));
+  fuse_exit_gathers();
 
   // every tensor that is moved between row groups must be a whole number of
   // 16-byte vectors, and a whole batch of it must be indexable with 32-bit
@@ -438,7 +505,8 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
 
   std::ostringstream os;
   os << "nodes=" << nodes_total << " decisions=" << decisions << " tensors=" << tensors.size()
-     << " packed_weights=" << packed.size() << " n_out=" << n_out << " dtype=" << dts;
+     << " packed_weights=" << packed.size() << " fused_gathers=" << fused_gathers << " n_out=" << n_out
+     << " dtype=" << dts;
   summary = os.str();
 }
 

@@ -64,6 +64,30 @@ def test_every_workload_spec_validates(name):
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
 
 
+def test_exit_gathers_fused_only_into_plain_conv_readers():
+    # an exit's carried copy is never made when only convolutions read it,
+    # as their main input, before the next decision; any other reader (a
+    # residual here) keeps the copy
+    wl = configs.build("resnet18_exit")
+    blob, man = wl.blob()
+    spec = lowering.lower(wl.arch, man)
+    rc, msg = _check(json.dumps(spec), len(blob), 64)
+    assert rc == 0 and "fused_gathers=3" in msg, msg
+    # a carried tensor that is also a residual keeps its copy
+    toy = {"version": 1, "dtype": "bf16", "input": {"name": "x", "shape": [8, 8, 64]}, "n_out": 10, "nodes": [
+        {"op": "conv", "src": "x", "dst": "a", "k": 1, "cout": 64, "act": "relu", "w": {"off": 0}},
+        {"op": "exit", "src": "a", "w": 8192, "b": 8192 + 2560, "T": 8192 + 2600, "ncls": 10, "tau": 0.5,
+         "index": 0, "final": False, "carry": [["a", "ac"]]},
+        {"op": "conv", "src": "ac", "dst": "b", "k": 1, "cout": 64, "act": "relu", "w": {"off": 0}},
+        {"op": "conv", "src": "b", "dst": "c", "k": 1, "cout": 64, "act": "relu", "w": {"off": 0}, "res": "ac"},
+        {"op": "exit", "src": "c", "w": 8192, "b": 8192 + 2560, "ncls": 10, "index": 1, "final": True}]}
+    rc, msg = _check(json.dumps(toy), 16384)
+    assert rc == 0 and "fused_gathers=0" in msg, msg
+    toy["nodes"][3]["res"] = None
+    rc, msg = _check(json.dumps(toy), 16384)
+    assert rc == 0 and "fused_gathers=1" in msg, msg
+
+
 def _mlp_spec():
     wl = configs.build("mlp_exit")
     blob, man = wl.blob()
