@@ -42,7 +42,12 @@ struct ConvP {
   int mt, nt;
   const int32_t* nc;       // device count of live images (<= nmax) or null
   int nmax;                // images the grid is sized for
-  const int32_t* rows;     // input image of output image i: rows[i] (a fused gather), or null: i
+  // fused gathers / scatters: image i of the layer reads input image
+  // srows[i] and residual image rrows[i] and writes output image drows[i]
+  // (null: i)
+  const int32_t* srows;
+  const int32_t* rrows;
+  const int32_t* drows;
   int ksplit;              // K ranges per tile (conv_lds_kernel); > 1: fp32 partials to `part`
   float* part;             // [ksplit][M][cout] partial sums (rows of the nmax images)
   const uint16_t* w;
@@ -62,6 +67,14 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 }
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
+
+// the element row (image * HoWo + pixel) that layer row `row` maps to
+// through an image list (null: itself)
+__device__ __forceinline__ size_t row_at(const int32_t* rows, int row, int HoWo) {
+  if (!rows) return static_cast<size_t>(row);
+  const int img = row / HoWo;
+  return static_cast<size_t>(rows[img]) * HoWo + (row - img * HoWo);
+}
 
 __device__ __forceinline__ float apply_act(float v, int act) {
   if (act == ACT_RELU) return v > 0.f ? v : 0.f;
@@ -111,7 +124,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
       const int img = m / HoWo;
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
-      const int simg = p.rows ? p.rows[img] : img;
+      const int simg = p.srows ? p.srows[img] : img;
       a_ih[i] = oh * p.stride - p.pad;
       a_iw[i] = ow * p.stride - p.pad;
       a_pix[i] = (simg * p.H + a_ih[i]) * p.W + a_iw[i];
@@ -261,9 +274,9 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * WTM + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         if (row >= M) continue;
-        const size_t o = (size_t)row * p.cout + col;
+        const size_t o = row_at(p.drows, row, HoWo) * p.cout + col;
         float v = fmaf(acc[a][b][r], sc, sh);
-        if (p.res) v += bf2f(p.res[o]);
+        if (p.res) v += bf2f(p.res[row_at(p.rrows, row, HoWo) * p.cout + col]);
         v = apply_act(v, p.act);
         if (p.out_f32)
           static_cast<float*>(p.dst)[o] = v;
@@ -342,7 +355,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
       const int img = m / HoWo;
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
-      const int simg = p.rows ? p.rows[img] : img;
+      const int simg = p.srows ? p.srows[img] : img;
       a_ih[j] = oh * p.stride - p.pad;
       a_iw[j] = ow * p.stride - p.pad;
       a_pix[j] = (simg * p.H + a_ih[j]) * p.W + a_iw[j];
@@ -481,15 +494,15 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
         const float4 lo = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8);
         const float4 hi = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8 + 4);
         float vv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        const size_t o = (size_t)row * p.cout + col;
         if (partial) {
-          float* d = p.part + (size_t)split * p.M * p.cout + o;
+          float* d = p.part + (size_t)split * p.M * p.cout + (size_t)row * p.cout + col;
           *reinterpret_cast<float4*>(d) = lo;
           *reinterpret_cast<float4*>(d + 4) = hi;
           continue;
         }
+        const size_t o = row_at(p.drows, row, HoWo) * p.cout + col;
         if (p.res) {
-          const uint4 rv = *reinterpret_cast<const uint4*>(p.res + o);
+          const uint4 rv = *reinterpret_cast<const uint4*>(p.res + row_at(p.rrows, row, HoWo) * p.cout + col);
           const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -1534,7 +1547,9 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.nmax = a.n;
   p.ksplit = 1;
   p.part = nullptr;
-  p.rows = a.src_rows;
+  p.srows = a.src_rows;
+  p.rrows = a.res_rows;
+  p.drows = a.dst_rows;
 
   // 16-byte A vectors need Cin % 8 == 0, and a power-of-two Cin when the tap
   // index is split off with a shift; anything else gathers element by element
@@ -1562,13 +1577,14 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
   // the halo kernels stage whole images from contiguous rows: a layer that
   // reads its input through a row list takes the implicit GEMM
-  if (vec_out && !a.src_rows && (conv3_wres(a, s) || conv3_halo(a, s))) return;
+  const bool listed = a.src_rows || a.res_rows || a.dst_rows;
+  if (vec_out && !listed && (conv3_wres(a, s) || conv3_halo(a, s))) return;
   if (vec_out) {
     // deep K on few pixels per image: K ranges of one tile on several
     // workgroups, fp32 partials summed in a fixed order by a second kernel
     // (the split depends on the layer's shape only, never on n)
     const int S = conv_ksplit(a.Ho, a.Wo, a.cout, p.K, a.out_f32 != 0);
-    const bool split = S > 1 && a.splitws &&
+    const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
                             : choose_lds(Mh, a.cout, p.Kp);

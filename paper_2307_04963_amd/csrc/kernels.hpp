@@ -46,7 +46,11 @@ struct ConvArgs {
   const uint16_t* zeros; // >= 16 zero bytes on the device (padding taps)
   const int32_t* ncount = nullptr;  // device count of live images (<= n) or null
   int nhint = 0;                    // expected live images for the tile choice (0: n)
-  const int32_t* src_rows = nullptr; // image i of the input is image src_rows[i] of src (a fused gather), or null
+  // fused gathers / scatters: image i of the layer reads image src_rows[i]
+  // of src and res_rows[i] of res and writes image dst_rows[i] of dst (null: i)
+  const int32_t* src_rows = nullptr;
+  const int32_t* res_rows = nullptr;
+  const int32_t* dst_rows = nullptr;
   float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split
   size_t splitws_bytes = 0;
 };

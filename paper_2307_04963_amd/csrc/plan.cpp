@@ -383,7 +383,10 @@ struct Run {
     a.zeros = p->d_zeros;
     a.ncount = r.nc;
     a.nhint = r.hint;
-    a.src_rows = nd.src_rows ? p->d_idx0 : nullptr;
+    auto list = [&](int which) -> const int32_t* { return which == 1 ? p->d_idx0 : which == 2 ? p->d_idx1 : nullptr; };
+    a.src_rows = list(nd.src_list);
+    a.res_rows = list(nd.res_list);
+    a.dst_rows = list(nd.dst_list);
     a.splitws = p->d_split;
     a.splitws_bytes = p->split_bytes;
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +

@@ -54,7 +54,10 @@ struct Node {
   int64_t scale_off = -1, shift_off = -1;    // fp32 [cout] byte offsets (or -1)
   int packed = -1;                           // index of packed bf16 weights
   bool pad_in = false;                       // reads the input padded to 8 channels
-  bool src_rows = false;                     // reads src through the stay list of the last exit
+  // fused gathers / scatters: which row list of the last decision maps this
+  // layer's images to those of src, res, dst (0: none, 1: the rows that
+  // stay (exit), 2: the rows that take the true branch (gate body))
+  int src_list = 0, res_list = 0, dst_list = 0;
   // heads: exit W [ncls][C], b [ncls], T [1]; gate u [C], v [1]; halt w [C]
   int64_t h_w = -1, h_b = -1, h_T = -1;
   int ncls = 0, hc = 0;
@@ -101,11 +104,13 @@ struct Spec {
   int nodes_total = 0;
   int pad_input_c = 0;
   int fused_gathers = 0;   // exit carries read in place through the row list
+  int fused_gates = 0;     // gates whose gathers and scatters are fused into the body convolutions
   int n_head_t = 0;      // fp32 weight matrices kept transposed on the device   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
 
   void parse(const std::string& json, size_t weights_bytes, int max_batch);
   void fuse_exit_gathers();
+  void fuse_gate_moves();
 };
 
 }  // namespace dycl

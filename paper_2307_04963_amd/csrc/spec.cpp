@@ -443,7 +443,7 @@ void Spec::fuse_exit_gathers() {
       }
       for (const Use& u : us) {
         u.node->src = from;
-        u.node->src_rows = true;
+        u.node->src_list = 1;
         TensorInfo& f = tensors[from];
         f.last = std::max(f.last, u.node->seq_pre);
       }
@@ -451,6 +451,84 @@ void Spec::fuse_exit_gathers() {
       ex.pairs.erase(ex.pairs.begin() + q);
       ++fused_gathers;
     }
+  }
+}
+
+// A gate's gathers and scatters fused into its body (Sec. 5.4: copies that
+// compute nothing stay out of the sub-DNN): the body convolutions read the
+// outer tensors through the gate's list of executing rows, and the layer that
+// produces a scattered value writes it straight into the outer tensor's rows.
+// Only for bodies of convolutions that run on the implicit GEMM anyway (the
+// halo kernels stage contiguous images), whose gathered copies are read only
+// as main input or residual, and whose scattered values are each written by
+// one convolution that reads its target at most as its residual (an element
+// read and then written by the same thread).
+void Spec::fuse_gate_moves() {
+  if (dt != DType::BF16) return;
+  auto halo_kind = [](const Node& nd, const TensorInfo& src) {
+    return nd.k == 3 && nd.stride == 1 && nd.pad == 1 && nd.src2 < 0 && nd.cin1 % 64 == 0 && nd.cout % 64 == 0 &&
+           !(src.H * src.W <= 128 && 2 * src.H * src.W < (src.H + 2) * (src.W + 2));
+  };
+  for (Node& g : nodes) {
+    if (g.kind != NodeKind::Gate) continue;
+    bool ok = !g.body.empty();
+    for (const Node& b : g.body) ok = ok && b.kind == NodeKind::Conv && !halo_kind(b, tensors[b.src]);
+    if (!ok) continue;
+    std::map<int, int> outer_of;   // gathered copy -> outer tensor
+    for (auto& pr : g.pairs) outer_of[pr.second] = pr.first;
+    for (const Node& b : g.body) {
+      if (b.src2 >= 0 && outer_of.count(b.src2)) ok = false;
+      if (b.dst >= 0 && outer_of.count(b.dst)) ok = false;
+    }
+    std::map<int, int> writer;     // scattered value -> index of the body conv that writes it
+    for (auto& pr : g.scatter) {
+      int w = -1, readers = 0;
+      for (size_t j = 0; j < g.body.size(); ++j) {
+        const Node& b = g.body[j];
+        if (b.dst == pr.first) w = static_cast<int>(j);
+        if (b.src == pr.first || b.src2 == pr.first || b.res == pr.first) ++readers;
+      }
+      if (w < 0 || readers) ok = false;
+      for (auto& q : g.scatter)
+        if (&q != &pr && q.first == pr.first) ok = false;
+      writer[pr.first] = w;
+    }
+    if (!ok) continue;
+    // the writer must not read its own target but as the residual, and no
+    // body conv after it may read the target at all
+    for (auto& pr : g.scatter) {
+      const int w = writer[pr.first];
+      const int target = pr.second;
+      for (size_t j = 0; j < g.body.size(); ++j) {
+        const Node& b = g.body[j];
+        auto is_target = [&](int t) { return t >= 0 && (t == target || (outer_of.count(t) && outer_of[t] == target)); };
+        if (static_cast<int>(j) == w && (is_target(b.src) || is_target(b.src2))) ok = false;
+        if (static_cast<int>(j) > w && (is_target(b.src) || is_target(b.src2) || is_target(b.res))) ok = false;
+      }
+    }
+    if (!ok) continue;
+    for (Node& b : g.body) {
+      if (outer_of.count(b.src)) {
+        b.src = outer_of[b.src];
+        b.src_list = 2;
+        tensors[b.src].last = std::max(tensors[b.src].last, b.seq_pre);
+      }
+      if (b.res >= 0 && outer_of.count(b.res)) {
+        b.res = outer_of[b.res];
+        b.res_list = 2;
+        tensors[b.res].last = std::max(tensors[b.res].last, b.seq_pre);
+      }
+    }
+    for (auto& pr : g.scatter) {
+      Node& b = g.body[writer[pr.first]];
+      tensors[pr.first].unused = true;
+      b.dst = pr.second;
+      b.dst_list = 2;
+    }
+    for (auto& pr : g.pairs) tensors[pr.second].unused = true;
+    g.pairs.clear();
+    g.scatter.clear();
+    ++fused_gates;
   }
 }
 
@@ -492,6 +570,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   if (ns.kind != Json::Array || ns.size() == 0) throw SpecError("nodes must be a non-empty array");
   for (size_t i = 0; i < ns.size(); ++i) nodes.push_back(b.node(ns.at(i), max_batch));
   fuse_exit_gathers();
+  fuse_gate_moves();
 
   // every tensor that is moved between row groups must be a whole number of
   // 16-byte vectors, and a whole batch of it must be indexable with 32-bit
@@ -505,7 +584,8 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
 
   std::ostringstream os;
   os << "nodes=" << nodes_total << " decisions=" << decisions << " tensors=" << tensors.size()
-     << " packed_weights=" << packed.size() << " fused_gathers=" << fused_gathers << " n_out=" << n_out
+     << " packed_weights=" << packed.size() << " fused_gathers=" << fused_gathers
+     << " fused_gates=" << fused_gates << " n_out=" << n_out
      << " dtype=" << dts;
   summary = os.str();
 }

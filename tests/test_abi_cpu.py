@@ -59,6 +59,12 @@ def test_every_workload_spec_validates(name):
     decisions = int(re.search(r"decisions=(\d+)", msg).group(1))
     want = {"mlp_exit": 3, "resnet18_exit": 4, "skipnet38": 19, "resnet50_exit": 4, "act_loop": 16}[name]
     assert decisions == want
+    # row moves fused into the convolutions: exit carries read in place, gate
+    # gathers / scatters of bodies that run on the implicit GEMM
+    fg = int(re.search(r"fused_gathers=(\d+)", msg).group(1))
+    fgt = int(re.search(r"fused_gates=(\d+)", msg).group(1))
+    assert (fg, fgt) == {"mlp_exit": (0, 0), "resnet18_exit": (3, 0), "skipnet38": (0, 12),
+                         "resnet50_exit": (3, 0), "act_loop": (0, 0)}[name]
     # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
     if name == "act_loop":
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
