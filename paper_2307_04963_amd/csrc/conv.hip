@@ -46,6 +46,7 @@ struct ConvP {
   // srows[i] and residual image rrows[i] and writes output image drows[i]
   // (null: i)
   const int32_t* srows;
+  const int32_t* s2rows;   // image list of src2 (the concatenated input)
   const int32_t* rrows;
   const int32_t* drows;
   int ksplit;              // K ranges per tile (conv_lds_kernel); > 1: fp32 partials to `part`
@@ -116,7 +117,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
 
   // per A row: pixel index of the window origin and its (ih0, iw0); rows
   // past M get an origin far outside the image, so every tap reads zero
-  int a_pix[PA], a_ih[PA], a_iw[PA];
+  int a_pix[PA], a_pix2[PA], a_ih[PA], a_iw[PA];
 #pragma unroll
   for (int i = 0; i < PA; ++i) {
     const int m = m0 + rsub + i * RPP;
@@ -125,13 +126,16 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
       const int simg = p.srows ? p.srows[img] : img;
+      const int s2img = p.s2rows ? p.s2rows[img] : img;
       a_ih[i] = oh * p.stride - p.pad;
       a_iw[i] = ow * p.stride - p.pad;
       a_pix[i] = (simg * p.H + a_ih[i]) * p.W + a_iw[i];
+      a_pix2[i] = (s2img * p.H + a_ih[i]) * p.W + a_iw[i];
     } else {
       a_ih[i] = -0x4000;
       a_iw[i] = -0x4000;
       a_pix[i] = 0;
+      a_pix2[i] = 0;
     }
   }
 
@@ -168,7 +172,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
         uint4 v = make_uint4(0, 0, 0, 0);
         const int ih = a_ih[i] + kh, iw = a_iw[i] + kw;
         if (kok && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W && rsub + i * RPP < BM)
-          v = *reinterpret_cast<const uint4*>(sp + (size_t)(a_pix[i] + doff) * cs + co);
+          v = *reinterpret_cast<const uint4*>(sp + (size_t)((ci >= p.cin1 ? a_pix2[i] : a_pix[i]) + doff) * cs + co);
         ra[i] = v;
       }
     } else {
@@ -347,7 +351,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   const int rbase = tid >> 3;                        // + j * NT / 8
   const int HoWo = p.Ho * p.Wo;
 
-  int a_pix[JA], a_ih[JA], a_iw[JA];
+  int a_pix[JA], a_pix2[JA], a_ih[JA], a_iw[JA];
 #pragma unroll
   for (int j = 0; j < JA; ++j) {
     const int m = m0 + rbase + j * (NT / 8);
@@ -356,13 +360,16 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
       const int rem = m - img * HoWo;
       const int oh = rem / p.Wo, ow = rem - (rem / p.Wo) * p.Wo;
       const int simg = p.srows ? p.srows[img] : img;
+      const int s2img = p.s2rows ? p.s2rows[img] : img;
       a_ih[j] = oh * p.stride - p.pad;
       a_iw[j] = ow * p.stride - p.pad;
       a_pix[j] = (simg * p.H + a_ih[j]) * p.W + a_iw[j];
+      a_pix2[j] = (s2img * p.H + a_ih[j]) * p.W + a_iw[j];
     } else {
       a_ih[j] = -0x4000;
       a_iw[j] = -0x4000;
       a_pix[j] = 0;
+      a_pix2[j] = 0;
     }
   }
   const uint16_t* wrow = p.w + (size_t)(n0 + rbase) * p.Kp + lchunk * 8;
@@ -395,7 +402,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
     for (int j = 0; j < JA; ++j) {
       const int ih = a_ih[j] + kh, iw = a_iw[j] + kw;
       const bool ok = kok && (unsigned)ih < (unsigned)p.H && (unsigned)iw < (unsigned)p.W;
-      const uint16_t* g = ok ? sp + (size_t)(a_pix[j] + doff) * cs + co : p.zeros;
+      const uint16_t* g = ok ? sp + (size_t)((ci >= p.cin1 ? a_pix2[j] : a_pix[j]) + doff) * cs + co : p.zeros;
       __builtin_amdgcn_global_load_lds((const void*)g, (lds_void_ptr)(sb + (j * NT + wave * 64) * 16), 16, 0, 0);
     }
 #pragma unroll
@@ -1548,6 +1555,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.ksplit = 1;
   p.part = nullptr;
   p.srows = a.src_rows;
+  p.s2rows = a.src2_rows;
   p.rrows = a.res_rows;
   p.drows = a.dst_rows;
 
@@ -1577,7 +1585,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
   // the halo kernels stage whole images from contiguous rows: a layer that
   // reads its input through a row list takes the implicit GEMM
-  const bool listed = a.src_rows || a.res_rows || a.dst_rows;
+  const bool listed = a.src_rows || a.src2_rows || a.res_rows || a.dst_rows;
   if (vec_out && !listed && (conv3_wres(a, s) || conv3_halo(a, s))) return;
   if (vec_out) {
     // deep K on few pixels per image: K ranges of one tile on several

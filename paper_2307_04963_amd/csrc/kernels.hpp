@@ -49,6 +49,7 @@ struct ConvArgs {
   // fused gathers / scatters: image i of the layer reads image src_rows[i]
   // of src and res_rows[i] of res and writes image dst_rows[i] of dst (null: i)
   const int32_t* src_rows = nullptr;
+  const int32_t* src2_rows = nullptr;
   const int32_t* res_rows = nullptr;
   const int32_t* dst_rows = nullptr;
   float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split

@@ -383,8 +383,11 @@ struct Run {
     a.zeros = p->d_zeros;
     a.ncount = r.nc;
     a.nhint = r.hint;
-    auto list = [&](int which) -> const int32_t* { return which == 1 ? p->d_idx0 : which == 2 ? p->d_idx1 : nullptr; };
+    auto list = [&](int which) -> const int32_t* {
+      return which == 1 ? p->d_idx0 : which == 2 ? p->d_idx1 : which == 3 ? orig : nullptr;
+    };
     a.src_rows = list(nd.src_list);
+    a.src2_rows = list(nd.src2_list);
     a.res_rows = list(nd.res_list);
     a.dst_rows = list(nd.dst_list);
     a.splitws = p->d_split;

@@ -56,8 +56,9 @@ struct Node {
   bool pad_in = false;                       // reads the input padded to 8 channels
   // fused gathers / scatters: which row list of the last decision maps this
   // layer's images to those of src, res, dst (0: none, 1: the rows that
-  // stay (exit), 2: the rows that take the true branch (gate body))
-  int src_list = 0, res_list = 0, dst_list = 0;
+  // stay (exit, halt), 2: the rows that take the true branch (gate body),
+  // 3: the original sample ids of the current rows)
+  int src_list = 0, src2_list = 0, res_list = 0, dst_list = 0;
   // heads: exit W [ncls][C], b [ncls], T [1]; gate u [C], v [1]; halt w [C]
   int64_t h_w = -1, h_b = -1, h_T = -1;
   int ncls = 0, hc = 0;
@@ -109,6 +110,7 @@ struct Spec {
   std::string summary;
 
   void parse(const std::string& json, size_t weights_bytes, int max_batch);
+  void fuse_original_order_reads();
   void fuse_exit_gathers();
   void fuse_gate_moves();
 };

@@ -426,7 +426,7 @@ void Spec::fuse_exit_gathers() {
   if (dt != DType::BF16) return;
   for (size_t i = 0; i < nodes.size(); ++i) {
     Node& ex = nodes[i];
-    if (ex.kind != NodeKind::Exit || ex.final_) continue;
+    if (!((ex.kind == NodeKind::Exit && !ex.final_) || ex.kind == NodeKind::Halt)) continue;
     size_t next = i + 1;
     while (next < nodes.size() && !is_decision(nodes[next])) ++next;
     for (size_t q = 0; q < ex.pairs.size();) {
@@ -436,7 +436,7 @@ void Spec::fuse_exit_gathers() {
       bool ok = !us.empty();
       for (const Use& u : us)
         ok = ok && u.conv_src && u.top > static_cast<long>(i) && u.top < static_cast<long>(next) && !u.node->pad_in &&
-             u.node->src2 < 0;
+             (u.node->src2 < 0 || u.node->src2_list == 3);
       if (!ok) {
         ++q;
         continue;
@@ -450,6 +450,53 @@ void Spec::fuse_exit_gathers() {
       tensors[to].unused = true;
       ex.pairs.erase(ex.pairs.begin() + q);
       ++fused_gathers;
+    }
+  }
+}
+
+// Reads of a tensor that is still in sample order, through copies carried
+// across decisions: a convolution reads the original through the original
+// ids of its rows (the list every run keeps), and carries that nothing reads
+// any more are dropped (the bounded loop's input is never copied).
+void Spec::fuse_original_order_reads() {
+  if (dt != DType::BF16) return;
+  std::map<int, int> root;   // carried copy -> the sample-order tensor it copies
+  for (const Node& nd : nodes) {
+    if (nd.kind != NodeKind::Exit && nd.kind != NodeKind::Halt) continue;
+    for (auto& pr : nd.pairs) {
+      const int from = pr.first;
+      if (root.count(from))
+        root[pr.second] = root[from];
+      else if (tensors[from].space == 0 && !tensors[from].parked)
+        root[pr.second] = from;
+    }
+  }
+  if (root.empty()) return;
+  for (Node& nd : nodes) {
+    if (nd.kind != NodeKind::Conv || nd.pad_in) continue;
+    if (nd.src2 >= 0 && root.count(nd.src2)) {
+      nd.src2 = root[nd.src2];
+      nd.src2_list = 3;
+      tensors[nd.src2].last = std::max(tensors[nd.src2].last, nd.seq_pre);
+    }
+  }
+  // drop carries whose copies nothing reads, until none is left
+  for (bool changed = true; changed;) {
+    changed = false;
+    for (Node& nd : nodes) {
+      if (nd.kind != NodeKind::Exit && nd.kind != NodeKind::Halt) continue;
+      for (size_t q = 0; q < nd.pairs.size();) {
+        std::vector<Use> us;
+        uses_of(nodes, nd.pairs[q].second, -1, us);
+        if (!us.empty()) {
+          ++q;
+          continue;
+        }
+        tensors[nd.pairs[q].second].unused = true;
+        nd.pairs.erase(nd.pairs.begin() + q);
+        ++fused_gathers;
+        changed = true;
+      }
     }
   }
 }
@@ -569,6 +616,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   const Json& ns = j.at("nodes");
   if (ns.kind != Json::Array || ns.size() == 0) throw SpecError("nodes must be a non-empty array");
   for (size_t i = 0; i < ns.size(); ++i) nodes.push_back(b.node(ns.at(i), max_batch));
+  fuse_original_order_reads();
   fuse_exit_gathers();
   fuse_gate_moves();
 

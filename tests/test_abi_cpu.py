@@ -64,7 +64,7 @@ def test_every_workload_spec_validates(name):
     fg = int(re.search(r"fused_gathers=(\d+)", msg).group(1))
     fgt = int(re.search(r"fused_gates=(\d+)", msg).group(1))
     assert (fg, fgt) == {"mlp_exit": (0, 0), "resnet18_exit": (3, 0), "skipnet38": (0, 12),
-                         "resnet50_exit": (3, 0), "act_loop": (0, 0)}[name]
+                         "resnet50_exit": (3, 0), "act_loop": (30, 0)}[name]
     # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
     if name == "act_loop":
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
