@@ -198,7 +198,9 @@ def layer_table(wl, plan, xt, at, logits, rec, stream, warmup):
     plan.profile(True)
     plan.run(xt, at, logits, rec, stream)
     torch.cuda.synchronize()
-    launches = [r for r in plan.profile_launches() if r["class"] in ("conv_bf16_mfma", "linear_f32")]
+    every = plan.profile_launches()
+    launches = [r for r in every if r["class"] in ("conv_bf16_mfma", "linear_f32")]
+    heads = [r for r in every if r["class"] in ("decision_heads", "gather_scatter", "compaction")]
     plan.profile(False)
     rows, cb_f, cb_t = [], 0.0, 0.0
     for i, r in enumerate(launches):
@@ -214,7 +216,13 @@ def layer_table(wl, plan, xt, at, logits, rec, stream, warmup):
                      "flop_per_byte": round(inten, 1), "bound": bound, "tflops": round(tf, 1),
                      "frac_peak": round(tf / PEAK_BF16_TFLOPS, 4), "frac_attainable": round(tf / attain, 4) if attain else None})
     cb = cb_f / (cb_t * 1e-3) / 1e12 if cb_t else 0.0
+    # HBM-bound routing steps of the same step: heads (pooling reads), compaction, row moves
+    hb = [{"class": r["class"], "us": round(r["ms"] * 1e3, 1), "mb": round(r["bytes"] / 1e6, 2),
+           "gbs": round(r["bytes"] / (r["ms"] * 1e-3) / 1e9, 0) if r["ms"] else 0.0,
+           "frac_hbm": round(r["bytes"] / (r["ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if r["ms"] else 0.0}
+          for r in heads]
     return {"workload": wl.name, "batch": int(xt.shape[0]), "branch_counts": plan.counts(), "ridge_flop_per_byte": RIDGE,
+            "hbm_steps": hb,
             "mfma_bound_layers": sum(r["bound"] == "mfma" for r in rows),
             "mfma_bound_flop_weighted_tflops": cb, "mfma_bound_frac_peak": cb / PEAK_BF16_TFLOPS, "layers": rows}
 

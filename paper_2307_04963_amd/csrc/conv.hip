@@ -1294,20 +1294,11 @@ TileCfg choose_lds(int M, int cout, int Kp) {
   return c64;
 }
 
-#ifndef DYCL_DEEP_NS
-#define DYCL_DEEP_NS 2
-#endif
-#ifndef DYCL_DEEP_MIN_K
-#define DYCL_DEEP_MIN_K 8
-#endif
 template <int BM, int BN, int WM, int WN, int KS>
 void go_lds(const ConvP& p, hipStream_t s, int S) {
-  constexpr int kDeep = (BM + BN) * 128 <= 32768 ? DYCL_DEEP_NS : 2;
   const dim3 grid(p.mt * p.nt * S);
   if (p.Kp == 64)
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
-  else if (kDeep > 2 && p.Kp >= 64 * DYCL_DEEP_MIN_K)
-    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, kDeep>), grid, dim3(64 * WM * WN), 0, s, p);
   else
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), grid, dim3(64 * WM * WN), 0, s, p);
 }
