@@ -1294,11 +1294,17 @@ TileCfg choose_lds(int M, int cout, int Kp) {
   return c64;
 }
 
+// stages: one for a single K step; four for 64 x 64 tiles with eight or
+// more K steps (64 KB of LDS: still two workgroups per CU, three steps of
+// loads in flight; measured 1-6 % faster end to end), else two
 template <int BM, int BN, int WM, int WN, int KS>
 void go_lds(const ConvP& p, hipStream_t s, int S) {
   const dim3 grid(p.mt * p.nt * S);
+  constexpr bool small = BM == 64 && BN == 64;
   if (p.Kp == 64)
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
+  else if (small && p.Kp >= 512)
+    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, small ? 4 : 2>), grid, dim3(64 * WM * WN), 0, s, p);
   else
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), grid, dim3(64 * WM * WN), 0, s, p);
 }
