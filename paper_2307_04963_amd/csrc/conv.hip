@@ -1281,20 +1281,27 @@ void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
   }
 }
 
-// direct-to-LDS kernel: the largest tile that still gives the chip enough
-// workgroups (measured on the layer shapes of the workloads)
+// direct-to-LDS kernel.  A workgroup's LDS (two stages) sets how many fit
+// on a CU: two of 128 x 128 (64 KB), three of 128 x 64 (48 KB); a grid runs
+// in ceil(tiles / resident) rounds.  Tiles are compared by rounds times tile
+// area, the time of the slowest CU (measured on the layer shapes of the
+// workloads; 256 x 256 tiles lost on every one of them)
 TileCfg choose_lds(int M, int cout, int Kp) {
-  const TileCfg c256{256, 256, 4, 2}, c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2},
-      c32{128, 32, 4, 1};
+  const TileCfg c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2}, c32{128, 32, 4, 1};
   if (cout < 64) return c32;
   // one K step: memory-bound; 128 x 64 tiles (24 KB of LDS, six workgroups
   // per CU) keep the most rows in flight (measured against 128 x 128, 64 x 64
   // and 256 x 256 on the ResNet 1x1 layers)
   if (Kp <= 64) return c12864;
-  if (cout >= 256 && tiles_of(c256, M, cout) >= 512) return c256;
-  if (cout >= 128 && tiles_of(c128, M, cout) >= 384) return c128;
-  if (tiles_of(c12864, M, cout) >= 512) return c12864;
-  return c64;
+  constexpr long kCUs = 256;
+  const long r128 = (tiles_of(c128, M, cout) + 2 * kCUs - 1) / (2 * kCUs);
+  const long t12864 = tiles_of(c12864, M, cout), r12864 = (t12864 + 3 * kCUs - 1) / (3 * kCUs);
+  // 128 x 128 when its rounds of double-area tiles take no longer, or when
+  // one tile column spans a short-K layer's channels, so that each input
+  // pixel (the bulk of its traffic) is fetched by one workgroup
+  if (cout >= 128 && (2 * r128 <= r12864 || (cout == 128 && Kp <= 256))) return c128;
+  // 64 x 64 only when 128 x 64 would leave most CUs with one workgroup
+  return t12864 > 256 ? c12864 : c64;
 }
 
 // stages: one for a single K step; four for 64 x 64 tiles with eight or
@@ -1315,7 +1322,6 @@ void go_lds(const ConvP& p, hipStream_t s, int S) {
 template <int KS>
 void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s, int S = 1) {
   switch (c.bm * 1000 + c.bn) {
-    case 256256: go_lds<256, 256, 4, 2, KS>(p, s, S); break;
     case 128128: go_lds<128, 128, 2, 2, KS>(p, s, S); break;
     case 128064: go_lds<128, 64, 2, 2, KS>(p, s, S); break;
     case 64064: go_lds<64, 64, 2, 2, KS>(p, s, S); break;
