@@ -1529,6 +1529,7 @@ int conv_cout_pad(int cout) {
 }
 
 void conv_bf16(const ConvArgs& a, hipStream_t s) {
+  if (a.cin == 3 && conv_rgb_stem(a, s)) return;
   ConvP p;
   p.src = a.src;
   p.src2 = a.src2;

@@ -57,6 +57,16 @@ struct ConvArgs {
 };
 void conv_bf16(const ConvArgs& a, hipStream_t s);
 
+// 7x7 stride-2 stems on 3-channel (RGB) input with 64 output channels,
+// W % 8 == 0, output rows of at most 112 pixels: a dedicated kernel reads
+// the 3-channel input directly (no channel padding).
+// conv_rgb_stem_fits says whether a shape qualifies; conv_rgb_stem launches
+// it for a conv_bf16 argument set with plain packed weights and returns
+// false (launching nothing) when the arguments do not qualify (row lists, a
+// residual, a device count, fp32 output, misaligned pointers).
+bool conv_rgb_stem_fits(int H, int W, int cin, int cout, int k, int stride, int pad);
+bool conv_rgb_stem(const ConvArgs& a, hipStream_t s);
+
 // K ranges per output tile for the layer shape (1: none).  A split layer
 // needs conv_ksplit_bytes of workspace; without it the layer runs unsplit
 // (the same sums in another order).  Depends on the shape only, so every

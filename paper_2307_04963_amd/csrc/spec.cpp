@@ -160,7 +160,8 @@ struct Builder {
         fail("fp32 specs support only linear layers (k 1 on 1x1 rows, bias, ReLU)");
       if (nd.w_k0 != 0 || nd.w_ldk != K) fail("fp32 linear weights must be dense [cout][cin]");
       nd.head_t = sp.n_head_t++;   // kept transposed on the device
-    } else if (sp.tensors[nd.src].external && nd.src2 < 0 && nd.cin1 < 8) {
+    } else if (sp.tensors[nd.src].external && nd.src2 < 0 && nd.cin1 < 8 &&
+               (nd.res >= 0 || !k::conv_rgb_stem_fits(nd.H, nd.W, nd.cin1, nd.cout, nd.k, nd.stride, nd.pad))) {
       // a stem on a narrow input: the input is zero-padded to 8 channels once
       // per run and the weights likewise, so the stem runs on 16-byte
       // vectors (the padded products are exact zeros)

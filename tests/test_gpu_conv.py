@@ -4,8 +4,10 @@ the launcher distinguishes: the halo-tiled kernel with register-resident
 weights (64 -> 64 channels, 3x3, stride 1: row tiles, partial row tiles,
 whole-image tiles with a ragged last tile, several tiles per workgroup), the
 direct-to-LDS implicit GEMM (1x1, 3x3, strided; with the K range of each
-tile split over workgroups for deep K on few pixels, and without) and the
-element-gathering kernel (3-channel stems, Cout not a multiple of 8).
+tile split over workgroups for deep K on few pixels, and without), the
+RGB stem kernel (3-channel input read directly: 7x7 stride 2, ragged units
+and pixel blocks) and the element-gathering kernel (other 3-channel stems,
+Cout not a multiple of 8).
 
 Bound per element: the fp32 accumulation error (K terms, gamma_K * sum |x w|)
 scaled by |scale|, the fp32 epilogue roundings, and half a bf16 ulp of the
@@ -45,7 +47,13 @@ CASES = [
     (3, 32, 32, 8, 64, 3, 1, 1, False, 1),      # 8-channel stem, weights in registers
     (300, 32, 32, 8, 64, 3, 1, 1, True, 1),     # several tiles per workgroup
     (5, 8, 8, 8, 64, 3, 1, 1, False, 2),        # image tiles, ragged
-    (3, 20, 20, 3, 64, 7, 2, 3, False, 1),      # 3-channel stem, element gathers
+    (3, 20, 20, 3, 64, 7, 2, 3, False, 1),      # 3-channel stem, W % 8 != 0: element gathers
+    (3, 224, 224, 3, 64, 7, 2, 3, False, 1),    # RGB stem kernel: 7x7 / 2, 112-pixel rows
+    (2, 42, 40, 3, 64, 7, 2, 3, False, 2),      # 21 x 20 output: ragged last unit, 2 pixel blocks, GELU
+    (3, 20, 104, 3, 64, 7, 2, 3, False, 0),     # 52-pixel rows: ragged pixel block
+    (2, 64, 64, 3, 64, 7, 2, 2, False, 1),      # pad 2 (even: no column offset)
+    (2, 224, 224, 3, 64, 7, 2, 3, True, 1),     # with a residual: element gathers
+    (7, 32, 32, 3, 64, 3, 1, 1, False, 1),      # 3x3 CIFAR stem on 3 channels: element gathers
     (5, 12, 12, 16, 32, 3, 1, 1, False, 1),
     (5, 12, 12, 64, 24, 3, 1, 1, True, 2),      # Cout not a multiple of 8
     (37, 4, 4, 512, 512, 3, 1, 1, False, 1),    # K split in 4, ragged last row tile
@@ -132,6 +140,13 @@ def test_conv_op_split_rows_are_independent():
     b = runtime.conv(x[:13].contiguous(), packed, 512, 3, 1, 1, None, None, None, 1)
     torch.cuda.synchronize()
     assert torch.equal(a[:13].view(torch.int16), b.view(torch.int16))
+
+
+def test_conv_op_full_rgb_stem_shape():
+    """The 7x7 / 2 stem of the ResNet-50 early-exit network at its benchmark
+    batch (256 x 224 x 224 x 3 -> 112 x 112 x 64, ReLU), 8 images checked
+    element by element."""
+    _case(256, 224, 224, 3, 64, 7, 2, 3, False, 1, seed=5)
 
 
 def test_conv_op_full_stage1_shape():
