@@ -60,11 +60,13 @@ struct ConvP {
   const uint16_t* zeros;   // >= 16 zero bytes: the source of padding taps
 };
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
-  u += 0x7fffu + ((u >> 16) & 1u);                    // nearest, ties to even
-  return static_cast<uint16_t>(u >> 16);
+// round to nearest even (v_cvt_pk_bf16_f32; NaN stays NaN), as every
+// kernel's epilogue
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  const bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
@@ -525,10 +527,10 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
           *reinterpret_cast<float4*>(d + 4) = make_float4(vv[4], vv[5], vv[6], vv[7]);
         } else {
           uint4 ov;
-          ov.x = f2bf(vv[0]) | (uint32_t(f2bf(vv[1])) << 16);
-          ov.y = f2bf(vv[2]) | (uint32_t(f2bf(vv[3])) << 16);
-          ov.z = f2bf(vv[4]) | (uint32_t(f2bf(vv[5])) << 16);
-          ov.w = f2bf(vv[6]) | (uint32_t(f2bf(vv[7])) << 16);
+          ov.x = pack_bf16(vv[0], vv[1]);
+          ov.y = pack_bf16(vv[2], vv[3]);
+          ov.z = pack_bf16(vv[4], vv[5]);
+          ov.w = pack_bf16(vv[6], vv[7]);
           *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.dst) + o) = ov;
         }
       }
@@ -1234,10 +1236,10 @@ __global__ __launch_bounds__(256) void ksplit_finish_kernel(const float* __restr
 #pragma unroll
   for (int q = 0; q < 8; ++q) vv[q] = apply_act(vv[q], act);
   uint4 ov;
-  ov.x = f2bf(vv[0]) | (uint32_t(f2bf(vv[1])) << 16);
-  ov.y = f2bf(vv[2]) | (uint32_t(f2bf(vv[3])) << 16);
-  ov.z = f2bf(vv[4]) | (uint32_t(f2bf(vv[5])) << 16);
-  ov.w = f2bf(vv[6]) | (uint32_t(f2bf(vv[7])) << 16);
+  ov.x = pack_bf16(vv[0], vv[1]);
+  ov.y = pack_bf16(vv[2], vv[3]);
+  ov.z = pack_bf16(vv[4], vv[5]);
+  ov.w = pack_bf16(vv[6], vv[7]);
   *reinterpret_cast<uint4*>(dst + o) = ov;
 }
 
