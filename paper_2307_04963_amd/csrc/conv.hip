@@ -472,9 +472,11 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
   }
 
   // epilogue through LDS: each wave stages 32 x WTN fp32 values (scale and
-  // shift applied), then every lane finishes 8 consecutive channels of a row
-  // (residual, activation, rounding) and writes them with one 16-byte store
-  __syncthreads();
+  // shift applied) in its own region, then every lane finishes 8
+  // consecutive channels of a row (residual, activation, rounding) and
+  // writes them with one 16-byte store.  The residual vectors of all the
+  // wave's rows are requested first, so their latency overlaps the staging.
+  __syncthreads();   // the main loop's last tiles are no longer read
   float* ep = reinterpret_cast<float*>(smem) + wave * 32 * EPW;
   float sc[TN], sh[TN];
   const bool partial = p.ksplit > 1;   // raw sums; the split reduction finishes them
@@ -484,6 +486,23 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
     sc[b] = (!partial && p.scale && col < p.cout) ? p.scale[col] : 1.0f;
     sh[b] = (!partial && p.shift && col < p.cout) ? p.shift[col] : 0.0f;
   }
+  constexpr int G = WTN / 8;           // 8-channel groups per row
+  constexpr int VI = 32 * G / 64;      // groups per lane in a 32-row block
+  uint4 rv[TM][VI];
+  if (p.res && !partial) {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int v = 0; v < VI; ++v) {
+        const int idx = v * 64 + lane;
+        const int rl = idx / G, g = idx - (idx / G) * G;
+        const int row = m0 + wm * WTM + a * 32 + rl;
+        const int col = n0 + wn * WTN + g * 8;
+        rv[a][v] = (row < M && col < p.cout)
+                       ? *reinterpret_cast<const uint4*>(p.res + row_at(p.rrows, row, HoWo) * p.cout + col)
+                       : make_uint4(0, 0, 0, 0);
+      }
+  }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
 #pragma unroll
@@ -491,10 +510,9 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EPW + b * 32 + (lane & 31)] = fmaf(acc[a][b][r], sc[b], sh[b]);
-    __syncthreads();
-    constexpr int G = WTN / 8;           // 8-channel groups per row
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own staging region: in-order LDS
 #pragma unroll
-    for (int v = 0; v < 32 * G / 64; ++v) {
+    for (int v = 0; v < VI; ++v) {
       const int idx = v * 64 + lane;
       const int rl = idx / G, g = idx - (idx / G) * G;
       const int row = m0 + wm * WTM + a * 32 + rl;
@@ -511,8 +529,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
         }
         const size_t o = row_at(p.drows, row, HoWo) * p.cout + col;
         if (p.res) {
-          const uint4 rv = *reinterpret_cast<const uint4*>(p.res + row_at(p.rrows, row, HoWo) * p.cout + col);
-          const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+          const uint32_t rw[4] = {rv[a][v].x, rv[a][v].y, rv[a][v].z, rv[a][v].w};
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             vv[2 * q] += __uint_as_float(rw[q] << 16);
@@ -535,7 +552,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
         }
       }
     }
-    __syncthreads();
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next block's staging
   }
 }
 
