@@ -24,6 +24,8 @@
 //
 // Epilogue: folded BatchNorm scale/shift (or bias), residual, ReLU or exact
 // GELU, then round-to-nearest-even bf16 or an fp32 store.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace dycl {
@@ -77,6 +79,13 @@ __device__ __forceinline__ size_t row_at(const int32_t* rows, int row, int HoWo)
   if (!rows) return static_cast<size_t>(row);
   const int img = row / HoWo;
   return static_cast<size_t>(rows[img]) * HoWo + (row - img * HoWo);
+}
+
+template <int ACT>
+__device__ __forceinline__ float act_t(float v) {
+  if (ACT == ACT_RELU) return v > 0.f ? v : 0.f;
+  if (ACT == ACT_GELU) return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+  return v;
 }
 
 __device__ __forceinline__ float apply_act(float v, int act) {
@@ -503,57 +512,67 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
                        : make_uint4(0, 0, 0, 0);
       }
   }
+  // the activation is chosen once, outside the epilogue's loops
+  auto epilogue = [&](auto act_c) __attribute__((always_inline)) {
+    constexpr int ACT = decltype(act_c)::value;
 #pragma unroll
-  for (int a = 0; a < TM; ++a) {
+    for (int a = 0; a < TM; ++a) {
 #pragma unroll
-    for (int b = 0; b < TN; ++b)
+      for (int b = 0; b < TN; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EPW + b * 32 + (lane & 31)] = fmaf(acc[a][b][r], sc[b], sh[b]);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own staging region: in-order LDS
+        for (int r = 0; r < 16; ++r)
+          ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EPW + b * 32 + (lane & 31)] = fmaf(acc[a][b][r], sc[b], sh[b]);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own staging region: in-order LDS
 #pragma unroll
-    for (int v = 0; v < VI; ++v) {
-      const int idx = v * 64 + lane;
-      const int rl = idx / G, g = idx - (idx / G) * G;
-      const int row = m0 + wm * WTM + a * 32 + rl;
-      const int col = n0 + wn * WTN + g * 8;
-      if (row < M && col < p.cout) {
-        const float4 lo = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8);
-        const float4 hi = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8 + 4);
-        float vv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        if (partial) {
-          float* d = p.part + (size_t)split * p.M * p.cout + (size_t)row * p.cout + col;
-          *reinterpret_cast<float4*>(d) = lo;
-          *reinterpret_cast<float4*>(d + 4) = hi;
-          continue;
-        }
-        const size_t o = row_at(p.drows, row, HoWo) * p.cout + col;
-        if (p.res) {
-          const uint32_t rw[4] = {rv[a][v].x, rv[a][v].y, rv[a][v].z, rv[a][v].w};
+      for (int v = 0; v < VI; ++v) {
+        const int idx = v * 64 + lane;
+        const int rl = idx / G, g = idx - (idx / G) * G;
+        const int row = m0 + wm * WTM + a * 32 + rl;
+        const int col = n0 + wn * WTN + g * 8;
+        if (row < M && col < p.cout) {
+          const float4 lo = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8);
+          const float4 hi = *reinterpret_cast<const float4*>(ep + rl * EPW + g * 8 + 4);
+          float vv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+          if (partial) {
+            float* d = p.part + (size_t)split * p.M * p.cout + (size_t)row * p.cout + col;
+            *reinterpret_cast<float4*>(d) = lo;
+            *reinterpret_cast<float4*>(d + 4) = hi;
+            continue;
+          }
+          const size_t o = row_at(p.drows, row, HoWo) * p.cout + col;
+          if (p.res) {
+            const uint32_t rw[4] = {rv[a][v].x, rv[a][v].y, rv[a][v].z, rv[a][v].w};
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            vv[2 * q] += __uint_as_float(rw[q] << 16);
-            vv[2 * q + 1] += __uint_as_float(rw[q] & 0xffff0000u);
+            for (int q = 0; q < 4; ++q) {
+              vv[2 * q] += __uint_as_float(rw[q] << 16);
+              vv[2 * q + 1] += __uint_as_float(rw[q] & 0xffff0000u);
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q) vv[q] = act_t<ACT>(vv[q]);
+          if (p.out_f32) {
+            float* d = static_cast<float*>(p.dst) + o;
+            *reinterpret_cast<float4*>(d) = make_float4(vv[0], vv[1], vv[2], vv[3]);
+            *reinterpret_cast<float4*>(d + 4) = make_float4(vv[4], vv[5], vv[6], vv[7]);
+          } else {
+            uint4 ov;
+            ov.x = pack_bf16(vv[0], vv[1]);
+            ov.y = pack_bf16(vv[2], vv[3]);
+            ov.z = pack_bf16(vv[4], vv[5]);
+            ov.w = pack_bf16(vv[6], vv[7]);
+            *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.dst) + o) = ov;
           }
         }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) vv[q] = apply_act(vv[q], p.act);
-        if (p.out_f32) {
-          float* d = static_cast<float*>(p.dst) + o;
-          *reinterpret_cast<float4*>(d) = make_float4(vv[0], vv[1], vv[2], vv[3]);
-          *reinterpret_cast<float4*>(d + 4) = make_float4(vv[4], vv[5], vv[6], vv[7]);
-        } else {
-          uint4 ov;
-          ov.x = pack_bf16(vv[0], vv[1]);
-          ov.y = pack_bf16(vv[2], vv[3]);
-          ov.z = pack_bf16(vv[4], vv[5]);
-          ov.w = pack_bf16(vv[6], vv[7]);
-          *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.dst) + o) = ov;
-        }
       }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next block's staging
     }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next block's staging
-  }
+  };
+  if (p.act == ACT_RELU)
+    epilogue(std::integral_constant<int, ACT_RELU>{});
+  else if (p.act == ACT_GELU)
+    epilogue(std::integral_constant<int, ACT_GELU>{});
+  else
+    epilogue(std::integral_constant<int, ACT_NONE>{});
 }
 
 // 16 bytes per lane from a raw buffer straight into LDS at `lds` + 16 * lane:
