@@ -1236,11 +1236,12 @@ __global__ __launch_bounds__(64 * (BM / (16 * WA) + 4)) void conv3h_kernel(Conv3
 // y[m, c..c+7] = finish(sum_s part[s][m][c..c+7]) with the splits added in
 // order s = 0, 1, ...: scale / shift, residual, activation, bf16 rounding,
 // as the single-range epilogue does.
+template <int ACT>
 __global__ __launch_bounds__(256) void ksplit_finish_kernel(const float* __restrict__ part, int S, int Mb, int cout,
                                                             const int32_t* nc, int nmax, int HoWo,
                                                             const float* __restrict__ scale,
                                                             const float* __restrict__ shift,
-                                                            const uint16_t* __restrict__ res, int act,
+                                                            const uint16_t* __restrict__ res,
                                                             uint16_t* __restrict__ dst) {
   const int M = (nc ? min(*nc, nmax) : nmax) * HoWo;
   const int C8 = cout >> 3;
@@ -1270,7 +1271,7 @@ __global__ __launch_bounds__(256) void ksplit_finish_kernel(const float* __restr
     }
   }
 #pragma unroll
-  for (int q = 0; q < 8; ++q) vv[q] = apply_act(vv[q], act);
+  for (int q = 0; q < 8; ++q) vv[q] = act_t<ACT>(vv[q]);
   uint4 ov;
   ov.x = pack_bf16(vv[0], vv[1]);
   ov.y = pack_bf16(vv[2], vv[3]);
@@ -1653,9 +1654,17 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
       else
         dispatch_lds<7>(c, p, s, S);
       const size_t items = static_cast<size_t>(p.M) * (a.cout / 8);
-      hipLaunchKernelGGL(ksplit_finish_kernel, dim3(static_cast<unsigned>((items + 255) / 256)), dim3(256), 0, s,
-                         a.splitws, S, p.M, a.cout, a.ncount, a.n, a.Ho * a.Wo, a.scale, a.shift, a.res, a.act,
-                         static_cast<uint16_t*>(a.dst));
+      const dim3 fgrid(static_cast<unsigned>((items + 255) / 256));
+      auto finish = [&](auto k) {
+        hipLaunchKernelGGL(k, fgrid, dim3(256), 0, s, a.splitws, S, p.M, a.cout, a.ncount, a.n, a.Ho * a.Wo, a.scale,
+                           a.shift, a.res, static_cast<uint16_t*>(a.dst));
+      };
+      if (a.act == ACT_RELU)
+        finish(ksplit_finish_kernel<ACT_RELU>);
+      else if (a.act == ACT_GELU)
+        finish(ksplit_finish_kernel<ACT_GELU>);
+      else
+        finish(ksplit_finish_kernel<ACT_NONE>);
       return;
     }
     if (a.k == 1)
