@@ -96,6 +96,23 @@ int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t
                  int pad, const float* scale, const float* shift, const uint16_t* res, int act, uint16_t* y,
                  void* workspace, size_t workspace_bytes, void* hip_stream);
 
+/*
+ * A convolution and the 3x3 / stride-2 / pad-1 max-pool that follows it in
+ * one launch (two tensor statements of one sub-DNN node, Sec. 5.3, fused):
+ *   y[i, ph, pw, co] = max over oh in [2 ph - 1, 2 ph + 1] and ow in
+ *                      [2 pw - 1, 2 pw + 1] inside [0, Ho) x [0, Wo) of
+ *                      the dycl_op_conv output (no residual)
+ * Hp = (Ho - 1) / 2 + 1, likewise Wp.  Only the pooled tensor is written.
+ * Taken for the ImageNet stem: cin 3, cout 64, k 7, stride 2, pad <= 3,
+ * W % 8 == 0, Wo <= 112, act 1 (ReLU); other arguments return
+ * DYCL_E_INVALID.  x [n][H][W][3], packed as for dycl_op_conv, scale /
+ * shift [64] float32 or NULL, y [n][Hp][Wp][64]; device pointers, 16-byte
+ * aligned; n >= 0 (0 does nothing).  Work is queued on hip_stream.
+ */
+int dycl_op_conv_maxpool(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed, int cout, int k,
+                         int stride, int pad, const float* scale, const float* shift, int act, uint16_t* y,
+                         void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -21,7 +21,7 @@ EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_plan_set_host_mode", "dycl_last
            "dycl_profile_read", "dycl_profile_launches", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
 # every symbol include/dycl_ops.h declares
 OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_move_rows", "dycl_op_conv_packed_bytes",
-               "dycl_op_conv_pack", "dycl_op_conv_workspace_bytes", "dycl_op_conv"]
+               "dycl_op_conv_pack", "dycl_op_conv_workspace_bytes", "dycl_op_conv", "dycl_op_conv_maxpool"]
 
 
 class DyclError(RuntimeError):
@@ -83,6 +83,8 @@ def _load():
     lib.dycl_op_conv.argtypes = [vp, i32, i32, i32, i32, vp, i32, i32, i32, i32, vp, vp, vp, i32, vp, vp, C.c_size_t,
                                  vp]
     lib.dycl_op_conv.restype = i32
+    lib.dycl_op_conv_maxpool.argtypes = [vp, i32, i32, i32, i32, vp, i32, i32, i32, i32, vp, vp, i32, vp, vp]
+    lib.dycl_op_conv_maxpool.restype = i32
     return lib
 
 

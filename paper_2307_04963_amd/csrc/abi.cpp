@@ -351,4 +351,52 @@ int dycl_op_conv(const uint16_t* x, int n, int H, int W, int cin, const uint16_t
   });
 }
 
+int dycl_op_conv_maxpool(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed, int cout, int k,
+                         int stride, int pad, const float* scale, const float* shift, int act, uint16_t* y,
+                         void* hip_stream) {
+  if (n < 0) return fail(DYCL_E_INVALID, "dycl_op_conv_maxpool: n < 0");
+  if (act != 1 || H < 1 || W < 1 || !dycl::k::conv_rgb_stem_fits(H, W, cin, cout, k, stride, pad))
+    return fail(DYCL_E_INVALID,
+                "dycl_op_conv_maxpool: needs cin 3, cout 64, k 7, stride 2, pad <= 3, W % 8 == 0, Wo <= 112, ReLU");
+  const long Ho = (static_cast<long>(H) + 2 * pad - k) / stride + 1, Wo = (static_cast<long>(W) + 2 * pad - k) / stride + 1;
+  const long lim = 1L << 31;
+  if (static_cast<long>(n) * H * W * cin >= lim || static_cast<long>(n) * Ho * Wo * cout >= lim)
+    return fail(DYCL_E_INVALID, "dycl_op_conv_maxpool: a tensor reaches 2^31 elements");
+  if (n == 0) return DYCL_OK;
+  if (!x || !packed || !y) return fail(DYCL_E_INVALID, "dycl_op_conv_maxpool: null x, packed weights or y");
+  if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(packed) | reinterpret_cast<uintptr_t>(y)) & 15)
+    return fail(DYCL_E_INVALID, "dycl_op_conv_maxpool: x, packed and y must be 16-byte aligned");
+  return guarded([&] {
+    dycl::k::ConvArgs a;
+    a.src = x;
+    a.src2 = nullptr;
+    a.cin1 = cin;
+    a.cin2 = 0;
+    a.n = n;
+    a.H = H;
+    a.W = W;
+    a.cin = cin;
+    a.Ho = static_cast<int>(Ho);
+    a.Wo = static_cast<int>(Wo);
+    a.cout = cout;
+    a.k = k;
+    a.stride = stride;
+    a.pad = pad;
+    a.w = packed;
+    a.Kp = static_cast<int>(dycl_op_conv_packed_bytes(cout, k, cin) / 2 / dycl::k::conv_cout_pad(cout));
+    a.scale = scale;
+    a.shift = shift;
+    a.res = nullptr;
+    a.act = act;
+    a.dst = y;
+    a.out_f32 = 0;
+    a.zeros = nullptr;
+    a.pool = 1;
+    if (!dycl::k::conv_rgb_stem(a, static_cast<hipStream_t>(hip_stream)))
+      throw dycl::HipError("dycl_op_conv_maxpool: the fused kernel declined the arguments");
+    if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_conv_maxpool: launch failed");
+    return DYCL_OK;
+  });
+}
+
 }  // extern "C"

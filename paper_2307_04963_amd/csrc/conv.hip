@@ -1568,6 +1568,7 @@ int conv_cout_pad(int cout) {
 }
 
 void conv_bf16(const ConvArgs& a, hipStream_t s) {
+  if (a.pool) return;   // only conv_rgb_stem fuses a max-pool (its dst is the pooled tensor)
   if (a.cin == 3 && conv_rgb_stem(a, s)) return;
   ConvP p;
   p.src = a.src;

@@ -54,6 +54,10 @@ struct ConvArgs {
   const int32_t* dst_rows = nullptr;
   float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split
   size_t splitws_bytes = 0;
+  // 1: a 3x3 / stride-2 / pad-1 max-pool of the output is fused in and dst
+  // holds the pooled tensor [n, (Ho - 1) / 2 + 1, (Wo - 1) / 2 + 1, cout]
+  // (conv_rgb_stem with ReLU only)
+  int pool = 0;
 };
 void conv_bf16(const ConvArgs& a, hipStream_t s);
 
@@ -63,7 +67,8 @@ void conv_bf16(const ConvArgs& a, hipStream_t s);
 // conv_rgb_stem_fits says whether a shape qualifies; conv_rgb_stem launches
 // it for a conv_bf16 argument set with plain packed weights and returns
 // false (launching nothing) when the arguments do not qualify (row lists, a
-// residual, a device count, fp32 output, misaligned pointers).
+// residual, a device count, fp32 output, misaligned pointers, a fused
+// max-pool without ReLU).
 bool conv_rgb_stem_fits(int H, int W, int cin, int cout, int k, int stride, int pad);
 bool conv_rgb_stem(const ConvArgs& a, hipStream_t s);
 

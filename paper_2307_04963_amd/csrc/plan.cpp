@@ -392,6 +392,17 @@ struct Run {
     a.dst_rows = list(nd.dst_list);
     a.splitws = p->d_split;
     a.splitws_bytes = p->split_bytes;
+    if (nd.pool) {
+      // stem with the max-pool fused in: the pooled tensor is all it writes
+      a.pool = 1;
+      const TensorInfo& d = sp.tensors[nd.dst];
+      const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + d.H * d.W * d.C) +
+                                  static_cast<double>(nd.cout) * nd.k * nd.k * cin);
+      launch(P_CONV, flops, bytes, [&] {
+        if (!k::conv_rgb_stem(a, s)) throw HipError("stem with fused max-pool: arguments the kernel does not take");
+      });
+      return;
+    }
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
                                 static_cast<double>(nd.cout) * nd.k * nd.k * cin);
     launch(P_CONV, flops, bytes, [&] { k::conv_bf16(a, s); });

@@ -54,6 +54,7 @@ struct Node {
   int64_t scale_off = -1, shift_off = -1;    // fp32 [cout] byte offsets (or -1)
   int packed = -1;                           // index of packed bf16 weights
   bool pad_in = false;                       // reads the input padded to 8 channels
+  bool pool = false;                         // a 3x3 / 2 max-pool fused in: dst is the pooled tensor
   // fused gathers / scatters: which row list of the last decision maps this
   // layer's images to those of src, res, dst (0: none, 1: the rows that
   // stay (exit, halt), 2: the rows that take the true branch (gate body),
@@ -106,6 +107,7 @@ struct Spec {
   int pad_input_c = 0;
   int fused_gathers = 0;   // exit carries read in place through the row list
   int fused_gates = 0;     // gates whose gathers and scatters are fused into the body convolutions
+  int fused_pools = 0;     // max-pools fused into the stem convolution that feeds them
   int n_head_t = 0;      // fp32 weight matrices kept transposed on the device   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
 
@@ -113,6 +115,7 @@ struct Spec {
   void fuse_original_order_reads();
   void fuse_exit_gathers();
   void fuse_gate_moves();
+  void fuse_stem_pools();
 };
 
 }  // namespace dycl

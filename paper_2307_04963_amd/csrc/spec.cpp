@@ -418,6 +418,33 @@ bool is_decision(const Node& nd) {
 
 }  // namespace
 
+// A stem convolution on the 3-channel input whose output only the 3x3 /
+// stride-2 max-pool right after it reads: the pooling runs in the stem
+// kernel's epilogue (ReLU outputs, whose maxima are exact on bf16 bits) and
+// the full-resolution output is never stored.
+void Spec::fuse_stem_pools() {
+  if (dt != DType::BF16) return;
+  for (size_t i = 0; i + 1 < nodes.size(); ++i) {
+    Node& c = nodes[i];
+    const Node& mp = nodes[i + 1];
+    if (c.kind != NodeKind::Conv || mp.kind != NodeKind::MaxPool || mp.src != c.dst) continue;
+    if (c.pad_in || c.pool || c.src2 >= 0 || c.res >= 0 || c.act != k::ACT_RELU || !tensors[c.src].external ||
+        c.src_list || c.src2_list || c.res_list || c.dst_list ||
+        !k::conv_rgb_stem_fits(c.H, c.W, c.cin1, c.cout, c.k, c.stride, c.pad))
+      continue;
+    std::vector<Use> us;
+    uses_of(nodes, c.dst, -1, us);
+    if (us.size() != 1) continue;   // another node reads the stem output
+    tensors[c.dst].unused = true;
+    c.dst = mp.dst;
+    c.pool = true;
+    TensorInfo& d = tensors[c.dst];
+    d.first = std::min(d.first, c.seq_pre);
+    nodes.erase(nodes.begin() + static_cast<long>(i) + 1);
+    ++fused_pools;
+  }
+}
+
 // The gather of an exit's carried tensor fused into its readers (a row
 // gather is a copy that computes nothing): when every reader of the carried
 // copy is a bf16 convolution that takes it as its main input before the next
@@ -617,6 +644,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   const Json& ns = j.at("nodes");
   if (ns.kind != Json::Array || ns.size() == 0) throw SpecError("nodes must be a non-empty array");
   for (size_t i = 0; i < ns.size(); ++i) nodes.push_back(b.node(ns.at(i), max_batch));
+  fuse_stem_pools();
   fuse_original_order_reads();
   fuse_exit_gathers();
   fuse_gate_moves();
@@ -634,7 +662,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   std::ostringstream os;
   os << "nodes=" << nodes_total << " decisions=" << decisions << " tensors=" << tensors.size()
      << " packed_weights=" << packed.size() << " fused_gathers=" << fused_gathers
-     << " fused_gates=" << fused_gates << " n_out=" << n_out
+     << " fused_gates=" << fused_gates << " fused_pools=" << fused_pools << " n_out=" << n_out
      << " dtype=" << dts;
   summary = os.str();
 }

@@ -38,6 +38,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRows = 4;       // output rows per unit (one per wave)
 constexpr int kCout = 64;      // output channels: four 16-wide MFMA blocks
@@ -48,15 +49,22 @@ struct alignas(4) U3 {
   uint32_t a, b, c;   // two pixels of 3 bf16 channels
 };
 
-template <int KS, int S, int MB>
+template <int KS, int S, int MB, bool POOL>
 struct StemGeom {
   static constexpr int PR = (kRows - 1) * S + KS;   // input rows of a unit
   static constexpr int PW = 16 * MB * S + 16;       // staged pixels per row (8 bytes each)
   static constexpr int W_BYTES = KS * 4 * 64 * 16;  // [kh][channel block][lane] 16-byte fragments
-  static constexpr int P_BYTES = PR * PW * 8;
   static constexpr int S_BYTES = 2 * kCout * 4;       // scale, shift
-  static constexpr int E_BYTES = kRows * 2 * 16 * kEStride * 2;   // two staging blocks per wave
-  static constexpr int BYTES = W_BYTES + P_BYTES + E_BYTES + S_BYTES;
+  // pooled: the unit's four row maxima over pixel triples ([row][pooled
+  // pixel][64 channels] bf16) take the staged input rows' place once the
+  // MFMAs are done; the carried row (the previous unit's last) has its own
+  static constexpr int WP = 8 * MB;                  // pooled pixels per row, at most
+  static constexpr int HP_BYTES = POOL ? kRows * WP * kCout * 2 : 0;
+  static constexpr int C_BYTES = POOL ? WP * kCout * 2 : 0;
+  static constexpr int P_BYTES = PR * PW * 8 > HP_BYTES ? PR * PW * 8 : HP_BYTES;
+  // staging blocks per wave: two (alternating) when stored, one when pooled
+  static constexpr int E_BYTES = kRows * (POOL ? 1 : 2) * 16 * kEStride * 2;
+  static constexpr int BYTES = W_BYTES + P_BYTES + E_BYTES + C_BYTES + S_BYTES;
 };
 
 struct StemP {
@@ -65,10 +73,21 @@ struct StemP {
   int Kp;
   const float* scale;
   const float* shift;
-  uint16_t* y;         // [n][Ho][Wo][64]
+  uint16_t* y;         // [n][Ho][Wo][64], or pooled: [n][Hp][Wp][64]
   int n, H, W, Ho, Wo, pad, off, act;
   int units, per_xcd; // units = n * ceil(Ho / 4); per_xcd = ceil(units / 8)
+  int Hp, Wp;          // pooled output (3x3 / stride 2 / pad 1 max-pool)
+  int parts, ranges;   // pooled: each image's units in `parts` consecutive ranges
 };
+
+// the larger of two non-negative bf16 values is the one with the larger
+// bits: element-wise maxima of 8 bf16 by 16-bit integer maxima
+__device__ __forceinline__ uint4 max_bf16x8(uint4 a, uint4 b) {
+  auto m = [](uint32_t x, uint32_t y) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, x), __builtin_bit_cast(u16x2, y)));
+  };
+  return make_uint4(m(a.x, b.x), m(a.y, b.y), m(a.z, b.z), m(a.w, b.w));
+}
 
 template <int ACT>
 __device__ __forceinline__ float act_of(float v) {
@@ -84,26 +103,79 @@ __device__ __forceinline__ int unit_of(int u, const StemP& p) {
   return (u >> 3) < p.per_xcd && t < p.units ? t : -1;
 }
 
-template <int KS, int S, int MB, int ACT>
+// The units a workgroup computes, in order.  Stored output: the unit slots
+// of unit_of.  Pooled output: ranges r = blockIdx.x, + gridDim.x, ... of
+// consecutive units of one image, walked in order so that a unit's last
+// stem row (the first pooled row of the next unit needs it) stays in LDS; a
+// range that starts inside an image first recomputes the unit before it,
+// only to fill that carried row.
+struct StemWork {
+  int t;          // unit (image * units per image + row group)
+  int slot;       // stored output: dispatch slot
+  int r, j, j1;   // pooled output: range, row group, end of the range's row groups
+  bool pre;       // pooled output: computed only for the carried row
+};
+
+template <bool POOL>
+__device__ __forceinline__ bool stem_first(int start, const StemP& p, int RG, StemWork& w) {
+  if constexpr (POOL) {
+    if (start >= p.ranges) return false;
+    const int img = start / p.parts, part = start - img * p.parts;
+    const int j0 = part * RG / p.parts;
+    w.r = start;
+    w.j1 = (part + 1) * RG / p.parts;
+    w.pre = j0 > 0;
+    w.j = j0 > 0 ? j0 - 1 : j0;
+    w.t = img * RG + w.j;
+    return true;
+  } else {
+    const int slots = 8 * p.per_xcd;
+    for (int u = start; u < slots; u += gridDim.x) {
+      const int t = unit_of(u, p);
+      if (t >= 0) {
+        w.slot = u;
+        w.t = t;
+        return true;
+      }
+    }
+    return false;
+  }
+}
+
+template <bool POOL>
+__device__ __forceinline__ bool stem_next(const StemWork& cur, const StemP& p, int RG, StemWork& w) {
+  if constexpr (POOL) {
+    if (cur.j + 1 < cur.j1) {
+      w = cur;
+      w.pre = false;
+      ++w.j;
+      ++w.t;
+      return true;
+    }
+    return stem_first<true>(cur.r + gridDim.x, p, RG, w);
+  } else {
+    return stem_first<false>(cur.slot + gridDim.x, p, RG, w);
+  }
+}
+
+template <int KS, int S, int MB, int ACT, bool POOL>
 __global__ __launch_bounds__(256, 2) void stem_rgb_kernel(StemP p) {
   constexpr int NP = kPairsPerThread;
-  using G = StemGeom<KS, S, MB>;
+  using G = StemGeom<KS, S, MB, POOL>;
+  static_assert(!POOL || ACT == ACT_RELU, "pooled maxima are taken on the bits of non-negative bf16 values");
   __shared__ __align__(16) char smem[G::BYTES];
   char* const wl = smem;
   char* const pl = smem + G::W_BYTES;
   uint16_t* const el = reinterpret_cast<uint16_t*>(smem + G::W_BYTES + G::P_BYTES);
-  float* const ss = reinterpret_cast<float*>(smem + G::W_BYTES + G::P_BYTES + G::E_BYTES);
+  uint16_t* const cl = reinterpret_cast<uint16_t*>(smem + G::W_BYTES + G::P_BYTES + G::E_BYTES);   // carried row
+  float* const ss = reinterpret_cast<float*>(smem + G::W_BYTES + G::P_BYTES + G::E_BYTES + G::C_BYTES);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
   const int RG = (p.Ho + kRows - 1) / kRows;
-  const int slots = 8 * p.per_xcd;
 
-  // first unit of this workgroup (grid size is a multiple of 8)
-  int u = blockIdx.x, unit = -1;
-  for (; u < slots; u += gridDim.x)
-    if ((unit = unit_of(u, p)) >= 0) break;
-  if (unit < 0) return;   // uniform over the workgroup
+  StemWork cur;
+  if (!stem_first<POOL>(blockIdx.x, p, RG, cur)) return;   // uniform over the workgroup
 
   // weights: fragment (kh, channel block cb, lane) holds output channel
   // 16 cb + l16 at K values (kw, c) = (2 g + j / 4, j % 4), j < 8 (zero
@@ -176,7 +248,7 @@ __global__ __launch_bounds__(256, 2) void stem_rgb_kernel(StemP p) {
       raw[i] = *reinterpret_cast<const U3*>(p.x + (inside[i] ? base + 3 * ((pinfo[i] >> 5) & 4095) : 0));
     }
   };
-  load(unit);
+  load(cur.t);
 
   while (true) {
     __syncthreads();   // the previous unit's MFMAs are done with the staged rows
@@ -192,12 +264,18 @@ __global__ __launch_bounds__(256, 2) void stem_rgb_kernel(StemP p) {
         *reinterpret_cast<uint4*>(pl + (pinfo[i] >> 17) * 16) = inside[i] ? o : make_uint4(0, 0, 0, 0);
       }
     }
+    if constexpr (POOL) {   // the previous unit's pooled rows overwrote the padding
+      const int npad = G::PW - p.W;
+      for (int e = tid; e < G::PR * npad; e += 256) {
+        const int pr = e / npad, k = e - pr * npad;
+        *reinterpret_cast<uint2*>(pl + (pr * G::PW + (k < p.off ? k : p.W + k)) * 8) = make_uint2(0, 0);
+      }
+    }
     __syncthreads();
 
-    int nu = u + gridDim.x, next = -1;
-    for (; nu < slots; nu += gridDim.x)
-      if ((next = unit_of(nu, p)) >= 0) break;
-    if (next >= 0) load(next);   // lands while this unit computes
+    StemWork nxt;
+    const bool more = stem_next<POOL>(cur, p, RG, nxt);
+    if (more) load(nxt.t);   // lands while this unit computes
 
     f32x4 acc[MB][4];
 #pragma unroll
@@ -227,63 +305,130 @@ __global__ __launch_bounds__(256, 2) void stem_rgb_kernel(StemP p) {
     }
 
     // epilogue: lane holds channels 16 cb + 4 g + i of pixel 16 mb + l16.
-    // Each 16-pixel block goes through one of two per-wave staging buffers
-    // (alternating, so a block's writes never wait for the previous block's
-    // reads) and leaves as 2 KB of whole pixels.
-    const int img = unit / RG, oh = (unit - img * RG) * kRows + wave;
+    // Stored: each 16-pixel block goes through one of two per-wave staging
+    // buffers (alternating, so a block's writes never wait for the previous
+    // block's reads) and leaves as 2 KB of whole pixels.  Pooled: through
+    // the wave's one staging buffer into the maxima over pixel triples.
+    const int img = cur.t / RG, oh = (cur.t - img * RG) * kRows + wave;
     float4 sc[4], sh[4];
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
       sc[cb] = *reinterpret_cast<const float4*>(ss + cb * 16 + 4 * g);
       sh[cb] = *reinterpret_cast<const float4*>(ss + kCout + cb * 16 + 4 * g);
     }
+    if constexpr (POOL) {
+      // maxima over pixel triples: lane (t8, q) takes pooled pixel 8 mb + t8
+      // (output columns 16 mb + 2 t8 - 1 .. + 1) and channels 8 q .. 8 q + 7;
+      // columns outside the output, and rows past it, enter as 0, the
+      // identity of a maximum of ReLU outputs
+      uint16_t* const ew = el + wave * 16 * kEStride;
+      uint16_t* const hp = reinterpret_cast<uint16_t*>(pl);   // [kRows][WP][64]
+      const int t8 = lane >> 3, q = lane & 7;
+      const uint4 zero = make_uint4(0, 0, 0, 0);
+      uint4 prev = zero;   // the previous block's pixel 15
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      uint16_t* const ew = el + (wave * 2 + (mb & 1)) * 16 * kEStride;
+      for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        const float a0 = act_of<ACT>(fmaf(acc[mb][cb][0], sc[cb].x, sh[cb].x));
-        const float a1 = act_of<ACT>(fmaf(acc[mb][cb][1], sc[cb].y, sh[cb].y));
-        const float a2 = act_of<ACT>(fmaf(acc[mb][cb][2], sc[cb].z, sh[cb].z));
-        const float a3 = act_of<ACT>(fmaf(acc[mb][cb][3], sc[cb].w, sh[cb].w));
-        // v_cvt_pk_bf16_f32: round to nearest even, as the other kernels' epilogues
-        const bf16x2 lo = {static_cast<__bf16>(a0), static_cast<__bf16>(a1)};
-        const bf16x2 hi = {static_cast<__bf16>(a2), static_cast<__bf16>(a3)};
-        *reinterpret_cast<uint2*>(ew + l16 * kEStride + cb * 16 + 4 * g) =
-            make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        for (int cb = 0; cb < 4; ++cb) {
+          const float a0 = act_of<ACT>(fmaf(acc[mb][cb][0], sc[cb].x, sh[cb].x));
+          const float a1 = act_of<ACT>(fmaf(acc[mb][cb][1], sc[cb].y, sh[cb].y));
+          const float a2 = act_of<ACT>(fmaf(acc[mb][cb][2], sc[cb].z, sh[cb].z));
+          const float a3 = act_of<ACT>(fmaf(acc[mb][cb][3], sc[cb].w, sh[cb].w));
+          const bf16x2 lo = {static_cast<__bf16>(a0), static_cast<__bf16>(a1)};
+          const bf16x2 hi = {static_cast<__bf16>(a2), static_cast<__bf16>(a3)};
+          *reinterpret_cast<uint2*>(ew + l16 * kEStride + cb * 16 + 4 * g) =
+              make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        const int c1 = 2 * t8;
+        const uint4 center = *reinterpret_cast<const uint4*>(ew + c1 * kEStride + q * 8);
+        const uint4 right = *reinterpret_cast<const uint4*>(ew + (c1 + 1) * kEStride + q * 8);
+        const uint4 left = t8 > 0 ? *reinterpret_cast<const uint4*>(ew + (c1 - 1) * kEStride + q * 8) : prev;
+        const uint4 last = *reinterpret_cast<const uint4*>(ew + 15 * kEStride + q * 8);
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next block's staging
+        const int ow = mb * 16 + c1;
+        uint4 m = ow < p.Wo ? center : zero;
+        if (ow + 1 < p.Wo) m = max_bf16x8(m, right);
+        if (ow >= 1 && ow - 1 < p.Wo) m = max_bf16x8(m, left);
+        if (oh >= p.Ho) m = zero;
+        *reinterpret_cast<uint4*>(hp + (wave * G::WP + mb * 8 + t8) * kCout + q * 8) = m;
+        prev = last;
       }
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      // lanes 16 apart take the four quarters of one pixel, so that each
-      // 16-lane phase of the read covers the 64 banks once
-      const int px = lane & 15, ow = mb * 16 + px;
-      const uint4* sp = reinterpret_cast<const uint4*>(ew + px * kEStride + (lane >> 4) * 16);
-      const uint4 v0 = sp[0], v1 = sp[1];
-      if (oh < p.Ho && ow < p.Wo) {
-        uint4* d = reinterpret_cast<uint4*>(p.y + ((static_cast<size_t>(img) * p.Ho + oh) * p.Wo + ow) * kCout +
-                                            (lane >> 4) * 16);
-        d[0] = v0;
-        d[1] = v1;
+      __syncthreads();   // every row's maxima are in LDS
+      // pooled rows 2 j (stem rows 4 j - 1 .. 4 j + 1: the carried row and
+      // the unit's first two) and 2 j + 1 (stem rows 4 j + 1 .. 4 j + 3)
+      const int j = cur.j, WP8 = p.Wp * 8;
+      if (!cur.pre) {
+        for (int e = tid; e < 2 * WP8; e += 256) {
+          const int pr = e >= WP8 ? 1 : 0, rem = e - pr * WP8, pw = rem >> 3, qq = rem & 7;
+          const int po = 2 * j + pr;
+          if (po >= p.Hp) continue;
+          const int o = pw * kCout + qq * 8;
+          const uint4 r1 = *reinterpret_cast<const uint4*>(hp + (pr * 2) * G::WP * kCout + o);
+          const uint4 r2 = *reinterpret_cast<const uint4*>(hp + (pr * 2 + 1) * G::WP * kCout + o);
+          const uint4 r0 = pr ? *reinterpret_cast<const uint4*>(hp + G::WP * kCout + o)
+                              : (j > 0 ? *reinterpret_cast<const uint4*>(cl + o) : zero);
+          *reinterpret_cast<uint4*>(p.y + ((static_cast<size_t>(img) * p.Hp + po) * p.Wp + pw) * kCout + qq * 8) =
+              max_bf16x8(max_bf16x8(r0, r1), r2);
+        }
+      }
+      __syncthreads();   // the carried row is read
+      for (int e = tid; e < WP8; e += 256)   // the unit's last stem row is carried
+        *reinterpret_cast<uint4*>(cl + e * 8) = *reinterpret_cast<const uint4*>(hp + 3 * G::WP * kCout + e * 8);
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        uint16_t* const ew = el + (wave * 2 + (mb & 1)) * 16 * kEStride;
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          const float a0 = act_of<ACT>(fmaf(acc[mb][cb][0], sc[cb].x, sh[cb].x));
+          const float a1 = act_of<ACT>(fmaf(acc[mb][cb][1], sc[cb].y, sh[cb].y));
+          const float a2 = act_of<ACT>(fmaf(acc[mb][cb][2], sc[cb].z, sh[cb].z));
+          const float a3 = act_of<ACT>(fmaf(acc[mb][cb][3], sc[cb].w, sh[cb].w));
+          // v_cvt_pk_bf16_f32: round to nearest even, as the other kernels' epilogues
+          const bf16x2 lo = {static_cast<__bf16>(a0), static_cast<__bf16>(a1)};
+          const bf16x2 hi = {static_cast<__bf16>(a2), static_cast<__bf16>(a3)};
+          *reinterpret_cast<uint2*>(ew + l16 * kEStride + cb * 16 + 4 * g) =
+              make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        // lanes 16 apart take the four quarters of one pixel, so that each
+        // 16-lane phase of the read covers the 64 banks once
+        const int px = lane & 15, ow = mb * 16 + px;
+        const uint4* sp = reinterpret_cast<const uint4*>(ew + px * kEStride + (lane >> 4) * 16);
+        const uint4 v0 = sp[0], v1 = sp[1];
+        if (oh < p.Ho && ow < p.Wo) {
+          uint4* d = reinterpret_cast<uint4*>(p.y + ((static_cast<size_t>(img) * p.Ho + oh) * p.Wo + ow) * kCout +
+                                              (lane >> 4) * 16);
+          d[0] = v0;
+          d[1] = v1;
+        }
       }
     }
-    if (next < 0) break;
-    u = nu;
-    unit = next;
+    if (!more) break;
+    cur = nxt;
   }
 }
 
 template <int KS, int S, int MB>
 bool go(const StemP& p, hipStream_t s) {
-  using G = StemGeom<KS, S, MB>;
+  using G = StemGeom<KS, S, MB, false>;
   if (p.off + p.W >= G::PW || G::PR * (p.W / 2) > 256 * kPairsPerThread) return false;
+  if (p.Hp) {   // pooled: ReLU only (maxima on the bits of non-negative values)
+    if (p.act != ACT_RELU) return false;
+    const int grid = p.ranges < 2 * 256 ? p.ranges : 2 * 256;
+    hipLaunchKernelGGL((stem_rgb_kernel<KS, S, MB, ACT_RELU, true>), dim3(grid), dim3(256), 0, s, p);
+    return true;
+  }
   int grid = 2 * 256;   // two workgroups per CU (about 62 KB of LDS each at 7x7)
   const int need = (p.units + 7) / 8 * 8;
   if (need < grid) grid = need;
   if (p.act == ACT_RELU)
-    hipLaunchKernelGGL((stem_rgb_kernel<KS, S, MB, ACT_RELU>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((stem_rgb_kernel<KS, S, MB, ACT_RELU, false>), dim3(grid), dim3(256), 0, s, p);
   else if (p.act == ACT_GELU)
-    hipLaunchKernelGGL((stem_rgb_kernel<KS, S, MB, ACT_GELU>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((stem_rgb_kernel<KS, S, MB, ACT_GELU, false>), dim3(grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL((stem_rgb_kernel<KS, S, MB, ACT_NONE>), dim3(grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((stem_rgb_kernel<KS, S, MB, ACT_NONE, false>), dim3(grid), dim3(256), 0, s, p);
   return true;
 }
 
@@ -305,7 +450,7 @@ bool conv_rgb_stem_fits(int H, int W, int cin, int cout, int k, int stride, int 
 bool conv_rgb_stem(const ConvArgs& a, hipStream_t s) {
   const bool aligned = (reinterpret_cast<uintptr_t>(a.src) | reinterpret_cast<uintptr_t>(a.dst)) % 16 == 0;
   if (!aligned || a.src2 || a.cin1 != 3 || a.res || a.out_f32 || a.ncount || a.src_rows || a.res_rows || a.dst_rows ||
-      !conv_rgb_stem_fits(a.H, a.W, a.cin, a.cout, a.k, a.stride, a.pad))
+      !conv_rgb_stem_fits(a.H, a.W, a.cin, a.cout, a.k, a.stride, a.pad) || (a.pool && a.act != ACT_RELU))
     return false;
   StemP p;
   p.x = a.src;
@@ -324,6 +469,18 @@ bool conv_rgb_stem(const ConvArgs& a, hipStream_t s) {
   p.act = a.act;
   p.units = a.n * ((a.Ho + kRows - 1) / kRows);
   p.per_xcd = (p.units + 7) / 8;
+  p.Hp = p.Wp = p.parts = p.ranges = 0;
+  if (a.pool) {
+    // pooled output: each image's row groups in consecutive ranges, enough
+    // ranges for two workgroups per CU (a range inside an image recomputes
+    // one row group)
+    const int RG = (a.Ho + kRows - 1) / kRows;
+    p.Hp = (a.Ho - 1) / 2 + 1;
+    p.Wp = (a.Wo - 1) / 2 + 1;
+    p.parts = (2 * 256 + a.n - 1) / a.n;
+    if (p.parts > RG) p.parts = RG;
+    p.ranges = a.n * p.parts;
+  }
   const int MB = a.Wo <= 32 ? 2 : a.Wo <= 64 ? 4 : 7;
   return MB == 2 ? go<7, 2, 2>(p, s) : MB == 4 ? go<7, 2, 4>(p, s) : go<7, 2, 7>(p, s);
 }

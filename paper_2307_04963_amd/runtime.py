@@ -152,6 +152,22 @@ def conv_workspace_bytes(n: int, H: int, W: int, cin: int, cout: int, k: int, st
     return int(lib.dycl_op_conv_workspace_bytes(n, H, W, cin, cout, k, stride, pad))
 
 
+def conv_maxpool(x: torch.Tensor, packed: torch.Tensor, cout: int, k: int, stride: int, pad: int, scale=None,
+                 shift=None, act: int = 1, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """dycl_op_conv_maxpool on device tensors: the convolution and the 3x3 /
+    stride-2 / pad-1 max-pool after it in one launch; returns the pooled
+    y [n, (Ho - 1) // 2 + 1, (Wo - 1) // 2 + 1, cout] bf16."""
+    n, H, W, cin = x.shape
+    Ho, Wo = (H + 2 * pad - k) // stride + 1, (W + 2 * pad - k) // stride + 1
+    Hp, Wp = (Ho - 1) // 2 + 1, (Wo - 1) // 2 + 1
+    y = out if out is not None else torch.empty((n, Hp, Wp, cout), dtype=torch.bfloat16, device=x.device)
+    s = stream if stream is not None else torch.cuda.current_stream(x.device)
+    ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+    check(lib.dycl_op_conv_maxpool(x.data_ptr(), n, H, W, cin, packed.data_ptr(), cout, k, stride, pad, ptr(scale),
+                                   ptr(shift), act, y.data_ptr(), s.cuda_stream))
+    return y
+
+
 def conv(x: torch.Tensor, packed: torch.Tensor, cout: int, k: int, stride: int, pad: int, scale=None, shift=None,
          res=None, act: int = 0, out: torch.Tensor | None = None, stream=None, workspace="auto") -> torch.Tensor:
     """dycl_op_conv on device tensors: x [n, H, W, cin] bf16, packed weights

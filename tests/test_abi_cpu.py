@@ -65,6 +65,9 @@ def test_every_workload_spec_validates(name):
     fgt = int(re.search(r"fused_gates=(\d+)", msg).group(1))
     assert (fg, fgt) == {"mlp_exit": (0, 0), "resnet18_exit": (3, 0), "skipnet38": (0, 12),
                          "resnet50_exit": (3, 0), "act_loop": (30, 0)}[name]
+    # the ImageNet stem's max-pool runs in the stem kernel's epilogue
+    fp = int(re.search(r"fused_pools=(\d+)", msg).group(1))
+    assert fp == (1 if name == "resnet50_exit" else 0)
     # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
     if name == "act_loop":
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
@@ -92,6 +95,29 @@ def test_exit_gathers_fused_only_into_plain_conv_readers():
     toy["nodes"][3]["res"] = None
     rc, msg = _check(json.dumps(toy), 16384)
     assert rc == 0 and "fused_gathers=1" in msg, msg
+
+
+def test_stem_pool_fused_only_when_the_pool_is_the_only_reader():
+    # 7x7 / 2 ReLU stem on a 3-channel input, then a 3x3 / 2 max-pool
+    wb = 64 * 147 * 2
+    head = {"op": "exit", "w": wb, "b": wb + 64 * 10 * 4, "ncls": 10, "index": 0, "final": True}
+
+    def spec(act="relu", extra_reader=False):
+        nodes = [{"op": "conv", "src": "x", "dst": "s", "k": 7, "stride": 2, "pad": 3, "cout": 64, "act": act,
+                  "w": {"off": 0}},
+                 {"op": "maxpool", "src": "s", "dst": "p"},
+                 dict(head, src="p")]
+        if extra_reader:
+            nodes.insert(2, {"op": "conv", "src": "s", "dst": "t", "k": 1, "cout": 64, "act": "relu",
+                             "w": {"off": 0, "ldk": 147, "k0": 0}})
+        return {"version": 1, "dtype": "bf16", "input": {"name": "x", "shape": [64, 64, 3]}, "n_out": 10,
+                "nodes": nodes}
+
+    nb = wb + 64 * 10 * 4 + 64
+    for sp, want in ((spec(), 1), (spec(act="none"), 0), (spec(extra_reader=True), 0)):
+        rc, msg = _check(json.dumps(sp), nb)
+        assert rc == 0, msg
+        assert f"fused_pools={want}" in msg, msg
 
 
 def _mlp_spec():
@@ -182,3 +208,14 @@ def test_conv_pack_and_validation():
     assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 128, 512, 3, 1, 1) == 0     # K = 1152
     assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 512, 128, 3, 1, 1) == 0     # cout < 256
     assert lib.dycl_op_conv_workspace_bytes(0, 4, 4, 512, 512, 3, 1, 1) == 0
+    # the fused stem + max-pool takes the ImageNet stem shape with ReLU only
+    mp = lambda **kw: lib.dycl_op_conv_maxpool(kw.get("x", p16), kw.get("n", 2), kw.get("H", 32), kw.get("W", 32),  # noqa: E731
+                                                kw.get("cin", 3), p16, kw.get("cout", 64), kw.get("k", 7),
+                                                kw.get("s", 2), kw.get("pad", 3), None, None, kw.get("act", 1),
+                                                kw.get("y", p16), None)
+    assert mp(act=0) == -1 and mp(act=2) == -1
+    assert mp(cin=8) == -1 and mp(cout=128) == -1 and mp(k=3) == -1 and mp(s=1) == -1
+    assert mp(W=36) == -1                                                  # W % 8
+    assert mp(W=256) == -1                                                 # rows of more than 112 outputs
+    assert mp(n=-1) == -1 and mp(x=None) == -1 and mp(y=C.c_void_p(264)) == -1
+    assert mp(n=0) == 0

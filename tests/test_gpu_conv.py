@@ -149,6 +149,59 @@ def test_conv_op_full_rgb_stem_shape():
     _case(256, 224, 224, 3, 64, 7, 2, 3, False, 1, seed=5)
 
 
+def _maxpool3s2(v):
+    """3x3 / stride-2 / pad-1 max-pool of [H, W, C] by its definition: the
+    maximum over the window's pixels inside the input."""
+    H, W, C = v.shape
+    Hp, Wp = (H - 1) // 2 + 1, (W - 1) // 2 + 1
+    out = np.empty((Hp, Wp, C), v.dtype)
+    for ph in range(Hp):
+        for pw in range(Wp):
+            r0, r1 = max(2 * ph - 1, 0), min(2 * ph + 2, H)
+            c0, c1 = max(2 * pw - 1, 0), min(2 * pw + 2, W)
+            out[ph, pw] = v[r0:r1, c0:c1].reshape(-1, C).max(axis=0)
+    return out
+
+
+@pytest.mark.parametrize("case", [(3, 224, 224, 3), (2, 42, 40, 3), (3, 20, 104, 3), (2, 64, 64, 2), (5, 8, 8, 3),
+                                  (2, 30, 16, 1)], ids=str)
+def test_conv_maxpool_op(case):
+    """The RGB stem with its max-pool fused in (n, H, W, pad; 7x7 / 2, 3 -> 64,
+    ReLU): bit for bit the max-pool of the unfused stem's bf16 output, and
+    within the convolution's bound of the oracle's float64 convolution and
+    max-pool (a maximum moves by at most the largest error in its window)."""
+    from paper_2307_04963_amd import runtime
+    n, H, W, pad = case
+    cin, cout, k = 3, 64, 7
+    rng = np.random.default_rng(hash(case) % (2 ** 31))
+    x = bf16_bits_to_f32(to_bf16_bits(rng.standard_normal((n, H, W, cin)).astype(np.float32)))
+    bound = np.sqrt(6.0 / (k * k * cin))
+    w = bf16_bits_to_f32(to_bf16_bits(rng.uniform(-bound, bound, (cout, k, k, cin)).astype(np.float32)))
+    sc = rng.uniform(0.5, 1.5, cout).astype(np.float32)
+    sh = rng.uniform(-0.3, 0.3, cout).astype(np.float32)
+    packed = torch.from_numpy(runtime.pack_conv_weights(to_bf16_bits(w)).view(np.int16)).cuda()
+    xt = _bits(x).cuda().view(torch.bfloat16)
+    sct, sht = torch.from_numpy(sc).cuda(), torch.from_numpy(sh).cuda()
+    yp = runtime.conv_maxpool(xt, packed, cout, k, 2, pad, sct, sht)
+    yc = runtime.conv(xt, packed, cout, k, 2, pad, sct, sht, None, 1)
+    torch.cuda.synchronize()
+    got = bf16_bits_to_f32(yp.cpu().view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
+    conv = bf16_bits_to_f32(yc.cpu().view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
+    wt = torch.from_numpy(w.astype(np.float64)).permute(0, 3, 1, 2)
+    K = k * k * cin
+    gamma = K * 2.0 ** -24 / (1 - K * 2.0 ** -24)
+    for i in range(n):
+        assert np.array_equal(got[i], _maxpool3s2(conv[i])), f"image {i}: fused and unfused pooling differ"
+        xi = torch.from_numpy(x[i].astype(np.float64)).permute(2, 0, 1)
+        acc = O.conv2d(xi, wt, 2, pad).permute(1, 2, 0).numpy()
+        mag = O.conv2d(xi.abs(), wt.abs(), 2, pad).permute(1, 2, 0).numpy()
+        v = np.maximum(acc * sc + sh, 0.0)
+        tol = 2.0 ** -8 * 1.001 * np.abs(v) + gamma * mag * np.abs(sc) + 2.0 ** -22 * (np.abs(acc * sc) + np.abs(sh))
+        ref, tp = _maxpool3s2(v), _maxpool3s2(tol)
+        bad = np.argwhere(np.abs(got[i] - ref) > tp)
+        assert bad.size == 0, f"image {i}: {len(bad)} pooled elements out of bound, first {tuple(bad[0])}"
+
+
 def test_conv_op_full_stage1_shape():
     """The first-stage layer of the ResNet-18 early-exit network at the
     benchmark batch (1024 x 32 x 32 x 64 -> 64, residual, ReLU), 8 images
