@@ -1633,6 +1633,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   // the halo kernels stage whole images from contiguous rows: a layer that
   // reads its input through a row list takes the implicit GEMM
   const bool listed = a.src_rows || a.src2_rows || a.res_rows || a.dst_rows;
+  if (conv3_narrow(a, s)) return;   // 16 / 32 channels: row lists allowed
   if (vec_out && !listed && (conv3_wres(a, s) || conv3_halo(a, s))) return;
   if (vec_out) {
     // deep K on few pixels per image: K ranges of one tile on several

@@ -72,6 +72,12 @@ void conv_bf16(const ConvArgs& a, hipStream_t s);
 bool conv_rgb_stem_fits(int H, int W, int cin, int cout, int k, int stride, int pad);
 bool conv_rgb_stem(const ConvArgs& a, hipStream_t s);
 
+// 3x3 / stride-1 / pad-1 layers with 16 -> 16 or 32 -> 32 channels on 16- or
+// 32-pixel-wide images (row lists and device counts allowed): a halo kernel
+// with all weights in registers.  Returns false (launching nothing) for
+// other arguments.
+bool conv3_narrow(const ConvArgs& a, hipStream_t s);
+
 // K ranges per output tile for the layer shape (1: none).  A split layer
 // needs conv_ksplit_bytes of workspace; without it the layer runs unsplit
 // (the same sums in another order).  Depends on the shape only, so every

@@ -6,8 +6,9 @@ whole-image tiles with a ragged last tile, several tiles per workgroup), the
 direct-to-LDS implicit GEMM (1x1, 3x3, strided; with the K range of each
 tile split over workgroups for deep K on few pixels, and without), the
 RGB stem kernel (3-channel input read directly: 7x7 stride 2, ragged units
-and pixel blocks) and the element-gathering kernel (other 3-channel stems,
-Cout not a multiple of 8).
+and pixel blocks), the narrow halo kernel (16 or 32 channels, weights in
+registers) and the element-gathering kernel (other 3-channel stems, Cout
+not a multiple of 8).
 
 Bound per element: the fp32 accumulation error (K terms, gamma_K * sum |x w|)
 scaled by |scale|, the fp32 epilogue roundings, and half a bf16 ulp of the
@@ -55,6 +56,12 @@ CASES = [
     (2, 224, 224, 3, 64, 7, 2, 3, True, 1),     # with a residual: element gathers
     (7, 32, 32, 3, 64, 3, 1, 1, False, 1),      # 3x3 CIFAR stem on 3 channels: element gathers
     (5, 12, 12, 16, 32, 3, 1, 1, False, 1),
+    (5, 32, 32, 16, 16, 3, 1, 1, True, 1),      # narrow halo kernel: 16 channels, 4-row units
+    (7, 32, 32, 16, 16, 3, 1, 1, False, 0),
+    (300, 32, 32, 16, 16, 3, 1, 1, True, 1),    # several units per workgroup
+    (3, 9, 16, 16, 16, 3, 1, 1, True, 1),       # 16-pixel rows: 8-row units, ragged last unit
+    (3, 16, 16, 32, 32, 3, 1, 1, True, 1),      # 32 channels
+    (4, 13, 32, 32, 32, 3, 1, 1, False, 2),     # 13 rows: ragged last unit, GELU
     (5, 12, 12, 64, 24, 3, 1, 1, True, 2),      # Cout not a multiple of 8
     (37, 4, 4, 512, 512, 3, 1, 1, False, 1),    # K split in 4, ragged last row tile
     (37, 8, 8, 512, 512, 3, 2, 1, True, 1),     # strided, K split in 4
