@@ -1,5 +1,8 @@
-// 3x3 / stride-1 / pad-1 convolution with 16 or 32 channels in and out (the
-// narrow CIFAR ResNets, e.g. SkipNet's first two stages).
+// 3x3 / stride-1 / pad-1 convolution with few channels: 16 -> 16 and 32 -> 32
+// (the narrow CIFAR ResNets, e.g. SkipNet's first two stages) and the
+// 8-channel (padded RGB) CIFAR stem to 16 channels.  (An 8 -> 64 stem is
+// faster on the register-weight halo kernel, whose 64-channel output tile
+// amortises the staged rows over four times the MFMA work.)
 //
 // With so few channels a layer is a stream of bytes (about 70 FLOP per
 // byte): the implicit GEMM's per-tap gathers (each input pixel fetched nine
@@ -8,11 +11,12 @@
 // of RT output rows of one image: the unit's input rows plus a one-pixel halo
 // are staged in LDS once (pixels padded to 48 or 80 bytes, so the 16 lanes
 // of a read phase hit distinct banks), and every tap reads a shifted window
-// of them.  All the weights live in registers (20 or 72 VGPRs per lane).
+// of them.  All the weights live in registers (12 to 72 VGPRs per lane).
 // v_mfma_f32_16x16x32_bf16 with the weights as A and pixels as B: a 32-wide
-// K step is two taps of 16 channels or one tap of 32, and a lane's result is
-// 4 consecutive output channels of one pixel, stored (after scale / shift,
-// residual, activation, rounding) as 8-byte pieces of contiguous pixel rows.
+// K step is four taps of 8 channels, two of 16 or one of 32, and a lane's
+// result is 4 consecutive output channels of one pixel, stored (after scale
+// / shift, residual, activation, rounding) as 8-byte pieces of contiguous
+// pixel rows.
 // Persistent: the next unit's input rows are loaded into registers while the
 // current one computes.  Images are addressed through the row lists (fused
 // gate gathers / scatters) and the live count of the device host modes.
@@ -28,17 +32,21 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kNL = 3;   // 16-byte input chunks per thread and unit, at most
 
-template <int C, int W>
+template <int CI, int CO, int W>
 struct NarrowGeom {
   static constexpr int WB = W / 16;              // 16-pixel blocks per row
   static constexpr int RPW = 2 / WB;             // rows per wave
   static constexpr int RT = 4 * RPW;             // output rows per unit
   static constexpr int PR = RT + 2;              // staged rows
   static constexpr int PWX = W + 2;              // staged pixels per row
-  static constexpr int PS = C == 16 ? 48 : 80;   // bytes per staged pixel
-  static constexpr int CB = C / 16;              // 16-channel blocks
-  static constexpr int KSTEPS = (9 * C + 31) / 32;
-  static constexpr int CH = C / 8;               // 16-byte chunks per pixel
+  // bytes per staged pixel: 16 consecutive pixels of one read phase hit
+  // distinct banks (16 B pixels are contiguous; 48 and 80 B pixels are
+  // 12 and 20 words apart)
+  static constexpr int PS = CI == 8 ? 16 : CI == 16 ? 48 : 80;
+  static constexpr int CB = CO / 16;             // 16-channel output blocks
+  static constexpr int CH = CI / 8;              // 16-byte chunks per input pixel
+  static constexpr int TPS = 32 / CI;            // taps per 32-wide K step
+  static constexpr int KSTEPS = (9 * CI + 31) / 32;
   static constexpr int CHUNKS = PR * W * CH;     // chunks per unit
   static constexpr int BYTES = PR * PWX * PS;
   static_assert(CHUNKS <= 256 * kNL, "input chunks per unit");
@@ -46,7 +54,7 @@ struct NarrowGeom {
 
 struct NarrowP {
   const uint16_t* x;
-  const uint16_t* w;   // [cout_pad][Kp], K = tap * C + ci
+  const uint16_t* w;   // [cout_pad][Kp], K = tap * CI + ci
   int Kp;
   const float* scale;
   const float* shift;
@@ -67,9 +75,9 @@ __device__ __forceinline__ float narrow_act(float v) {
   return v;
 }
 
-template <int C, int W, int ACT, bool RES>
+template <int CI, int CO, int W, int ACT, bool RES>
 __global__ __launch_bounds__(256) void conv3n_kernel(NarrowP p) {
-  using G = NarrowGeom<C, W>;
+  using G = NarrowGeom<CI, CO, W>;
   __shared__ __align__(16) char pl[G::BYTES];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
@@ -100,14 +108,13 @@ __global__ __launch_bounds__(256) void conv3n_kernel(NarrowP p) {
   }
 
   // B operand offsets (bytes in the staged rows) of this lane's taps: step
-  // s, lane group g: tap 2 s + g / 2, channels 8 (g & 1) .. (16 channels)
-  // or tap s, channels 8 g .. (32 channels); a tap past the ninth reads a
-  // halo pixel, which is zero
+  // s, lane group g: tap TPS s + g / CH, channels 8 (g % CH) .. + 7 (K is
+  // tap-major, so these are the lane's K values 32 s + 8 g ..); a tap past
+  // the ninth reads a halo pixel, which is zero
   int toff[G::KSTEPS];
 #pragma unroll
   for (int s = 0; s < G::KSTEPS; ++s) {
-    const int tap = C == 16 ? 2 * s + (g >> 1) : s;
-    const int ch = C == 16 ? (g & 1) : g;
+    const int tap = G::TPS * s + g / G::CH, ch = g % G::CH;
     toff[s] = tap < 9 ? ((tap / 3) * G::PWX + (tap % 3)) * G::PS + ch * 16 : -1;
   }
 
@@ -119,7 +126,7 @@ __global__ __launch_bounds__(256) void conv3n_kernel(NarrowP p) {
     const int q = tid + 256 * i, pr = q / (W * G::CH), rem = q - pr * (W * G::CH);
     const int px = rem / G::CH, c = rem - px * G::CH;
     crow[i] = q < G::CHUNKS ? pr : -0x40000000;
-    csrc[i] = (pr * W + px) * C + c * 8;
+    csrc[i] = (pr * W + px) * CI + c * 8;
     clds[i] = (pr * G::PWX + px + 1) * G::PS + c * 16;
   }
   uint4 raw[kNL];
@@ -127,7 +134,7 @@ __global__ __launch_bounds__(256) void conv3n_kernel(NarrowP p) {
   auto load = [&](int t) {
     const int img = t / RG, oh0 = (t - img * RG) * G::RT;
     const int simg = p.srows ? p.srows[img] : img;
-    const int64_t base = (static_cast<int64_t>(simg) * p.H + oh0 - 1) * W * C;
+    const int64_t base = (static_cast<int64_t>(simg) * p.H + oh0 - 1) * W * CI;
 #pragma unroll
     for (int i = 0; i < kNL; ++i) {
       const int ih = oh0 - 1 + crow[i];
@@ -178,7 +185,7 @@ __global__ __launch_bounds__(256) void conv3n_kernel(NarrowP p) {
             float v[4] = {fmaf(acc[b][cb][0], sc[cb].x, sh[cb].x), fmaf(acc[b][cb][1], sc[cb].y, sh[cb].y),
                           fmaf(acc[b][cb][2], sc[cb].z, sh[cb].z), fmaf(acc[b][cb][3], sc[cb].w, sh[cb].w)};
             if (RES) {
-              const uint2 rv = *reinterpret_cast<const uint2*>(p.res + (static_cast<size_t>(rimg) * p.H * W + pix) * C + c0);
+              const uint2 rv = *reinterpret_cast<const uint2*>(p.res + (static_cast<size_t>(rimg) * p.H * W + pix) * CO + c0);
               v[0] += __uint_as_float(rv.x << 16);
               v[1] += __uint_as_float(rv.x & 0xffff0000u);
               v[2] += __uint_as_float(rv.y << 16);
@@ -187,7 +194,7 @@ __global__ __launch_bounds__(256) void conv3n_kernel(NarrowP p) {
             // v_cvt_pk_bf16_f32: round to nearest even, as the other kernels' epilogues
             const bf16x2 lo = {static_cast<__bf16>(narrow_act<ACT>(v[0])), static_cast<__bf16>(narrow_act<ACT>(v[1]))};
             const bf16x2 hi = {static_cast<__bf16>(narrow_act<ACT>(v[2])), static_cast<__bf16>(narrow_act<ACT>(v[3]))};
-            *reinterpret_cast<uint2*>(p.y + (static_cast<size_t>(dimg) * p.H * W + pix) * C + c0) =
+            *reinterpret_cast<uint2*>(p.y + (static_cast<size_t>(dimg) * p.H * W + pix) * CO + c0) =
                 make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
           }
         }
@@ -198,30 +205,31 @@ __global__ __launch_bounds__(256) void conv3n_kernel(NarrowP p) {
   }
 }
 
-template <int C, int W>
+template <int CI, int CO, int W>
 void go(const NarrowP& p, hipStream_t s) {
-  const int RG = (p.H + NarrowGeom<C, W>::RT - 1) / NarrowGeom<C, W>::RT;
+  const int RG = (p.H + NarrowGeom<CI, CO, W>::RT - 1) / NarrowGeom<CI, CO, W>::RT;
   const long units = static_cast<long>(p.n) * RG;
-  // the workgroups the CUs hold at once (registers: five per CU at 16
-  // channels, three at 32)
-  const long resident = (C == 16 ? 5 : 3) * 256;
+  // the workgroups the CUs hold at once (registers: five per CU with the
+  // small weight sets, three with 32 -> 32)
+  const long resident = (CI * CO <= 256 ? 5 : 3) * 256;
   const int grid = static_cast<int>(units < resident ? units : resident);
   auto launch = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, s, p); };
   const bool res = p.res != nullptr;
   if (p.act == ACT_RELU)
-    res ? launch(conv3n_kernel<C, W, ACT_RELU, true>) : launch(conv3n_kernel<C, W, ACT_RELU, false>);
+    res ? launch(conv3n_kernel<CI, CO, W, ACT_RELU, true>) : launch(conv3n_kernel<CI, CO, W, ACT_RELU, false>);
   else if (p.act == ACT_GELU)
-    res ? launch(conv3n_kernel<C, W, ACT_GELU, true>) : launch(conv3n_kernel<C, W, ACT_GELU, false>);
+    res ? launch(conv3n_kernel<CI, CO, W, ACT_GELU, true>) : launch(conv3n_kernel<CI, CO, W, ACT_GELU, false>);
   else
-    res ? launch(conv3n_kernel<C, W, ACT_NONE, true>) : launch(conv3n_kernel<C, W, ACT_NONE, false>);
+    res ? launch(conv3n_kernel<CI, CO, W, ACT_NONE, true>) : launch(conv3n_kernel<CI, CO, W, ACT_NONE, false>);
 }
 
 }  // namespace
 
 bool conv3_narrow(const ConvArgs& a, hipStream_t s) {
-  const int C = a.cin;
-  if (a.k != 3 || a.stride != 1 || a.pad != 1 || a.src2 || a.out_f32 || a.pool || a.cout != C || (C != 16 && C != 32) ||
-      (a.W != 16 && a.W != 32) || a.Ho != a.H || a.Wo != a.W || a.H < 1 || a.Kp < ((9 * C + 31) / 32) * 32)
+  const int CI = a.cin, CO = a.cout;
+  const bool pair = (CI == 16 && CO == 16) || (CI == 32 && CO == 32) || (CI == 8 && CO == 16);
+  if (a.k != 3 || a.stride != 1 || a.pad != 1 || a.src2 || a.out_f32 || a.pool || !pair || (a.W != 16 && a.W != 32) ||
+      a.Ho != a.H || a.Wo != a.W || a.H < 1 || a.Kp < ((9 * CI + 31) / 32) * 32)
     return false;
   if ((reinterpret_cast<uintptr_t>(a.src) | reinterpret_cast<uintptr_t>(a.dst) | reinterpret_cast<uintptr_t>(a.res) |
        reinterpret_cast<uintptr_t>(a.w) | reinterpret_cast<uintptr_t>(a.scale) | reinterpret_cast<uintptr_t>(a.shift)) &
@@ -242,10 +250,12 @@ bool conv3_narrow(const ConvArgs& a, hipStream_t s) {
   p.rrows = a.res_rows;
   p.drows = a.dst_rows;
   p.act = a.act;
-  if (C == 16)
-    a.W == 32 ? go<16, 32>(p, s) : go<16, 16>(p, s);
+  if (CI == 16)
+    a.W == 32 ? go<16, 16, 32>(p, s) : go<16, 16, 16>(p, s);
+  else if (CI == 32)
+    a.W == 32 ? go<32, 32, 32>(p, s) : go<32, 32, 16>(p, s);
   else
-    a.W == 32 ? go<32, 32>(p, s) : go<32, 16>(p, s);
+    a.W == 32 ? go<8, 16, 32>(p, s) : go<8, 16, 16>(p, s);
   return true;
 }
 

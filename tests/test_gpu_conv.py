@@ -62,6 +62,9 @@ CASES = [
     (3, 9, 16, 16, 16, 3, 1, 1, True, 1),       # 16-pixel rows: 8-row units, ragged last unit
     (3, 16, 16, 32, 32, 3, 1, 1, True, 1),      # 32 channels
     (4, 13, 32, 32, 32, 3, 1, 1, False, 2),     # 13 rows: ragged last unit, GELU
+    (5, 32, 32, 8, 16, 3, 1, 1, False, 1),      # 8-channel stem to 16: four taps per K step
+    (3, 16, 16, 8, 16, 3, 1, 1, True, 2),
+    (6, 11, 16, 8, 64, 3, 1, 1, True, 0),       # 8 -> 64 stays on the register-weight halo kernel
     (5, 12, 12, 64, 24, 3, 1, 1, True, 2),      # Cout not a multiple of 8
     (37, 4, 4, 512, 512, 3, 1, 1, False, 1),    # K split in 4, ragged last row tile
     (37, 8, 8, 512, 512, 3, 2, 1, True, 1),     # strided, K split in 4
