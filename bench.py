@@ -53,10 +53,15 @@ def measured_traffic(workload: str, batch: int):
         if " = " in line:
             k, v = line.strip().split(" = ", 1)
             kv[k] = v
-    src = os.path.join(ROOT, kv.get("kernel_source", ""))
-    if not os.path.isfile(src):
+    # the conv class spans several sources: the hash is over their bytes in
+    # the order listed
+    srcs = [os.path.join(ROOT, f) for f in kv.get("kernel_source", "").split()]
+    if not srcs or not all(os.path.isfile(f) for f in srcs):
         return None, "kernel source named by the summary is missing"
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != kv.get("kernel_source_sha256"):
+    h = hashlib.sha256()
+    for f in srcs:
+        h.update(open(f, "rb").read())
+    if h.hexdigest() != kv.get("kernel_source_sha256"):
         return None, "conv kernel changed since the counters were taken"
     return float(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
@@ -334,7 +339,7 @@ def main():
         "config": {"workload": args.workload, "batch": B, "input": list(wl.arch["input"]),
                    "branch_counts": counts, "host_mode": args.host_mode, "parallelism": "single GPU"},
         "host_modes": host_modes,
-        "roofline": {"bound": "mfma", "kernel": "conv_bf16_mfma (implicit-GEMM conv / linear)",
+        "roofline": {"bound": "mfma", "kernel": "conv_bf16_mfma (bf16 MFMA convolutions and linears: halo-tiled, narrow, RGB stem, implicit GEMM)",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
