@@ -31,7 +31,8 @@ size_t dycl_op_compact_workspace(int64_t n);
 /*
  * Stable two-way partition of rows 0..n-1 by flags[i] != 0.
  *   flags        [n] uint8, 16-byte aligned.
- *   orig         [n] int32 original ids of the rows, or NULL (id = row).
+ *   orig         [n] int32 original ids of the rows, 16-byte aligned, or NULL
+ *                (id = row).
  *   idx1, org1   [n] int32 outputs: rows with a set flag, in increasing row
  *                order, and their ids (org1 may be NULL).
  *   idx0, org0   the same for the clear flags (org0 may be NULL).

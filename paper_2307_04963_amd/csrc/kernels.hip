@@ -557,10 +557,10 @@ void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, in
 
 // ------------------------------------------------- large-n compaction ----
 // Reduce-then-scan over blocks of 4096 flags: (1) every block counts its
-// set flags, (2) one workgroup turns the counts into per-block output
-// offsets, (3) every block ranks its flags again (16 per thread, loaded as
-// one 16-byte vector; wave prefix sums by shuffles, waves combined through
-// LDS) and writes both lists.  Order is preserved (stable partition).
+// set flags (16 per thread, one 16-byte load), (2) one workgroup turns the
+// counts into per-block output offsets, (3) every block ranks its flags
+// again by ballots, stages its partition in LDS and writes both lists with
+// coalesced stores.  Order is preserved (stable partition).
 
 constexpr int kCompactBlock = 4096;
 
@@ -590,126 +590,205 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
   return x;
 }
 
-__global__ __launch_bounds__(256) void compact_count_kernel(const uint8_t* __restrict__ flags, size_t n,
+// Each workgroup counts kCountSub consecutive blocks: every thread loads its
+// 16 flags of each block (all loads in flight together), the waves reduce
+// by shuffles and LDS combines the four waves.
+constexpr int kCountSub = 8;
+
+__global__ __launch_bounds__(256) void compact_count_kernel(const uint8_t* __restrict__ flags, size_t n, int nb,
                                                             int32_t* __restrict__ bcount, const int32_t* nc) {
-  __shared__ int ws[4];
+  __shared__ int ws[4][kCountSub];
   if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
-  uint8_t v[16];
-  const size_t i0 = static_cast<size_t>(blockIdx.x) * kCompactBlock + threadIdx.x * 16;
-  int c = i0 < n ? flag_count16(flags, i0, n, v) : 0;
-  c = wave_incl_scan(c);
-  if ((threadIdx.x & 63) == 63) ws[threadIdx.x >> 6] = c;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t blk = static_cast<size_t>(blockIdx.x) * kCountSub * kCompactBlock;
+  const size_t g0 = blk + threadIdx.x * 16;
+  int c[kCountSub];
+  if (blk + static_cast<size_t>(kCountSub) * kCompactBlock <= n) {
+    uint4 q[kCountSub];
+#pragma unroll
+    for (int b = 0; b < kCountSub; ++b) q[b] = *reinterpret_cast<const uint4*>(flags + g0 + b * kCompactBlock);
+#pragma unroll
+    for (int b = 0; b < kCountSub; ++b) {
+      const uint32_t w[4] = {q[b].x, q[b].y, q[b].z, q[b].w};
+      int k = 0;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) k += ((w[j >> 2] >> (8 * (j & 3))) & 0xff) != 0;
+      c[b] = k;
+    }
+  } else {
+    uint8_t v[16];
+#pragma unroll
+    for (int b = 0; b < kCountSub; ++b) {
+      const size_t i0 = g0 + b * kCompactBlock;
+      c[b] = i0 < n ? flag_count16(flags, i0, n, v) : 0;
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < kCountSub; ++b) {
+    const int x = wave_incl_scan(c[b]);
+    if (lane == 63) ws[wave][b] = x;
+  }
   __syncthreads();
-  if (threadIdx.x == 0) bcount[blockIdx.x] = ws[0] + ws[1] + ws[2] + ws[3];
+  if (threadIdx.x < kCountSub) {
+    const int b = blockIdx.x * kCountSub + threadIdx.x;
+    if (b < nb) bcount[b] = ws[0][threadIdx.x] + ws[1][threadIdx.x] + ws[2][threadIdx.x] + ws[3][threadIdx.x];
+  }
 }
+
+// One workgroup, rounds of 16384 block counts: the counts are staged in LDS
+// with coalesced loads (all 16 per thread in flight together), each thread
+// prefix-sums 16 consecutive ones (its sum scanned across the workgroup:
+// shuffles within a wave, LDS across waves) and puts their offsets back in
+// place, and the offsets leave with coalesced stores.  Offsets within a
+// round fit 32 bits (at most 2^26).
+constexpr int kScanRound = 16 * 1024;
 
 __global__ __launch_bounds__(1024) void compact_scan_kernel(const int32_t* __restrict__ bcount, int nb, size_t n,
                                                             int64_t* __restrict__ boff, int32_t* counts,
                                                             const int32_t* nc) {
-  __shared__ int64_t ws[16];
-  __shared__ int64_t carry;
+  __shared__ __align__(16) int32_t sc[kScanRound];
+  __shared__ int ws[16];
   if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
-  if (threadIdx.x == 0) carry = 0;
-  __syncthreads();
-  for (int b0 = 0; b0 < nb; b0 += 1024) {
-    const int b = b0 + threadIdx.x;
-    const int c = b < nb ? bcount[b] : 0;
-    int x = wave_incl_scan(c);
-    if ((threadIdx.x & 63) == 63) ws[threadIdx.x >> 6] = x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int64_t carry = 0;                                // ones in the blocks of earlier rounds
+  for (int b0 = 0; b0 < nb; b0 += kScanRound) {
+    const int m = min(kScanRound, nb - b0);
+    int ld[kScanRound / 1024];
+#pragma unroll
+    for (int r = 0; r < kScanRound / 1024; ++r) {
+      const int k = r * 1024 + tid;
+      ld[r] = k < m ? bcount[b0 + k] : 0;
+    }
+#pragma unroll
+    for (int r = 0; r < kScanRound / 1024; ++r) sc[r * 1024 + tid] = ld[r];
     __syncthreads();
-    int64_t before = carry;
-    for (int w = 0; w < (int)(threadIdx.x >> 6); ++w) before += ws[w];
-    if (b < nb) boff[b] = before + x - c;     // ones before block b
+    int4 q[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) q[j] = reinterpret_cast<const int4*>(sc)[tid * 4 + j];
+    int c[16] = {q[0].x, q[0].y, q[0].z, q[0].w, q[1].x, q[1].y, q[1].z, q[1].w,
+                 q[2].x, q[2].y, q[2].z, q[2].w, q[3].x, q[3].y, q[3].z, q[3].w};
+    int sum = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sum += c[j];
+    const int x = wave_incl_scan(sum);
+    if (lane == 63) ws[wave] = x;
     __syncthreads();
-    if (threadIdx.x == 1023) carry = before + x;
+    int run = x - sum, total = 0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+      if (w < wave) run += ws[w];
+      total += ws[w];
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int cj = c[j];
+      c[j] = run;                                   // ones of this round before block tid * 16 + j
+      run += cj;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      reinterpret_cast<int4*>(sc)[tid * 4 + j] = make_int4(c[4 * j], c[4 * j + 1], c[4 * j + 2], c[4 * j + 3]);
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kScanRound / 1024; ++r) {
+      const int k = r * 1024 + tid;
+      if (k < m) boff[b0 + k] = carry + sc[k];
+    }
+    carry += total;
     __syncthreads();
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     counts[0] = static_cast<int32_t>(carry);
     counts[1] = static_cast<int32_t>(static_cast<int64_t>(n) - carry);
   }
 }
 
+// A block of 4096 flags in 4 rounds of 1024, 4 consecutive flags per lane
+// (one 32-bit load; the ids as one 16-byte load).  An element's rank among
+// the block's ones is the ones of earlier rounds, of earlier waves (LDS), of
+// lower lanes (for each of the 4 positions, mbcnt of that position's ballot)
+// and of the lane's own earlier elements; its rank among the zeros is its
+// block index minus that.  The block's partition is staged in LDS, ones from
+// the front and zeros from the back, and both runs are then written with
+// consecutive lanes on consecutive elements.
 __global__ __launch_bounds__(256) void compact_write_kernel(const uint8_t* __restrict__ flags,
                                                             const int32_t* __restrict__ orig, size_t n,
                                                             const int64_t* __restrict__ boff, int32_t* idx1,
                                                             int32_t* org1, int32_t* idx0, int32_t* org0,
                                                             const int32_t* nc) {
-  // 4 rounds of 1024 consecutive flags, 4 per lane (one 32-bit load): the
-  // lanes' counts are prefix-summed by shuffles within the wave and through
-  // LDS across the 4 waves; each lane then writes its elements to
-  // consecutive slots, so a wave fills one contiguous run of each list
-  __shared__ int wc1[4], wc0[4];
+  __shared__ int32_t sidx[kCompactBlock], sorg[kCompactBlock];
+  __shared__ int wc[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const size_t blk0 = static_cast<size_t>(blockIdx.x) * kCompactBlock;
   if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
   if (blk0 >= n) return;
-  int64_t base1 = boff[blockIdx.x];
-  int64_t base0 = static_cast<int64_t>(blk0) - base1;
+  const int nblk = static_cast<int>(min(n - blk0, static_cast<size_t>(kCompactBlock)));
+  int ones = 0;                                     // ones in earlier rounds
   for (int rd = 0; rd < kCompactBlock / 1024; ++rd) {
-    const size_t e = blk0 + static_cast<size_t>(rd) * 1024 + static_cast<size_t>(tid) * 4;
+    const int l0 = rd * 1024 + tid * 4;             // block index of the lane's first element
+    const size_t e = blk0 + l0;
+    const int nv = max(0, min(4, nblk - l0));
     uint8_t v[4] = {0, 0, 0, 0};
-    int nv = 0;
-    if (e + 4 <= n) {
+    int32_t id[4] = {0, 0, 0, 0};
+    if (nv == 4) {
       const uint32_t w = *reinterpret_cast<const uint32_t*>(flags + e);
 #pragma unroll
       for (int j = 0; j < 4; ++j) v[j] = (w >> (8 * j)) & 0xff;
-      nv = 4;
+      if (orig) {
+        const int4 q = *reinterpret_cast<const int4*>(orig + e);
+        id[0] = q.x;
+        id[1] = q.y;
+        id[2] = q.z;
+        id[3] = q.w;
+      }
     } else {
+#pragma unroll
       for (int j = 0; j < 4; ++j)
-        if (e + j < n) {
+        if (j < nv) {
           v[j] = flags[e + j];
-          ++nv;
+          if (orig) id[j] = orig[e + j];
         }
     }
-    int c1 = 0;
+    if (!orig)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) c1 += (j < nv && v[j] != 0);
-    const int c0 = nv - c1;
-    const int s1 = wave_incl_scan(c1), s0 = wave_incl_scan(c0);
-    if (lane == 63) {
-      wc1[wave] = s1;
-      wc0[wave] = s0;
+      for (int j = 0; j < 4; ++j) id[j] = static_cast<int32_t>(e + j);
+    int below = 0, wtot = 0;                        // ones of lower lanes; of the wave
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint64_t b = __ballot(j < nv && v[j] != 0);
+      below += __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b >> 32),
+                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(b), 0));
+      wtot += __popcll(b);
     }
+    if (lane == 0) wc[wave] = wtot;
     __syncthreads();
-    int64_t o1 = base1 + s1 - c1, o0 = base0 + s0 - c0;
-    int t1 = 0, t0 = 0;
+    int r1 = ones + below, rtot = 0;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      if (w < wave) {
-        o1 += wc1[w];
-        o0 += wc0[w];
-      }
-      t1 += wc1[w];
-      t0 += wc0[w];
-    }
-    int32_t id[4];
-    if (orig && nv == 4) {
-      const int4 q = *reinterpret_cast<const int4*>(orig + e);
-      id[0] = q.x;
-      id[1] = q.y;
-      id[2] = q.z;
-      id[3] = q.w;
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) id[j] = j < nv ? (orig ? orig[e + j] : static_cast<int32_t>(e + j)) : 0;
+      if (w < wave) r1 += wc[w];
+      rtot += wc[w];
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      if (j >= nv) break;
-      if (v[j]) {
-        idx1[o1] = static_cast<int32_t>(e + j);
-        if (org1) org1[o1] = id[j];
-        ++o1;
-      } else {
-        idx0[o0] = static_cast<int32_t>(e + j);
-        if (org0) org0[o0] = id[j];
-        ++o0;
+      if (j < nv) {
+        const int slot = v[j] ? r1 : kCompactBlock - 1 - (l0 + j - r1);
+        sidx[slot] = static_cast<int32_t>(e + j);
+        sorg[slot] = id[j];
+        r1 += v[j] != 0;
       }
     }
-    base1 += t1;
-    base0 += t0;
+    ones += rtot;
     __syncthreads();
+  }
+  const int64_t base1 = boff[blockIdx.x], base0 = static_cast<int64_t>(blk0) - base1;
+  for (int k = tid; k < ones; k += 256) {
+    idx1[base1 + k] = sidx[k];
+    if (org1) org1[base1 + k] = sorg[k];
+  }
+  const int zeros = nblk - ones;
+  for (int k = tid; k < zeros; k += 256) {
+    idx0[base0 + k] = sidx[kCompactBlock - 1 - k];
+    if (org0) org0[base0 + k] = sorg[kCompactBlock - 1 - k];
   }
 }
 
@@ -723,7 +802,8 @@ void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t*
   const int nb = static_cast<int>((n + kCompactBlock - 1) / kCompactBlock);
   int64_t* boff = static_cast<int64_t*>(workspace);
   int32_t* bcount = reinterpret_cast<int32_t*>(boff + nb);
-  hipLaunchKernelGGL(compact_count_kernel, dim3(nb), dim3(256), 0, s, flags, n, bcount, nc);
+  hipLaunchKernelGGL(compact_count_kernel, dim3((nb + kCountSub - 1) / kCountSub), dim3(256), 0, s, flags, n, nb,
+                     bcount, nc);
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, s, bcount, nb, n, boff, counts, nc);
   hipLaunchKernelGGL(compact_write_kernel, dim3(nb), dim3(256), 0, s, flags, orig, n, boff, idx1, org1, idx0, org0,
                      nc);

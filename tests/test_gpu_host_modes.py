@@ -108,6 +108,25 @@ def test_device_mode_oracle_parity(name):
     assert rep["ok"], rep
 
 
+def test_large_batch_partition_all_modes():
+    # above 16384 rows a decision's partition takes the reduce-then-scan
+    # kernels; device and graph modes hand them the live count on the device
+    rt = _rt()
+    B = 40000
+    wl, plan = _plan("mlp_exit", max_batch=B)
+    print(f"[host-modes] mlp_exit B={B} (large partition)", flush=True)
+    x, aux = wl.inputs(B)
+    ref = _run(rt, plan, wl, x, aux, "sync")
+    for mode in ("device", "graph"):
+        _same(ref, _run(rt, plan, wl, x, aux, mode))
+    rows = np.arange(0, B, 37)
+    xf, auxf = wl.inputs_f32(B)
+    oref = O.from_workload(wl).run(xf[rows], None if auxf is None else auxf[rows])
+    rep = compare(wl, ref, oref, rows=rows)
+    print(rep, flush=True)
+    assert rep["ok"], rep
+
+
 @pytest.mark.parametrize("tau,want", [(0.0, 0), (1.5, 2)])
 def test_device_mode_forced_exits(tau, want):
     # tau 0: every row leaves at the first head and later kernels find no

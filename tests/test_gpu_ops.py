@@ -1,7 +1,8 @@
 """Routing primitives through include/dycl_ops.h on the GPU: the stable
 two-way partition (single-workgroup form up to 16384 rows, reduce-then-scan
-above) bit-exact against numpy at every density (none, rare, half, all set)
-and ragged sizes, and row gathers / scatters byte-exact."""
+above) bit-exact against numpy at every density (none,
+rare, half, all set) and ragged sizes, also on a reused workspace that
+starts out dirty, and row gathers / scatters byte-exact."""
 
 import ctypes as C
 
@@ -46,6 +47,35 @@ def test_compact_is_a_stable_partition(n, density):
     np.testing.assert_array_equal(g1[:len(ones)], orig[ones])
     np.testing.assert_array_equal(i0[:len(zeros)], zeros)
     np.testing.assert_array_equal(g0[:len(zeros)], orig[zeros])
+
+
+def test_compact_reuses_a_dirty_workspace():
+    # every call rewrites the per-block counts and offsets it reads: a
+    # workspace full of garbage, then reused by a smaller call, gives exact
+    # partitions
+    import torch
+    L = _lib()
+    ws_bytes = L.lib.dycl_op_compact_workspace(300007)
+    ws = torch.full((ws_bytes,), 0xC3, dtype=torch.uint8, device="cuda")
+    for n, density in ((300007, 0.3), (70001, 0.7)):
+        print(f"[compact] dirty workspace n={n} density={density}", flush=True)
+        rng = np.random.default_rng(n)
+        flags = (rng.random(n) < density).astype(np.uint8)
+        orig = rng.permutation(n).astype(np.int32)
+        f, o = torch.from_numpy(flags).cuda(), torch.from_numpy(orig).cuda()
+        outs = [torch.full((n,), -7, dtype=torch.int32, device="cuda") for _ in range(4)]
+        counts = torch.zeros(2, dtype=torch.int32, device="cuda")
+        L.check(L.lib.dycl_op_compact(C.c_void_p(f.data_ptr()), C.c_void_p(o.data_ptr()), n,
+                                      *[C.c_void_p(t.data_ptr()) for t in outs], C.c_void_p(counts.data_ptr()),
+                                      C.c_void_p(ws.data_ptr()), ws_bytes, None))
+        torch.cuda.synchronize()
+        ones, zeros = np.nonzero(flags)[0], np.nonzero(flags == 0)[0]
+        assert counts.cpu().tolist() == [len(ones), len(zeros)]
+        i1, g1, i0, g0 = [t.cpu().numpy() for t in outs]
+        np.testing.assert_array_equal(i1[:len(ones)], ones)
+        np.testing.assert_array_equal(g1[:len(ones)], orig[ones])
+        np.testing.assert_array_equal(i0[:len(zeros)], zeros)
+        np.testing.assert_array_equal(g0[:len(zeros)], orig[zeros])
 
 
 def test_compact_empty_and_null_ids():
