@@ -20,6 +20,21 @@ namespace dycl {
 
 namespace {
 
+// bf16 <-> fp32 on the host, rounding to nearest even (finite values: the
+// weights and their batch-norm scales)
+float host_f32(uint16_t b) {
+  const uint32_t u = static_cast<uint32_t>(b) << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+uint16_t host_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
 void hip_check(hipError_t e, const char* what) {
   if (e != hipSuccess) throw HipError(std::string(what) + ": " + hipGetErrorString(e));
 }
@@ -99,10 +114,34 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
   // ... and every bf16 contraction's weights packed to [cout_pad][Kp] with
   // zero rows / columns, so tile loads never leave the array
   const uint8_t* hb = static_cast<const uint8_t*>(weights);
+  auto hf32 = [&](int64_t off, int i) {
+    float v;
+    std::memcpy(&v, hb + off + static_cast<size_t>(i) * 4, 4);
+    return v;
+  };
   for (Packed& q : sp.packed) {
     std::vector<uint16_t> h(static_cast<size_t>(q.cout_pad) * q.Kp, 0);
     for (int co = 0; co < q.cout; ++co) {
       const uint8_t* row = hb + q.w_off + (static_cast<size_t>(co) * q.w_ldk + q.w_k0) * 2;
+      if (q.w2_off >= 0) {
+        // a folded projection: [W_c | (scale_p / scale_c) W_p] with the
+        // layer's scale scale_c (fold_scale); a channel whose scale_c is 0
+        // keeps only the projection, at scale 1
+        const uint8_t* row2 = hb + q.w2_off + (static_cast<size_t>(co) * q.w2_ldk + q.w2_k0) * 2;
+        const float s1 = q.scale1_off >= 0 ? hf32(q.scale1_off, co) : 1.0f;
+        const float s2 = q.scale2_off >= 0 ? hf32(q.scale2_off, co) : 1.0f;
+        const bool main = s1 != 0.0f;
+        const float r = main ? s2 / s1 : s2;
+        uint16_t* dst = &h[static_cast<size_t>(co) * q.Kp];
+        const int k1 = q.K - q.cin2;
+        if (main) std::memcpy(dst, row, static_cast<size_t>(k1) * 2);
+        for (int c = 0; c < q.cin2; ++c) {
+          uint16_t b;
+          std::memcpy(&b, row2 + static_cast<size_t>(c) * 2, 2);
+          dst[k1 + c] = host_bf16(r * host_f32(b));
+        }
+        continue;
+      }
       for (int t = 0; t < q.taps; ++t)
         std::memcpy(&h[static_cast<size_t>(co) * q.Kp + static_cast<size_t>(t) * q.cin_pack],
                     row + static_cast<size_t>(t) * q.cin_src * 2, static_cast<size_t>(q.cin_src) * 2);
@@ -112,6 +151,25 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     q.dev = static_cast<uint16_t*>(ptr);
     p->weight_bytes += h.size() * 2;
     hip_check(hipMemcpy(q.dev, h.data(), h.size() * 2, hipMemcpyHostToDevice), "packed weights upload");
+  }
+
+  // folded projections: the layer's scales (1 where the block's own scale
+  // is 0) and the summed shifts, [scale | shift]
+  p->fold_shift.assign(sp.n_fold_shift, nullptr);
+  for (const Node& nd : sp.nodes) {
+    if (!nd.fold) continue;
+    std::vector<float> ss(2 * static_cast<size_t>(nd.cout));
+    for (int co = 0; co < nd.cout; ++co) {
+      const float s1 = nd.scale_off >= 0 ? hf32(nd.scale_off, co) : 1.0f;
+      ss[co] = s1 != 0.0f ? s1 : 1.0f;
+      ss[nd.cout + co] =
+          (nd.shift_off >= 0 ? hf32(nd.shift_off, co) : 0.0f) + (nd.shift2_off >= 0 ? hf32(nd.shift2_off, co) : 0.0f);
+    }
+    void* ptr = nullptr;
+    if (hipMalloc(&ptr, ss.size() * 4) != hipSuccess) throw OomError("folded scale / shift: hipMalloc failed");
+    p->fold_shift[nd.fold_shift] = static_cast<float*>(ptr);
+    p->weight_bytes += ss.size() * 4;
+    hip_check(hipMemcpy(ptr, ss.data(), ss.size() * 4, hipMemcpyHostToDevice), "folded scale / shift upload");
   }
 
   // fp32 weight matrices [rows][cols] kept transposed ([cols][rows]): exit
@@ -215,6 +273,8 @@ void plan_free(dycl_plan* p) {
   for (Packed& q : p->spec.packed)
     if (q.dev) hipFree(q.dev);
   for (float* h : p->head_t)
+    if (h) hipFree(h);
+  for (float* h : p->fold_shift)
     if (h) hipFree(h);
   for (void* b : p->buffers)
     if (b) hipFree(b);
@@ -374,8 +434,8 @@ struct Run {
     a.pad = nd.pad;
     a.w = q->dev;
     a.Kp = q->Kp;
-    a.scale = f32(nd.scale_off);
-    a.shift = f32(nd.shift_off);
+    a.scale = nd.fold ? p->fold_shift[nd.fold_shift] : f32(nd.scale_off);
+    a.shift = nd.fold ? p->fold_shift[nd.fold_shift] + nd.cout : f32(nd.shift_off);
     a.res = nd.res >= 0 ? static_cast<const uint16_t*>(tp[nd.res]) : nullptr;
     a.act = nd.act;
     a.dst = tp[nd.dst];

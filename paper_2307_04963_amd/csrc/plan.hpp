@@ -55,6 +55,13 @@ struct Node {
   int packed = -1;                           // index of packed bf16 weights
   bool pad_in = false;                       // reads the input padded to 8 channels
   bool pool = false;                         // a 3x3 / 2 max-pool fused in: dst is the pooled tensor
+  // a 1x1 projection shortcut folded in as src2: the packed weights carry
+  // the block's own weights and the projection's scaled by the ratio of the
+  // two scales; the run takes the block's scale and the summed shifts
+  // (plan-owned [scale | shift] vector fold_shift)
+  int64_t shift2_off = -1;
+  bool fold = false;
+  int fold_shift = -1;
   // fused gathers / scatters: which row list of the last decision maps this
   // layer's images to those of src, res, dst (0: none, 1: the rows that
   // stay (exit, halt), 2: the rows that take the true branch (gate body),
@@ -82,6 +89,12 @@ struct Packed {
   // taps x cin_src weights per output channel in the blob, stored as
   // taps x cin_pack (zero-filled) when the input channels are padded
   int taps = 1, cin_src = 0, cin_pack = 0;
+  // a folded projection: a second 1x1 block of cin2 columns appended to K,
+  // its rows multiplied by scale_2 / scale_1 (fp32 scales, or 1) before the
+  // bf16 rounding
+  int64_t w2_off = -1, w2_ldk = 0, w2_k0 = 0;
+  int cin2 = 0;
+  int64_t scale1_off = -1, scale2_off = -1;
   uint16_t* dev = nullptr;
 };
 
@@ -108,6 +121,8 @@ struct Spec {
   int fused_gathers = 0;   // exit carries read in place through the row list
   int fused_gates = 0;     // gates whose gathers and scatters are fused into the body convolutions
   int fused_pools = 0;     // max-pools fused into the stem convolution that feeds them
+  int fused_projections = 0;   // 1x1 projection shortcuts folded into the block's last 1x1 convolution
+  int n_fold_shift = 0;        // summed shift vectors of the folded projections
   int n_head_t = 0;      // fp32 weight matrices kept transposed on the device   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
 
@@ -116,6 +131,7 @@ struct Spec {
   void fuse_exit_gathers();
   void fuse_gate_moves();
   void fuse_stem_pools();
+  void fuse_projections();
 };
 
 }  // namespace dycl
@@ -146,6 +162,7 @@ struct dycl_plan {
   uint16_t* d_zeros = nullptr;   // 256 zero bytes: source of convolution padding taps
   uint16_t* d_xpad = nullptr;    // input padded to 8 channels (stems with Cin < 8)
   std::vector<float*> head_t;    // transposed fp32 weights: exit heads [C][ncls], fp32 linears [cin][cout]
+  std::vector<float*> fold_shift;   // folded projections: [scale | shift of the block's last conv + the projection's]
   size_t workspace_bytes = 0, weight_bytes = 0;
   // profiling
   bool profile = false;

@@ -445,6 +445,68 @@ void Spec::fuse_stem_pools() {
   }
 }
 
+// A 1x1 stride-1 projection shortcut P = scale_p * (W_p x) + shift_p whose
+// only reader is the block's last 1x1 convolution, as its residual:
+//   y = act(scale_c * (W_c h) + shift_c + P)
+//     = act(scale_c * ([W_c | (scale_p / scale_c) W_p] [h; x]) + (shift_c + shift_p)),
+// one contraction over the channel concatenation of h and x (src2); the
+// block's own weights stay as they are and the projection's rows carry the
+// ratio of the scales (one bf16 rounding, in place of the rounding of P).
+// The projection's output is never written nor read back.  Top-level nodes
+// only, with no decision between the two (the rows of x and h then match).
+void Spec::fuse_projections() {
+  if (dt != DType::BF16) return;
+  for (size_t i = 0; i < nodes.size(); ++i) {
+    Node& c = nodes[i];
+    if (c.kind != NodeKind::Conv || c.k != 1 || c.stride != 1 || c.pad != 0 || c.src2 >= 0 || c.res < 0 ||
+        c.pad_in || c.pool || c.cin1 % 8 || c.src_list || c.res_list || c.dst_list)
+      continue;
+    long j = -1;
+    bool between = false;   // a decision between the projection and c
+    for (long t = static_cast<long>(i) - 1; t >= 0; --t) {
+      if (nodes[t].kind == NodeKind::Conv && nodes[t].dst == c.res) {
+        j = t;
+        break;
+      }
+      between = between || is_decision(nodes[t]);
+    }
+    if (j < 0 || between) continue;
+    const Node& pn = nodes[j];
+    if (pn.k != 1 || pn.stride != 1 || pn.pad != 0 || pn.src2 >= 0 || pn.res >= 0 || pn.act != k::ACT_NONE ||
+        pn.pad_in || pn.pool || pn.cout != c.cout || pn.H != c.H || pn.W != c.W || pn.cin1 % 8 ||
+        pn.src_list || pn.dst_list || tensors[pn.dst].external)
+      continue;
+    std::vector<Use> us;
+    uses_of(nodes, pn.dst, -1, us);
+    if (us.size() != 1 || us[0].node != &c) continue;
+    const Packed& q1 = packed[c.packed];
+    Packed q = q1;
+    q.w2_off = pn.w_off;
+    q.w2_ldk = pn.w_ldk;
+    q.w2_k0 = pn.w_k0;
+    q.cin2 = pn.cin1;
+    q.scale1_off = c.scale_off;
+    q.scale2_off = pn.scale_off;
+    q.K = c.cin1 + pn.cin1;
+    q.Kp = (q.K + k::kBK - 1) / k::kBK * k::kBK;
+    q.dev = nullptr;
+    packed.push_back(q);
+    c.packed = static_cast<int>(packed.size()) - 1;
+    c.src2 = pn.src;
+    c.cin2 = pn.cin1;
+    c.res = -1;
+    c.fold = true;
+    c.shift2_off = pn.shift_off;
+    c.fold_shift = n_fold_shift++;
+    tensors[pn.dst].unused = true;
+    TensorInfo& x = tensors[pn.src];
+    x.last = std::max(x.last, c.seq_pre);
+    nodes.erase(nodes.begin() + j);
+    --i;
+    ++fused_projections;
+  }
+}
+
 // The gather of an exit's carried tensor fused into its readers (a row
 // gather is a copy that computes nothing): when every reader of the carried
 // copy is a bf16 convolution that takes it as its main input before the next
@@ -645,6 +707,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   if (ns.kind != Json::Array || ns.size() == 0) throw SpecError("nodes must be a non-empty array");
   for (size_t i = 0; i < ns.size(); ++i) nodes.push_back(b.node(ns.at(i), max_batch));
   fuse_stem_pools();
+  fuse_projections();
   fuse_original_order_reads();
   fuse_exit_gathers();
   fuse_gate_moves();
@@ -662,7 +725,8 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
   std::ostringstream os;
   os << "nodes=" << nodes_total << " decisions=" << decisions << " tensors=" << tensors.size()
      << " packed_weights=" << packed.size() << " fused_gathers=" << fused_gathers
-     << " fused_gates=" << fused_gates << " fused_pools=" << fused_pools << " n_out=" << n_out
+     << " fused_gates=" << fused_gates << " fused_pools=" << fused_pools
+     << " fused_projections=" << fused_projections << " n_out=" << n_out
      << " dtype=" << dts;
   summary = os.str();
 }

@@ -68,6 +68,9 @@ def test_every_workload_spec_validates(name):
     # the ImageNet stem's max-pool runs in the stem kernel's epilogue
     fp = int(re.search(r"fused_pools=(\d+)", msg).group(1))
     assert fp == (1 if name == "resnet50_exit" else 0)
+    # the stride-1 projection shortcut of the first bottleneck folds into the block's last 1x1 conv
+    fpr = int(re.search(r"fused_projections=(\d+)", msg).group(1))
+    assert fpr == (1 if name == "resnet50_exit" else 0)
     # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
     if name == "act_loop":
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
@@ -118,6 +121,41 @@ def test_stem_pool_fused_only_when_the_pool_is_the_only_reader():
         rc, msg = _check(json.dumps(sp), nb)
         assert rc == 0, msg
         assert f"fused_pools={want}" in msg, msg
+
+
+def test_projection_folded_only_into_its_sole_linear_reader():
+    # h = relu(conv1x1(x)); p = conv1x1(x) (the projection); y = relu(conv1x1(h) + p)
+    wb = 64 * 64 * 2
+
+    def spec(p_act="none", p_stride=1, extra_reader=False, decision_between=False):
+        head = {"op": "exit", "w": wb, "b": wb + 64 * 10 * 4, "ncls": 10, "final": True}
+        nodes = [{"op": "conv", "src": "x", "dst": "h", "k": 1, "cout": 64, "act": "relu", "w": {"off": 0}},
+                 {"op": "conv", "src": "x", "dst": "p", "k": 1, "stride": p_stride, "cout": 64, "act": p_act,
+                  "w": {"off": 0}},
+                 {"op": "conv", "src": "h" if p_stride == 1 else "hs", "dst": "y", "k": 1, "cout": 64,
+                  "act": "relu", "w": {"off": 0}, "res": "p"},
+                 dict(head, src="y", index=1)]
+        if p_stride != 1:
+            nodes.insert(2, {"op": "conv", "src": "h", "dst": "hs", "k": 1, "stride": 2, "cout": 64, "act": "relu",
+                             "w": {"off": 0}})
+        if extra_reader:
+            nodes.insert(-1, {"op": "conv", "src": "p", "dst": "z", "k": 1, "cout": 64, "act": "relu",
+                              "w": {"off": 0}})
+            nodes[-1]["src"] = "z"
+        if decision_between:
+            nodes.insert(2, dict(head, src="p", final=False, tau=0.5, index=0, T=wb + 64 * 10 * 4,
+                                 carry=[["h", "hc"], ["p", "pc"]]))
+            nodes[3]["src"], nodes[3]["res"] = "hc", "pc"
+        return {"version": 1, "dtype": "bf16", "input": {"name": "x", "shape": [8, 8, 64]}, "n_out": 10,
+                "nodes": nodes}
+
+    nb = wb + 64 * 10 * 4 + 64
+    cases = ((spec(), 1), (spec(p_act="relu"), 0), (spec(p_stride=2), 0), (spec(extra_reader=True), 0),
+             (spec(decision_between=True), 0))
+    for sp, want in cases:
+        rc, msg = _check(json.dumps(sp), nb)
+        assert rc == 0, msg
+        assert f"fused_projections={want}" in msg, (want, msg)
 
 
 def _mlp_spec():
