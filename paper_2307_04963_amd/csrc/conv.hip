@@ -49,6 +49,7 @@ struct ConvP {
   // (null: i)
   const int32_t* srows;
   const int32_t* s2rows;   // image list of src2 (the concatenated input)
+  int H2, W2, s2;          // src2: spatial shape and the stride it is read at
   const int32_t* rrows;
   const int32_t* drows;
   int ksplit;              // K ranges per tile (conv_lds_kernel); > 1: fp32 partials to `part`
@@ -141,7 +142,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
       a_ih[i] = oh * p.stride - p.pad;
       a_iw[i] = ow * p.stride - p.pad;
       a_pix[i] = (simg * p.H + a_ih[i]) * p.W + a_iw[i];
-      a_pix2[i] = (s2img * p.H + a_ih[i]) * p.W + a_iw[i];
+      a_pix2[i] = (s2img * p.H2 + a_ih[i] * p.s2) * p.W2 + a_iw[i] * p.s2;
     } else {
       a_ih[i] = -0x4000;
       a_iw[i] = -0x4000;
@@ -375,7 +376,7 @@ __global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
       a_ih[j] = oh * p.stride - p.pad;
       a_iw[j] = ow * p.stride - p.pad;
       a_pix[j] = (simg * p.H + a_ih[j]) * p.W + a_iw[j];
-      a_pix2[j] = (s2img * p.H + a_ih[j]) * p.W + a_iw[j];
+      a_pix2[j] = (s2img * p.H2 + a_ih[j] * p.s2) * p.W2 + a_iw[j] * p.s2;
     } else {
       a_ih[j] = -0x4000;
       a_iw[j] = -0x4000;
@@ -1573,6 +1574,9 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   ConvP p;
   p.src = a.src;
   p.src2 = a.src2;
+  p.H2 = a.src2_H > 0 ? a.src2_H : a.H;
+  p.W2 = a.src2_W > 0 ? a.src2_W : a.W;
+  p.s2 = a.src2_stride > 0 ? a.src2_stride : 1;
   p.cin1 = a.cin1;
   p.cin2 = a.cin2;
   p.H = a.H;

@@ -32,7 +32,9 @@ int conv_cout_pad(int cout);
 
 struct ConvArgs {
   const uint16_t* src;   // [n, H, W, cin1] bf16 NHWC
-  const uint16_t* src2;  // [n, 1, 1, cin2] (channel concat, k == 1 only) or null
+  const uint16_t* src2;  // [n, H2, W2, cin2] channel concat (k == 1, pad 0 only), read at output pixel
+                         // (oh, ow) from (oh * src2_stride, ow * src2_stride), or null
+  int src2_H = 0, src2_W = 0, src2_stride = 1;   // 0: src2 has the spatial shape of src
   int cin1, cin2;        // cin = cin1 + cin2
   int n, H, W, cin, Ho, Wo, cout, k, stride, pad;
   const uint16_t* w;     // packed [cout_pad][Kp] bf16, K order (kh, kw, ci)

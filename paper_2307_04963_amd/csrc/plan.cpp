@@ -420,6 +420,11 @@ struct Run {
     k::ConvArgs a;
     a.src = nd.pad_in ? p->d_xpad : static_cast<const uint16_t*>(tp[nd.src]);
     a.src2 = nd.src2 >= 0 ? static_cast<const uint16_t*>(tp[nd.src2]) : nullptr;
+    if (nd.src2 >= 0) {
+      a.src2_H = sp.tensors[nd.src2].H;
+      a.src2_W = sp.tensors[nd.src2].W;
+      a.src2_stride = nd.s2;
+    }
     a.cin1 = nd.pad_in ? sp.pad_input_c : nd.cin1;
     a.cin2 = nd.cin2;
     a.n = n;

@@ -60,6 +60,7 @@ struct Node {
   // two scales; the run takes the block's scale and the summed shifts
   // (plan-owned [scale | shift] vector fold_shift)
   int64_t shift2_off = -1;
+  int s2 = 1;            // src2 is read at this stride (a folded strided projection)
   bool fold = false;
   int fold_shift = -1;
   // fused gathers / scatters: which row list of the last decision maps this

@@ -445,11 +445,12 @@ void Spec::fuse_stem_pools() {
   }
 }
 
-// A 1x1 stride-1 projection shortcut P = scale_p * (W_p x) + shift_p whose
+// A 1x1 projection shortcut P = scale_p * (W_p x) + shift_p (any stride s) whose
 // only reader is the block's last 1x1 convolution, as its residual:
 //   y = act(scale_c * (W_c h) + shift_c + P)
 //     = act(scale_c * ([W_c | (scale_p / scale_c) W_p] [h; x]) + (shift_c + shift_p)),
-// one contraction over the channel concatenation of h and x (src2); the
+// one contraction over the channel concatenation of h and x (src2, read at
+// stride s: output pixel (i, j) takes x at (s i, s j)); the
 // block's own weights stay as they are and the projection's rows carry the
 // ratio of the scales (one bf16 rounding, in place of the rounding of P).
 // The projection's output is never written nor read back.  Top-level nodes
@@ -472,8 +473,8 @@ void Spec::fuse_projections() {
     }
     if (j < 0 || between) continue;
     const Node& pn = nodes[j];
-    if (pn.k != 1 || pn.stride != 1 || pn.pad != 0 || pn.src2 >= 0 || pn.res >= 0 || pn.act != k::ACT_NONE ||
-        pn.pad_in || pn.pool || pn.cout != c.cout || pn.H != c.H || pn.W != c.W || pn.cin1 % 8 ||
+    if (pn.k != 1 || pn.pad != 0 || pn.src2 >= 0 || pn.res >= 0 || pn.act != k::ACT_NONE ||
+        pn.pad_in || pn.pool || pn.cout != c.cout || pn.Ho != c.H || pn.Wo != c.W || pn.cin1 % 8 ||
         pn.src_list || pn.dst_list || tensors[pn.dst].external)
       continue;
     std::vector<Use> us;
@@ -494,6 +495,7 @@ void Spec::fuse_projections() {
     c.packed = static_cast<int>(packed.size()) - 1;
     c.src2 = pn.src;
     c.cin2 = pn.cin1;
+    c.s2 = pn.stride;
     c.res = -1;
     c.fold = true;
     c.shift2_off = pn.shift_off;
@@ -523,17 +525,29 @@ void Spec::fuse_exit_gathers() {
       const int from = ex.pairs[q].first, to = ex.pairs[q].second;
       std::vector<Use> us;
       uses_of(nodes, to, -1, us);
+      // a reader is a convolution taking the copy as its main input, or as
+      // the concatenated input of a folded projection (src2 with no list)
+      auto src2_read = [&](const Use& u) {
+        const Node& nd = *u.node;
+        return !u.conv_src && nd.kind == NodeKind::Conv && nd.src2 == to && nd.src2_list == 0 && nd.src != to &&
+               nd.res != to && nd.park_src != to;
+      };
       bool ok = !us.empty();
       for (const Use& u : us)
-        ok = ok && u.conv_src && u.top > static_cast<long>(i) && u.top < static_cast<long>(next) && !u.node->pad_in &&
-             (u.node->src2 < 0 || u.node->src2_list == 3);
+        ok = ok && u.top > static_cast<long>(i) && u.top < static_cast<long>(next) && !u.node->pad_in &&
+             ((u.conv_src && (u.node->src2 < 0 || u.node->src2_list == 3 || u.node->src2_list == 1)) || src2_read(u));
       if (!ok) {
         ++q;
         continue;
       }
       for (const Use& u : us) {
-        u.node->src = from;
-        u.node->src_list = 1;
+        if (u.conv_src) {
+          u.node->src = from;
+          u.node->src_list = 1;
+        } else {
+          u.node->src2 = from;
+          u.node->src2_list = 1;
+        }
         TensorInfo& f = tensors[from];
         f.last = std::max(f.last, u.node->seq_pre);
       }

@@ -68,9 +68,9 @@ def test_every_workload_spec_validates(name):
     # the ImageNet stem's max-pool runs in the stem kernel's epilogue
     fp = int(re.search(r"fused_pools=(\d+)", msg).group(1))
     assert fp == (1 if name == "resnet50_exit" else 0)
-    # the stride-1 projection shortcut of the first bottleneck folds into the block's last 1x1 conv
+    # each stage's projection shortcut (stride 1, then 2) folds into its block's last 1x1 conv
     fpr = int(re.search(r"fused_projections=(\d+)", msg).group(1))
-    assert fpr == (1 if name == "resnet50_exit" else 0)
+    assert fpr == (4 if name == "resnet50_exit" else 0)
     # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
     if name == "act_loop":
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
@@ -150,7 +150,7 @@ def test_projection_folded_only_into_its_sole_linear_reader():
                 "nodes": nodes}
 
     nb = wb + 64 * 10 * 4 + 64
-    cases = ((spec(), 1), (spec(p_act="relu"), 0), (spec(p_stride=2), 0), (spec(extra_reader=True), 0),
+    cases = ((spec(), 1), (spec(p_act="relu"), 0), (spec(p_stride=2), 1), (spec(extra_reader=True), 0),
              (spec(decision_between=True), 0))
     for sp, want in cases:
         rc, msg = _check(json.dumps(sp), nb)
