@@ -252,7 +252,7 @@ def main():
         copy_probe()
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the executor runs on one GPU; --gpus {args.gpus} is not supported "
               "(samples are independent, so a multi-GPU run would shard the batch; not built)", file=sys.stderr)
         sys.exit(2)
 
