@@ -49,6 +49,37 @@ def test_compact_is_a_stable_partition(n, density):
     np.testing.assert_array_equal(g0[:len(zeros)], orig[zeros])
 
 
+def test_compact_scan_carries_across_rounds():
+    # 2^26 + 4097 rows: 16385 blocks of 4096 flags, one more than a scan round
+    # holds, so the block offsets of the second round start from the first
+    # round's total
+    import torch
+    L = _lib()
+    n = (1 << 26) + 4097
+    print(f"[compact] n={n} (two scan rounds)", flush=True)
+    rng = np.random.default_rng(26)
+    flags = (rng.random(n, dtype=np.float32) < 0.5).astype(np.uint8)
+    flags[-4097:] = 1                       # the second round's block: all set
+    f = torch.from_numpy(flags).cuda()
+    o = torch.arange(n, dtype=torch.int32, device="cuda").flip(0).contiguous()
+    outs = [torch.empty((n,), dtype=torch.int32, device="cuda") for _ in range(4)]
+    counts = torch.zeros(2, dtype=torch.int32, device="cuda")
+    ws_bytes = L.lib.dycl_op_compact_workspace(n)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    L.check(L.lib.dycl_op_compact(C.c_void_p(f.data_ptr()), C.c_void_p(o.data_ptr()), n,
+                                  *[C.c_void_p(t.data_ptr()) for t in outs], C.c_void_p(counts.data_ptr()),
+                                  C.c_void_p(ws.data_ptr()), ws_bytes, None))
+    torch.cuda.synchronize()
+    ones = np.flatnonzero(flags).astype(np.int32)
+    zeros = np.flatnonzero(flags == 0).astype(np.int32)
+    assert counts.cpu().tolist() == [len(ones), len(zeros)]
+    i1, g1, i0, g0 = [t.cpu().numpy() for t in outs]
+    np.testing.assert_array_equal(i1[:len(ones)], ones)
+    np.testing.assert_array_equal(g1[:len(ones)], n - 1 - ones)
+    np.testing.assert_array_equal(i0[:len(zeros)], zeros)
+    np.testing.assert_array_equal(g0[:len(zeros)], n - 1 - zeros)
+
+
 def test_compact_reuses_a_dirty_workspace():
     # every call rewrites the per-block counts and offsets it reads: a
     # workspace full of garbage, then reused by a smaller call, gives exact
