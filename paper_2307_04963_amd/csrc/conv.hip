@@ -636,6 +636,12 @@ struct Conv3P {
   int RS, segs, PW, NP;    // rows per patch segment, segments, patch width, patch pixels
   int tiles, tpi;          // tiles; tiles per image (row mode) or 0 (image mode)
   const int32_t* nc;       // device count of live images (<= n) or null
+  // image mode only: image i of the layer is image srows[i] of src, rrows[i]
+  // of res, drows[i] of dst (null: i); listed tensors are addressed from
+  // their first byte, so their size stays below 2^31 bytes (host check)
+  const int32_t* srows;
+  const int32_t* rrows;
+  const int32_t* drows;
 };
 
 constexpr int kW3Patch = 256;                      // patch pixels per buffer (= kHP)
@@ -700,6 +706,19 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
       int img, oh0, m0, lim;
       tile_geom(t - 1, img, oh0, m0, lim);
       const char* sb = sbuf + ((t - 1 - t_begin) & 1) * kW3RB;
+      if (p.drows) {
+        // listed output: a row's image through drows, offsets from dst's start
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int u = k * NL + st, row = u >> 3, pos = u & 7;
+          const int sg = row / HW, px = row - sg * HW;
+          const uint32_t o = row < lim ? static_cast<uint32_t>((p.drows[img + sg] * HW + px) * 128 + rsw(row, pos) * 16)
+                                       : 0xC0000000u;
+          const u32x4 v = *reinterpret_cast<const u32x4*>(sb + u * 16);
+          buffer_store16(p.dst, 0x7fffffffu, o, v);
+        }
+        continue;
+      }
       uint16_t* const dbase = p.dst + (size_t)m0 * 64;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -723,6 +742,10 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
     const int ld = tid - 4 * 64, lw = wv - 4;
     const int rowb = p.W * CIN * 2, imgb = p.H * rowb;
     uint32_t vofs[JP];
+    // listed input (image mode): a slot's segment and its offset inside the
+    // image (vseg -1: a slot that never holds data); the row ids of a tile's
+    // segments are requested with the previous tile's loads
+    int vseg[JP], rid[JP];
 #pragma unroll
     for (int j = 0; j < JP; ++j) {
       const int u = j * NL + ld, q = u / SLOTS, ch = u - (u / SLOTS) * SLOTS;
@@ -732,29 +755,61 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
       bool data = q < p.NP && ch < 8 && pc >= 1 && pc <= p.W;
       if (!p.tpi) data = data && pr >= 1 && pr <= p.H;
       vofs[j] = data ? static_cast<uint32_t>(sg * imgb + (pr - 1) * rowb + (pc - 1) * CIN * 2 + ch * 16) : 0xC0000000u;
+      vseg[j] = data ? sg : -1;
+      if (data) vofs[j] -= static_cast<uint32_t>(sg * imgb);
+      if (!p.srows) vofs[j] += data ? static_cast<uint32_t>(sg * imgb) : 0u;
+      rid[j] = 0;
     }
+    // residual slots (listed residual): segment and pixel of each row
+    auto fetch_rids = [&](int t) __attribute__((always_inline)) {
+      int img, oh0, m0, lim;
+      tile_geom(t, img, oh0, m0, lim);
+#pragma unroll
+      for (int j = 0; j < JP; ++j) rid[j] = vseg[j] >= 0 && img + vseg[j] < n ? p.srows[img + vseg[j]] : -1;
+    };
+    if (p.srows) fetch_rids(t_begin);
     for (int t = t_begin; t <= t_end; ++t) {
       if (t < t_end) {
         const int buf = (t - t_begin) & 1;
         int img, oh0, m0, lim;
         tile_geom(t, img, oh0, m0, lim);
         const int nimg = p.tpi ? 1 : min(p.segs, n - img);
-        const uint16_t* pbase = p.src + (size_t)img * p.H * p.W * CIN;
-        const uint32_t pbytes = static_cast<uint32_t>(nimg) * imgb, tofs = static_cast<uint32_t>(oh0) * rowb;
         char* pb = pbuf + buf * kW3PB;
+        if (p.srows) {
 #pragma unroll
-        for (int j = 0; j < JP; ++j)
-          buffer_load_lds16(pbase, pbytes, vofs[j] + tofs, (lds_void_ptr)(pb + (j * NL + lw * 64) * 16));
+          for (int j = 0; j < JP; ++j) {
+            const uint32_t o = rid[j] >= 0 ? static_cast<uint32_t>(rid[j]) * imgb + vofs[j] : 0xC0000000u;
+            buffer_load_lds16(p.src, 0x7fffffffu, o, (lds_void_ptr)(pb + (j * NL + lw * 64) * 16));
+          }
+        } else {
+          const uint16_t* pbase = p.src + (size_t)img * p.H * p.W * CIN;
+          const uint32_t pbytes = static_cast<uint32_t>(nimg) * imgb, tofs = static_cast<uint32_t>(oh0) * rowb;
+#pragma unroll
+          for (int j = 0; j < JP; ++j)
+            buffer_load_lds16(pbase, pbytes, vofs[j] + tofs, (lds_void_ptr)(pb + (j * NL + lw * 64) * 16));
+        }
         if (RES) {
           char* rb = rbuf + buf * kW3RB;
-          const uint16_t* rbase = p.res + (size_t)m0 * 64;
+          if (p.rrows) {
 #pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const int u = k * NL + ld, row = u >> 3, pos = u & 7;
-            buffer_load_lds16(rbase, static_cast<uint32_t>(lim) * 128, row * 128 + rsw(row, pos) * 16,
-                              (lds_void_ptr)(rb + (k * NL + lw * 64) * 16));
+            for (int k = 0; k < 8; ++k) {
+              const int u = k * NL + ld, row = u >> 3, pos = u & 7;
+              const int sg = row / HW, px = row - sg * HW;
+              const uint32_t o = row < lim ? static_cast<uint32_t>((p.rrows[img + sg] * HW + px) * 128 + rsw(row, pos) * 16)
+                                           : 0xC0000000u;
+              buffer_load_lds16(p.res, 0x7fffffffu, o, (lds_void_ptr)(rb + (k * NL + lw * 64) * 16));
+            }
+          } else {
+            const uint16_t* rbase = p.res + (size_t)m0 * 64;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+              const int u = k * NL + ld, row = u >> 3, pos = u & 7;
+              buffer_load_lds16(rbase, static_cast<uint32_t>(lim) * 128, row * 128 + rsw(row, pos) * 16,
+                                (lds_void_ptr)(rb + (k * NL + lw * 64) * 16));
+            }
           }
         }
+        if (p.srows && t + 1 < t_end) fetch_rids(t + 1);
       }
       all_barrier();                      // tile t is in LDS for the compute waves
     }
@@ -1441,6 +1496,15 @@ bool conv3_wres(const ConvArgs& a, hipStream_t s) {
   p.NP = g.NP;
   p.tiles = g.mtiles;
   p.nc = a.ncount;
+  // row lists: image mode only, no concatenated input, and every listed
+  // tensor small enough for 31-bit byte offsets from its start
+  const bool listed = a.src_rows || a.res_rows || a.dst_rows;
+  if (listed && (stem || g.tpi != 0 || a.src2_rows || a.list_rows <= 0 ||
+                 static_cast<long>(a.list_rows) * a.H * a.W * 128 > 0x7ffffff0L))
+    return false;
+  p.srows = a.src_rows;
+  p.rrows = a.res_rows;
+  p.drows = a.dst_rows;
   const int grid = p.tiles < cus ? p.tiles : cus;
   auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(512), 0, s, p); };
 #define DYCL_W(CIN)                                                     \
@@ -1634,11 +1698,12 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   // the direct-to-LDS kernel stores 8 channels per 16-byte vector
   const bool vec_out = a.cout % 8 == 0 && (reinterpret_cast<uintptr_t>(a.dst) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.res) & 15) == 0 && a.zeros != nullptr;
-  // the halo kernels stage whole images from contiguous rows: a layer that
-  // reads its input through a row list takes the implicit GEMM
+  // the streamed-weight halo kernel stages whole images from contiguous
+  // rows: a layer with row lists takes the register-weight halo kernel
+  // (image mode) or the implicit GEMM
   const bool listed = a.src_rows || a.src2_rows || a.res_rows || a.dst_rows;
   if (conv3_narrow(a, s)) return;   // 16 / 32 channels: row lists allowed
-  if (vec_out && !listed && (conv3_wres(a, s) || conv3_halo(a, s))) return;
+  if (vec_out && (listed ? conv3_wres(a, s) : (conv3_wres(a, s) || conv3_halo(a, s)))) return;
   if (vec_out) {
     // deep K on few pixels per image: K ranges of one tile on several
     // workgroups, fp32 partials summed in a fixed order by a second kernel

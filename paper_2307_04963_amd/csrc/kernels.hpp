@@ -54,6 +54,7 @@ struct ConvArgs {
   const int32_t* src2_rows = nullptr;
   const int32_t* res_rows = nullptr;
   const int32_t* dst_rows = nullptr;
+  int list_rows = 0;     // rows of the tensors read or written through a list (0: no list)
   float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split
   size_t splitws_bytes = 0;
   // 1: a 3x3 / stride-2 / pad-1 max-pool of the output is fused in and dst

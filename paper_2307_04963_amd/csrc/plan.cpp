@@ -455,6 +455,7 @@ struct Run {
     a.src2_rows = list(nd.src2_list);
     a.res_rows = list(nd.res_list);
     a.dst_rows = list(nd.dst_list);
+    if (a.src_rows || a.res_rows || a.dst_rows) a.list_rows = p->max_batch;
     a.splitws = p->d_split;
     a.splitws_bytes = p->split_bytes;
     if (nd.pool) {

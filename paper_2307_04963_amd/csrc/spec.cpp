@@ -616,9 +616,12 @@ void Spec::fuse_original_order_reads() {
 // read and then written by the same thread).
 void Spec::fuse_gate_moves() {
   if (dt != DType::BF16) return;
+  // bodies on the streamed-weight halo kernel cannot take row lists; the
+  // register-weight one (64 -> 64 channels) can on whole-image tiles
   auto halo_kind = [](const Node& nd, const TensorInfo& src) {
+    const bool wres_images = nd.cin1 == 64 && nd.cout == 64 && src.H * src.W <= 128;
     return nd.k == 3 && nd.stride == 1 && nd.pad == 1 && nd.src2 < 0 && nd.cin1 % 64 == 0 && nd.cout % 64 == 0 &&
-           !(src.H * src.W <= 128 && 2 * src.H * src.W < (src.H + 2) * (src.W + 2));
+           !(src.H * src.W <= 128 && 2 * src.H * src.W < (src.H + 2) * (src.W + 2)) && !wres_images;
   };
   for (Node& g : nodes) {
     if (g.kind != NodeKind::Gate) continue;
