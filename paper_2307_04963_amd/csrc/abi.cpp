@@ -229,6 +229,7 @@ int dycl_op_compact(const uint8_t* flags, const int32_t* orig, int64_t n, int32_
   }
   if (!flags || !idx1 || !idx0) return fail(DYCL_E_INVALID, "dycl_op_compact: null flags or index output");
   if (reinterpret_cast<uintptr_t>(flags) & 15) return fail(DYCL_E_INVALID, "dycl_op_compact: flags must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(orig) & 15) return fail(DYCL_E_INVALID, "dycl_op_compact: orig must be 16-byte aligned");
   const size_t need = dycl_op_compact_workspace(n);
   if (need && (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 7)))
     return fail(DYCL_E_INVALID, "dycl_op_compact: workspace missing, too small or misaligned (need " +
