@@ -327,8 +327,14 @@ __device__ __forceinline__ void wait_vm_barrier() {
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// One K step (NS 1) is the memory-bound 1x1 case, whose speed follows the
+// number of workgroups in flight: its registers are capped for five waves
+// per SIMD (128 x 64 tiles: 85 VGPRs, the accumulators out of AGPRs, no
+// spill), where unconstrained it takes 85 + 32 AGPRs and runs four; a cap
+// for six spills.
 template <int BM, int BN, int WM, int WN, int KS, int NS = 2>
-__global__ __launch_bounds__(64 * WM* WN) void conv_lds_kernel(ConvP p) {
+__global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS == 1 ? 5 : 1))) void conv_lds_kernel(
+    ConvP p) {
   constexpr int NT = 64 * WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -1384,9 +1390,9 @@ void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
 TileCfg choose_lds(int M, int cout, int Kp) {
   const TileCfg c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2}, c32{128, 32, 4, 1};
   if (cout < 64) return c32;
-  // one K step: memory-bound; 128 x 64 tiles (24 KB of LDS, six workgroups
-  // per CU) keep the most rows in flight (measured against 128 x 128, 64 x 64
-  // and 256 x 256 on the ResNet 1x1 layers)
+  // one K step: memory-bound; 128 x 64 tiles (24 KB of LDS, five workgroups
+  // per CU by registers) keep the most rows in flight (measured against
+  // 128 x 128, 64 x 64 and 256 x 256 on the ResNet 1x1 layers)
   if (Kp <= 64) return c12864;
   constexpr long kCUs = 256;
   const long r128 = (tiles_of(c128, M, cout) + 2 * kCUs - 1) / (2 * kCUs);
