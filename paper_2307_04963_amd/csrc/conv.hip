@@ -476,6 +476,14 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
     issue(0, 0);
     wait_vm_barrier<0>();
     compute(0);
+  } else if (NS == 2 && nk == 2) {
+    // both K steps fit the two stages: the second is requested at once, so
+    // its latency overlaps the first one's rather than following its MFMAs
+    issue(1, 1);
+    wait_vm_barrier<JA + JB>();
+    compute(0);
+    wait_vm_barrier<0>();
+    compute(1);
   } else {
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + NS - 2 < nk)
