@@ -44,6 +44,9 @@ CASES = [
     (40, 8, 8, 256, 256, 3, 1, 1, False, 1),
     (4, 16, 16, 64, 128, 3, 2, 1, False, 1),    # strided
     (4, 16, 16, 128, 256, 1, 1, 0, False, 0),   # 1x1
+    (5, 15, 15, 128, 256, 1, 1, 0, True, 1),    # 1x1, two K steps requested together, ragged last tile
+    (7, 14, 14, 128, 512, 1, 2, 0, False, 1),   # strided 1x1, two K steps
+    (60, 14, 14, 64, 256, 1, 1, 0, True, 1),    # 1x1, one K step, ragged last tile
     (6, 8, 8, 256, 512, 3, 1, 1, True, 1),
     (3, 32, 32, 8, 64, 3, 1, 1, False, 1),      # 8-channel stem, weights in registers
     (300, 32, 32, 8, 64, 3, 1, 1, True, 1),     # several tiles per workgroup
