@@ -46,6 +46,28 @@ int dycl_op_compact(const uint8_t* flags, const int32_t* orig, int64_t n, int32_
                     void* hip_stream);
 
 /*
+ * Allocation-free dycl_op_compact, for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, results and
+ * errors as dycl_op_compact without the workspace pair; it calls no
+ * allocating routine.  The block counts and offsets of the reduce-then-scan
+ * form (or the ids of a small partition whose org1 / org0 is NULL) live in
+ * a library-owned static device array of DYCL_OP_COMPACT_NOALLOC_SCRATCH
+ * bytes, one per GPU the library runs on, held until the process ends; its
+ * device address is resolved on the first call on each device.
+ *   0 <= n <= DYCL_OP_COMPACT_NOALLOC_MAX_N (2^28); larger n returns
+ *   DYCL_E_INVALID.  n == 0 writes counts = {0, 0} with a kernel.
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents (nothing in it needs clearing: each entry is written before it is
+ * read): calls that overlap on one GPU (concurrent streams, threads) race
+ * and must be serialised by the caller.
+ */
+#define DYCL_OP_COMPACT_NOALLOC_MAX_N (1LL << 28)
+#define DYCL_OP_COMPACT_NOALLOC_SCRATCH ((((1LL << 28) + 4095) / 4096) * 12 + 256)
+int dycl_op_compact_noalloc(const uint8_t* flags, const int32_t* orig, int64_t n, int32_t* idx1, int32_t* org1,
+                            int32_t* idx0, int32_t* org0, int32_t* counts, void* hip_stream);
+
+/*
  * Row move: for r < n, row (dst_idx ? dst_idx[r] : r) of dst receives row
  * (src_idx ? src_idx[r] : r) of src; rows are row_bytes long (a multiple of
  * 16; dst and src 16-byte aligned).  A gather passes src_idx, a scatter

@@ -20,7 +20,7 @@ STATUS = {0: "DYCL_OK", -1: "DYCL_E_INVALID", -2: "DYCL_E_SPEC", -3: "DYCL_E_WEI
 EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_plan_set_host_mode", "dycl_last_counts", "dycl_plan_info", "dycl_profile_enable",
            "dycl_profile_read", "dycl_profile_launches", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
 # every symbol include/dycl_ops.h declares
-OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_move_rows", "dycl_op_conv_packed_bytes",
+OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_compact_noalloc", "dycl_op_move_rows", "dycl_op_conv_packed_bytes",
                "dycl_op_conv_pack", "dycl_op_conv_workspace_bytes", "dycl_op_conv", "dycl_op_conv_maxpool"]
 
 
@@ -72,6 +72,8 @@ def _load():
     lib.dycl_op_compact_workspace.restype = C.c_size_t
     lib.dycl_op_compact.argtypes = [vp, vp, C.c_int64, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
     lib.dycl_op_compact.restype = i32
+    lib.dycl_op_compact_noalloc.argtypes = [vp, vp, C.c_int64, vp, vp, vp, vp, vp, vp]
+    lib.dycl_op_compact_noalloc.restype = i32
     lib.dycl_op_move_rows.argtypes = [vp, vp, vp, vp, C.c_size_t, C.c_int64, vp]
     lib.dycl_op_move_rows.restype = i32
     lib.dycl_op_conv_packed_bytes.argtypes = [i32, i32, i32]

@@ -205,6 +205,12 @@ const char* dycl_last_error(void) { return g_err.c_str(); }
 
 #include "../../include/dycl_ops.h"
 
+static_assert(DYCL_OP_COMPACT_NOALLOC_MAX_N == static_cast<long long>(dycl::k::kScratchCompactMaxN),
+              "header and library disagree on the no-alloc compaction's limit");
+static_assert(DYCL_OP_COMPACT_NOALLOC_SCRATCH == static_cast<long long>(dycl::k::kScratchBytes),
+              "header and library disagree on the static scratch size");
+
+
 extern "C" {
 
 size_t dycl_op_compact_workspace(int64_t n) {
@@ -251,6 +257,39 @@ int dycl_op_compact(const uint8_t* flags, const int32_t* orig, int64_t n, int32_
       dycl::k::compact_large(flags, orig, static_cast<size_t>(n), idx1, org1, idx0, org0, counts, workspace, s);
     }
     if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_compact: launch failed");
+    return DYCL_OK;
+  });
+}
+
+int dycl_op_compact_noalloc(const uint8_t* flags, const int32_t* orig, int64_t n, int32_t* idx1, int32_t* org1,
+                            int32_t* idx0, int32_t* org0, int32_t* counts, void* hip_stream) {
+  if (n < 0 || static_cast<uint64_t>(n) > dycl::k::kScratchCompactMaxN)
+    return fail(DYCL_E_INVALID, "dycl_op_compact_noalloc: n outside [0, " +
+                                    std::to_string(dycl::k::kScratchCompactMaxN) + "] (the static scratch's limit)");
+  if (!counts) return fail(DYCL_E_INVALID, "dycl_op_compact_noalloc: null counts");
+  if (n > 0 && (!flags || !idx1 || !idx0))
+    return fail(DYCL_E_INVALID, "dycl_op_compact_noalloc: null flags or index output");
+  if (reinterpret_cast<uintptr_t>(flags) & 15)
+    return fail(DYCL_E_INVALID, "dycl_op_compact_noalloc: flags must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(orig) & 15)
+    return fail(DYCL_E_INVALID, "dycl_op_compact_noalloc: orig must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  return guarded([&] {
+    // resolved once per device, with the device current; never the symbol itself
+    uint8_t* ws = static_cast<uint8_t*>(dycl::k::compact_scratch());
+    if (!ws) throw dycl::HipError("dycl_op_compact_noalloc: the static scratch's device address is unavailable");
+    if (n == 0) {
+      dycl::k::final_counts(nullptr, 0, counts, s);   // counts = {0, 0}, written by a kernel
+    } else if (n <= 16384) {
+      // single workgroup, no block offsets; ids the caller does not want land in the scratch
+      int32_t* w = reinterpret_cast<int32_t*>(ws);
+      dycl::k::compact(flags, orig, static_cast<int>(n), idx1, org1 ? org1 : w, idx0, org0 ? org0 : w + n, counts, s);
+    } else {
+      // block counts and offsets in the scratch: every entry below the
+      // block count is written before it is read, so nothing is cleared
+      dycl::k::compact_large(flags, orig, static_cast<size_t>(n), idx1, org1, idx0, org0, counts, ws, s);
+    }
+    if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_compact_noalloc: launch failed");
     return DYCL_OK;
   });
 }

@@ -6,6 +6,8 @@
 // row gathers, so the next sub-network runs on a packed subset.
 #include "kernels.hpp"
 
+#include <mutex>
+
 namespace dycl {
 namespace k {
 
@@ -807,6 +809,32 @@ void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t*
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, s, bcount, nb, n, boff, counts, nc);
   hipLaunchKernelGGL(compact_write_kernel, dim3(nb), dim3(256), 0, s, flags, orig, n, boff, idx1, org1, idx0, org0,
                      nc);
+}
+
+// Library-owned scratch of the allocation-free compaction entry point: the
+// block counts and block offsets of up to kScratchCompactMaxN flags (or the
+// two id lists of a small partition whose caller passes none).  Each GPU the
+// library runs on holds one copy until the process ends.  In host code the
+// array's name is not a device address: compact_scratch() resolves it once
+// per device and only that address is ever handed to a kernel.
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+static_assert(((kScratchCompactMaxN + kCompactBlock - 1) / kCompactBlock) * (sizeof(int32_t) + sizeof(int64_t)) + 256 <=
+                  kScratchBytes,
+              "scratch too small for the largest reduce-then-scan partition it takes");
+static_assert(8 * 16384 <= kScratchBytes, "scratch too small for the ids of a single-workgroup partition");
+
+void* compact_scratch() {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    addr[dev] = ptr;
+  }
+  return addr[dev];
 }
 
 // ------------------------------------------------------------ row moves ---

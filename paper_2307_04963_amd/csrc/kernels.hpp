@@ -151,6 +151,16 @@ size_t compact_workspace(size_t n);
 void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t* idx1, int32_t* org1, int32_t* idx0,
                    int32_t* org0, int32_t* counts, void* workspace, hipStream_t s, const int32_t* nc = nullptr);
 
+// Device address, on the current device, of the library's static compaction
+// scratch (kScratchBytes, 256-byte aligned), resolved on the first call per
+// device; null if it cannot be resolved.  Enough for compact_large of up to
+// kScratchCompactMaxN flags, or 8 * n bytes of ids for n <= 16384.  Every
+// call on one device shares it: calls that overlap there race.
+constexpr size_t kScratchCompactMaxN = size_t(1) << 28;
+constexpr size_t kScratchBytes = ((kScratchCompactMaxN + 4095) / 4096) * (sizeof(int32_t) + sizeof(int64_t)) + 256;
+constexpr int kMaxDevices = 64;
+void* compact_scratch();
+
 // dst row (dst_idx ? dst_idx[r] : r) = src row (src_idx ? src_idx[r] : r),
 // r < n; row_bytes is a multiple of 16.
 void move_rows(void* dst, const int32_t* dst_idx, const void* src, const int32_t* src_idx, size_t row_bytes, int n,

@@ -41,6 +41,16 @@ def test_ops_reject_bad_arguments_without_gpu():
     assert lib.dycl_op_move_rows(None, None, None, None, 16, 3, None) == -1
     assert lib.dycl_op_move_rows(C.c_void_p(16), None, C.c_void_p(32), None, 24, 3, None) == -1   # row_bytes % 16
     assert lib.dycl_op_move_rows(None, None, None, None, 16, 0, None) == 0
+    # the allocation-free compaction rejects sizes beyond its static scratch
+    # and bad pointers before touching a device
+    big = lib.DYCL_OP_COMPACT_NOALLOC_MAX_N if hasattr(lib, "DYCL_OP_COMPACT_NOALLOC_MAX_N") else (1 << 28)
+    assert lib.dycl_op_compact_noalloc(None, None, big + 1, None, None, None, None, C.c_void_p(16), None) == -1
+    assert "static scratch" in _lib.last_error()
+    assert lib.dycl_op_compact_noalloc(None, None, -1, None, None, None, None, C.c_void_p(16), None) == -1
+    assert lib.dycl_op_compact_noalloc(None, None, 5, None, None, None, None, C.c_void_p(16), None) == -1
+    assert lib.dycl_op_compact_noalloc(None, None, 5, None, None, None, None, None, None) == -1
+    assert lib.dycl_op_compact_noalloc(C.c_void_p(17), None, 5, C.c_void_p(64), None, C.c_void_p(64), None,
+                                       C.c_void_p(64), None) == -1                     # misaligned flags
 
 
 def _check(spec, blob_bytes, max_batch=8):
