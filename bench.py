@@ -19,7 +19,10 @@ Prints one JSON line:
                steps: algorithmic FLOPs of the executed rows / kernel time,
                against the bf16 dense MFMA peak;
   cpu_baseline the oracle (plain per-sample CPU interpreter) on a bounded
-               sample of the same workload.
+               sample of the same workload, on every host core (parallel
+               across samples) and on one core;
+  other_workloads  samples/s of the other four workloads at their own
+               batches (device host mode, same step count).
 """
 
 from __future__ import annotations
@@ -83,31 +86,51 @@ def _cpu_info():
     return model, os.cpu_count(), smt
 
 
-def _time_oracle(wl, acc: str, seconds: float):
+def _oracle_worker(args):
+    """One host core: the float64 oracle on samples start, start + stride, ...
+    of the workload's batch (cycled), one by one, for about `seconds`."""
+    name, batch, start, stride, seconds = args
+    import torch
+    torch.set_num_threads(1)
     from oracle import dycl_oracle as O
-    o = O.from_workload(wl, acc)
-    x, aux = wl.inputs_f32(64)
+    from workloads import configs
+    wl = configs.build(name)
+    rows = list(range(start, batch, stride)) or [start % batch]
+    x, aux = wl.inputs_f32(max(rows) + 1)
+    o = O.from_workload(wl, "f64")
     n, t0 = 0, time.perf_counter()
     while True:
-        o.run_sample(x[n % 64], None if aux is None else float(aux[n % 64]))
+        i = rows[n % len(rows)]
+        o.run_sample(x[i], None if aux is None else float(aux[i]))
         n += 1
         el = time.perf_counter() - t0
         if (el >= seconds and n >= 2) or el >= 4 * seconds:
-            break
-    return n, el
+            return n, el
 
 
-def cpu_baseline(wl, seconds: float):
-    """The oracle (per-sample interpreter, torch CPU ops) timed on this
-    host: float64 accumulation (the reference) and float32."""
-    import torch
-    n64, el64 = _time_oracle(wl, "f64", seconds)
-    n32, el32 = _time_oracle(wl, "f32", seconds / 2)
+def cpu_baseline(wl, batch: int, seconds: float):
+    """The oracle (the plain per-sample interpreter, float64 accumulation,
+    bf16 storage) on this host's cores, parallel across samples (one process
+    per core, one thread each), and on one core alone."""
+    import multiprocessing as mp
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    cores = max(1, min(cores, 16))
+    span = min(batch, 256)           # the first samples of the batch, in their routing mix
+    with mp.get_context("spawn").Pool(cores) as pool:
+        par = pool.map(_oracle_worker, [(wl.name, span, r, cores, seconds) for r in range(cores)])
+        single = pool.map(_oracle_worker, [(wl.name, span, 0, 1, seconds)])[0]
+    value = sum(n / el for n, el in par)
     model, ncpu, smt = _cpu_info()
-    return {"value": n64 / el64, "unit": "samples/s", "cores": torch.get_num_threads(), "kind": "oracle",
-            "sample": f"{n64} samples of {wl.name} (the first 64 of the batch, cycled) run one by one with float64 "
-                      f"accumulation and bf16 storage, {el64:.1f} s",
-            "acc32_value": n32 / el32, "acc32_sample": f"{n32} samples, {el32:.1f} s",
+    done = sum(n for n, _ in par)
+    return {"value": value, "unit": "samples/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} samples of {wl.name} (the first {span} of the batch, cycled, split over {cores} "
+                      f"processes of one thread) run one by one with float64 accumulation and bf16 storage, "
+                      f"about {seconds:.0f} s per process",
+            "single_core_value": single[0] / single[1],
+            "single_core_sample": f"{single[0]} samples in {single[1]:.1f} s on one thread",
             "cpu_model": model, "logical_cpus": ncpu, "smt_active": smt}
 
 
@@ -142,9 +165,12 @@ def hbm_kernels(stream, reps: int = 10):
     b.record(stream)
     torch.cuda.synchronize()
     us = a.elapsed_time(b) * 1e3 / reps
-    nbytes = n * (1 + 4 + 8)      # flags, ids in; one index and one id out per element
+    nbytes = n * (1 + 4)          # the partition itself: a flag read and one 4-byte index written per element
+    moved = n * (1 + 4 + 8)       # with the original ids carried: ids read, one id written per element
     out["compaction_2^26"] = {"us": us, "algorithmic_bytes": nbytes, "gbs": nbytes / (us * 1e-6) / 1e9,
-                              "frac": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+                              "frac": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                              "bytes_with_ids": moved, "gbs_with_ids": moved / (us * 1e-6) / 1e9,
+                              "frac_with_ids": moved / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
     del flags, orig, outs, ws
 
     row, rows, total = 56 * 56 * 256 * 2, 182, 256
@@ -179,6 +205,41 @@ def copy_probe():
     print(json.dumps({"copy_probe_bytes": 2 * a.numel(), "copies": 3}), flush=True)
 
 
+def other_workloads(skip: str, steps: int, warmup: int, stream):
+    """Samples/s of every other workload at its own batch, in device host
+    mode, timed like the headline (HIP events around exactly `steps` runs)."""
+    import torch
+    from paper_2307_04963_amd import runtime
+    from workloads import configs
+    res = {}
+    for name in configs.NAMES:
+        if name == skip:
+            continue
+        wl = configs.build(name)
+        B = configs.DEFAULT_BATCH[name]
+        plan = runtime.Plan.from_workload(wl, B)
+        x, aux = wl.inputs(B)
+        xt, at = runtime.device_inputs(wl, x, aux)
+        logits = torch.empty((B, plan.n_out), dtype=torch.float32, device="cuda")
+        rec = torch.empty((B, 4), dtype=torch.int32, device="cuda")
+        plan.set_host_mode("device")
+        for _ in range(warmup):
+            plan.run(xt, at, logits, rec, stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            plan.run(xt, at, logits, rec, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        res[name] = {"batch": B, "dtype": wl.arch["dtype"], "ms_per_step": ms, "samples_per_s": B / (ms * 1e-3),
+                     "branch_counts": plan.counts(), "host_mode": "device"}
+        plan.close()
+        del xt, at, logits, rec
+    return res
+
+
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per HBM byte where the two bounds meet
 
 
@@ -187,16 +248,6 @@ def layer_table(wl, plan, xt, at, logits, rec, stream, warmup):
     FLOPs and bytes (executed rows only) and its HIP-event time; the bound
     is the layer's attainable rate min(peak, intensity x HBM peak)."""
     import torch
-    from paper_2307_04963_amd.lowering import lower
-    blob, man = wl.blob()
-    names = []
-
-    def walk(nodes):
-        for nd in nodes:
-            if nd["op"] in ("conv", "output"):
-                names.append(nd.get("dst", "output"))
-            walk(nd.get("body", []))
-    walk(lower(wl.arch, man)["nodes"])
     plan.set_host_mode("sync")
     for _ in range(max(warmup, 1)):
         plan.run(xt, at, logits, rec, stream)
@@ -216,13 +267,13 @@ def layer_table(wl, plan, xt, at, logits, rec, stream, warmup):
         if bound == "mfma":
             cb_f += r["flops"]
             cb_t += r["ms"]
-        rows.append({"layer": names[i] if i < len(names) else f"launch{i}", "us": round(r["ms"] * 1e3, 1),
+        rows.append({"layer": r["label"], "us": round(r["ms"] * 1e3, 1),
                      "gflop": round(r["flops"] / 1e9, 3), "mb": round(r["bytes"] / 1e6, 2),
                      "flop_per_byte": round(inten, 1), "bound": bound, "tflops": round(tf, 1),
                      "frac_peak": round(tf / PEAK_BF16_TFLOPS, 4), "frac_attainable": round(tf / attain, 4) if attain else None})
     cb = cb_f / (cb_t * 1e-3) / 1e12 if cb_t else 0.0
     # HBM-bound routing steps of the same step: heads (pooling reads), compaction, row moves
-    hb = [{"class": r["class"], "us": round(r["ms"] * 1e3, 1), "mb": round(r["bytes"] / 1e6, 2),
+    hb = [{"class": r["class"], "node": r["label"], "us": round(r["ms"] * 1e3, 1), "mb": round(r["bytes"] / 1e6, 2),
            "gbs": round(r["bytes"] / (r["ms"] * 1e-3) / 1e9, 0) if r["ms"] else 0.0,
            "frac_hbm": round(r["bytes"] / (r["ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if r["ms"] else 0.0}
           for r in heads]
@@ -237,9 +288,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="resnet18_exit")
+    ap.add_argument("--workload", default="resnet50_exit")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the device-mode throughput of the other workloads")
     ap.add_argument("--batch", type=int, default=0)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm-kernels", action="store_true")
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-scaling copy")
@@ -349,10 +402,12 @@ def main():
     }
     plan.close()
     del xt, at, logits, rec
+    if not args.no_other_workloads:
+        out["other_workloads"] = other_workloads(args.workload, args.steps, args.warmup, stream)
     if not args.no_hbm_kernels:
         out["hbm_kernels"] = hbm_kernels(stream)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, B, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

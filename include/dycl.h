@@ -167,6 +167,15 @@ const char* dycl_profile_class(int i);
 int dycl_profile_launches(dycl_plan* plan, double* rows, int cap);
 
 /*
+ * Label of launch i of the rows dycl_profile_launches returned: the node it
+ * belongs to - a layer by the tensor it writes (with the projection folded
+ * into it, or the fused max-pool), a decision as "exit k", "gate k" or
+ * "halt k".  "" for an index out of range or an invalid plan.  The string
+ * lives in the plan until its next profiled run.
+ */
+const char* dycl_profile_launch_label(const dycl_plan* plan, int i);
+
+/*
  * Host-only validation of a spec against a blob size and a batch bound (no
  * HIP call): parses, checks every reference and weight range, propagates
  * shapes, and writes a one-line summary into `summary` (may be NULL).

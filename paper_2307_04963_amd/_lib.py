@@ -18,7 +18,7 @@ STATUS = {0: "DYCL_OK", -1: "DYCL_E_INVALID", -2: "DYCL_E_SPEC", -3: "DYCL_E_WEI
 
 # every symbol include/dycl.h declares
 EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_plan_set_host_mode", "dycl_last_counts", "dycl_plan_info", "dycl_profile_enable",
-           "dycl_profile_read", "dycl_profile_launches", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
+           "dycl_profile_read", "dycl_profile_launches", "dycl_profile_launch_label", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
 # every symbol include/dycl_ops.h declares
 OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_compact_noalloc", "dycl_op_move_rows", "dycl_op_conv_packed_bytes",
                "dycl_op_conv_pack", "dycl_op_conv_workspace_bytes", "dycl_op_conv", "dycl_op_conv_maxpool"]
@@ -60,6 +60,8 @@ def _load():
     lib.dycl_profile_read.restype = i32
     lib.dycl_profile_launches.argtypes = [vp, C.POINTER(C.c_double), i32]
     lib.dycl_profile_launches.restype = i32
+    lib.dycl_profile_launch_label.argtypes = [vp, i32]
+    lib.dycl_profile_launch_label.restype = C.c_char_p
     lib.dycl_profile_class.argtypes = [i32]
     lib.dycl_profile_class.restype = C.c_char_p
     lib.dycl_spec_check.argtypes = [C.c_char_p, C.c_size_t, i32, C.c_char_p, C.c_size_t]

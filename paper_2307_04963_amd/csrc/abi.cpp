@@ -171,6 +171,11 @@ int dycl_profile_launches(dycl_plan* plan, double* rows, int cap) {
   return static_cast<int>(n);
 }
 
+const char* dycl_profile_launch_label(const dycl_plan* plan, int i) {
+  if (!valid(plan) || i < 0 || static_cast<size_t>(i) >= plan->last_run_labels.size()) return "";
+  return plan->last_run_labels[static_cast<size_t>(i)].c_str();
+}
+
 const char* dycl_profile_class(int i) {
   if (i < 0 || i >= dycl::P_COUNT) return "";
   return kClassNames[i];
@@ -209,7 +214,6 @@ static_assert(DYCL_OP_COMPACT_NOALLOC_MAX_N == static_cast<long long>(dycl::k::k
               "header and library disagree on the no-alloc compaction's limit");
 static_assert(DYCL_OP_COMPACT_NOALLOC_SCRATCH == static_cast<long long>(dycl::k::kScratchBytes),
               "header and library disagree on the static scratch size");
-
 
 extern "C" {
 

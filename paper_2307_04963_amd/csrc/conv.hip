@@ -24,6 +24,7 @@
 //
 // Epilogue: folded BatchNorm scale/shift (or bias), residual, ReLU or exact
 // GELU, then round-to-nearest-even bf16 or an fp32 store.
+#include <stdexcept>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -52,6 +53,14 @@ struct ConvP {
   int H2, W2, s2;          // src2: spatial shape and the stride it is read at
   const int32_t* rrows;
   const int32_t* drows;
+  // a folded projection (conv_lds_kernel, no K split): its kfold K steps
+  // (the last ones of the packed layout) run first; then every sum becomes
+  // bf16(fsp * acc + fbp) * finv, the rounded projection output in the
+  // units of the block's own sum, which the remaining steps add to
+  int kfold;
+  const float* fsp;
+  const float* fbp;
+  const float* finv;
   int ksplit;              // K ranges per tile (conv_lds_kernel); > 1: fp32 partials to `part`
   float* part;             // [ksplit][M][cout] partial sums (rows of the nmax images)
   const uint16_t* w;
@@ -400,6 +409,10 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
   auto issue = [&](int kt, int stage) __attribute__((always_inline)) {
     char* sb = smem + stage * STAGE;
     kt += kb;
+    if constexpr (NS >= 2) {
+      // a folded projection's steps (the last kfold of the layout) come first
+      if (p.kfold) kt = kt < p.kfold ? kt + (nk_all - p.kfold) : kt - p.kfold;
+    }
     const int kidx = kt * 64 + lchunk * 8;
     int tap = 0, ci = kidx;
     if constexpr (KS != 1) {
@@ -464,6 +477,35 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
     }
   };
 
+  // a folded projection: once its K steps are summed, each sum becomes the
+  // projection's output as the unfused layer stores it (scale, shift, bf16
+  // rounding), divided by the block's scale, so the block's own steps add
+  // to it and the epilogue's scale / shift finish the residual sum
+  float fsp[TN], fbp[TN], finv[TN];
+  if constexpr (NS >= 2) {
+    if (p.kfold) {
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int col = n0 + wn * WTN + b * 32 + (lane & 31);
+        const bool in = col < p.cout;
+        fsp[b] = in ? p.fsp[col] : 0.f;
+        fbp[b] = in ? p.fbp[col] : 0.f;
+        finv[b] = in ? p.finv[col] : 0.f;
+      }
+    }
+  }
+  auto fold_round = [&]() __attribute__((always_inline)) {
+    if constexpr (NS >= 2) {
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            acc[a][b][r] = bf2f(f2bf(fmaf(acc[a][b][r], fsp[b], fbp[b]))) * finv[b];
+    }
+  };
+
   // NS-stage pipeline: the loads of step kt+NS-1 are issued while step kt
   // is computed; the stage they fill was read in step kt-1, which every wave
   // finished before the barrier of step kt
@@ -482,6 +524,7 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
     issue(1, 1);
     wait_vm_barrier<JA + JB>();
     compute(0);
+    if (p.kfold == 1) fold_round();
     wait_vm_barrier<0>();
     compute(1);
   } else {
@@ -492,6 +535,7 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
         wait_vm_barrier<0>();
       if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
       compute(kt % NS);
+      if (kt + 1 == p.kfold) fold_round();
     }
   }
 
@@ -1683,6 +1727,14 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.nmax = a.n;
   p.ksplit = 1;
   p.part = nullptr;
+  p.kfold = a.kfold;
+  p.fsp = a.fold_sp;
+  p.fbp = a.fold_bp;
+  p.finv = a.fold_inv;
+  if (a.kfold && (!a.src2 || a.cin1 % kBK || a.cin2 != a.kfold * kBK || a.k != 1 || a.res || a.out_f32 ||
+                  !a.fold_sp || !a.fold_bp || !a.fold_inv || a.cout % 8 || (reinterpret_cast<uintptr_t>(a.dst) & 15) ||
+                  !a.zeros))
+    throw std::invalid_argument("folded projection: arguments the implicit-GEMM kernel does not take");
   p.srows = a.src_rows;
   p.s2rows = a.src2_rows;
   p.rrows = a.res_rows;
@@ -1723,7 +1775,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
     // workgroups, fp32 partials summed in a fixed order by a second kernel
     // (the split depends on the layer's shape only, never on n)
     const int S = conv_ksplit(a.Ho, a.Wo, a.cout, p.K, a.out_f32 != 0);
-    const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows &&
+    const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
                             : choose_lds(Mh, a.cout, p.Kp);

@@ -57,6 +57,14 @@ struct ConvArgs {
   int list_rows = 0;     // rows of the tensors read or written through a list (0: no list)
   float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split
   size_t splitws_bytes = 0;
+  // a folded projection shortcut (src2 holds its input, its weights are
+  // the last cin2 K columns, cin1 and cin2 multiples of kBK): the kfold K
+  // steps of src2 run first and their sum becomes bf16(fold_sp * acc +
+  // fold_bp) * fold_inv before the block's own steps add to it (0: none)
+  int kfold = 0;
+  const float* fold_sp = nullptr;
+  const float* fold_bp = nullptr;
+  const float* fold_inv = nullptr;
   // 1: a 3x3 / stride-2 / pad-1 max-pool of the output is fused in and dst
   // holds the pooled tensor [n, (Ho - 1) / 2 + 1, (Wo - 1) / 2 + 1, cout]
   // (conv_rgb_stem with ReLU only)

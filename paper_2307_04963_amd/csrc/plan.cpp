@@ -98,7 +98,7 @@ void assign_buffers(dycl_plan* p, int max_batch) {
 
 int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_t weights_bytes) {
   Spec& sp = p->spec;
-  sp.parse(json, weights_bytes, p->max_batch);
+  sp.parse(json, weights_bytes, p->max_batch, weights);
   hip_check(hipSetDevice(p->device), "hipSetDevice");
 
   // weights: the blob as is (fp32 vectors, heads, fp32 linear layers) ...
@@ -124,22 +124,14 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     for (int co = 0; co < q.cout; ++co) {
       const uint8_t* row = hb + q.w_off + (static_cast<size_t>(co) * q.w_ldk + q.w_k0) * 2;
       if (q.w2_off >= 0) {
-        // a folded projection: [W_c | (scale_p / scale_c) W_p] with the
-        // layer's scale scale_c (fold_scale); a channel whose scale_c is 0
-        // keeps only the projection, at scale 1
+        // a folded projection: [W_c | W_p], both as stored; a channel whose
+        // own scale is 0 keeps only the projection block
         const uint8_t* row2 = hb + q.w2_off + (static_cast<size_t>(co) * q.w2_ldk + q.w2_k0) * 2;
         const float s1 = q.scale1_off >= 0 ? hf32(q.scale1_off, co) : 1.0f;
-        const float s2 = q.scale2_off >= 0 ? hf32(q.scale2_off, co) : 1.0f;
-        const bool main = s1 != 0.0f;
-        const float r = main ? s2 / s1 : s2;
         uint16_t* dst = &h[static_cast<size_t>(co) * q.Kp];
         const int k1 = q.K - q.cin2;
-        if (main) std::memcpy(dst, row, static_cast<size_t>(k1) * 2);
-        for (int c = 0; c < q.cin2; ++c) {
-          uint16_t b;
-          std::memcpy(&b, row2 + static_cast<size_t>(c) * 2, 2);
-          dst[k1 + c] = host_bf16(r * host_f32(b));
-        }
+        if (s1 != 0.0f) std::memcpy(dst, row, static_cast<size_t>(k1) * 2);
+        std::memcpy(dst + k1, row2, static_cast<size_t>(q.cin2) * 2);
         continue;
       }
       for (int t = 0; t < q.taps; ++t)
@@ -153,23 +145,27 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     hip_check(hipMemcpy(q.dev, h.data(), h.size() * 2, hipMemcpyHostToDevice), "packed weights upload");
   }
 
-  // folded projections: the layer's scales (1 where the block's own scale
-  // is 0) and the summed shifts, [scale | shift]
+  // folded projections: [scale | shift | s_p | b_p | 1 / scale] of the
+  // block's last convolution (scale 1 where it is 0) and the projection
   p->fold_shift.assign(sp.n_fold_shift, nullptr);
   for (const Node& nd : sp.nodes) {
     if (!nd.fold) continue;
-    std::vector<float> ss(2 * static_cast<size_t>(nd.cout));
-    for (int co = 0; co < nd.cout; ++co) {
-      const float s1 = nd.scale_off >= 0 ? hf32(nd.scale_off, co) : 1.0f;
-      ss[co] = s1 != 0.0f ? s1 : 1.0f;
-      ss[nd.cout + co] =
-          (nd.shift_off >= 0 ? hf32(nd.shift_off, co) : 0.0f) + (nd.shift2_off >= 0 ? hf32(nd.shift2_off, co) : 0.0f);
+    const size_t C = static_cast<size_t>(nd.cout);
+    std::vector<float> ss(5 * C);
+    for (size_t co = 0; co < C; ++co) {
+      const float s1 = nd.scale_off >= 0 ? hf32(nd.scale_off, static_cast<int>(co)) : 1.0f;
+      const float sc = s1 != 0.0f ? s1 : 1.0f;
+      ss[co] = sc;
+      ss[C + co] = nd.shift_off >= 0 ? hf32(nd.shift_off, static_cast<int>(co)) : 0.0f;
+      ss[2 * C + co] = nd.scale2_off >= 0 ? hf32(nd.scale2_off, static_cast<int>(co)) : 1.0f;
+      ss[3 * C + co] = nd.shift2_off >= 0 ? hf32(nd.shift2_off, static_cast<int>(co)) : 0.0f;
+      ss[4 * C + co] = 1.0f / sc;
     }
     void* ptr = nullptr;
-    if (hipMalloc(&ptr, ss.size() * 4) != hipSuccess) throw OomError("folded scale / shift: hipMalloc failed");
+    if (hipMalloc(&ptr, ss.size() * 4) != hipSuccess) throw OomError("folded projection constants: hipMalloc failed");
     p->fold_shift[nd.fold_shift] = static_cast<float*>(ptr);
     p->weight_bytes += ss.size() * 4;
-    hip_check(hipMemcpy(ptr, ss.data(), ss.size() * 4, hipMemcpyHostToDevice), "folded scale / shift upload");
+    hip_check(hipMemcpy(ptr, ss.data(), ss.size() * 4, hipMemcpyHostToDevice), "folded projection constants upload");
   }
 
   // fp32 weight matrices [rows][cols] kept transposed ([cols][rows]): exit
@@ -314,6 +310,7 @@ struct Run {
   int B;
   bool device;               // counts stay on the device
   std::vector<void*> tp;     // tensor pointers
+  std::string label;         // the node being enqueued (profiling labels)
   const int32_t* orig;       // original ids of the current rows
   int orig_next = 0;         // which d_orig buffer the next compaction fills
 
@@ -340,7 +337,7 @@ struct Run {
     f();
     hip_check(hipGetLastError(), "kernel launch");
     hip_check(hipEventRecord(b, s), "hipEventRecord");
-    p->pending.push_back({cls, a, b, flops, bytes});
+    p->pending.push_back({cls, a, b, flops, bytes, label});
   }
 
   const float* f32(int64_t off) const { return off < 0 ? nullptr : reinterpret_cast<const float*>(p->d_blob + off); }
@@ -441,6 +438,12 @@ struct Run {
     a.Kp = q->Kp;
     a.scale = nd.fold ? p->fold_shift[nd.fold_shift] : f32(nd.scale_off);
     a.shift = nd.fold ? p->fold_shift[nd.fold_shift] + nd.cout : f32(nd.shift_off);
+    if (nd.fold) {
+      a.kfold = nd.cin2 / k::kBK;
+      a.fold_sp = p->fold_shift[nd.fold_shift] + 2 * nd.cout;
+      a.fold_bp = p->fold_shift[nd.fold_shift] + 3 * nd.cout;
+      a.fold_inv = p->fold_shift[nd.fold_shift] + 4 * nd.cout;
+    }
     a.res = nd.res >= 0 ? static_cast<const uint16_t*>(tp[nd.res]) : nullptr;
     a.act = nd.act;
     a.dst = tp[nd.dst];
@@ -474,10 +477,28 @@ struct Run {
     launch(P_CONV, flops, bytes, [&] { k::conv_bf16(a, s); });
   }
 
+  // what a profiled launch belongs to: a layer by the tensor it writes (a
+  // folded projection named with it), a decision by its kind and index
+  std::string node_label(const Node& nd) const {
+    const Spec& sp = p->spec;
+    switch (nd.kind) {
+      case NodeKind::Conv:
+        return sp.tensors[nd.dst].name + (nd.fold ? " (+ projection of " + sp.tensors[nd.src2].name + ")" : "") +
+               (nd.pool ? " (+ max-pool)" : "");
+      case NodeKind::MaxPool: return "maxpool " + sp.tensors[nd.dst].name;
+      case NodeKind::Exit: return "exit " + std::to_string(nd.index);
+      case NodeKind::Gate: return "gate " + std::to_string(nd.index);
+      case NodeKind::Halt: return "halt " + std::to_string(nd.index);
+      case NodeKind::Output: return "output";
+    }
+    return "";
+  }
+
   void exec(const std::vector<Node>& nodes, Rows& rows) {
     Spec& sp = p->spec;
     for (const Node& nd : nodes) {
       const int n = rows.n;
+      if (p->profile) label = node_label(nd);
       switch (nd.kind) {
         case NodeKind::Conv:
           if (n > 0) conv(nd, rows);
@@ -550,6 +571,7 @@ struct Run {
             move_pairs(nd.pairs, nullptr, p->d_idx1, run);     // gather the executing rows
             Rows body = run;
             exec(nd.body, body);
+            if (p->profile) label = node_label(nd);
             move_pairs(nd.scatter, p->d_idx1, nullptr, run);   // scatter the block outputs back
           }
           break;
@@ -644,6 +666,7 @@ void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logit
   if (p->pending.size() > 8192) profile_flush(p);
   if (p->profile) {
     p->last_run.clear();
+    p->last_run_labels.clear();
     p->last_run_begin = p->pending.size();
   }
   Run r;
@@ -745,7 +768,10 @@ void profile_flush(dycl_plan* p) {
     row.ms += ms;
     row.flops += e.flops;
     row.bytes += e.bytes;
-    if (i >= p->last_run_begin) p->last_run.push_back({static_cast<double>(e.cls), ms, e.flops, e.bytes});
+    if (i >= p->last_run_begin) {
+      p->last_run.push_back({static_cast<double>(e.cls), ms, e.flops, e.bytes});
+      p->last_run_labels.push_back(e.label);
+    }
     p->ev_free.push_back(e.a);
     p->ev_free.push_back(e.b);
   }

@@ -55,11 +55,13 @@ struct Node {
   int packed = -1;                           // index of packed bf16 weights
   bool pad_in = false;                       // reads the input padded to 8 channels
   bool pool = false;                         // a 3x3 / 2 max-pool fused in: dst is the pooled tensor
-  // a 1x1 projection shortcut folded in as src2: the packed weights carry
-  // the block's own weights and the projection's scaled by the ratio of the
-  // two scales; the run takes the block's scale and the summed shifts
-  // (plan-owned [scale | shift] vector fold_shift)
-  int64_t shift2_off = -1;
+  // a 1x1 projection shortcut folded in as src2: the packed weights are
+  // [W_c | W_p]; the kernel runs the projection's K steps first, rounds
+  // s_p * acc + b_p to bf16 exactly as the unfused projection stores it,
+  // and carries it into the block's own sum divided by the block's scale
+  // (plan-owned vector fold_shift: [scale | shift | s_p | b_p | 1 / scale],
+  // scale 1 and W_c zero for a channel whose scale is 0)
+  int64_t scale2_off = -1, shift2_off = -1;
   int s2 = 1;            // src2 is read at this stride (a folded strided projection)
   bool fold = false;
   int fold_shift = -1;
@@ -90,12 +92,12 @@ struct Packed {
   // taps x cin_src weights per output channel in the blob, stored as
   // taps x cin_pack (zero-filled) when the input channels are padded
   int taps = 1, cin_src = 0, cin_pack = 0;
-  // a folded projection: a second 1x1 block of cin2 columns appended to K,
-  // its rows multiplied by scale_2 / scale_1 (fp32 scales, or 1) before the
-  // bf16 rounding
+  // a folded projection: a second 1x1 block of cin2 columns appended to K
+  // (the projection's weights as stored); rows whose scale_1 is 0 keep only
+  // that block
   int64_t w2_off = -1, w2_ldk = 0, w2_k0 = 0;
   int cin2 = 0;
-  int64_t scale1_off = -1, scale2_off = -1;
+  int64_t scale1_off = -1;
   uint16_t* dev = nullptr;
 };
 
@@ -123,11 +125,14 @@ struct Spec {
   int fused_gates = 0;     // gates whose gathers and scatters are fused into the body convolutions
   int fused_pools = 0;     // max-pools fused into the stem convolution that feeds them
   int fused_projections = 0;   // 1x1 projection shortcuts folded into the block's last 1x1 convolution
-  int n_fold_shift = 0;        // summed shift vectors of the folded projections
+  int n_fold_shift = 0;        // constant vectors of the folded projections
   int n_head_t = 0;      // fp32 weight matrices kept transposed on the device   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
+  const uint8_t* host_w = nullptr;   // the host weight blob during parse, when given
 
-  void parse(const std::string& json, size_t weights_bytes, int max_batch);
+  // weights: the host blob when it is at hand (plan creation), or null
+  // (validation only); the projection fold reads the batch-norm scales
+  void parse(const std::string& json, size_t weights_bytes, int max_batch, const void* weights = nullptr);
   void fuse_original_order_reads();
   void fuse_exit_gathers();
   void fuse_gate_moves();
@@ -163,7 +168,7 @@ struct dycl_plan {
   uint16_t* d_zeros = nullptr;   // 256 zero bytes: source of convolution padding taps
   uint16_t* d_xpad = nullptr;    // input padded to 8 channels (stems with Cin < 8)
   std::vector<float*> head_t;    // transposed fp32 weights: exit heads [C][ncls], fp32 linears [cin][cout]
-  std::vector<float*> fold_shift;   // folded projections: [scale | shift of the block's last conv + the projection's]
+  std::vector<float*> fold_shift;   // folded projections: [scale | shift | s_p | b_p | 1 / scale] of 5 x cout
   size_t workspace_bytes = 0, weight_bytes = 0;
   // profiling
   bool profile = false;
@@ -172,11 +177,13 @@ struct dycl_plan {
     int cls;
     hipEvent_t a, b;
     double flops, bytes;
+    std::string label;   // the node the launch belongs to
   };
   std::vector<Pending> pending;
   dycl::ProfileRow prof[dycl::P_COUNT];
   // launches of the last profiled run: {class, ms, flops, bytes}
   std::vector<std::array<double, 4>> last_run;
+  std::vector<std::string> last_run_labels;
   size_t last_run_begin = 0;
   hipStream_t last_stream = nullptr;
   // host mode (dycl_host_mode) and the last run's: whether its branch

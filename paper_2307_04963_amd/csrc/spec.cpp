@@ -1,5 +1,7 @@
 // Specification parsing, validation and shape propagation (host only; no
 // HIP call happens here, so every check runs without a GPU).
+#include <cmath>
+#include <cstring>
 #include <algorithm>
 #include <map>
 #include <sstream>
@@ -459,8 +461,10 @@ void Spec::fuse_projections() {
   if (dt != DType::BF16) return;
   for (size_t i = 0; i < nodes.size(); ++i) {
     Node& c = nodes[i];
+    // both K blocks whole 64-wide K steps, so the kernel can finish the
+    // projection's sum before the block's own starts; 8-channel output vectors
     if (c.kind != NodeKind::Conv || c.k != 1 || c.stride != 1 || c.pad != 0 || c.src2 >= 0 || c.res < 0 ||
-        c.pad_in || c.pool || c.cin1 % 8 || c.src_list || c.res_list || c.dst_list)
+        c.pad_in || c.pool || c.cin1 % k::kBK || c.cout % 8 || c.src_list || c.res_list || c.dst_list)
       continue;
     long j = -1;
     bool between = false;   // a decision between the projection and c
@@ -474,9 +478,21 @@ void Spec::fuse_projections() {
     if (j < 0 || between) continue;
     const Node& pn = nodes[j];
     if (pn.k != 1 || pn.pad != 0 || pn.src2 >= 0 || pn.res >= 0 || pn.act != k::ACT_NONE ||
-        pn.pad_in || pn.pool || pn.cout != c.cout || pn.Ho != c.H || pn.Wo != c.W || pn.cin1 % 8 ||
+        pn.pad_in || pn.pool || pn.cout != c.cout || pn.Ho != c.H || pn.Wo != c.W || pn.cin1 % k::kBK ||
         pn.src_list || pn.dst_list || tensors[pn.dst].external)
       continue;
+    // the rounded projection is carried into the block's sum divided by the
+    // block's scale: every nonzero scale must have a finite, moderate inverse
+    // (weights unknown here, as in a validation-only parse: assumed so)
+    if (host_w && c.scale_off >= 0) {
+      bool fine = true;
+      for (int co = 0; co < c.cout && fine; ++co) {
+        float sc;
+        std::memcpy(&sc, host_w + c.scale_off + static_cast<size_t>(co) * 4, 4);
+        fine = sc == 0.0f || (std::isfinite(sc) && std::fabs(sc) >= 0x1p-64f && std::fabs(sc) <= 0x1p64f);
+      }
+      if (!fine) continue;
+    }
     std::vector<Use> us;
     uses_of(nodes, pn.dst, -1, us);
     if (us.size() != 1 || us[0].node != &c) continue;
@@ -487,7 +503,6 @@ void Spec::fuse_projections() {
     q.w2_k0 = pn.w_k0;
     q.cin2 = pn.cin1;
     q.scale1_off = c.scale_off;
-    q.scale2_off = pn.scale_off;
     q.K = c.cin1 + pn.cin1;
     q.Kp = (q.K + k::kBK - 1) / k::kBK * k::kBK;
     q.dev = nullptr;
@@ -498,6 +513,7 @@ void Spec::fuse_projections() {
     c.s2 = pn.stride;
     c.res = -1;
     c.fold = true;
+    c.scale2_off = pn.scale_off;
     c.shift2_off = pn.shift_off;
     c.fold_shift = n_fold_shift++;
     tensors[pn.dst].unused = true;
@@ -686,8 +702,9 @@ void Spec::fuse_gate_moves() {
   }
 }
 
-void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
+void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch, const void* weights) {
   *this = Spec();
+  host_w = static_cast<const uint8_t*>(weights);
   Json j = Json::parse(json);
   if (j.kind != Json::Object) throw SpecError("the spec must be a JSON object");
   if (j.get_int("version", 1) != 1) throw SpecError("unsupported spec version");
@@ -746,6 +763,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch) {
      << " fused_projections=" << fused_projections << " n_out=" << n_out
      << " dtype=" << dts;
   summary = os.str();
+  host_w = nullptr;   // the caller's blob is not kept
 }
 
 }  // namespace dycl

@@ -101,7 +101,8 @@ class Plan:
         rows = (C.c_double * (4 * max(n, 1)))()
         n = min(n, check(lib.dycl_profile_launches(self._h, rows, n)))
         return [{"class": lib.dycl_profile_class(int(rows[4 * i])).decode(), "ms": rows[4 * i + 1],
-                 "flops": rows[4 * i + 2], "bytes": rows[4 * i + 3]} for i in range(n)]
+                 "flops": rows[4 * i + 2], "bytes": rows[4 * i + 3],
+                 "label": lib.dycl_profile_launch_label(self._h, i).decode()} for i in range(n)]
 
 
 def decode_records(rec: np.ndarray):

@@ -75,19 +75,21 @@ def test_single_conv_and_classifier(cin, ncls, k, stride):
     assert (rec.cpu().numpy()[:, 0] == 0).all()
 
 
-@pytest.mark.parametrize("stride", [1, 2])
-def test_folded_projection_with_zero_scales(stride):
+@pytest.mark.parametrize("stride,tiny", [(1, False), (2, False), (1, True)])
+def test_folded_projection_with_zero_scales(stride, tiny):
     # h = relu(1x1(x)) and the projection p = 1x1(x) (linear), both at
     # `stride`; y = relu(1x1(h) + p) with a third of the block's scales 0:
-    # the plan folds p into y's convolution (the projection rows scaled by
-    # the ratio of the scales; a channel of scale 0 keeps only p).  The
-    # reference keeps the unfused storage points (p rounded to bf16); the
-    # fold rounds the scaled projection weights instead, one bf16 rounding
-    # of the same size.
+    # the plan folds p into y's convolution (the projection's K steps
+    # first, its sum scaled, shifted and rounded to bf16 as the unfused
+    # projection stores it, then carried into the block's sum; a channel of
+    # scale 0 keeps only p).  The reference keeps the unfused layers, so the
+    # two differ only by accumulation order.  `tiny`: one block scale is an
+    # fp32 denormal, whose inverse would overflow; the plan must not fold
+    # then, and the result stays finite and equal.
     import torch
     from paper_2307_04963_amd import runtime
     rng = np.random.default_rng(70 + stride)
-    B, HW, cin, cmid, cout, ncls = 5, 8, 64, 32, 64, 10
+    B, HW, cin, cmid, cout, ncls = 5, 8, 64, 64, 64, 10
     blob, man = bytearray(), {}
 
     def add(name, arr, dt):
@@ -102,6 +104,8 @@ def test_folded_projection_with_zero_scales(stride):
     ap, bp = rng.uniform(0.5, 1.5, cout).astype(np.float32), rng.uniform(-0.2, 0.2, cout).astype(np.float32)
     ac, bc = rng.uniform(0.5, 1.5, cout).astype(np.float32), rng.uniform(-0.2, 0.2, cout).astype(np.float32)
     ac[::3] = 0.0
+    if tiny:
+        ac[1] = 1e-40
     for name, arr, dt in (("wh", wh, "bf16"), ("wp", wp, "bf16"), ("wc", wc, "bf16"), ("ah", ah, "f32"),
                           ("bh", bh, "f32"), ("ap", ap, "f32"), ("bp", bp, "f32"), ("ac", ac, "f32"),
                           ("bc", bc, "f32")):
@@ -119,7 +123,7 @@ def test_folded_projection_with_zero_scales(stride):
                       {"op": "exit", "src": "y", "w": man["hw"], "b": man["hb"], "ncls": ncls, "index": 0,
                        "final": True}]}
     plan = runtime.Plan(json.dumps(spec), bytes(blob), 8)
-    print(f"[fold] stride={stride}", flush=True)
+    print(f"[fold] stride={stride} tiny={tiny}", flush=True)
     x = q(rng.standard_normal((B, HW, HW, cin)))
     xt = torch.from_numpy(to_bf16_bits(x.astype(np.float32)).view(np.int16).copy()).view(torch.bfloat16).cuda()
     logits = torch.zeros((B, ncls), device="cuda")
@@ -134,5 +138,7 @@ def test_folded_projection_with_zero_scales(stride):
         y = q(np.maximum(conv(h, wc, 1, 0) * ac + bc + p, 0.0))
         ref.append(hw.astype(np.float64) @ y.reshape(-1, cout).mean(0) + hb)
     ref = np.stack(ref)
-    assert np.abs(got - ref).max() <= 5e-3 * max(1.0, np.abs(ref).max()), np.abs(got - ref).max()
+    assert np.isfinite(got).all()
+    # one bf16 rounding of y (or of p) may flip between accumulation orders
+    assert np.abs(got - ref).max() <= 1e-3 * max(1.0, np.abs(ref).max()), np.abs(got - ref).max()
     plan.close()
