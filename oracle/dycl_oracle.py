@@ -21,10 +21,22 @@ kind of dynamic network:
       projection.
   act  a bounded loop (Sec. 2.2: loops carry a constant maximum iteration
       count); a halting unit stops the loop per input.
+  seq_decoder  a generative network (Table 1, En-Decoder: an encoder state
+      fed to an LSTM that emits one token per step): greedy decoding, each
+      step's token read back as the next step's input, until the end token
+      or the length bound (the bounded loop of Sec. 2.2 again); the token
+      choice is the per-input decision.
 
 Numerics.  Contractions accumulate in float64 (``acc="f64"``, the
-reference) or float32 (``acc="f32"``, used only to measure how far two
-correct accumulation orders drift apart).  The bf16 workloads store every
+reference) or in one of four float32 orders, used only to find the samples
+whose routing two correct accumulation orders of the same network disagree
+on (Eq. 2 fixes the result only up to the order of rounding):
+``"f32"`` the library's float32 convolution / product, ``"f32r"`` the same
+over the input channels in reverse order, ``"f32c"`` the input channels in
+blocks of 16 (each block's sum over its channels and taps exact, rounded to
+float32, the blocks added in float32 in channel order: the shape of a
+16-deep matrix-core step), ``"f32n"`` the library's float32 convolution
+without its oneDNN path (im2col and a matrix product).  The bf16 workloads store every
 conv / linear output in bf16: ``q`` rounds to float32, then to bf16 with
 round-to-nearest-even, exactly where the GPU stores bf16.  Heads (global
 average pool, head linear, softmax / sigmoid) and the final logits stay
@@ -33,7 +45,10 @@ float32 statistic with a float32 threshold, the precision the GPU decides in.
 
 The margin of a sample is the smallest distance between a decision
 statistic it evaluated and that decision's threshold (forced decisions - the
-last exit head, the last loop step - carry none).
+last exit head, the last loop step - carry none).  A decoder's decision is
+the argmax over the step's float32 logits (ties to the lowest index); its
+statistic is the gap between the two largest logits, whose threshold is 0,
+and every step's choice counts (the last step's token is still emitted).
 
 Parity pins for every function here live in the CPU test-suite: brute-force
 loops on tiny inputs, closed forms, invariants and path enumeration.
@@ -42,6 +57,7 @@ loops on tiny inputs, closed forms, invariants and path enumeration.
 from __future__ import annotations
 
 import math
+import warnings
 from dataclasses import dataclass
 
 import numpy as np
@@ -55,12 +71,27 @@ NO_EXIT = -1
 # --------------------------------------------------------------------------
 
 
+ACC_F32 = ("f32", "f32r", "f32c", "f32n")
+
+
 def _dt(acc):
     if acc == "f64":
         return torch.float64
-    if acc == "f32":
+    if acc in ACC_F32:
         return torch.float32
     raise ValueError(acc)
+
+
+def _chunked(f, x, w, ci_axis_w, block=16):
+    """sum over input-channel blocks of f(x[block], w[block]) computed in
+    float64, each block rounded to float32, the blocks added in float32."""
+    out = None
+    for c0 in range(0, x.shape[0], block):
+        xs = x[c0:c0 + block].to(torch.float64)
+        ws = w.narrow(ci_axis_w, c0, min(block, x.shape[0] - c0)).to(torch.float64)
+        part = f(xs, ws).to(torch.float32)
+        out = part if out is None else out + part
+    return out
 
 
 def q(t: torch.Tensor) -> torch.Tensor:
@@ -92,12 +123,26 @@ def conv2d(x: torch.Tensor, w: torch.Tensor, stride: int, pad: int, acc="f64") -
     in the accumulation precision (a library convolution is the step).
     """
     dt = _dt(acc)
+    if acc == "f32r":
+        return F.conv2d(x.to(dt).flip(0)[None], w.to(dt).flip(1), stride=stride, padding=pad)[0]
+    if acc == "f32c":
+        return _chunked(lambda a, b: F.conv2d(a[None], b, stride=stride, padding=pad)[0], x, w, 1)
+    if acc == "f32n":
+        with warnings.catch_warnings():
+            warnings.simplefilter("ignore")
+            with torch.backends.mkldnn.flags(enabled=False):
+                return F.conv2d(x.to(dt)[None], w.to(dt), stride=stride, padding=pad)[0]
     return F.conv2d(x.to(dt)[None], w.to(dt), stride=stride, padding=pad)[0]
 
 
 def linear(W: torch.Tensor, v: torch.Tensor, acc="f64") -> torch.Tensor:
-    """W @ v in the accumulation precision."""
+    """W @ v in the accumulation precision (``"f32n"``: the library's float32
+    product, as ``"f32"``)."""
     dt = _dt(acc)
+    if acc == "f32r":
+        return W.to(dt).flip(-1) @ v.to(dt).flip(0)
+    if acc == "f32c":
+        return _chunked(lambda a, b: b @ a, v, W, W.dim() - 1)
     return W.to(dt) @ v.to(dt)
 
 
@@ -147,6 +192,7 @@ class Result:
     skip_mask: int             # bit i set <=> gate i chose identity / shortcut
     margin: float              # min |statistic - threshold| over decisions
     trail: tuple = ()          # the non-forced decision statistics, in order
+    tokens: tuple = ()         # tokens a decoder emitted, in order
 
 
 class Oracle:
@@ -204,6 +250,8 @@ class Oracle:
             return self._skipnet(xt.permute(2, 0, 1))
         if fam == "act":
             return self._act(xt, aux)
+        if fam == "seq_decoder":
+            return self._decoder(xt)
         raise ValueError(fam)
 
     def _mlp(self, h):
@@ -285,6 +333,38 @@ class Oracle:
                 return Result(f32(z).numpy().astype(np.float32), NO_EXIT, t, 0, margin, tuple(trail))
         raise AssertionError("unreachable")
 
+    def _decoder(self, x):
+        a, W = self.arch, self.W
+        H, L, eos = a["hidden"], a["max_len"], a["eos"]
+        dt = _dt(self.acc)
+
+        def sig(v):
+            return 1.0 / (1.0 + torch.exp(-v.to(dt)))
+
+        # encoder state: h0 = bf16(tanh(W_enc x + b_enc)), c0 = 0
+        h = q(torch.tanh(linear(W["enc.w"], x, self.acc).to(dt) + W["enc.b"].to(dt)))
+        c = torch.zeros(H, dtype=torch.float64)
+        tok, toks, margin, trail = a["bos"], [], math.inf, []
+        for t in range(1, L + 1):
+            # LSTM step on [h; embedding of the previous token]; gate order
+            # input, forget, cell, output; the gate pre-activations are a
+            # linear layer's output and are stored in bf16
+            g = q(linear(W["lstm.w"], torch.cat([h, W["emb"][tok]]), self.acc).to(dt) + W["lstm.b"].to(dt))
+            i, f, u, o = sig(g[:H]), sig(g[H:2 * H]), torch.tanh(g[2 * H:3 * H]), sig(g[3 * H:])
+            c = f32(f * c.to(dt) + i * u)                   # cell state kept in float32
+            h = q(o * torch.tanh(c.to(dt)))                 # hidden state stored in bf16
+            z = f32(linear(W["out.w"], h, self.acc).to(dt) + W["out.b"].to(dt))   # float32 logits
+            zmax = float(z.max())
+            tok = int(torch.nonzero(z == zmax)[0, 0])       # ties: the lowest index
+            second = float(torch.cat([z[:tok], z[tok + 1:]]).max())
+            gap = zmax - second
+            margin = min(margin, gap)
+            trail.append(gap)
+            toks.append(tok)
+            if tok == eos or t == L:
+                return Result(z.numpy().astype(np.float32), NO_EXIT, t, 0, margin, tuple(trail), tuple(toks))
+        raise AssertionError("unreachable")
+
     # ---- batch ----------------------------------------------------------
     def run(self, X: np.ndarray, AUX: np.ndarray | None = None, indices=None):
         """Run the samples ``indices`` (default: all) one after another.
@@ -300,7 +380,16 @@ class Oracle:
             "skip_mask": np.array([r.skip_mask for r in res], dtype=np.uint64),
             "margin": np.array([r.margin for r in res], dtype=np.float64),
             "trail": [r.trail for r in res],
+            "tokens": _pad_tokens([r.tokens for r in res], self.arch.get("max_len", 0)),
         }
+
+
+def _pad_tokens(seqs, width):
+    """[n, width] int32: each sequence's tokens, then -1."""
+    out = np.full((len(seqs), width), -1, dtype=np.int32)
+    for i, s in enumerate(seqs):
+        out[i, :len(s)] = s
+    return out
 
 
 def from_workload(wl, acc="f64") -> Oracle:

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 from oracle import dycl_oracle as O
-from tests._parity import compare
+from tests._parity import compare, oracle_ref
 from tests.dynn_modules import module_for, input_shape
 
 pytestmark = pytest.mark.gpu
@@ -35,6 +35,6 @@ def test_frontend_plan_runs_like_the_lowered_one(name):
     for k in ("exit_index", "iterations", "skip_mask"):
         assert np.array_equal(a[k], b[k]), k
     assert a["counts"] == b["counts"]
-    ref = O.from_workload(wl).run(*wl.inputs_f32(B))
+    ref = oracle_ref(wl, *wl.inputs_f32(B))
     rep = compare(wl, a, ref)
     assert rep["ok"], rep

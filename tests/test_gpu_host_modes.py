@@ -16,7 +16,7 @@ import numpy as np
 import pytest
 
 from oracle import dycl_oracle as O
-from tests._parity import compare
+from tests._parity import compare, oracle_ref
 from workloads import configs
 
 pytestmark = pytest.mark.gpu
@@ -102,7 +102,7 @@ def test_device_mode_oracle_parity(name):
     x, aux = wl.inputs(B)
     gpu = _run(rt, plan, wl, x, aux, "device")
     xf, auxf = wl.inputs_f32(B)
-    ref = O.from_workload(wl).run(xf, auxf)
+    ref = oracle_ref(wl, xf, auxf)
     rep = compare(wl, gpu, ref)
     print(name, rep, flush=True)
     assert rep["ok"], rep
@@ -121,7 +121,7 @@ def test_large_batch_partition_all_modes():
         _same(ref, _run(rt, plan, wl, x, aux, mode))
     rows = np.arange(0, B, 37)
     xf, auxf = wl.inputs_f32(B)
-    oref = O.from_workload(wl).run(xf[rows], None if auxf is None else auxf[rows])
+    oref = oracle_ref(wl, xf[rows], None if auxf is None else auxf[rows])
     rep = compare(wl, ref, oref, rows=rows)
     print(rep, flush=True)
     assert rep["ok"], rep

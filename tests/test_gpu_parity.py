@@ -1,25 +1,35 @@
 """GPU parity: the HIP path through the C ABI against the oracle.
 
 * every workload at a small batch (several tiles, ragged tails), element by
-  element;
+  element, with the float32-accumulating oracle run beside it to mark the
+  oracle-unstable samples;
 * every workload at its full batch, in the launch configuration the
-  benchmark times, on sampled rows the oracle recomputes one by one;
+  benchmark times (device host mode), on EVERY row, against the stored
+  full-batch oracle results (written by the script beside them, which calls
+  only the oracle); the calibrated workloads and the four literal ones;
 * edge cases: empty batch, one sample, over-sized batch, forced routing of
   every density (nobody / everybody leaves at a decision), and branch
   counts that agree with the per-sample records.
+
+Routing must be bit-exact except on near-tie samples (a decision within 1e-3
+of its threshold) and oracle-unstable ones (float32 and float64 oracle runs
+disagree); every category is printed.  Eq. 2 and RQ1 (Table 3: no
+inconsistent output) are the statements these check.
 """
+
+import os
 
 import numpy as np
 import pytest
 
 from oracle import dycl_oracle as O
-from tests._parity import compare
+from tests._parity import compare, load_golden, oracle_ref
 from workloads import configs
 
 pytestmark = pytest.mark.gpu
 
 SMALL = {"mlp_exit": 37, "resnet18_exit": 37, "skipnet38": 45, "resnet50_exit": 5, "act_loop": 300}
-SAMPLED = {"mlp_exit": 64, "resnet18_exit": 24, "skipnet38": 24, "resnet50_exit": 4, "act_loop": 64}
+LITERAL = ["mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit"]
 
 _cache = {}
 
@@ -31,11 +41,11 @@ def _rt():
     return runtime
 
 
-def _plan(name, wl=None, max_batch=None):
+def _plan(name, wl=None, max_batch=None, literal=False):
     rt = _rt()
-    key = (name, max_batch, id(wl) if wl is not None else None)
+    key = (name, max_batch, id(wl) if wl is not None else None, literal)
     if key not in _cache:
-        wl = wl or configs.build(name)
+        wl = wl or configs.build(name, calibrated=not literal)
         _cache[key] = (wl, rt.Plan.from_workload(wl, max_batch or configs.DEFAULT_BATCH[name]))
     return _cache[key]
 
@@ -66,28 +76,55 @@ def test_small_batch_parity(name):
     x, aux = wl.inputs(B)
     gpu = rt.run_numpy(plan, wl, x, aux)
     xf, auxf = wl.inputs_f32(B)
-    ref = O.from_workload(wl).run(xf, auxf)
+    ref = oracle_ref(wl, xf, auxf)
     rep = compare(wl, gpu, ref)
     print(name, rep, flush=True)
     assert rep["ok"], rep
     _check_counts(wl, gpu)
 
 
-@pytest.mark.parametrize("name", configs.NAMES)
-def test_full_batch_sampled_parity(name):
+def _full_batch(name, literal):
     rt = _rt()
-    wl, plan = _plan(name)
+    wl, plan = _plan(name, literal=literal)
     B = configs.DEFAULT_BATCH[name]
-    print(f"[parity-full] {name} B={B}", flush=True)
+    ref = load_golden(wl, literal)
+    print(f"[parity-full] {name}{' literal' if literal else ''} B={B} every row, device host mode", flush=True)
     x, aux = wl.inputs(B)
-    gpu = rt.run_numpy(plan, wl, x, aux)
-    rng = np.random.default_rng(7)
-    k = min(B, SAMPLED[name])
-    rows = np.unique(np.concatenate([[0, B - 1], rng.choice(B, k - 2, replace=False)]))
-    xf, auxf = wl.inputs_f32(B)
-    ref = O.from_workload(wl).run(xf, auxf, indices=rows)
-    rep = compare(wl, gpu, ref, rows)
+    plan.set_host_mode("device")
+    try:
+        gpu = rt.run_numpy(plan, wl, x, aux)
+    finally:
+        plan.set_host_mode("sync")
+    dump = os.environ.get("DYCL_PARITY_DUMP")
+    if dump:   # the GPU results, for inspection beside the stored oracle results
+        os.makedirs(dump, exist_ok=True)
+        np.savez_compressed(os.path.join(dump, f"{name}{'_literal' if literal else ''}.npz"),
+                            **{k: v for k, v in gpu.items() if k != "counts"})
+    return wl, gpu, ref
+
+
+@pytest.mark.parametrize("name", configs.NAMES)
+def test_full_batch_every_row_parity(name):
+    wl, gpu, ref = _full_batch(name, False)
+    rep = compare(wl, gpu, ref)
     print(name, rep, "counts", gpu["counts"], flush=True)
+    assert rep["samples"] == configs.DEFAULT_BATCH[name]
+    assert rep["ok"], rep
+    _check_counts(wl, gpu)
+
+
+@pytest.mark.parametrize("name", LITERAL)
+def test_literal_variant_full_batch_parity(name):
+    """The literal reading of the workload descriptions (BatchNorm at its
+    eval defaults, heads and gates as drawn).  Its logits reach 10^2-10^3,
+    where 2e-2 absolute is below float32's own spacing; the logits bound is
+    four times the distance between the oracle's float32- and
+    float64-accumulating runs (the floor of two correct accumulation orders),
+    and never below 2e-2.  Routing is held to the same rule as everywhere."""
+    wl, gpu, ref = _full_batch(name, True)
+    tol = max(2e-2, 4.0 * float(ref["logit_floor_f32_vs_f64"]))
+    rep = compare(wl, gpu, ref, logit_tol=tol)
+    print(name, "literal", rep, "counts", gpu["counts"], flush=True)
     assert rep["ok"], rep
     _check_counts(wl, gpu)
 

@@ -134,8 +134,20 @@ def _check_exit_network(arch, W, x, stats):
         k = consistent[0]
         assert res["exit_index"][i] == k == _first_exit(ps, arch["tau"])
         np.testing.assert_allclose(res["logits"][i], stats[i][k][0], rtol=1e-6, atol=1e-6)
+        _check_trail(res, i, ps[:min(k + 1, len(ps) - 1)], arch["tau"])
         seen.add(k)
     return seen
+
+
+def _check_trail(res, i, stats, thr):
+    """The oracle's decision trail is the statistics of the decisions the
+    enumerated path evaluates (forced ones excluded), in order, and its
+    margin is their smallest distance to the threshold."""
+    trail = res["trail"][i]
+    assert len(trail) == len(stats)
+    np.testing.assert_allclose(trail, np.asarray(stats, dtype=np.float64), rtol=2e-6, atol=1e-7)
+    want = min((abs(float(np.float32(v)) - float(np.float32(thr))) for v in stats), default=math.inf)
+    assert res["margin"][i] == pytest.approx(want, rel=1e-5, abs=2e-7)
 
 
 def test_tiny_mlp_exit_paths():
@@ -188,6 +200,7 @@ def test_tiny_skipnet_paths():
         want_mask = sum(1 << i for i, d in enumerate(path) if not d)
         assert int(res["skip_mask"][j]) == want_mask
         np.testing.assert_allclose(res["logits"][j], z, rtol=1e-6, atol=1e-6)
+        _check_trail(res, j, N.skipnet_path(arch, W, x[j], path)[1], 0.5)
         masks.add(want_mask)
     assert len(masks) >= 3
 
@@ -205,6 +218,7 @@ def test_tiny_act_paths_and_one_step_closed_form():
         assert len(Ns) == 1
         n = Ns[0]
         assert res["iterations"][i] == n
+        _check_trail(res, i, [traj[t][1] for t in range(min(n, 4))], 0.99)   # step 5 is forced
         z = W["W2"].astype(np.float64) @ traj[n - 1][0] + W["b2"]
         np.testing.assert_allclose(res["logits"][i], z, rtol=1e-6, atol=1e-6)
         iters.add(n)
@@ -306,3 +320,49 @@ def test_eq1_metrics_closed_forms():
     c = a.copy()
     c[0] = -a[0] + 10 * (np.arange(4) == (np.argmin(a[0])))   # argmax moves
     assert O.eta(c, a) == pytest.approx(0.2)
+
+
+# ------------------------------------------ float32 accumulation orders ----
+
+@pytest.mark.parametrize("acc", O.ACC_F32)
+def test_f32_orders_within_the_float32_summation_bound(acc):
+    # every float32 order is a correct evaluation: within the textbook
+    # bound of float32 recursive summation, gamma_K * sum |x| |w| with
+    # gamma_K = K u / (1 - K u), u = 2^-24, of the exact (float64) sums
+    g = torch.Generator().manual_seed(5)
+    x = torch.randn(40, 7, 6, generator=g, dtype=torch.float64)
+    w = torch.randn(5, 40, 3, 3, generator=g, dtype=torch.float64)
+    y = O.conv2d(x, w, 1, 1, acc)
+    assert y.dtype == torch.float32
+    ref = O.conv2d(x, w, 1, 1, "f64")
+    mag = O.conv2d(x.abs(), w.abs(), 1, 1, "f64")
+    K, u = 40 * 9, 2.0 ** -24
+    assert ((y.double() - ref).abs() <= K * u / (1 - K * u) * mag + 1e-300).all()
+    W = torch.randn(9, 70, generator=g, dtype=torch.float64)
+    v = torch.randn(70, generator=g, dtype=torch.float64)
+    z = O.linear(W, v, acc)
+    assert z.dtype == torch.float32
+    assert ((z.double() - W @ v).abs() <= 70 * u / (1 - 70 * u) * (W.abs() @ v.abs())).all()
+
+
+def test_f32_block_order_is_exact_below_one_block():
+    # 16 input channels or fewer form one block: its sum is exact and is
+    # rounded to float32 once, so it equals the float64 result rounded
+    g = torch.Generator().manual_seed(6)
+    x = torch.randn(16, 5, 5, generator=g, dtype=torch.float64)
+    w = torch.randn(3, 16, 3, 3, generator=g, dtype=torch.float64)
+    assert torch.equal(O.conv2d(x, w, 1, 1, "f32c"), O.conv2d(x, w, 1, 1, "f64").to(torch.float32))
+    W = torch.randn(4, 16, generator=g, dtype=torch.float64)
+    v = torch.randn(16, generator=g, dtype=torch.float64)
+    assert torch.equal(O.linear(W, v, "f32c"), (W @ v).to(torch.float32))
+
+
+def test_f32_orders_are_distinct_orders():
+    # the orders are different summations of the same terms: on long sums
+    # they differ somewhere in the last bits, and never by more than the bound
+    g = torch.Generator().manual_seed(7)
+    x = torch.randn(256, 6, 6, generator=g, dtype=torch.float64)
+    w = torch.randn(8, 256, 3, 3, generator=g, dtype=torch.float64)
+    ys = {a: O.conv2d(x, w, 1, 1, a) for a in O.ACC_F32}
+    assert not torch.equal(ys["f32"], ys["f32c"])
+    assert not torch.equal(ys["f32"], ys["f32r"])

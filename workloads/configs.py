@@ -242,6 +242,14 @@ def arch_act(hidden=1024, d_in=1024, d_out=1024, max_steps=16, tau=0.99):
             "n_out": d_out, "max_steps": max_steps, "tau": tau}
 
 
+def arch_decoder(d_in=512, hidden=512, embed=256, vocab=4096, max_len=24, eos=0, bos=1):
+    """Greedy LSTM decoder: h0 = tanh(W_enc x + b_enc), c0 = 0, then one token
+    per step until the end token `eos` or `max_len` tokens; the first step
+    reads the start token `bos`."""
+    return {"family": "seq_decoder", "dtype": "bf16", "input": [d_in], "hidden": hidden, "embed": embed,
+            "vocab": vocab, "n_out": vocab, "max_len": max_len, "eos": eos, "bos": bos}
+
+
 ARCHS = {
     "mlp_exit": lambda: arch_mlp_exit(),
     "resnet18_exit": lambda: arch_resnet_exit("basic", 32, [64, 128, 256, 512], [2, 2, 2, 2], 100, 0.8,
@@ -250,6 +258,7 @@ ARCHS = {
     "resnet50_exit": lambda: arch_resnet_exit("bottleneck", 224, [64, 128, 256, 512], [3, 4, 6, 3], 1000,
                                               0.7, 7, 2, True, stem_out=64),
     "act_loop": lambda: arch_act(),
+    "lstm_decoder": lambda: arch_decoder(),
 }
 
 
@@ -325,6 +334,19 @@ def raw_workload(name: str, arch: dict | None = None) -> Workload:
         _add(wl, "w_halt", "f32", linear_default(name, "w_halt", (H,), H))
         _add(wl, "W2", "bf16", linear_default(name, "W2", (O, H), H))
         _add(wl, "b2", "f32", np.zeros(O))
+    elif fam == "seq_decoder":
+        H, D, E, V = arch["hidden"], arch["input"][0], arch["embed"], arch["vocab"]
+        # PyTorch's defaults: nn.Linear U(+-1/sqrt(fan_in)) for the encoder,
+        # nn.Embedding N(0, 1), nn.LSTM U(+-1/sqrt(hidden)) for weights and
+        # both biases (summed here), nn.Linear for the output projection
+        _add(wl, "enc.w", "bf16", linear_default(name, "enc.w", (H, D), D))
+        _add(wl, "enc.b", "f32", linear_default(name, "enc.b", (H,), D))
+        _add(wl, "emb", "bf16", _n(name, "emb", V * E).astype(np.float32).reshape(V, E))
+        _add(wl, "lstm.w", "bf16", linear_default(name, "lstm.w", (4 * H, H + E), H))
+        _add(wl, "lstm.b", "f32", linear_default(name, "lstm.b_ih", (4 * H,), H)
+             + linear_default(name, "lstm.b_hh", (4 * H,), H))
+        _add(wl, "out.w", "bf16", linear_default(name, "out.w", (V, H), H))
+        _add(wl, "out.b", "f32", linear_default(name, "out.b", (V,), H))
     else:
         raise ValueError(fam)
     return wl
