@@ -27,6 +27,11 @@ Per workload (the choices are listed with their reasons in the design notes):
   above; then, gate by gate in order, the gate pre-activation u.GAP(x) is
   standardised over the calibration batch as routed by the earlier gates,
   and the seeded N(0, 1.5) offset is added.
+* End token (LSTM decoder): the output bias of the end token is raised by an
+  offset found by bisection so that the greedy decodings of the calibration
+  batch are DECODER_MEAN_LEN tokens long on average (with the drawn bias the
+  end token is almost never the most likely one, and every sequence would
+  run to the length bound).
 """
 
 from __future__ import annotations
@@ -46,7 +51,8 @@ from workloads import configs  # noqa: E402
 
 BN_EPS = configs.BN_EPS
 GAMMA_LAST = 0.1
-CALIB_BATCH = {"mlp_exit": 4096, "resnet18_exit": 512, "skipnet38": 1024, "resnet50_exit": 64}
+CALIB_BATCH = {"mlp_exit": 4096, "resnet18_exit": 512, "skipnet38": 1024, "resnet50_exit": 64, "lstm_decoder": 256}
+DECODER_MEAN_LEN = 8.0
 
 
 def _bisect(frac_fn, target, lo, hi, increasing=True, iters=60):
@@ -189,6 +195,34 @@ def calibrate_skipnet(wl, n):
     return net.out
 
 
+def _decoder_lengths(args):
+    """Greedy decoding lengths of calibration samples [lo, hi) with the end
+    token's bias raised by `offset` (one worker process)."""
+    name, offset, lo, hi = args
+    torch.set_num_threads(1)
+    from .dycl_oracle import Oracle
+    wl = configs.raw_workload(name)
+    W = wl.weights_f32()
+    W["out.b"] = W["out.b"].copy()
+    W["out.b"][wl.arch["eos"]] += np.float32(offset)
+    x, _ = wl.inputs_f32(hi, 0, stream="calib")
+    return Oracle(wl.arch, W).run(x, None, indices=range(lo, hi))["iterations"]
+
+
+def calibrate_decoder(wl, n):
+    import multiprocessing as mp
+    procs = max(1, min(16, os.cpu_count() or 1))
+    step = (n + procs - 1) // procs
+    with mp.get_context("spawn").Pool(procs) as pool:
+        def mean_len(offset):
+            parts = pool.map(_decoder_lengths, [(wl.name, offset, lo, min(n, lo + step)) for lo in range(0, n, step)])
+            return float(np.concatenate(parts).mean())
+        off = _bisect(mean_len, DECODER_MEAN_LEN, 0.0, 32.0, increasing=False, iters=24)
+    b = wl.weights_f32()["out.b"].copy()
+    b[wl.arch["eos"]] += np.float32(off)
+    return {"out.b": b, "_eos_offset": np.array(off)}
+
+
 def calibrate(name: str):
     wl = configs.raw_workload(name)
     n = CALIB_BATCH[name]
@@ -200,6 +234,8 @@ def calibrate(name: str):
         out = calibrate_resnet(wl, n)
     elif fam == "skipnet":
         out = calibrate_skipnet(wl, n)
+    elif fam == "seq_decoder":
+        out = calibrate_decoder(wl, n)
     else:
         raise ValueError(f"{name} needs no calibration")
     os.makedirs(configs.CALIB_DIR, exist_ok=True)

@@ -347,9 +347,10 @@ class Oracle:
         tok, toks, margin, trail = a["bos"], [], math.inf, []
         for t in range(1, L + 1):
             # LSTM step on [h; embedding of the previous token]; gate order
-            # input, forget, cell, output; the gate pre-activations are a
-            # linear layer's output and are stored in bf16
-            g = q(linear(W["lstm.w"], torch.cat([h, W["emb"][tok]]), self.acc).to(dt) + W["lstm.b"].to(dt))
+            # input, forget, cell, output.  The cell is the epilogue of the
+            # gate linear layer: its pre-activations stay float32, and what
+            # the layer stores is the cell state (float32) and h (bf16)
+            g = f32(linear(W["lstm.w"], torch.cat([h, W["emb"][tok]]), self.acc).to(dt) + W["lstm.b"].to(dt))
             i, f, u, o = sig(g[:H]), sig(g[H:2 * H]), torch.tanh(g[2 * H:3 * H]), sig(g[3 * H:])
             c = f32(f * c.to(dt) + i * u)                   # cell state kept in float32
             h = q(o * torch.tanh(c.to(dt)))                 # hidden state stored in bf16

@@ -188,3 +188,35 @@ def act_static(arch, W, x, b_s):
         S = np.float32(S + p)
         out.append((h, float(S)))
     return out
+
+
+def lstm_step(Wl, bl, h, e, c):
+    """One LSTM cell on [h; e] in float64, no rounding: gates input, forget,
+    cell, output in blocks of H.  Returns (h', c')."""
+    H = h.shape[0]
+    g = Wl @ np.concatenate([h, e]) + bl
+    sg = 1.0 / (1.0 + np.exp(-g))
+    i, f, u, o = sg[:H], sg[H:2 * H], np.tanh(g[2 * H:3 * H]), sg[3 * H:]
+    c2 = f * c + i * u
+    return o * np.tanh(c2), c2
+
+
+def decoder_path(arch, W, x, toks):
+    """The decoder run along a fixed token sequence `toks` (the token fed at
+    step t + 1 is toks[t]), with the storage points of the workload: gate
+    pre-activations and the cell state rounded to float32, h to bf16, logits
+    float32.  Returns the logits of every step."""
+    H = arch["hidden"]
+    f64 = lambda k: W[k].astype(np.float64)  # noqa: E731
+    h = q_np(np.tanh(f64("enc.w") @ x.astype(np.float64) + f64("enc.b")))
+    c = np.zeros(H)
+    prev, zs = arch["bos"], []
+    for tok in toks:
+        g = f32_np(f64("lstm.w") @ np.concatenate([h, f64("emb")[prev]]) + f64("lstm.b"))
+        sg = 1.0 / (1.0 + np.exp(-g))
+        i, f, u, o = sg[:H], sg[H:2 * H], np.tanh(g[2 * H:3 * H]), sg[3 * H:]
+        c = f32_np(f * c + i * u)
+        h = q_np(o * np.tanh(c))
+        zs.append(f32_np(f64("out.w") @ h + f64("out.b")))
+        prev = tok
+    return zs

@@ -4,8 +4,8 @@ The contract (Eq. 2: the compiled host program equals the dynamic network on
 every input; RQ1, Table 3: zero inconsistent outputs) is checked per sample.
 A sample falls in one of these categories:
 
-  exact       routing (exit index, iteration count, skip mask) identical to
-              the oracle's;
+  exact       routing (exit index, iteration count, skip mask, and a
+              decoder's emitted tokens) identical to the oracle's;
   near-tie    some decision the float64 oracle evaluated lies within 1e-3 of
               its threshold (its fp32 margin is below 1e-3);
   unstable    one of the oracle's float32 accumulation orders routes the
@@ -42,6 +42,17 @@ LOGIT_TOL = {"bf16": 2e-2, "f32": 1e-4}
 ROUTE_KEYS = ("exit_index", "iterations", "skip_mask")
 
 
+def _route_keys(ref):
+    """Routing fields: the records, and a decoder's emitted tokens."""
+    return ROUTE_KEYS + (("tokens",) if np.asarray(ref.get("tokens", np.zeros((0, 0)))).shape[-1] else ())
+
+
+def _differ(a, b):
+    a, b = np.asarray(a), np.asarray(b)
+    d = a != b
+    return d.any(axis=1) if d.ndim == 2 else d
+
+
 def oracle_ref(wl, x_f32, aux, indices=None):
     """Float64 oracle results for `indices` plus the unstable flags from the
     oracle's float32 accumulation orders on the same samples."""
@@ -50,8 +61,8 @@ def oracle_ref(wl, x_f32, aux, indices=None):
     for acc in O.ACC_F32:
         r = O.from_workload(wl, acc).run(x_f32, aux, indices=indices)
         d = np.zeros(len(r64["exit_index"]), dtype=bool)
-        for k in ROUTE_KEYS:
-            d |= r64[k] != r[k]
+        for k in _route_keys(r64):
+            d |= _differ(r64[k], r[k])
         apart[acc] = d
     r64["unstable"] = np.logical_or.reduce([apart[a] for a in O.ACC_F32])
     r64["unstable_f32"] = apart["f32"]
@@ -78,6 +89,8 @@ def histogram(ref, arch):
         return np.bincount(ref["exit_index"], minlength=len(arch.get("heads", []))).tolist()
     if fam == "act":
         return np.bincount(ref["iterations"], minlength=arch["max_steps"] + 1)[1:].tolist()
+    if fam == "seq_decoder":
+        return np.bincount(ref["iterations"], minlength=arch["max_len"] + 1)[1:].tolist()
     bits = [(np.asarray(ref["skip_mask"], dtype=np.uint64) >> np.uint64(i)) & np.uint64(1)
             for i in range(len(arch["blocks"]))]
     return [int(b.sum()) for b in bits]           # samples that skip each gate
@@ -87,10 +100,11 @@ def compare(wl, gpu: dict, ref: dict, rows=None, logit_tol=None):
     """gpu: results for the whole batch; ref: oracle results for `rows`
     (default: all), with an `unstable` flag per row when known."""
     rows = np.arange(len(ref["exit_index"])) if rows is None else np.asarray(rows)
-    g = {k: np.asarray(gpu[k])[rows] for k in ("logits",) + ROUTE_KEYS}
+    keys = _route_keys(ref)
+    g = {k: np.asarray(gpu[k])[rows] for k in ("logits",) + keys}
     route_ok = np.ones(len(rows), dtype=bool)
-    for k in ROUTE_KEYS:
-        route_ok &= g[k] == np.asarray(ref[k])
+    for k in keys:
+        route_ok &= ~_differ(g[k], ref[k])
     tie = np.asarray(ref["margin"]) < NEAR_TIE
     unstable = np.asarray(ref.get("unstable", np.zeros(len(rows), dtype=bool)), dtype=bool)
     bad_route = ~route_ok & ~tie & ~unstable

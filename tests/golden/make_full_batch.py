@@ -5,7 +5,8 @@ their literal form: BatchNorm at its eval defaults, heads and gates as
 drawn), the oracle runs every sample with float64 accumulation (the
 reference) and with each of its four float32 accumulation orders (other
 correct evaluations of the same network).  Stored per sample: the float64
-run's logits, exit index, iteration count, skip mask, decision margin (the
+run's logits, exit index, iteration count, skip mask, emitted tokens (the
+decoder; -1 past the end), decision margin (the
 smallest |statistic - threshold| over the decisions it evaluated) and
 decision trail, and whether some float32 order routed the sample
 differently ("oracle-unstable": a property of the network, measured without
@@ -69,7 +70,7 @@ def run_oracle(name, literal, acc, batch, procs):
     with mp.get_context("spawn").Pool(procs) as pool:
         parts = sorted(pool.map(_worker, jobs), key=lambda t: t[0])
     out = {}
-    for k in ("logits", "exit_index", "iterations", "skip_mask", "margin"):
+    for k in ("logits", "exit_index", "iterations", "skip_mask", "margin", "tokens"):
         out[k] = np.concatenate([p[k] for _, p in parts])
     out["trail"] = [t for _, p in parts for t in p["trail"]]
     return out
@@ -85,7 +86,7 @@ def make(name: str, literal: bool, procs: int):
     for acc in ACC_F32:
         r = run_oracle(name, literal, acc, B, procs)
         diff[acc] = ((r64["exit_index"] != r["exit_index"]) | (r64["iterations"] != r["iterations"])
-                     | (r64["skip_mask"] != r["skip_mask"]))
+                     | (r64["skip_mask"] != r["skip_mask"]) | (r64["tokens"] != r["tokens"]).any(axis=1))
         if acc == "f32":
             r32 = r
     same = ~np.logical_or.reduce([diff[a] for a in ACC_F32])
@@ -99,7 +100,7 @@ def make(name: str, literal: bool, procs: int):
     np.savez_compressed(
         golden_path(name, literal), fingerprint=np.array(fingerprint(wl, B)), batch=np.array(B),
         logits=r64["logits"].astype(np.float32), exit_index=r64["exit_index"], iterations=r64["iterations"],
-        skip_mask=r64["skip_mask"], margin=r64["margin"], trail=trail, unstable=~same,
+        skip_mask=r64["skip_mask"], tokens=r64["tokens"], margin=r64["margin"], trail=trail, unstable=~same,
         unstable_f32=diff["f32"], **{f"routed_apart_{a}": diff[a] for a in ACC_F32},
         logit_floor_f32_vs_f64=np.array(floor))
     print(f"{name}{' (literal)' if literal else ''}: B={B} unstable={int((~same).sum())} "

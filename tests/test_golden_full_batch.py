@@ -11,8 +11,8 @@ from oracle import dycl_oracle as O
 from tests._parity import load_golden
 from workloads import configs
 
-CASES = [(n, False) for n in configs.NAMES] + [(n, True) for n in
-                                                ("mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit")]
+CASES = ([(n, False) for n in configs.NAMES] + [("lstm_decoder", False)] * ("lstm_decoder" not in configs.NAMES)
+         + [(n, True) for n in ("mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit")])
 
 
 @pytest.mark.parametrize("name,literal", CASES)
@@ -26,6 +26,8 @@ def test_golden_rows_reproduce(name, literal):
     np.testing.assert_array_equal(r["logits"], g["logits"][rows])
     for k in ("exit_index", "iterations", "skip_mask", "margin"):
         np.testing.assert_array_equal(r[k], g[k][rows])
+    if "tokens" in g:
+        np.testing.assert_array_equal(r["tokens"], g["tokens"][rows])
     for j, i in enumerate(rows):
         t = g["trail"][i]
         np.testing.assert_array_equal(np.asarray(r["trail"][j]), t[~np.isnan(t)])

@@ -366,3 +366,108 @@ def test_f32_orders_are_distinct_orders():
     ys = {a: O.conv2d(x, w, 1, 1, a) for a in O.ACC_F32}
     assert not torch.equal(ys["f32"], ys["f32c"])
     assert not torch.equal(ys["f32"], ys["f32r"])
+
+
+# ------------------------------------------------------ the LSTM decoder ----
+
+def test_naive_lstm_cell_is_the_library_cell():
+    # the independent reference's cell equations and gate order against
+    # torch.nn.LSTMCell (float64, bias_hh zero): W = [W_hh | W_ih]
+    g = torch.Generator().manual_seed(8)
+    H, E = 6, 4
+    cell = torch.nn.LSTMCell(E, H).double()
+    with torch.no_grad():
+        for p in cell.parameters():
+            p.copy_(torch.randn(p.shape, generator=g, dtype=torch.float64))
+        cell.bias_hh.zero_()
+    h = torch.randn(H, generator=g, dtype=torch.float64)
+    c = torch.randn(H, generator=g, dtype=torch.float64)
+    e = torch.randn(E, generator=g, dtype=torch.float64)
+    hl, cl = cell(e[None], (h[None], c[None]))
+    Wl = torch.cat([cell.weight_hh, cell.weight_ih], dim=1).detach().numpy()
+    hn, cn = N.lstm_step(Wl, cell.bias_ih.detach().numpy(), h.numpy(), e.numpy(), c.numpy())
+    np.testing.assert_allclose(hn, hl[0].detach().numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(cn, cl[0].detach().numpy(), rtol=1e-12, atol=1e-14)
+
+
+def _tiny_decoder(eos_shift):
+    arch = configs.arch_decoder(d_in=6, hidden=4, embed=3, vocab=5, max_len=4, out_gain=8.0)
+    wl = configs.raw_workload("tiny_dec", arch)
+    W = wl.weights_f32()
+    W["out.b"] = W["out.b"].copy()
+    W["out.b"][arch["eos"]] += np.float32(eos_shift)
+    return arch, wl, W
+
+
+@pytest.mark.parametrize("eos_shift", [0.0, -0.3])
+def test_tiny_decoder_paths(eos_shift):
+    # every token sequence of length <= max_len is evaluated as a static
+    # network along that sequence; exactly one is self-consistent (each
+    # token is its step's argmax, lowest index on ties; the end token or the
+    # length bound ends it) and the oracle emits it, with that path's last
+    # logits and its gaps as the decision trail
+    arch, wl, W = _tiny_decoder(eos_shift)
+    V, L, eos = arch["vocab"], arch["max_len"], arch["eos"]
+    x, _ = wl.inputs_f32(12)
+    res = O.Oracle(arch, W).run(x)
+    lengths = set()
+    for i in range(12):
+        consistent = []
+        for n in range(1, L + 1):
+            for seq in itertools.product(range(V), repeat=n):
+                if any(t == eos for t in seq[:-1]) or (n < L and seq[-1] != eos):
+                    continue
+                zs = N.decoder_path(arch, W, x[i], seq)
+                if all(int(np.argmax(z)) == t for z, t in zip(zs, seq)):
+                    consistent.append((seq, zs))
+        assert len(consistent) == 1
+        seq, zs = consistent[0]
+        n = len(seq)
+        assert res["iterations"][i] == n and res["exit_index"][i] == -1 and res["skip_mask"][i] == 0
+        assert list(res["tokens"][i][:n]) == list(seq) and (res["tokens"][i][n:] == -1).all()
+        np.testing.assert_allclose(res["logits"][i], zs[-1], rtol=1e-6, atol=1e-6)
+        gaps = [float(np.sort(z)[-1] - np.sort(z)[-2]) for z in zs]
+        _check_trail(res, i, gaps, 0.0)
+        lengths.add(n)
+    assert len(lengths) >= 2
+
+
+def test_decoder_special_cases():
+    arch, wl, W = _tiny_decoder(0.0)
+    x, _ = wl.inputs_f32(6)
+    # the end token always wins: every sequence is that token alone
+    Wb = dict(W, **{"out.b": W["out.b"] + np.where(np.arange(arch["vocab"]) == arch["eos"], 1e4, 0.0)
+                    .astype(np.float32)})
+    r = O.Oracle(arch, Wb).run(x)
+    assert (r["iterations"] == 1).all() and (r["tokens"][:, 0] == arch["eos"]).all()
+    # the end token never wins: every sequence runs to the length bound
+    Wn = dict(W, **{"out.b": W["out.b"] - np.where(np.arange(arch["vocab"]) == arch["eos"], 1e4, 0.0)
+                    .astype(np.float32)})
+    r = O.Oracle(arch, Wn).run(x)
+    assert (r["iterations"] == arch["max_len"]).all() and (r["tokens"] != arch["eos"]).all()
+    # a bound of one step: one token, the argmax of the first step's logits
+    a1 = dict(arch, max_len=1)
+    r = O.Oracle(a1, W).run(x)
+    for i in range(6):
+        z = N.decoder_path(a1, W, x[i], [0])[0]
+        assert r["iterations"][i] == 1 and r["tokens"][i][0] == int(np.argmax(z))
+        np.testing.assert_allclose(r["logits"][i], z, rtol=1e-6, atol=1e-6)
+
+
+def test_decoder_workload_invariants():
+    wl = configs.build("lstm_decoder")
+    a = wl.arch
+    x, _ = wl.inputs_f32(24)
+    r = O.from_workload(wl).run(x)
+    L = a["max_len"]
+    for i in range(24):
+        n = r["iterations"][i]
+        assert 1 <= n <= L
+        assert (r["tokens"][i][:n] >= 0).all() and (r["tokens"][i][n:] == -1).all()
+        if n < L:
+            assert r["tokens"][i][n - 1] == a["eos"]      # only the end token stops early
+        assert not (r["tokens"][i][:n - 1] == a["eos"]).any()
+    # batch-split invariance
+    r2 = O.from_workload(wl).run(x, indices=range(10, 24))
+    np.testing.assert_array_equal(r2["tokens"], r["tokens"][10:])
+    np.testing.assert_array_equal(r2["logits"], r["logits"][10:])

@@ -38,7 +38,7 @@ BN_EPS = 1e-5
 
 NAMES = ["mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit", "act_loop"]
 DEFAULT_BATCH = {"mlp_exit": 64, "resnet18_exit": 1024, "skipnet38": 2048,
-                 "resnet50_exit": 256, "act_loop": 4096}
+                 "resnet50_exit": 256, "act_loop": 4096, "lstm_decoder": 1024}
 
 
 # --------------------------------------------------------------------------
@@ -242,12 +242,15 @@ def arch_act(hidden=1024, d_in=1024, d_out=1024, max_steps=16, tau=0.99):
             "n_out": d_out, "max_steps": max_steps, "tau": tau}
 
 
-def arch_decoder(d_in=512, hidden=512, embed=256, vocab=4096, max_len=24, eos=0, bos=1):
+def arch_decoder(d_in=512, hidden=512, embed=256, vocab=4096, max_len=24, eos=0, bos=1, out_gain=32.0):
     """Greedy LSTM decoder: h0 = tanh(W_enc x + b_enc), c0 = 0, then one token
     per step until the end token `eos` or `max_len` tokens; the first step
-    reads the start token `bos`."""
+    reads the start token `bos`.  The output layer is drawn with gain
+    `out_gain` over nn.Linear's default range (a trained decoder's output
+    distribution is peaked; at gain 1 the two largest logits of a step lie
+    ~1e-2 apart)."""
     return {"family": "seq_decoder", "dtype": "bf16", "input": [d_in], "hidden": hidden, "embed": embed,
-            "vocab": vocab, "n_out": vocab, "max_len": max_len, "eos": eos, "bos": bos}
+            "vocab": vocab, "n_out": vocab, "max_len": max_len, "eos": eos, "bos": bos, "out_gain": out_gain}
 
 
 ARCHS = {
@@ -345,8 +348,9 @@ def raw_workload(name: str, arch: dict | None = None) -> Workload:
         _add(wl, "lstm.w", "bf16", linear_default(name, "lstm.w", (4 * H, H + E), H))
         _add(wl, "lstm.b", "f32", linear_default(name, "lstm.b_ih", (4 * H,), H)
              + linear_default(name, "lstm.b_hh", (4 * H,), H))
-        _add(wl, "out.w", "bf16", linear_default(name, "out.w", (V, H), H))
-        _add(wl, "out.b", "f32", linear_default(name, "out.b", (V,), H))
+        g = arch["out_gain"]
+        _add(wl, "out.w", "bf16", g * linear_default(name, "out.w", (V, H), H))
+        _add(wl, "out.b", "f32", g * linear_default(name, "out.b", (V,), H))
     else:
         raise ValueError(fam)
     return wl
