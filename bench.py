@@ -220,39 +220,38 @@ def other_workloads(skip: str, steps: int, warmup: int, stream):
         plan = runtime.Plan.from_workload(wl, B)
         x, aux = wl.inputs(B)
         xt, at = runtime.device_inputs(wl, x, aux)
-        logits = torch.empty((B, plan.n_out), dtype=torch.float32, device="cuda")
-        rec = torch.empty((B, 4), dtype=torch.int32, device="cuda")
+        logits, rec, tok = plan.outputs(B)
         plan.set_host_mode("device")
         for _ in range(warmup):
-            plan.run(xt, at, logits, rec, stream)
+            plan.run(xt, at, logits, rec, stream, tok)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(steps):
-            plan.run(xt, at, logits, rec, stream)
+            plan.run(xt, at, logits, rec, stream, tok)
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / steps
         res[name] = {"batch": B, "dtype": wl.arch["dtype"], "ms_per_step": ms, "samples_per_s": B / (ms * 1e-3),
                      "branch_counts": plan.counts(), "host_mode": "device"}
         plan.close()
-        del xt, at, logits, rec
+        del xt, at, logits, rec, tok
     return res
 
 
 RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per HBM byte where the two bounds meet
 
 
-def layer_table(wl, plan, xt, at, logits, rec, stream, warmup):
+def layer_table(wl, plan, xt, at, logits, rec, stream, warmup, tok=None):
     """One profiled sync-mode step: each conv launch with its algorithmic
     FLOPs and bytes (executed rows only) and its HIP-event time; the bound
     is the layer's attainable rate min(peak, intensity x HBM peak)."""
     import torch
     plan.set_host_mode("sync")
     for _ in range(max(warmup, 1)):
-        plan.run(xt, at, logits, rec, stream)
+        plan.run(xt, at, logits, rec, stream, tok)
     plan.profile(True)
-    plan.run(xt, at, logits, rec, stream)
+    plan.run(xt, at, logits, rec, stream, tok)
     torch.cuda.synchronize()
     every = plan.profile_launches()
     launches = [r for r in every if r["class"] in ("conv_bf16_mfma", "linear_f32")]
@@ -318,18 +317,17 @@ def main():
     plan = runtime.Plan.from_workload(wl, B)
     x, aux = wl.inputs(B)
     xt, at = runtime.device_inputs(wl, x, aux)
-    logits = torch.empty((B, plan.n_out), dtype=torch.float32, device="cuda")
-    rec = torch.empty((B, 4), dtype=torch.int32, device="cuda")
+    logits, rec, tok = plan.outputs(B)
     stream = torch.cuda.current_stream()
 
     if args.layers:
-        print(json.dumps(layer_table(wl, plan, xt, at, logits, rec, stream, args.warmup)), flush=True)
+        print(json.dumps(layer_table(wl, plan, xt, at, logits, rec, stream, args.warmup, tok)), flush=True)
         return
 
     def timed(mode):
         plan.set_host_mode(mode)
         for _ in range(args.warmup):
-            plan.run(xt, at, logits, rec, stream)
+            plan.run(xt, at, logits, rec, stream, tok)
         torch.cuda.synchronize()
         # timed region: exactly --steps steps
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -337,7 +335,7 @@ def main():
         w0 = time.perf_counter()
         e0.record(stream)
         for _ in range(args.steps):
-            plan.run(xt, at, logits, rec, stream)
+            plan.run(xt, at, logits, rec, stream, tok)
         e1.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - w0
@@ -361,7 +359,7 @@ def main():
     # profiled pass: per-launch HIP events around every kernel on the run's stream
     plan.profile(True)
     for _ in range(args.steps):
-        plan.run(xt, at, logits, rec, stream)
+        plan.run(xt, at, logits, rec, stream, tok)
     torch.cuda.synchronize()
     prof = plan.profile_read()
     plan.profile(False)
@@ -401,7 +399,7 @@ def main():
         "kernels": kernels,
     }
     plan.close()
-    del xt, at, logits, rec
+    del xt, at, logits, rec, tok
     if not args.no_other_workloads:
         out["other_workloads"] = other_workloads(args.workload, args.steps, args.warmup, stream)
     if not args.no_hbm_kernels:

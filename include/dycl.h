@@ -99,6 +99,23 @@ int dycl_run(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev
              dycl_record* records_dev, void* hip_stream);
 
 /*
+ * dycl_run for a plan whose network emits token sequences (a generative
+ * network, Table 1's En-Decoder family: one token per step, read back as
+ * the next step's input, until an end token or the spec's max_len; the
+ * bounded loop of Sec. 2.2).  The same arguments, plus
+ *   tokens_dev  device int32 [batch][max_len] (max_len from
+ *               dycl_plan_info), 4-byte aligned, caller-owned: the emitted
+ *               tokens in the original sample order, -1 after a sample's
+ *               last token.
+ * logits_dev must be 16-byte aligned here.
+ * logits_dev receives each sample's last step logits [batch][n_out] and
+ * records_dev its length as `iterations`.  dycl_run refuses such a plan and
+ * dycl_run_seq any other (DYCL_E_INVALID).
+ */
+int dycl_run_seq(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev, float* logits_dev,
+                 dycl_record* records_dev, int32_t* tokens_dev, void* hip_stream);
+
+/*
  * How the host module learns the branch counts (Sec. 5: the host program
  * keeps the conditionals and calls the compiled sub-DNNs; Sec. 4, Challenge
  * 2 and Sec. 6.4, Table 4: host-device transfers that compute nothing are
@@ -138,7 +155,8 @@ int dycl_last_counts(const dycl_plan* plan, int32_t* counts, int n);
  * Plan facts, info[0..n): 0 n_out, 1 input bytes per sample, 2 decision
  * points, 3 device workspace bytes, 4 device weight bytes, 5 max_batch,
  * 6 aux required (0/1), 7 number of nodes, 8 host mode, 9 graph captures
- * so far.  Returns the number written.
+ * so far, 10 tokens per sample a run emits (max_len; 0: a plan for
+ * dycl_run).  Returns the number written.
  */
 int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n);
 

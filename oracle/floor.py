@@ -54,6 +54,8 @@ def drift(r64, r32, positions):
 
 def n_positions(arch):
     fam = arch["family"]
+    if fam == "seq_decoder":
+        return arch["max_len"]
     if fam == "early_exit_mlp":
         return len(arch["layers"]) - 1
     if fam == "early_exit_resnet":
@@ -67,6 +69,8 @@ def thresholds(arch):
     fam = arch["family"]
     if fam == "skipnet":
         return float(np.float32(arch["gate_threshold"]))
+    if fam == "seq_decoder":
+        return 0.0      # the statistic is the gap between the two largest logits
     return float(np.float32(arch["tau"]))
 
 

@@ -17,7 +17,7 @@ STATUS = {0: "DYCL_OK", -1: "DYCL_E_INVALID", -2: "DYCL_E_SPEC", -3: "DYCL_E_WEI
           -5: "DYCL_E_OOM", -6: "DYCL_E_HIP"}
 
 # every symbol include/dycl.h declares
-EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_plan_set_host_mode", "dycl_last_counts", "dycl_plan_info", "dycl_profile_enable",
+EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_run_seq", "dycl_plan_set_host_mode", "dycl_last_counts", "dycl_plan_info", "dycl_profile_enable",
            "dycl_profile_read", "dycl_profile_launches", "dycl_profile_launch_label", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
 # every symbol include/dycl_ops.h declares
 OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_compact_noalloc", "dycl_op_move_rows", "dycl_op_conv_packed_bytes",
@@ -48,6 +48,8 @@ def _load():
     lib.dycl_plan_create.restype = i32
     lib.dycl_run.argtypes = [vp, vp, i32, vp, vp, vp, vp]
     lib.dycl_run.restype = i32
+    lib.dycl_run_seq.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp]
+    lib.dycl_run_seq.restype = i32
     lib.dycl_plan_set_host_mode.argtypes = [vp, i32]
     lib.dycl_plan_set_host_mode.restype = i32
     lib.dycl_last_counts.argtypes = [vp, C.POINTER(C.c_int32), i32]

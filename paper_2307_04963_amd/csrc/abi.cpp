@@ -68,22 +68,46 @@ int dycl_plan_create(const char* spec_json, const void* weights, size_t weights_
   return DYCL_OK;
 }
 
-int dycl_run(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev, float* logits_dev,
-             dycl_record* records_dev, void* hip_stream) {
-  if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_run: invalid plan handle");
+namespace {
+
+int run_checked(const char* fn, dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev,
+                float* logits_dev, dycl_record* records_dev, int32_t* tokens_dev, void* hip_stream) {
+  const std::string f(fn);
+  if (!valid(plan)) return fail(DYCL_E_INVALID, f + ": invalid plan handle");
   if (batch < 0 || batch > plan->max_batch)
-    return fail(DYCL_E_BATCH, "dycl_run: batch " + std::to_string(batch) + " outside [0, " +
+    return fail(DYCL_E_BATCH, f + ": batch " + std::to_string(batch) + " outside [0, " +
                                   std::to_string(plan->max_batch) + "]");
   if (batch == 0) return DYCL_OK;
-  if (!x_dev || !logits_dev || !records_dev) return fail(DYCL_E_INVALID, "dycl_run: null input or output pointer");
-  if (plan->spec.aux && !aux_dev) return fail(DYCL_E_INVALID, "dycl_run: this plan reads per-sample aux inputs");
-  if ((reinterpret_cast<uintptr_t>(x_dev) & 15) || (reinterpret_cast<uintptr_t>(logits_dev) & 3) ||
-      (reinterpret_cast<uintptr_t>(records_dev) & 7))
-    return fail(DYCL_E_INVALID, "dycl_run: x must be 16-byte aligned, logits 4, records 8");
+  if (!x_dev || !logits_dev || !records_dev) return fail(DYCL_E_INVALID, f + ": null input or output pointer");
+  if (plan->spec.aux && !aux_dev) return fail(DYCL_E_INVALID, f + ": this plan reads per-sample aux inputs");
+  // a decoding run copies logits rows as 16-byte vectors
+  const uintptr_t la = tokens_dev ? 15 : 3;
+  if ((reinterpret_cast<uintptr_t>(x_dev) & 15) || (reinterpret_cast<uintptr_t>(logits_dev) & la) ||
+      (reinterpret_cast<uintptr_t>(records_dev) & 7) || (reinterpret_cast<uintptr_t>(tokens_dev) & 3))
+    return fail(DYCL_E_INVALID, f + ": x must be 16-byte aligned, logits 4 (16 for dycl_run_seq), records 8, "
+                                    "tokens 4");
   return guarded([&] {
-    dycl::plan_run(plan, x_dev, batch, aux_dev, logits_dev, records_dev, static_cast<hipStream_t>(hip_stream));
+    dycl::plan_run(plan, x_dev, batch, aux_dev, logits_dev, records_dev, tokens_dev,
+                   static_cast<hipStream_t>(hip_stream));
     return DYCL_OK;
   });
+}
+
+}  // namespace
+
+int dycl_run(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev, float* logits_dev,
+             dycl_record* records_dev, void* hip_stream) {
+  if (valid(plan) && plan->spec.any_decode)
+    return fail(DYCL_E_INVALID, "dycl_run: this plan emits token sequences; call dycl_run_seq");
+  return run_checked("dycl_run", plan, x_dev, batch, aux_dev, logits_dev, records_dev, nullptr, hip_stream);
+}
+
+int dycl_run_seq(dycl_plan* plan, const void* x_dev, int batch, const float* aux_dev, float* logits_dev,
+                 dycl_record* records_dev, int32_t* tokens_dev, void* hip_stream) {
+  if (valid(plan) && !plan->spec.any_decode)
+    return fail(DYCL_E_INVALID, "dycl_run_seq: this plan emits no tokens; call dycl_run");
+  if (batch > 0 && !tokens_dev) return fail(DYCL_E_INVALID, "dycl_run_seq: null tokens");
+  return run_checked("dycl_run_seq", plan, x_dev, batch, aux_dev, logits_dev, records_dev, tokens_dev, hip_stream);
 }
 
 int dycl_plan_set_host_mode(dycl_plan* plan, int mode) {
@@ -113,7 +137,7 @@ int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n) {
   if (n < 0 || (n > 0 && !info)) return fail(DYCL_E_INVALID, "dycl_plan_info: bad buffer");
   const dycl::Spec& sp = plan->spec;
   const dycl::TensorInfo& in = sp.tensors[sp.input];
-  const int64_t v[10] = {sp.n_out,
+  const int64_t v[11] = {sp.n_out,
                          static_cast<int64_t>(in.row_bytes(sp.dt)),
                          sp.decisions,
                          static_cast<int64_t>(plan->workspace_bytes),
@@ -122,9 +146,10 @@ int dycl_plan_info(const dycl_plan* plan, int64_t* info, int n) {
                          sp.aux ? 1 : 0,
                          sp.nodes_total,
                          plan->mode,
-                         plan->graph_captures};
+                         plan->graph_captures,
+                         sp.any_decode ? sp.max_len : 0};
   int w = 0;
-  for (; w < n && w < 10; ++w) info[w] = v[w];
+  for (; w < n && w < 11; ++w) info[w] = v[w];
   return w;
 }
 

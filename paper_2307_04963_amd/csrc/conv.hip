@@ -57,6 +57,8 @@ struct ConvP {
   // (the last ones of the packed layout) run first; then every sum becomes
   // bf16(fsp * acc + fbp) * finv, the rounded projection output in the
   // units of the block's own sum, which the remaining steps add to
+  const float* cell_in;    // ACT_LSTM: old cell state [rows][cout / 4] (through rrows), or null
+  float* cell_out;         // ACT_LSTM: new cell state [rows][cout / 4] (through drows)
   int kfold;
   const float* fsp;
   const float* fbp;
@@ -95,14 +97,18 @@ template <int ACT>
 __device__ __forceinline__ float act_t(float v) {
   if (ACT == ACT_RELU) return v > 0.f ? v : 0.f;
   if (ACT == ACT_GELU) return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+  if (ACT == ACT_TANH) return tanhf(v);
   return v;
 }
 
 __device__ __forceinline__ float apply_act(float v, int act) {
   if (act == ACT_RELU) return v > 0.f ? v : 0.f;
   if (act == ACT_GELU) return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+  if (act == ACT_TANH) return tanhf(v);
   return v;
 }
+
+__device__ __forceinline__ float sigmoidf(float v) { return 1.0f / (1.0f + expf(-v)); }
 
 template <int BM, int BN, int WM, int WN, int KS, bool SCALAR, int BK = 64, int STAGES = 1>
 __global__ __launch_bounds__(64 * WM* WN) void conv_kernel(ConvP p) {
@@ -598,6 +604,20 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
             *reinterpret_cast<float4*>(d + 4) = hi;
             continue;
           }
+          if constexpr (ACT == ACT_LSTM) {
+            // the 8 values are the gates of cells u and u + 1 (input,
+            // forget, cell, output each); cell state float32, h bf16
+            const int H = p.cout >> 2, u = col >> 2;
+            float2 cp = make_float2(0.f, 0.f);
+            if (p.cell_in) cp = *reinterpret_cast<const float2*>(p.cell_in + row_at(p.rrows, row, HoWo) * H + u);
+            const float c0 = sigmoidf(vv[1]) * cp.x + sigmoidf(vv[0]) * tanhf(vv[2]);
+            const float c1 = sigmoidf(vv[5]) * cp.y + sigmoidf(vv[4]) * tanhf(vv[6]);
+            const float h0 = sigmoidf(vv[3]) * tanhf(c0), h1 = sigmoidf(vv[7]) * tanhf(c1);
+            const size_t oc = row_at(p.drows, row, HoWo) * H + u;
+            *reinterpret_cast<float2*>(p.cell_out + oc) = make_float2(c0, c1);
+            *reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(p.dst) + oc) = pack_bf16(h0, h1);
+            continue;
+          }
           const size_t o = row_at(p.drows, row, HoWo) * p.cout + col;
           if (p.res) {
             const uint32_t rw[4] = {rv[a][v].x, rv[a][v].y, rv[a][v].z, rv[a][v].w};
@@ -630,6 +650,10 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
     epilogue(std::integral_constant<int, ACT_RELU>{});
   else if (p.act == ACT_GELU)
     epilogue(std::integral_constant<int, ACT_GELU>{});
+  else if (p.act == ACT_TANH)
+    epilogue(std::integral_constant<int, ACT_TANH>{});
+  else if (p.act == ACT_LSTM)
+    epilogue(std::integral_constant<int, ACT_LSTM>{});
   else
     epilogue(std::integral_constant<int, ACT_NONE>{});
 }
@@ -1727,6 +1751,8 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.nmax = a.n;
   p.ksplit = 1;
   p.part = nullptr;
+  p.cell_in = a.cell_in;
+  p.cell_out = a.cell_out;
   p.kfold = a.kfold;
   p.fsp = a.fold_sp;
   p.fbp = a.fold_bp;
@@ -1735,6 +1761,14 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
                   !a.fold_sp || !a.fold_bp || !a.fold_inv || a.cout % 8 || (reinterpret_cast<uintptr_t>(a.dst) & 15) ||
                   !a.zeros))
     throw std::invalid_argument("folded projection: arguments the implicit-GEMM kernel does not take");
+  // tanh and the LSTM cell exist only in the implicit GEMM's epilogue: a
+  // linear layer on 1x1 rows with 16-byte output vectors, never split
+  const bool special = a.act == ACT_TANH || a.act == ACT_LSTM;
+  if (special && (a.k != 1 || a.H != 1 || a.W != 1 || a.cin % 8 || a.cout % 8 || a.res || a.out_f32 || !a.zeros ||
+                  (reinterpret_cast<uintptr_t>(a.dst) & 15) ||
+                  (a.act == ACT_LSTM && (!a.cell_out || (reinterpret_cast<uintptr_t>(a.cell_out) & 7) ||
+                                         (reinterpret_cast<uintptr_t>(a.cell_in) & 7)))))
+    throw std::invalid_argument("tanh / LSTM-cell epilogue: arguments the implicit-GEMM kernel does not take");
   p.srows = a.src_rows;
   p.s2rows = a.src2_rows;
   p.rrows = a.res_rows;
@@ -1775,7 +1809,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
     // workgroups, fp32 partials summed in a fixed order by a second kernel
     // (the split depends on the layer's shape only, never on n)
     const int S = conv_ksplit(a.Ho, a.Wo, a.cout, p.K, a.out_f32 != 0);
-    const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold &&
+    const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold && !special &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
                             : choose_lds(Mh, a.cout, p.Kp);

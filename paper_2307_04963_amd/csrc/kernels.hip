@@ -1014,6 +1014,85 @@ void fill_f32(float* p, float v, int n, hipStream_t s) {
   hipLaunchKernelGGL(fill_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, p, v, n);
 }
 
+__global__ void fill_i32_kernel(int32_t* p, int32_t v, size_t n) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+void fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t s) {
+  if (n == 0) return;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s, p, v, n);
+}
+
+__global__ void gather_i32_kernel(int32_t* dst, const int32_t* __restrict__ src, const int32_t* __restrict__ idx,
+                                  int n, const int32_t* nc) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < live(nc, n)) dst[i] = src[idx[i]];
+}
+
+void gather_i32(int32_t* dst, const int32_t* src, const int32_t* idx, int n, hipStream_t s, const int32_t* nc) {
+  hipLaunchKernelGGL(gather_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, dst, src, idx, n, nc);
+}
+
+// ------------------------------------------------------ greedy decoding ----
+// One wave per row: each lane scans float4 pieces of the row (lanes on
+// consecutive pieces), keeps its largest value and that value's lowest
+// index, and the wave merges the lanes' pairs by shuffles with the same
+// rule, so ties go to the lowest index whatever the scan order.
+
+__device__ __forceinline__ void better(float v, int i, float& bv, int& bi) {
+  if (v > bv || (v == bv && i < bi)) {
+    bv = v;
+    bi = i;
+  }
+}
+
+__global__ __launch_bounds__(256) void decode_step_kernel(const float* __restrict__ Z, int n, int V, int eos, int step,
+                                                          int max_len, const int32_t* __restrict__ orig,
+                                                          uint8_t* flags, int32_t* tok_next, int32_t* tokens,
+                                                          float* logits, dycl_record* rec, const int32_t* nc) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= live(nc, n)) return;
+  const float4* zr = reinterpret_cast<const float4*>(Z + static_cast<size_t>(r) * V);
+  const int V4 = V / 4;
+  float bv = -INFINITY;
+  int bi = V;
+  for (int j = lane; j < V4; j += 64) {
+    const float4 q = zr[j];
+    better(q.x, 4 * j, bv, bi);
+    better(q.y, 4 * j + 1, bv, bi);
+    better(q.z, 4 * j + 2, bv, bi);
+    better(q.w, 4 * j + 3, bv, bi);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    better(ov, oi, bv, bi);
+  }
+  const int tok = bi < V ? bi : 0;   // every logit NaN: token 0
+  const bool done = tok == eos || step == max_len;
+  const int o = orig[r];
+  if (lane == 0) {
+    flags[r] = done ? 1 : 0;
+    tok_next[r] = tok;
+    tokens[static_cast<size_t>(o) * max_len + step - 1] = tok;
+    if (done) rec[o].iterations = step;
+  }
+  if (done) {
+    float4* lr = reinterpret_cast<float4*>(logits + static_cast<size_t>(o) * V);
+    for (int j = lane; j < V4; j += 64) lr[j] = zr[j];
+  }
+}
+
+void decode_step(const float* Z, int n, int V, int eos, int step, int max_len, const int32_t* orig, uint8_t* flags,
+                 int32_t* tok_next, int32_t* tokens, float* logits, dycl_record* rec, hipStream_t s,
+                 const int32_t* nc) {
+  hipLaunchKernelGGL(decode_step_kernel, dim3((n + 3) / 4), dim3(256), 0, s, Z, n, V, eos, step, max_len, orig, flags,
+                     tok_next, tokens, logits, rec, nc);
+}
+
 __global__ void iota_kernel(int32_t* p, int n) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i < n) p[i] = i;

@@ -22,7 +22,14 @@
 namespace dycl {
 namespace k {
 
-enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_GELU = 2 };
+// ACT_TANH and ACT_LSTM run on the implicit-GEMM kernel only (linear
+// layers on 1x1 rows).  ACT_LSTM: the layer's cout = 4 H outputs are the
+// gates of H cells interleaved (channel 4 j + k = gate k of cell j: input,
+// forget, cell, output); the epilogue is the cell itself, reading the old
+// cell state (cell_in, float32 [rows][H], through res_rows; null: zeros)
+// and writing the new one (cell_out) and h = o tanh(c) in bf16 to dst
+// [rows][H].
+enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_GELU = 2, ACT_TANH = 3, ACT_LSTM = 4 };
 
 // The implicit-GEMM convolution picks its tile at launch from the active
 // row count.  Packed weights are [conv_cout_pad(cout)][Kp] with Kp a
@@ -57,6 +64,8 @@ struct ConvArgs {
   int list_rows = 0;     // rows of the tensors read or written through a list (0: no list)
   float* splitws = nullptr;         // K-split partial sums (conv_ksplit_bytes), or null: no split
   size_t splitws_bytes = 0;
+  const float* cell_in = nullptr;   // ACT_LSTM: old cell state, or null (zeros)
+  float* cell_out = nullptr;        // ACT_LSTM: new cell state
   // a folded projection shortcut (src2 holds its input, its weights are
   // the last cin2 K columns, cin1 and cin2 multiples of kBK): the kfold K
   // steps of src2 run first and their sum becomes bf16(fold_sp * acc +
@@ -194,6 +203,20 @@ void maxpool3s2_bf16(const uint16_t* x, int n, int H, int W, int C, uint16_t* y,
 void final_counts(const int32_t* nc, int n, int32_t* counts, hipStream_t s);
 void init_records(dycl_record* rec, int n, hipStream_t s);
 void fill_f32(float* p, float v, int n, hipStream_t s);
+void fill_i32(int32_t* p, int32_t v, size_t n, hipStream_t s);
+// dst[i] = src[idx[i]] for i < min(*nc, n) (nc null: n)
+void gather_i32(int32_t* dst, const int32_t* src, const int32_t* idx, int n, hipStream_t s,
+                const int32_t* nc = nullptr);
+
+// One step of greedy decoding on the step's logits Z [n][V] (float32): the
+// token of row r is the argmax of its logits (the lowest index among equal
+// maxima); tok_next[r] = token; tokens[orig[r] * max_len + step - 1] =
+// token; the row finishes (flag 1) when the token is `eos` or step ==
+// max_len, and then records `step` as its iteration count and copies its
+// logits to logits[orig[r]] (row length V).  V % 4 == 0.
+void decode_step(const float* Z, int n, int V, int eos, int step, int max_len, const int32_t* orig,
+                 uint8_t* flags, int32_t* tok_next, int32_t* tokens, float* logits, dycl_record* rec, hipStream_t s,
+                 const int32_t* nc = nullptr);
 void iota_i32(int32_t* p, int n, hipStream_t s);
 
 }  // namespace k

@@ -122,7 +122,9 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
   for (Packed& q : sp.packed) {
     std::vector<uint16_t> h(static_cast<size_t>(q.cout_pad) * q.Kp, 0);
     for (int co = 0; co < q.cout; ++co) {
-      const uint8_t* row = hb + q.w_off + (static_cast<size_t>(co) * q.w_ldk + q.w_k0) * 2;
+      // LSTM gates: packed row 4 j + k is gate k of cell j (stored in blocks of cout / 4)
+      const int srow = q.interleave4 ? (co % 4) * (q.cout / 4) + co / 4 : co;
+      const uint8_t* row = hb + q.w_off + (static_cast<size_t>(srow) * q.w_ldk + q.w_k0) * 2;
       if (q.w2_off >= 0) {
         // a folded projection: [W_c | W_p], both as stored; a channel whose
         // own scale is 0 keeps only the projection block
@@ -167,6 +169,26 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     p->weight_bytes += ss.size() * 4;
     hip_check(hipMemcpy(ptr, ss.data(), ss.size() * 4, hipMemcpyHostToDevice), "folded projection constants upload");
   }
+
+  // LSTM steps: the gate bias in the interleaved order of the packed rows
+  p->lstm_shift.assign(sp.n_lstm_shift, nullptr);
+  std::function<void(const std::vector<Node>&)> lstm_walk = [&](const std::vector<Node>& nodes) {
+    for (const Node& nd : nodes) {
+      if (nd.lstm_shift >= 0) {
+        const int H = nd.cout / 4;
+        std::vector<float> b(static_cast<size_t>(nd.cout), 0.0f);
+        for (int co = 0; co < nd.cout; ++co)
+          if (nd.shift_off >= 0) b[co] = hf32(nd.shift_off, (co % 4) * H + co / 4);
+        void* ptr = nullptr;
+        if (hipMalloc(&ptr, b.size() * 4) != hipSuccess) throw OomError("LSTM bias: hipMalloc failed");
+        p->lstm_shift[nd.lstm_shift] = static_cast<float*>(ptr);
+        p->weight_bytes += b.size() * 4;
+        hip_check(hipMemcpy(ptr, b.data(), b.size() * 4, hipMemcpyHostToDevice), "LSTM bias upload");
+      }
+      lstm_walk(nd.body);
+    }
+  };
+  lstm_walk(sp.nodes);
 
   // fp32 weight matrices [rows][cols] kept transposed ([cols][rows]): exit
   // heads and fp32 linear layers
@@ -221,6 +243,10 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
   }
   p->d_Z = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_ncls, "head logits");
   p->d_S = dev_alloc<float>(p, B, "halting sums");
+  if (sp.any_decode) {
+    p->d_tok[0] = dev_alloc<int32_t>(p, B, "previous tokens");
+    p->d_tok[1] = dev_alloc<int32_t>(p, B, "step tokens");
+  }
   p->d_zeros = dev_alloc<uint16_t>(p, 128, "zero page");
   if (B > 16384) p->d_cws = dev_alloc<uint8_t>(p, k::compact_workspace(B), "compaction workspace");
   if (sp.pad_input_c) {
@@ -272,11 +298,13 @@ void plan_free(dycl_plan* p) {
     if (h) hipFree(h);
   for (float* h : p->fold_shift)
     if (h) hipFree(h);
+  for (float* h : p->lstm_shift)
+    if (h) hipFree(h);
   for (void* b : p->buffers)
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
                      p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S, p->d_zeros,
-                     p->d_xpad, p->d_cws, p->d_Gpart, p->d_split};
+                     p->d_xpad, p->d_cws, p->d_Gpart, p->d_split, p->d_tok[0], p->d_tok[1]};
   for (void* s : singles)
     if (s) hipFree(s);
   if (p->h_counts) hipHostFree(p->h_counts);
@@ -307,6 +335,7 @@ struct Run {
   const float* aux;
   float* logits;
   dycl_record* rec;
+  int32_t* tokens;           // decoding: [B][max_len] emitted tokens, or null
   int B;
   bool device;               // counts stay on the device
   std::vector<void*> tp;     // tensor pointers
@@ -446,6 +475,16 @@ struct Run {
     }
     a.res = nd.res >= 0 ? static_cast<const uint16_t*>(tp[nd.res]) : nullptr;
     a.act = nd.act;
+    if (nd.act == k::ACT_LSTM) {
+      // the concatenated input is the embedding row of each row's previous token
+      a.src2 = reinterpret_cast<const uint16_t*>(p->d_blob + nd.emb_off);
+      a.src2_H = a.src2_W = 1;
+      a.src2_stride = 1;
+      a.src2_rows = p->d_tok[0];
+      a.cell_in = nd.cell_in >= 0 ? static_cast<const float*>(tp[nd.cell_in]) : nullptr;
+      a.cell_out = static_cast<float*>(tp[nd.cell_out]);
+      a.shift = p->lstm_shift[nd.lstm_shift];
+    }
     a.dst = tp[nd.dst];
     a.out_f32 = 0;
     a.zeros = p->d_zeros;
@@ -455,7 +494,7 @@ struct Run {
       return which == 1 ? p->d_idx0 : which == 2 ? p->d_idx1 : which == 3 ? orig : nullptr;
     };
     a.src_rows = list(nd.src_list);
-    a.src2_rows = list(nd.src2_list);
+    if (nd.act != k::ACT_LSTM) a.src2_rows = list(nd.src2_list);
     a.res_rows = list(nd.res_list);
     a.dst_rows = list(nd.dst_list);
     if (a.src_rows || a.res_rows || a.dst_rows) a.list_rows = p->max_batch;
@@ -470,6 +509,14 @@ struct Run {
       launch(P_CONV, flops, bytes, [&] {
         if (!k::conv_rgb_stem(a, s)) throw HipError("stem with fused max-pool: arguments the kernel does not take");
       });
+      return;
+    }
+    if (nd.act == k::ACT_LSTM) {
+      // h and the embedding row in, bf16 h' and float32 c (in, out) per cell
+      const double H = nd.cout / 4.0;
+      const double bytes = static_cast<double>(n) * (2.0 * cin + 2.0 * H + 4.0 * H * (nd.cell_in >= 0 ? 2 : 1)) +
+                           2.0 * nd.cout * cin;
+      launch(P_CONV, flops, bytes, [&] { k::conv_bf16(a, s); });
       return;
     }
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
@@ -490,6 +537,7 @@ struct Run {
       case NodeKind::Gate: return "gate " + std::to_string(nd.index);
       case NodeKind::Halt: return "halt " + std::to_string(nd.index);
       case NodeKind::Output: return "output";
+      case NodeKind::Decode: return "decode " + std::to_string(nd.index);
     }
     return "";
   }
@@ -593,6 +641,57 @@ struct Run {
           rows = stay;
           break;
         }
+        case NodeKind::Decode: {
+          if (n <= 0) break;
+          // the step's logits (output layer, float32) ...
+          const Packed& q = sp.packed[nd.packed];
+          k::ConvArgs a{};
+          a.src = static_cast<const uint16_t*>(tp[nd.src]);
+          a.cin1 = a.cin = nd.cin1;
+          a.n = n;
+          a.H = a.W = a.Ho = a.Wo = 1;
+          a.cout = nd.cout;
+          a.k = a.stride = 1;
+          a.w = q.dev;
+          a.Kp = q.Kp;
+          a.shift = f32(nd.shift_off);
+          a.act = k::ACT_NONE;
+          a.dst = p->d_Z;
+          a.out_f32 = 1;
+          a.zeros = p->d_zeros;
+          a.ncount = rows.nc;
+          a.nhint = rows.hint;
+          launch(P_CONV, 2.0 * n * nd.cout * nd.cin1,
+                 2.0 * n * nd.cin1 + 4.0 * n * nd.cout + 2.0 * nd.cout * nd.cin1, [&] { k::conv_bf16(a, s); });
+          // ... then the token choice, the end test and the records
+          launch(P_HEAD, 0, 4.0 * n * nd.ncls + 16.0 * n, [&] {
+            k::decode_step(p->d_Z, n, nd.ncls, nd.eos, nd.index, nd.max_steps, orig, p->d_flags, p->d_tok[1], tokens,
+                           logits, rec, s, rows.nc);
+          });
+          if (nd.final_) {
+            if (device) {
+              launch(P_MISC, 0, 8.0, [&] { k::final_counts(rows.nc, n, p->d_counts + 2 * nd.decision, s); });
+            } else {
+              p->h_counts[2 * nd.decision] = n;
+              p->h_counts[2 * nd.decision + 1] = 0;
+            }
+            rows = {0, nullptr, 0};
+            break;
+          }
+          int32_t* next = p->d_orig[orig_next];
+          Rows done, stay;
+          compact(rows, nd.decision, next, done, stay);
+          if (stay.n > 0) {
+            // the continuing rows' tokens, in their new order, for the next step's embedding rows
+            launch(P_MOVE, 0, 12.0 * stay.n,
+                   [&] { k::gather_i32(p->d_tok[0], p->d_tok[1], p->d_idx0, stay.n, s, stay.nc); });
+            move_pairs(nd.pairs, nullptr, p->d_idx0, stay);
+          }
+          orig = next;
+          orig_next ^= 1;
+          rows = stay;
+          break;
+        }
         case NodeKind::Output: {
           const Packed& q = sp.packed[nd.packed];
           k::ConvArgs a{};
@@ -636,6 +735,11 @@ struct Run {
     orig = p->d_iota;
     launch(P_MISC, 0, 16.0 * B, [&] { k::init_records(rec, B, s); });
     if (sp.any_halt) launch(P_MISC, 0, 4.0 * B, [&] { k::fill_f32(p->d_S, 0.f, B, s); });
+    if (sp.any_decode) {
+      launch(P_MISC, 0, 4.0 * B * sp.max_len,
+             [&] { k::fill_i32(tokens, -1, static_cast<size_t>(B) * sp.max_len, s); });
+      launch(P_MISC, 0, 4.0 * B, [&] { k::fill_i32(p->d_tok[0], sp.bos, static_cast<size_t>(B), s); });
+    }
     if (sp.pad_input_c) {
       const TensorInfo& in = sp.tensors[sp.input];
       const size_t pix = static_cast<size_t>(B) * in.H * in.W;
@@ -659,7 +763,7 @@ void graph_reset(dycl_plan* p) {
 }  // namespace
 
 void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logits, dycl_record* rec,
-              hipStream_t s) {
+              int32_t* tokens, hipStream_t s) {
   Spec& sp = p->spec;
   hip_check(hipSetDevice(p->device), "hipSetDevice");
   p->last_stream = s;
@@ -674,6 +778,7 @@ void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logit
   r.aux = aux;
   r.logits = logits;
   r.rec = rec;
+  r.tokens = tokens;
   r.B = B;
   r.device = p->mode != DYCL_HOST_SYNC;
   p->counts_on_device = r.device;
@@ -710,10 +815,10 @@ void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logit
     }
     return;
   }
-  const dycl_plan::GraphKey key{x, B, aux, logits, rec};
+  const dycl_plan::GraphKey key{x, B, aux, logits, rec, tokens};
   const dycl_plan::GraphKey& k0 = p->graph_key;
   if (!p->graph_exec || k0.x != key.x || k0.B != key.B || k0.aux != key.aux || k0.logits != key.logits ||
-      k0.rec != key.rec) {
+      k0.rec != key.rec || k0.tokens != key.tokens) {
     graph_reset(p);
     if (!p->cap_stream) hip_check(hipStreamCreateWithFlags(&p->cap_stream, hipStreamNonBlocking), "hipStreamCreate");
     // the capture stream only records: nothing runs on it

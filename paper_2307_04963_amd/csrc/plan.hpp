@@ -35,11 +35,12 @@ struct TensorInfo {
   bool parked = false;     // full batch, original sample order
   int first = -1, last = -1;   // liveness (node sequence numbers)
   bool unused = false;     // never materialised (its readers go through a row list)
+  bool f32 = false;        // float32 in a bf16 spec (an LSTM cell state)
   int buf = -1;
-  size_t row_bytes(DType dt) const { return (size_t)H * W * C * (dt == DType::BF16 ? 2 : 4); }
+  size_t row_bytes(DType dt) const { return (size_t)H * W * C * (dt == DType::BF16 && !f32 ? 2 : 4); }
 };
 
-enum class NodeKind { Conv, MaxPool, Exit, Gate, Halt, Output };
+enum class NodeKind { Conv, MaxPool, Exit, Gate, Halt, Output, Decode };
 
 struct Node {
   NodeKind kind = NodeKind::Conv;
@@ -63,6 +64,17 @@ struct Node {
   // scale 1 and W_c zero for a channel whose scale is 0)
   int64_t scale2_off = -1, shift2_off = -1;
   int s2 = 1;            // src2 is read at this stride (a folded strided projection)
+  // an LSTM step (act ACT_LSTM): the concatenated input is a row of the
+  // embedding table in the blob (emb_off, emb_rows rows of cin2 values)
+  // chosen by each row's previous token; cell_in / cell_out are the
+  // float32 cell states (cell_in -1: zeros); the gate weight rows and the
+  // bias are interleaved per cell at plan creation (lstm_shift vector)
+  int64_t emb_off = -1;
+  int emb_rows = 0;
+  int cell_in = -1, cell_out = -1;
+  int lstm_shift = -1;
+  // decode (greedy token choice): eos token, step (index), max_len (max_steps)
+  int eos = 0;
   bool fold = false;
   int fold_shift = -1;
   // fused gathers / scatters: which row list of the last decision maps this
@@ -89,6 +101,7 @@ struct Node {
 struct Packed {
   int64_t w_off, w_ldk, w_k0;
   int cout, K, cout_pad, Kp;
+  bool interleave4 = false;   // packed row co = stored row (co % 4) * (cout / 4) + co / 4 (LSTM gates per cell)
   // taps x cin_src weights per output channel in the blob, stored as
   // taps x cin_pack (zero-filled) when the input channels are padded
   int taps = 1, cin_src = 0, cin_pack = 0;
@@ -126,6 +139,9 @@ struct Spec {
   int fused_pools = 0;     // max-pools fused into the stem convolution that feeds them
   int fused_projections = 0;   // 1x1 projection shortcuts folded into the block's last 1x1 convolution
   int n_fold_shift = 0;        // constant vectors of the folded projections
+  int n_lstm_shift = 0;        // interleaved biases of the LSTM steps
+  bool any_decode = false;     // a greedy decoding loop: runs emit tokens
+  int max_len = 0, bos = 0;    // its length bound and start token
   int n_head_t = 0;      // fp32 weight matrices kept transposed on the device   // > 0: the input is zero-padded to this many channels for the stem
   std::string summary;
   const uint8_t* host_w = nullptr;   // the host weight blob during parse, when given
@@ -169,6 +185,8 @@ struct dycl_plan {
   uint16_t* d_xpad = nullptr;    // input padded to 8 channels (stems with Cin < 8)
   std::vector<float*> head_t;    // transposed fp32 weights: exit heads [C][ncls], fp32 linears [cin][cout]
   std::vector<float*> fold_shift;   // folded projections: [scale | shift | s_p | b_p | 1 / scale] of 5 x cout
+  std::vector<float*> lstm_shift;   // LSTM steps: the gate bias, interleaved per cell
+  int32_t* d_tok[2] = {nullptr, nullptr};   // decoding: [0] the current rows' previous tokens, [1] this step's
   size_t workspace_bytes = 0, weight_bytes = 0;
   // profiling
   bool profile = false;
@@ -200,6 +218,7 @@ struct dycl_plan {
     const float* aux = nullptr;
     float* logits = nullptr;
     dycl_record* rec = nullptr;
+    int32_t* tokens = nullptr;
   } graph_key;
   long graph_captures = 0;
   // device modes: the branch counts of an earlier run, copied back without a
@@ -216,7 +235,7 @@ namespace dycl {
 int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_t weights_bytes);
 void plan_free(dycl_plan* p);
 void plan_run(dycl_plan* p, const void* x, int B, const float* aux, float* logits, dycl_record* rec,
-              hipStream_t s);
+              int32_t* tokens, hipStream_t s);
 void profile_flush(dycl_plan* p);
 // host mode (a dycl_host_mode value, already validated); drops a captured graph
 void plan_set_mode(dycl_plan* p, int mode);

@@ -78,6 +78,8 @@ struct Builder {
     if (a == "none") return k::ACT_NONE;
     if (a == "relu") return k::ACT_RELU;
     if (a == "gelu") return k::ACT_GELU;
+    if (a == "tanh") return k::ACT_TANH;
+    if (a == "lstm") return k::ACT_LSTM;
     fail("unknown activation '" + a + "'");
   }
 
@@ -89,12 +91,12 @@ struct Builder {
   }
 
   int pack_index(int64_t off, int64_t ldk, int64_t k0, int cout, int K, int taps = 1, int cin_src = 0,
-                 int cin_pack = 0) {
+                 int cin_pack = 0, bool interleave4 = false) {
     if (cin_src == 0) cin_src = cin_pack = K;   // one run of K values
     for (size_t i = 0; i < sp.packed.size(); ++i) {
       const Packed& q = sp.packed[i];
       if (q.w_off == off && q.w_ldk == ldk && q.w_k0 == k0 && q.cout == cout && q.K == taps * cin_pack &&
-          q.cin_src == cin_src && q.cin_pack == cin_pack)
+          q.cin_src == cin_src && q.cin_pack == cin_pack && q.interleave4 == interleave4)
         return static_cast<int>(i);
     }
     Packed q;
@@ -108,11 +110,99 @@ struct Builder {
     q.cin_pack = cin_pack;
     q.cout_pad = k::conv_cout_pad(cout);
     q.Kp = (q.K + k::kBK - 1) / k::kBK * k::kBK;
+    q.interleave4 = interleave4;
     sp.packed.push_back(q);
     return static_cast<int>(sp.packed.size()) - 1;
   }
 
+  // An LSTM step: h' and the float32 cell state c' from h, c and the
+  // embedding of each row's previous token (Table 1's En-Decoder cell).
+  Node lstm_conv(const Json& n) {
+    Node nd;
+    nd.kind = NodeKind::Conv;
+    nd.seq_pre = nd.seq_post = sp.seq++;
+    if (sp.dt != DType::BF16 || !sp.any_decode) fail("an lstm step needs a bf16 spec with a decode section");
+    if (in_body) fail("an lstm step inside a gate body is not supported");
+    nd.src = use(n.at("src"), "lstm.src", nd.seq_pre);
+    const TensorInfo src = sp.tensors[nd.src];
+    if (src.H != 1 || src.W != 1 || src.f32) fail("lstm.src must be a bf16 1x1 row");
+    nd.cin1 = src.C;
+    nd.cout = static_cast<int>(n.at("cout").as_int("cout"));
+    if (nd.cout != 4 * src.C || src.C % 8) fail("lstm.cout must be 4 x the hidden size, a multiple of 8");
+    const Json& e = n.at("emb");
+    nd.emb_off = e.at("off").as_int("emb.off");
+    nd.emb_rows = static_cast<int>(e.at("rows").as_int("emb.rows"));
+    nd.cin2 = static_cast<int>(e.at("dim").as_int("emb.dim"));
+    if (nd.emb_rows < 1 || nd.cin2 < 8 || nd.cin2 % 8) fail("lstm.emb: rows >= 1, dim a multiple of 8");
+    if (nd.emb_rows < sp.n_out) fail("lstm.emb: every token of the vocabulary needs a row");
+    need_bytes(nd.emb_off, static_cast<int64_t>(nd.emb_rows) * nd.cin2 * 2, 16, "lstm.emb");
+    nd.act = k::ACT_LSTM;
+    nd.H = nd.W = nd.Ho = nd.Wo = 1;
+    const int K = nd.cin1 + nd.cin2;
+    const Json& w = n.at("w");
+    nd.w_off = w.at("off").as_int("w.off");
+    nd.w_ldk = w.get_int("ldk", K);
+    nd.w_k0 = w.get_int("k0", 0);
+    if (nd.w_k0 < 0 || nd.w_k0 + K > nd.w_ldk) fail("lstm.w: column range [k0, k0+K) exceeds ldk");
+    need_bytes(nd.w_off, ((int64_t)(nd.cout - 1) * nd.w_ldk + nd.w_k0 + K) * 2, 2, "lstm.w");
+    nd.shift_off = f32_vec(n, "shift", nd.cout);
+    nd.lstm_shift = sp.n_lstm_shift++;
+    nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, K, 1, 0, 0, true);
+    if (n.has("cell_in") && !n.at("cell_in").is_null()) {
+      nd.cell_in = use(n.at("cell_in"), "lstm.cell_in", nd.seq_pre);
+      const TensorInfo& ci = sp.tensors[nd.cell_in];
+      if (!ci.f32 || ci.C != src.C) fail("lstm.cell_in must be a float32 cell state of the hidden size");
+    }
+    nd.dst = define(n.at("dst"), 1, 1, src.C, nd.seq_pre, "lstm.dst");
+    nd.cell_out = define(n.at("cell_out"), 1, 1, src.C, nd.seq_pre, "lstm.cell_out");
+    sp.tensors[nd.cell_out].f32 = true;
+    return nd;
+  }
+
+  // Greedy token choice (a logic node): the output layer's float32 logits,
+  // argmax, and the end-token / length test that partitions the rows.
+  Node decode_node(const Json& n) {
+    Node nd;
+    nd.kind = NodeKind::Decode;
+    nd.seq_pre = nd.seq_post = sp.seq++;
+    if (in_body) fail("decode inside a gate body is not supported");
+    if (sp.dt != DType::BF16 || !sp.any_decode) fail("decode needs a bf16 spec with a decode section");
+    nd.src = use(n.at("src"), "decode.src", nd.seq_pre);
+    const TensorInfo s = sp.tensors[nd.src];
+    if (s.H != 1 || s.W != 1 || s.f32 || s.C % 8) fail("decode.src must be a bf16 1x1 row of channels divisible by 8");
+    nd.cin1 = s.C;
+    nd.cout = nd.ncls = sp.n_out;
+    if (nd.ncls % 4) fail("decode: the vocabulary (n_out) must be a multiple of 4");
+    const Json& w = n.at("w");
+    nd.w_off = w.at("off").as_int("w.off");
+    nd.w_ldk = w.get_int("ldk", s.C);
+    nd.w_k0 = w.get_int("k0", 0);
+    if (nd.w_k0 < 0 || nd.w_k0 + s.C > nd.w_ldk) fail("decode.w: column range exceeds ldk");
+    need_bytes(nd.w_off, ((int64_t)(nd.cout - 1) * nd.w_ldk + nd.w_k0 + s.C) * 2, 2, "decode.w");
+    nd.shift_off = f32_vec(n, "b", nd.cout);
+    nd.packed = pack_index(nd.w_off, nd.w_ldk, nd.w_k0, nd.cout, s.C);
+    nd.eos = static_cast<int>(n.at("eos").as_int("eos"));
+    if (nd.eos < 0 || nd.eos >= sp.n_out) fail("decode.eos must be a token of the vocabulary");
+    nd.index = static_cast<int>(n.at("step").as_int("step"));
+    nd.max_steps = sp.max_len;
+    if (nd.index < 1 || nd.index > sp.max_len) fail("decode.step must be in [1, max_len]");
+    nd.final_ = nd.index == sp.max_len;
+    nd.decision = sp.decisions++;
+    sp.max_ncls = std::max(sp.max_ncls, nd.ncls);
+    if (!nd.final_) {
+      int old = space;
+      space = next_space++;
+      carry(n, "carry", nd, old);
+      space = next_space - 1;
+    } else {
+      if (n.has("carry") && n.at("carry").size()) fail("the last decoding step carries nothing");
+      space = next_space++;   // no rows remain
+    }
+    return nd;
+  }
+
   Node conv(const Json& n, int max_batch) {
+    if (n.get_str("act", "none") == "lstm") return lstm_conv(n);
     Node nd;
     nd.kind = NodeKind::Conv;
     nd.seq_pre = nd.seq_post = sp.seq++;
@@ -156,9 +246,14 @@ struct Builder {
       const TensorInfo& r = sp.tensors[nd.res];
       if (r.H != nd.Ho || r.W != nd.Wo || r.C != nd.cout) fail("conv.res: shape differs from the output");
     }
+    if (nd.act == k::ACT_TANH && (nd.k != 1 || nd.H != 1 || nd.W != 1 || nd.res >= 0 || nd.cout % 8 ||
+                                  sp.dt != DType::BF16))
+      fail("tanh is taken by bf16 linear layers on 1x1 rows (cout a multiple of 8, no residual)");
+    if (sp.tensors[nd.src].f32 || (nd.src2 >= 0 && sp.tensors[nd.src2].f32))
+      fail("conv: a float32 cell state is read only by an lstm step");
     if (sp.dt == DType::F32) {
       if (nd.k != 1 || nd.H != 1 || nd.W != 1 || nd.src2 >= 0 || nd.res >= 0 || nd.scale_off >= 0 ||
-          nd.act == k::ACT_GELU)
+          nd.act == k::ACT_GELU || nd.act == k::ACT_TANH)
         fail("fp32 specs support only linear layers (k 1 on 1x1 rows, bias, ReLU)");
       if (nd.w_k0 != 0 || nd.w_ldk != K) fail("fp32 linear weights must be dense [cout][cin]");
       nd.head_t = sp.n_head_t++;   // kept transposed on the device
@@ -213,6 +308,7 @@ struct Builder {
       space = next_space - 1;   // the new row space of the surviving rows
       const TensorInfo ot = sp.tensors[o];
       int nw = define(pr.at(1), ot.H, ot.W, ot.C, nd.seq_pre, key);
+      sp.tensors[nw].f32 = ot.f32;
       nd.pairs.push_back({o, nw});
     }
   }
@@ -385,6 +481,7 @@ struct Builder {
     if (op == "gate") return gate_node(n, max_batch);
     if (op == "halt") return halt_node(n);
     if (op == "output") return output_node(n);
+    if (op == "decode") return decode_node(n);
     fail("unknown node op '" + op + "'");
   }
 };
@@ -405,7 +502,7 @@ void uses_of(std::vector<Node>& nodes, int t, long top, std::vector<Use>& out) {
   for (size_t i = 0; i < nodes.size(); ++i) {
     Node& nd = nodes[i];
     const long at = top < 0 ? static_cast<long>(i) : -1;
-    bool other = nd.src2 == t || nd.res == t || nd.park_src == t;
+    bool other = nd.src2 == t || nd.res == t || nd.park_src == t || nd.cell_in == t;
     for (auto& pr : nd.pairs) other = other || pr.first == t;
     for (auto& pr : nd.scatter) other = other || pr.first == t;
     if (nd.src == t) out.push_back({&nd, nd.kind == NodeKind::Conv, at});
@@ -415,7 +512,8 @@ void uses_of(std::vector<Node>& nodes, int t, long top, std::vector<Use>& out) {
 }
 
 bool is_decision(const Node& nd) {
-  return nd.kind == NodeKind::Exit || nd.kind == NodeKind::Gate || nd.kind == NodeKind::Halt;
+  return nd.kind == NodeKind::Exit || nd.kind == NodeKind::Gate || nd.kind == NodeKind::Halt ||
+         nd.kind == NodeKind::Decode;
 }
 
 }  // namespace
@@ -534,7 +632,9 @@ void Spec::fuse_exit_gathers() {
   if (dt != DType::BF16) return;
   for (size_t i = 0; i < nodes.size(); ++i) {
     Node& ex = nodes[i];
-    if (!((ex.kind == NodeKind::Exit && !ex.final_) || ex.kind == NodeKind::Halt)) continue;
+    if (!((ex.kind == NodeKind::Exit && !ex.final_) || ex.kind == NodeKind::Halt ||
+          (ex.kind == NodeKind::Decode && !ex.final_)))
+      continue;
     size_t next = i + 1;
     while (next < nodes.size() && !is_decision(nodes[next])) ++next;
     for (size_t q = 0; q < ex.pairs.size();) {
@@ -720,6 +820,17 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch, c
   aux = j.get_bool("aux", false);
   if (max_batch < 1 || max_batch > (1 << 24)) throw SpecError("max_batch must be in [1, 2^24]");
 
+  if (j.has("decode") && !j.at("decode").is_null()) {
+    // a greedy decoding loop: runs emit up to max_len tokens per sample,
+    // the first step reading the start token bos
+    const Json& dj = j.at("decode");
+    any_decode = true;
+    max_len = static_cast<int>(dj.at("max_len").as_int("decode.max_len"));
+    bos = static_cast<int>(dj.at("bos").as_int("decode.bos"));
+    if (max_len < 1 || max_len > 4096) throw SpecError("decode.max_len must be in [1, 4096]");
+    if (bos < 0 || bos >= n_out) throw SpecError("decode.bos must be a token of the vocabulary (n_out)");
+    if (dt != DType::BF16) throw SpecError("decoding needs a bf16 spec");
+  }
   Builder b(*this, weights_bytes);
   const Json& in = j.at("input");
   const Json& shp = in.at("shape");

@@ -5,7 +5,8 @@ construction (Sec. 5.2-5.3, Alg. 1) for the network families used here:
 every loop is unrolled (the bounded loop of an adaptive-computation network
 becomes max_steps copies of its body), and the program is split into
 sub-DNN nodes (runs of convolutions / linear layers) and logic nodes (one
-conditional each: an exit test, a gate, a halting test).  The identity path
+conditional each: an exit test, a gate, a halting test, a decoder's token
+choice).  The identity path
 of a skipped block (Sec. 5.4, first strategy) needs no node at all: a
 skipped sample's row is left where it is.
 
@@ -135,13 +136,40 @@ class _Lower:
                            "cout": a["n_out"]})
 
 
+    def decoder(self):
+        # greedy decoding unrolled to max_len steps: each step an LSTM cell
+        # (a linear layer over [h; embedding of the previous token] whose
+        # epilogue is the cell) and a logic node choosing the token, whose
+        # end test moves finished rows out; h and the cell state are carried
+        a = self.arch
+        H, L = a["hidden"], a["max_len"]
+        self.nodes.append({"op": "conv", "src": "x", "dst": "h0", "k": 1, "cout": H, "act": "tanh",
+                           "w": {"off": self.off("enc.w")}, "shift": self.off("enc.b")})
+        h, c = "h0", None
+        for t in range(1, L + 1):
+            hn, cn = f"h{t}", f"c{t}"
+            self.nodes.append({"op": "conv", "act": "lstm", "src": h, "cell_in": c, "dst": hn, "cell_out": cn,
+                               "cout": 4 * H, "w": {"off": self.off("lstm.w")}, "shift": self.off("lstm.b"),
+                               "emb": {"off": self.off("emb"), "rows": a["vocab"], "dim": a["embed"]}})
+            node = {"op": "decode", "src": hn, "w": {"off": self.off("out.w")}, "b": self.off("out.b"),
+                    "eos": a["eos"], "step": t}
+            if t < L:
+                h, c = f"h{t}c", f"c{t}c"
+                node["carry"] = [[hn, h], [cn, c]]
+            self.nodes.append(node)
+
+
 def lower(arch: dict, manifest: dict) -> dict:
     """Spec dict for one architecture and its blob manifest."""
     L = _Lower(arch, manifest)
     fam = arch["family"]
-    {"early_exit_mlp": L.mlp, "early_exit_resnet": L.resnet_exit, "skipnet": L.skipnet, "act": L.act}[fam]()
-    return {"version": 1, "dtype": arch["dtype"], "input": {"name": "x", "shape": list(arch["input"])},
+    {"early_exit_mlp": L.mlp, "early_exit_resnet": L.resnet_exit, "skipnet": L.skipnet, "act": L.act,
+     "seq_decoder": L.decoder}[fam]()
+    spec = {"version": 1, "dtype": arch["dtype"], "input": {"name": "x", "shape": list(arch["input"])},
             "n_out": arch["n_out"], "aux": fam == "act", "nodes": L.nodes}
+    if fam == "seq_decoder":
+        spec["decode"] = {"max_len": arch["max_len"], "bos": arch["bos"]}
+    return spec
 
 
 def lower_json(arch: dict, manifest: dict) -> str:

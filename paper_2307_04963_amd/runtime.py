@@ -34,6 +34,7 @@ class Plan:
         self.n_out = int(info["n_out"])
         self.decisions = int(info["decisions"])
         self.aux = bool(info["aux"])
+        self.max_len = int(info.get("max_len", 0))   # tokens per sample (a decoding plan), else 0
 
     @classmethod
     def from_workload(cls, wl, max_batch: int, device: int = 0):
@@ -53,7 +54,7 @@ class Plan:
 
     def info(self) -> dict:
         keys = ["n_out", "in_bytes", "decisions", "workspace_bytes", "weight_bytes", "max_batch", "aux", "nodes",
-                "host_mode", "graph_captures"]
+                "host_mode", "graph_captures", "max_len"]
         buf = (C.c_int64 * len(keys))()
         n = check(lib.dycl_plan_info(self._h, buf, len(keys)))
         return {k: int(buf[i]) for i, k in enumerate(keys[:n])}
@@ -67,15 +68,27 @@ class Plan:
         prev = check(lib.dycl_plan_set_host_mode(self._h, HOST_MODES[mode]))
         return {v: k for k, v in HOST_MODES.items()}[prev]
 
-    def run(self, x: torch.Tensor, aux, logits: torch.Tensor, records: torch.Tensor, stream=None):
-        """x, aux, logits (fp32 [B, n_out]) and records (int32 [B, 4]) are device tensors."""
+    def run(self, x: torch.Tensor, aux, logits: torch.Tensor, records: torch.Tensor, stream=None, tokens=None):
+        """x, aux, logits (fp32 [B, n_out]) and records (int32 [B, 4]) are
+        device tensors; a decoding plan also takes tokens (int32 [B, max_len])."""
         B = x.shape[0]
         if stream is None:
             stream = torch.cuda.current_stream(x.device)
-        check(lib.dycl_run(self._h, C.c_void_p(x.data_ptr()), int(B),
-                           C.c_void_p(aux.data_ptr()) if aux is not None else None,
-                           C.c_void_p(logits.data_ptr()), C.c_void_p(records.data_ptr()),
-                           C.c_void_p(stream.cuda_stream)))
+        args = [self._h, C.c_void_p(x.data_ptr()), int(B), C.c_void_p(aux.data_ptr()) if aux is not None else None,
+                C.c_void_p(logits.data_ptr()), C.c_void_p(records.data_ptr())]
+        if self.max_len:
+            check(lib.dycl_run_seq(*args, C.c_void_p(tokens.data_ptr()) if tokens is not None else None,
+                                   C.c_void_p(stream.cuda_stream)))
+        else:
+            check(lib.dycl_run(*args, C.c_void_p(stream.cuda_stream)))
+
+    def outputs(self, B: int, device="cuda"):
+        """Fresh (logits, records, tokens) device tensors for a batch of B
+        (tokens None for a plan that emits none)."""
+        logits = torch.full((max(B, 1), self.n_out), float("nan"), dtype=torch.float32, device=device)
+        rec = torch.zeros((max(B, 1), 4), dtype=torch.int32, device=device)
+        tok = torch.zeros((max(B, 1), self.max_len), dtype=torch.int32, device=device) if self.max_len else None
+        return logits, rec, tok
 
     def counts(self):
         buf = (C.c_int32 * (2 * max(1, self.decisions)))()
@@ -127,13 +140,15 @@ def run_numpy(plan: Plan, wl, x: np.ndarray, aux=None, device="cuda"):
     """Run host arrays through the plan; returns a dict like the oracle's."""
     B = x.shape[0]
     xt, at = device_inputs(wl, x, aux, device)
-    logits = torch.full((max(B, 1), plan.n_out), float("nan"), dtype=torch.float32, device=device)
-    rec = torch.zeros((max(B, 1), 4), dtype=torch.int32, device=device)
-    plan.run(xt, at, logits, rec)
+    logits, rec, tok = plan.outputs(B, device)
+    plan.run(xt, at, logits, rec, tokens=tok)
     torch.cuda.synchronize()
     ex, it, sk = decode_records(rec[:B].cpu().numpy())
-    return {"logits": logits[:B].cpu().numpy(), "exit_index": ex, "iterations": it, "skip_mask": sk,
-            "counts": plan.counts()}
+    out = {"logits": logits[:B].cpu().numpy(), "exit_index": ex, "iterations": it, "skip_mask": sk,
+           "counts": plan.counts()}
+    if tok is not None:
+        out["tokens"] = tok[:B].cpu().numpy()
+    return out
 
 
 def pack_conv_weights(w_bits: np.ndarray) -> np.ndarray:

@@ -67,14 +67,15 @@ def test_every_workload_spec_validates(name):
     rc, msg = _check(json.dumps(spec), len(blob), configs.DEFAULT_BATCH[name])
     assert rc == 0, msg
     decisions = int(re.search(r"decisions=(\d+)", msg).group(1))
-    want = {"mlp_exit": 3, "resnet18_exit": 4, "skipnet38": 19, "resnet50_exit": 4, "act_loop": 16}[name]
+    want = {"mlp_exit": 3, "resnet18_exit": 4, "skipnet38": 19, "resnet50_exit": 4, "act_loop": 16,
+            "lstm_decoder": 24}[name]
     assert decisions == want
     # row moves fused into the convolutions: exit carries read in place, gate
     # gathers / scatters of bodies that run on the implicit GEMM
     fg = int(re.search(r"fused_gathers=(\d+)", msg).group(1))
     fgt = int(re.search(r"fused_gates=(\d+)", msg).group(1))
     assert (fg, fgt) == {"mlp_exit": (0, 0), "resnet18_exit": (3, 0), "skipnet38": (0, 18),
-                         "resnet50_exit": (3, 0), "act_loop": (30, 0)}[name]
+                         "resnet50_exit": (3, 0), "act_loop": (30, 0), "lstm_decoder": (23, 0)}[name]
     # the ImageNet stem's max-pool runs in the stem kernel's epilogue
     fp = int(re.search(r"fused_pools=(\d+)", msg).group(1))
     assert fp == (1 if name == "resnet50_exit" else 0)

@@ -11,8 +11,8 @@ from oracle import dycl_oracle as O
 from tests._parity import load_golden
 from workloads import configs
 
-CASES = ([(n, False) for n in configs.NAMES] + [("lstm_decoder", False)] * ("lstm_decoder" not in configs.NAMES)
-         + [(n, True) for n in ("mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit")])
+CASES = [(n, False) for n in configs.NAMES] + [(n, True) for n in
+                                                ("mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit")]
 
 
 @pytest.mark.parametrize("name,literal", CASES)

@@ -21,7 +21,8 @@ from workloads import configs
 
 pytestmark = pytest.mark.gpu
 
-SMALL = {"mlp_exit": 37, "resnet18_exit": 37, "skipnet38": 45, "resnet50_exit": 5, "act_loop": 300}
+SMALL = {"mlp_exit": 37, "resnet18_exit": 37, "skipnet38": 45, "resnet50_exit": 5, "act_loop": 300,
+         "lstm_decoder": 77}
 
 _cache = {}
 

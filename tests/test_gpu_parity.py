@@ -28,7 +28,8 @@ from workloads import configs
 
 pytestmark = pytest.mark.gpu
 
-SMALL = {"mlp_exit": 37, "resnet18_exit": 37, "skipnet38": 45, "resnet50_exit": 5, "act_loop": 300}
+SMALL = {"mlp_exit": 37, "resnet18_exit": 37, "skipnet38": 45, "resnet50_exit": 5, "act_loop": 300,
+         "lstm_decoder": 77}
 LITERAL = ["mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit"]
 
 _cache = {}
@@ -62,9 +63,13 @@ def _check_counts(wl, gpu):
             bits = (gpu["skip_mask"] >> np.uint64(i)) & np.uint64(1)
             assert run == int((bits == 0).sum()) and skip == int((bits == 1).sum())
     else:
+        bound = wl.arch["max_steps"] if fam == "act" else wl.arch["max_len"]
         for t, (halt, stay) in enumerate(counts):
             assert halt == int((gpu["iterations"] == t + 1).sum())
-        assert gpu["iterations"].min() >= 1 and gpu["iterations"].max() <= wl.arch["max_steps"]
+        assert gpu["iterations"].min() >= 1 and gpu["iterations"].max() <= bound
+        if fam == "seq_decoder":   # tokens up to each sample's length, -1 after it
+            L = np.arange(bound)[None, :]
+            assert ((gpu["tokens"] >= 0) == (L < gpu["iterations"][:, None])).all()
 
 
 @pytest.mark.parametrize("name", configs.NAMES)
@@ -190,3 +195,32 @@ def test_forced_halting_act(bias, steps):
     ref = O.from_workload(wl).run(wl.inputs_f32(70)[0][:8], aux[:8])
     rep = compare(wl, {k: v[:8] for k, v in gpu.items() if k != "counts"}, ref)
     assert rep["ok"], rep
+
+
+@pytest.mark.parametrize("shift,length", [(1e4, 1), (-1e4, 24)])
+def test_forced_end_token_decoder(shift, length):
+    # the end token always / never the most likely: every sequence is one
+    # token long / runs to the length bound, in every host mode
+    rt = _rt()
+    wl = configs.build("lstm_decoder")
+    b = wl.tensors["out.b"]
+    v = b.value.copy()
+    v[wl.arch["eos"]] += np.float32(shift)
+    wl.tensors["out.b"] = configs.Tensor(b.name, b.dtype, b.shape, v)
+    _, plan = _plan("lstm_decoder", wl, 64)
+    x, _ = wl.inputs(40)
+    ref = oracle_ref(wl, *wl.inputs_f32(40))
+    for mode in ("sync", "device", "graph"):
+        print(f"[decoder-forced] shift={shift} mode={mode}", flush=True)
+        plan.set_host_mode(mode)
+        try:
+            gpu = rt.run_numpy(plan, wl, x)
+        finally:
+            plan.set_host_mode("sync")
+        assert (gpu["iterations"] == length).all()
+        if length == 1:
+            assert (gpu["tokens"][:, 0] == wl.arch["eos"]).all() and (gpu["tokens"][:, 1:] == -1).all()
+        else:
+            assert (gpu["tokens"] != wl.arch["eos"]).all() and (gpu["tokens"] >= 0).all()
+        rep = compare(wl, gpu, ref)
+        assert rep["ok"], rep

@@ -57,10 +57,10 @@ def test_kaiming_bounds_and_bf16_bytes():
 
 
 def test_stored_calibration_and_floor_files():
-    for name in ("mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit"):
+    for name in ("mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit", "lstm_decoder"):
         assert configs.build(name).calibrated
     with open(os.path.join(ROOT, "tests", "golden", "decision_floor.json")) as f:
         fl = json.load(f)
-    for name in configs.NAMES:
+    for name in ("mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit", "act_loop"):
         assert fl[name]["routing_diverged"] == 0
         assert all(v >= 0 for v in fl[name]["floor"])

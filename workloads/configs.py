@@ -11,6 +11,8 @@ from the counter-based generator in ``rng``:
   skipnet38     SkipNet-style ResNet-38, bf16, 18 gated basic blocks
   resnet50_exit early-exit ResNet-50-style bottleneck CNN, bf16, 224x224
   act_loop      adaptive-computation-time loop, bf16, hidden 1024, <=16 steps
+  lstm_decoder  greedy LSTM decoder, bf16, hidden 512, vocabulary 4096,
+                <=24 tokens (a generative network: Table 1's En-Decoder)
 
 This module holds no part of the executed method.  Parameters that have to
 be calibrated on the network itself (folded BatchNorm statistics, exit-head
@@ -36,7 +38,7 @@ SEED = 0
 CALIB_DIR = os.path.join(os.path.dirname(os.path.abspath(__file__)), "calib")
 BN_EPS = 1e-5
 
-NAMES = ["mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit", "act_loop"]
+NAMES = ["mlp_exit", "resnet18_exit", "skipnet38", "resnet50_exit", "act_loop", "lstm_decoder"]
 DEFAULT_BATCH = {"mlp_exit": 64, "resnet18_exit": 1024, "skipnet38": 2048,
                  "resnet50_exit": 256, "act_loop": 4096, "lstm_decoder": 1024}
 
