@@ -297,7 +297,7 @@ def main():
     ap.add_argument("--copy-probe", action="store_true", help="only run the counter-scaling copy")
     ap.add_argument("--layers", action="store_true",
                     help="only the per-layer table: one profiled sync-mode step, every conv launch timed")
-    ap.add_argument("--host-mode", default="device", choices=["sync", "device", "graph"],
+    ap.add_argument("--host-mode", default="device", choices=["sync", "device", "graph", "persistent"],
                     help="host mode of the headline value (all three are timed)")
     args = ap.parse_args()
     if args.copy_probe:
@@ -342,7 +342,8 @@ def main():
         return e0.elapsed_time(e1) / args.steps, wall * 1e3 / args.steps, plan.counts()
 
     modes = {}
-    for mode in [m for m in ("sync", "device", "graph") if m != args.host_mode] + [args.host_mode]:
+    all_modes = ("sync", "device", "graph") + (("persistent",) if args.workload == "act_loop" else ())
+    for mode in [m for m in all_modes if m != args.host_mode] + [args.host_mode]:
         modes[mode] = timed(mode)
     ms, wall_ms, counts = modes[args.host_mode]
     assert all(m[2] == counts for m in modes.values()), "host modes disagree on the branch counts"

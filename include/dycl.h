@@ -133,11 +133,18 @@ int dycl_run_seq(dycl_plan* plan, const void* x_dev, int batch, const float* aux
  *                     batch size and the same x / aux / logits / records
  *                     pointers (any change re-captures).  While profiling is
  *                     enabled, runs are launched without the graph.
+ *   DYCL_HOST_PERSISTENT  DYCL_HOST_DEVICE, except that the bounded loop of an
+ *                     adaptive-computation-time network (Sec. 2.2) runs as one
+ *                     cooperative launch: every step's layer, halting test and
+ *                     compaction in one kernel, with grid-wide barriers between
+ *                     the phases of a step (max_batch <= 4096).  Bit for bit the
+ *                     same results; on MI355X the barriers across the 8 XCDs cost
+ *                     more than the per-step launches they replace.
  * Results are identical in every mode.  Returns the previous mode, or
  * DYCL_E_INVALID for an unknown mode.  Not to be called while a run of the
  * plan is being enqueued.
  */
-typedef enum { DYCL_HOST_SYNC = 0, DYCL_HOST_DEVICE = 1, DYCL_HOST_GRAPH = 2 } dycl_host_mode;
+typedef enum { DYCL_HOST_SYNC = 0, DYCL_HOST_DEVICE = 1, DYCL_HOST_GRAPH = 2, DYCL_HOST_PERSISTENT = 3 } dycl_host_mode;
 int dycl_plan_set_host_mode(dycl_plan* plan, int mode);
 
 /*

@@ -112,7 +112,7 @@ int dycl_run_seq(dycl_plan* plan, const void* x_dev, int batch, const float* aux
 
 int dycl_plan_set_host_mode(dycl_plan* plan, int mode) {
   if (!valid(plan)) return fail(DYCL_E_INVALID, "dycl_plan_set_host_mode: invalid plan handle");
-  if (mode != DYCL_HOST_SYNC && mode != DYCL_HOST_DEVICE && mode != DYCL_HOST_GRAPH)
+  if (mode != DYCL_HOST_SYNC && mode != DYCL_HOST_DEVICE && mode != DYCL_HOST_GRAPH && mode != DYCL_HOST_PERSISTENT)
     return fail(DYCL_E_INVALID, "dycl_plan_set_host_mode: unknown mode " + std::to_string(mode));
   const int prev = plan->mode;
   const int rc = guarded([&] {

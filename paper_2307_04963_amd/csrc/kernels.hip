@@ -5,6 +5,7 @@
 // branch each sample takes is then materialised by a stable compaction and
 // row gathers, so the next sub-network runs on a packed subset.
 #include "kernels.hpp"
+#include "halt_row.hpp"
 
 #include <mutex>
 
@@ -461,29 +462,9 @@ __global__ __launch_bounds__(64) void halt_kernel(const uint16_t* __restrict__ h
                                                   dycl_record* rec, const int32_t* nc, int n) {
   const int r = blockIdx.x, lane = threadIdx.x;
   if (r >= live(nc, n)) return;
-  const uint16_t* row = h + (size_t)r * C;
-  float d = 0.f;
-  for (int c = lane * 8; c < C; c += 64 * 8) {
-    const uint4 v = *reinterpret_cast<const uint4*>(row + c);
-    d = fmaf(__uint_as_float(v.x << 16), w[c + 0], d);
-    d = fmaf(__uint_as_float(v.x & 0xffff0000u), w[c + 1], d);
-    d = fmaf(__uint_as_float(v.y << 16), w[c + 2], d);
-    d = fmaf(__uint_as_float(v.y & 0xffff0000u), w[c + 3], d);
-    d = fmaf(__uint_as_float(v.z << 16), w[c + 4], d);
-    d = fmaf(__uint_as_float(v.z & 0xffff0000u), w[c + 5], d);
-    d = fmaf(__uint_as_float(v.w << 16), w[c + 6], d);
-    d = fmaf(__uint_as_float(v.w & 0xffff0000u), w[c + 7], d);
-  }
-  d = wave_sum(d);
-  if (lane == 0) {
-    const int o = orig ? orig[r] : r;
-    const float p = 1.0f / (1.0f + expf(-(d + aux[o])));
-    const float Sn = S[o] + p;
-    S[o] = Sn;
-    const bool stop = (Sn >= tau) || (step == max_steps);
-    flags[r] = stop ? 1 : 0;
-    if (stop) rec[o].iterations = step;
-  }
+  const int o = orig ? orig[r] : r;
+  const bool stop = halt_row(h + (size_t)r * C, C, w, aux[o], S, o, step, max_steps, tau, rec, lane);
+  if (lane == 0) flags[r] = stop ? 1 : 0;
 }
 
 void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux, const int32_t* orig, float* S,

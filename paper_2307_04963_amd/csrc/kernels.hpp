@@ -219,5 +219,36 @@ void decode_step(const float* Z, int n, int V, int eos, int step, int max_len, c
                  const int32_t* nc = nullptr);
 void iota_i32(int32_t* p, int n, hipStream_t s);
 
+// The bounded loop of an adaptive-computation-time network, every step in
+// one cooperative launch (one workgroup per CU, grid barriers between the
+// phases of a step): step t computes h_t = bf16(GELU(W1 [h_{t-1}; x] + b1))
+// for the running rows (step 1: the x columns only, h_0 = 0), the halting
+// unit (S += sigmoid(wh . h_t + aux), halt at S >= tau or t == steps),
+// parks the halted rows' h_t in sample order and compacts the running
+// rows.  Bit for bit what the per-step kernels compute.  Rows start in
+// sample order; B <= act_loop_max_rows().
+struct ActLoopArgs {
+  const uint16_t* x;   // [B][D] bf16
+  const uint16_t* w;   // packed W1 [>= H][Kp] bf16, K = [h | x] (H + D)
+  int Kp;
+  const float* b1;     // [H]
+  const float* wh;     // [H]
+  const float* aux;    // [B]
+  uint16_t* h0;        // two [B][H] bf16 state buffers
+  uint16_t* h1;
+  uint16_t* park;      // [B][H] bf16, sample order
+  float* S;            // [B], zero
+  uint8_t* flags;      // [B]
+  int32_t* counts;     // branch counts, decision d0 + t - 1 for step t
+  int d0;
+  dycl_record* rec;
+  const uint16_t* zeros;
+  int B, H, D, steps;
+  float tau;
+};
+size_t act_loop_max_rows();
+bool act_loop_fits(int B, int H, int D);
+void act_loop(const ActLoopArgs& a, hipStream_t s);
+
 }  // namespace k
 }  // namespace dycl

@@ -94,6 +94,61 @@ void assign_buffers(dycl_plan* p, int max_batch) {
   for (size_t b = 0; b < p->buffers.size(); ++b) p->buffers[b] = dev_alloc<uint8_t>(p, p->buffer_bytes[b], "activation buffer");
 }
 
+// The unrolled loop of an adaptive-computation-time network: for t = 1..T a
+// GELU linear layer h_t = GELU(W1 [h_{t-1}; x] + b1) (t = 1: the x columns
+// of W1 alone) and its halting test, the states parked into one tensor,
+// then the output layer.  Such a loop can run as one persistent launch.
+void detect_act_loop(dycl_plan* p) {
+  const Spec& sp = p->spec;
+  auto& L = p->act;
+  L = dycl_plan::ActLoop{};
+  const auto& nd = sp.nodes;
+  for (size_t i = 0; i + 2 < nd.size(); ++i) {
+    const Node& c1 = nd[i];
+    if (c1.kind != NodeKind::Conv || nd[i + 1].kind != NodeKind::Halt || c1.act != k::ACT_GELU || c1.src2 >= 0 ||
+        !sp.tensors[c1.src].external || c1.H != 1 || c1.W != 1 || c1.res >= 0 || c1.scale_off >= 0 ||
+        c1.src_list != 0)
+      continue;
+    const Node& h1 = nd[i + 1];
+    const int T = h1.max_steps, Hd = c1.cout, D = c1.cin1;
+    if (h1.index != 1 || T < 2 || i + 2 * static_cast<size_t>(T) >= nd.size() || c1.w_k0 != Hd ||
+        c1.w_ldk != Hd + D || h1.src != c1.dst)
+      continue;
+    bool ok = true;
+    int packed = -1;
+    for (int t = 1; t <= T && ok; ++t) {
+      const Node& c = nd[i + 2 * (t - 1)];
+      const Node& h = nd[i + 2 * (t - 1) + 1];
+      ok = c.kind == NodeKind::Conv && h.kind == NodeKind::Halt && c.act == k::ACT_GELU && c.cout == Hd &&
+           c.w_off == c1.w_off && c.shift_off == c1.shift_off && c.scale_off < 0 && c.res < 0 && c.H == 1 &&
+           c.W == 1 && !c.pad_in && c.dst_list == 0 && h.src == c.dst && h.index == t && h.max_steps == T &&
+           h.h_w == h1.h_w && h.tau == h1.tau && h.park_dst == h1.park_dst && h.park_src == c.dst &&
+           h.decision == h1.decision + t - 1 && h.hc == Hd;
+      if (ok && t > 1)
+        ok = c.src_list == 1 && c.cin1 == Hd && c.src2 == c1.src && c.src2_list == 3 && c.cin2 == D &&
+             c.w_k0 == 0 && c.w_ldk == Hd + D && (packed < 0 || packed == c.packed);
+      if (ok && t > 1) packed = c.packed;
+    }
+    const size_t end = i + 2 * static_cast<size_t>(T);
+    if (!ok || packed < 0 || nd[end].kind != NodeKind::Output || nd[end].src != h1.park_dst) continue;
+    if (!k::act_loop_fits(p->max_batch, Hd, D)) return;
+    L.ok = true;
+    L.begin = i;
+    L.end = end;
+    L.packed = packed;
+    L.hidden = Hd;
+    L.d_in = D;
+    L.steps = T;
+    L.d0 = h1.decision;
+    L.park = h1.park_dst;
+    L.input = c1.src;
+    L.b1 = c1.shift_off;
+    L.wh = h1.h_w;
+    L.tau = h1.tau;
+    return;
+  }
+}
+
 }  // namespace
 
 int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_t weights_bytes) {
@@ -210,6 +265,11 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
 
   assign_buffers(p, p->max_batch);
   const int B = p->max_batch;
+  detect_act_loop(p);
+  if (p->act.ok) {
+    p->act.h[0] = dev_alloc<uint16_t>(p, static_cast<size_t>(B) * p->act.hidden, "persistent loop state");
+    p->act.h[1] = dev_alloc<uint16_t>(p, static_cast<size_t>(B) * p->act.hidden, "persistent loop state");
+  }
   p->d_flags = dev_alloc<uint8_t>(p, B, "flags");
   p->d_idx1 = dev_alloc<int32_t>(p, B, "idx1");
   p->d_org1 = dev_alloc<int32_t>(p, B, "org1");
@@ -304,7 +364,8 @@ void plan_free(dycl_plan* p) {
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
                      p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S, p->d_zeros,
-                     p->d_xpad, p->d_cws, p->d_Gpart, p->d_split, p->d_tok[0], p->d_tok[1]};
+                     p->d_xpad, p->d_cws, p->d_Gpart, p->d_split, p->d_tok[0], p->d_tok[1], p->act.h[0],
+                     p->act.h[1]};
   for (void* s : singles)
     if (s) hipFree(s);
   if (p->h_counts) hipHostFree(p->h_counts);
@@ -542,9 +603,54 @@ struct Run {
     return "";
   }
 
-  void exec(const std::vector<Node>& nodes, Rows& rows) {
+  void exec(const std::vector<Node>& nodes, Rows& rows) { exec_range(nodes, 0, nodes.size(), rows); }
+
+  // the persistent launch of an adaptive-computation-time loop (device
+  // host mode): every step of nodes [act.begin, act.end) in one kernel
+  void act_loop() {
+    const Spec& sp = p->spec;
+    const auto& L = p->act;
+    const Packed& q = sp.packed[L.packed];
+    k::ActLoopArgs a;
+    a.x = static_cast<const uint16_t*>(tp[L.input]);
+    a.w = q.dev;
+    a.Kp = q.Kp;
+    a.b1 = f32(L.b1);
+    a.wh = f32(L.wh);
+    a.aux = aux;
+    a.h0 = L.h[0];
+    a.h1 = L.h[1];
+    a.park = static_cast<uint16_t*>(tp[L.park]);
+    a.S = p->d_S;
+    a.flags = p->d_flags;
+    a.counts = p->d_counts;
+    a.d0 = L.d0;
+    a.rec = rec;
+    a.zeros = p->d_zeros;
+    a.B = B;
+    a.H = L.hidden;
+    a.D = L.d_in;
+    a.steps = L.steps;
+    a.tau = L.tau;
+    // work bound: every row for every step (the live rows are on the device)
+    const double flops = 2.0 * B * L.hidden * (L.d_in + (L.steps - 1.0) * (L.hidden + L.d_in));
+    const double bytes = 2.0 * B * (L.d_in + 2.0 * L.steps * L.hidden) + 2.0 * L.hidden * (L.hidden + L.d_in);
+    launch(P_CONV, flops, bytes, [&] { k::act_loop(a, s); });
+  }
+
+  void exec_range(const std::vector<Node>& nodes, size_t first, size_t last, Rows& rows) {
     Spec& sp = p->spec;
-    for (const Node& nd : nodes) {
+    for (size_t ni = first; ni < last; ++ni) {
+      const Node& nd = nodes[ni];
+      // the persistent host mode runs the loop in one launch; the others
+      // launch its steps one by one
+      if (&nodes == &sp.nodes && p->act.ok && p->mode == DYCL_HOST_PERSISTENT && ni == p->act.begin) {
+        if (p->profile) label = "act loop (persistent)";
+        act_loop();
+        rows = {0, nullptr, 0};   // every row halted
+        ni = p->act.end - 1;
+        continue;
+      }
       const int n = rows.n;
       if (p->profile) label = node_label(nd);
       switch (nd.kind) {

@@ -187,6 +187,17 @@ struct dycl_plan {
   std::vector<float*> fold_shift;   // folded projections: [scale | shift | s_p | b_p | 1 / scale] of 5 x cout
   std::vector<float*> lstm_shift;   // LSTM steps: the gate bias, interleaved per cell
   int32_t* d_tok[2] = {nullptr, nullptr};   // decoding: [0] the current rows' previous tokens, [1] this step's
+  // an adaptive-computation-time loop run as one persistent launch in the
+  // device host mode: top-level nodes [begin, end) (the unrolled steps'
+  // convolutions and halting tests), the Output node at `end`
+  struct ActLoop {
+    bool ok = false;
+    size_t begin = 0, end = 0;
+    int packed = -1, hidden = 0, d_in = 0, steps = 0, d0 = 0, park = -1, input = -1;
+    int64_t b1 = -1, wh = -1;
+    float tau = 0.f;
+    uint16_t* h[2] = {nullptr, nullptr};
+  } act;
   size_t workspace_bytes = 0, weight_bytes = 0;
   // profiling
   bool profile = false;

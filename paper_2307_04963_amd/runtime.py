@@ -19,7 +19,7 @@ check = _lib.check
 lib = _lib.lib
 
 
-HOST_MODES = {"sync": 0, "device": 1, "graph": 2}
+HOST_MODES = {"sync": 0, "device": 1, "graph": 2, "persistent": 3}
 
 
 class Plan:
@@ -61,8 +61,10 @@ class Plan:
 
     def set_host_mode(self, mode: str) -> str:
         """'sync' (read the branch counts back at each decision), 'device'
-        (counts stay on the device, count-guarded launches) or 'graph'
-        (device mode replayed from a captured HIP graph); returns the previous mode."""
+        (counts stay on the device, count-guarded launches), 'graph'
+        (device mode replayed from a captured HIP graph) or 'persistent'
+        (device mode with a bounded halting loop in one launch); returns the
+        previous mode."""
         if mode not in HOST_MODES:
             raise ValueError(f"host mode must be one of {sorted(HOST_MODES)}")
         prev = check(lib.dycl_plan_set_host_mode(self._h, HOST_MODES[mode]))

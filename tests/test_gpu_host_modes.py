@@ -53,7 +53,7 @@ def _run(rt, plan, wl, x, aux, mode):
 
 def _same(a, b):
     assert np.array_equal(a["logits"], b["logits"], equal_nan=True)
-    for k in ("exit_index", "iterations", "skip_mask"):
+    for k in ("exit_index", "iterations", "skip_mask") + (("tokens",) if "tokens" in a else ()):
         assert np.array_equal(a[k], b[k]), k
     assert a["counts"] == b["counts"]
 
@@ -67,7 +67,7 @@ def test_modes_agree_bitwise(name, size):
     print(f"[host-modes] {name} B={B}", flush=True)
     x, aux = wl.inputs(B)
     ref = _run(rt, plan, wl, x, aux, "sync")
-    for mode in ("device", "graph"):
+    for mode in ("device", "graph", "persistent"):
         got = _run(rt, plan, wl, x, aux, mode)
         _same(ref, got)
     print(name, "counts", ref["counts"], flush=True)
