@@ -8,6 +8,7 @@
 #include "halt_row.hpp"
 
 #include <mutex>
+#include <stdexcept>
 
 namespace dycl {
 namespace k {
@@ -300,6 +301,182 @@ void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int
                  uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s, const int32_t* nc) {
   hipLaunchKernelGGL(exit_decide_kernel, dim3(n), dim3(64), 0, s, Z, ncls, T, tau, final_, head, orig, flags,
                      logits, n_out, rec, nc, n);
+}
+
+// ------------------------------------------------- sliced exit head ----
+// Wide exit heads (C x ncls beyond the fused kernel): the head linear
+// z = W g + b over K = C is cut into slices of about 128 so that a launch has
+// many short sums instead of a few long ones (the long chains left the
+// linear waiting on its loads).  head_partial_kernel: workgroup (row group of
+// 8, 64 classes, slice s) sums its slice, its four waves taking interleaved
+// k and meeting in LDS in wave order; head_decide_kernel: one workgroup per
+// row adds the slices in order, the bias, and takes the exit decision.  The
+// slices depend on C alone, so every row count sums in the same order.  Both
+// kernels issue all their loads before the first wait: a few long dependent
+// load rounds, not the arithmetic, were what bounded these launches.
+
+int head_slices(int K) { return K <= 128 ? 1 : (K + 127) / 128; }
+bool head_sliced_fits(int K, int ncls) { return K >= 1 && K <= 2048 && ncls >= 1 && ncls <= 1024; }
+
+__global__ __launch_bounds__(256) void head_partial_kernel(const float* __restrict__ G, int n, int K,
+                                                           const float* __restrict__ Wt, int N, int S,
+                                                           float* __restrict__ P, int nP, const int32_t* nc) {
+  constexpr int R = 8, KSMAX = 132;
+  __shared__ float xs[R][KSMAX];
+  __shared__ float red[4][R][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gy = (N + 63) / 64;
+  const int s = blockIdx.x % S, rest = blockIdx.x / S;
+  const int cb = rest % gy, rg = rest / gy;
+  n = live(nc, n);
+  const int m0 = rg * R;
+  if (m0 >= n) return;
+  const int k0 = static_cast<int>(static_cast<long>(K) * s / S), k1 = static_cast<int>(static_cast<long>(K) * (s + 1) / S);
+  const int ks = k1 - k0;   // at most 128: S = ceil(K / 128)
+  const int col = cb * 64 + lane, cc = col < N ? col : N - 1;
+  // every load of the workgroup is issued before the first wait: the wave's
+  // weights (k = w + 4 i of the slice, addresses clamped into the slice) and
+  // the rows' features (clamped into the live rows)
+  constexpr int KI = (KSMAX + 3) / 4;
+  float wv[KI];
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const int kk = min(w + 4 * i, ks - 1);
+    wv[i] = Wt[static_cast<size_t>(k0 + kk) * N + cc];
+  }
+  constexpr int XI = (R * KSMAX + 255) / 256;
+  float xv[XI];
+#pragma unroll
+  for (int i = 0; i < XI; ++i) {
+    const int e = min(static_cast<int>(threadIdx.x) + 256 * i, R * ks - 1);
+    const int r = e / ks, kk = e - r * ks;
+    xv[i] = G[static_cast<size_t>(min(m0 + r, n - 1)) * K + k0 + kk];
+  }
+#pragma unroll
+  for (int i = 0; i < XI; ++i) {
+    const int e = threadIdx.x + 256 * i;
+    if (e < R * ks) {
+      const int r = e / ks, kk = e - r * ks;
+      xs[r][kk] = m0 + r < n ? xv[i] : 0.f;
+    }
+  }
+  __syncthreads();
+  float acc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[r] = 0.f;
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const int kk = w + 4 * i;
+    if (kk < ks)
+#pragma unroll
+      for (int r = 0; r < R; ++r) acc[r] = fmaf(xs[r][kk], wv[i], acc[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) red[w][r][lane] = acc[r];
+  __syncthreads();
+  // 256 threads finish 8 rows x 64 columns: thread -> (row w + 4 q, column lane)
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int r = w + 4 * q;
+    if (m0 + r < n && col < N)
+      P[(static_cast<size_t>(s) * nP + m0 + r) * N + col] =
+          ((red[0][r][lane] + red[1][r][lane]) + red[2][r][lane]) + red[3][r][lane];
+  }
+}
+
+// One workgroup per row: thread t holds classes t + 256 q (q < 4); it loads
+// every slice of all of them before adding (SP >= S slices, addresses
+// clamped), adds the slices in order and the bias, and the four waves meet
+// in LDS, in wave order, for the row's maximum and exponential sum.
+template <int SP>
+__global__ __launch_bounds__(256) void head_decide_kernel(const float* __restrict__ P, int nP, int S, int ncls,
+                                                          const float* __restrict__ bias, const float* __restrict__ Tp,
+                                                          float tau, int final_, int head,
+                                                          const int32_t* __restrict__ orig, uint8_t* flags,
+                                                          float* __restrict__ logits, int n_out, dycl_record* rec,
+                                                          const int32_t* nc, int n) {
+  constexpr int JQ = 4;   // ncls <= 1024
+  __shared__ float wred[2][4];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r = blockIdx.x;
+  if (r >= live(nc, n)) return;
+  float pv[JQ][SP];
+#pragma unroll
+  for (int q = 0; q < JQ; ++q) {
+    const int j = min(tid + 256 * q, ncls - 1);
+#pragma unroll
+    for (int sl = 0; sl < SP; ++sl)
+      pv[q][sl] = P[(static_cast<size_t>(min(sl, S - 1)) * nP + r) * ncls + j];
+  }
+  float z[JQ];
+#pragma unroll
+  for (int q = 0; q < JQ; ++q) {
+    const int j = tid + 256 * q;
+    float v = pv[q][0];
+#pragma unroll
+    for (int sl = 1; sl < SP; ++sl)
+      if (sl < S) v += pv[q][sl];
+    z[q] = j < ncls ? v + (bias ? bias[j] : 0.f) : 0.f;
+  }
+  bool ex = final_ != 0;
+  if (!ex) {
+    const float T = *Tp;
+    float m = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < JQ; ++q)
+      if (tid + 256 * q < ncls) m = fmaxf(m, z[q]);
+    m = wave_max(m);
+    if (lane == 0) wred[0][w] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(wred[0][0], wred[0][1]), fmaxf(wred[0][2], wred[0][3]));
+    float sm = 0.f;
+#pragma unroll
+    for (int q = 0; q < JQ; ++q)
+      if (tid + 256 * q < ncls) sm += expf((z[q] - m) / T);
+    sm = wave_sum(sm);
+    if (lane == 0) wred[1][w] = sm;
+    __syncthreads();
+    sm = ((wred[1][0] + wred[1][1]) + wred[1][2]) + wred[1][3];
+    ex = (1.0f / sm) >= tau;
+  }
+  if (ex) {
+    const int o = orig ? orig[r] : r;
+#pragma unroll
+    for (int q = 0; q < JQ; ++q)
+      if (tid + 256 * q < ncls) logits[static_cast<size_t>(o) * n_out + tid + 256 * q] = z[q];
+    if (tid == 0 && head >= 0) rec[o].exit_index = head;
+  }
+  if (tid == 0) flags[r] = ex ? 1 : 0;
+}
+
+size_t head_partials_floats(int K, int n, int ncls) {
+  return static_cast<size_t>(head_slices(K)) * n * ncls;
+}
+
+void exit_head_sliced(const float* G, int n, int K, const float* Wt, const float* bias, int ncls, const float* T,
+                      float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits, int n_out,
+                      dycl_record* rec, float* P, hipStream_t s, const int32_t* nc) {
+  if (!head_sliced_fits(K, ncls)) throw std::invalid_argument("exit_head_sliced: K or class count out of range");
+  if (n <= 0) return;
+  const int S = head_slices(K), gy = (ncls + 63) / 64;
+  hipLaunchKernelGGL(head_partial_kernel, dim3(((n + 7) / 8) * gy * S), dim3(256), 0, s, G, n, K, Wt, ncls, S, P, n,
+                     nc);
+  const dim3 g(n), b(256);
+  if (S <= 1)
+    hipLaunchKernelGGL(head_decide_kernel<1>, g, b, 0, s, P, n, S, ncls, bias, T, tau, final_, head, orig, flags,
+                       logits, n_out, rec, nc, n);
+  else if (S <= 2)
+    hipLaunchKernelGGL(head_decide_kernel<2>, g, b, 0, s, P, n, S, ncls, bias, T, tau, final_, head, orig, flags,
+                       logits, n_out, rec, nc, n);
+  else if (S <= 4)
+    hipLaunchKernelGGL(head_decide_kernel<4>, g, b, 0, s, P, n, S, ncls, bias, T, tau, final_, head, orig, flags,
+                       logits, n_out, rec, nc, n);
+  else if (S <= 8)
+    hipLaunchKernelGGL(head_decide_kernel<8>, g, b, 0, s, P, n, S, ncls, bias, T, tau, final_, head, orig, flags,
+                       logits, n_out, rec, nc, n);
+  else
+    hipLaunchKernelGGL(head_decide_kernel<16>, g, b, 0, s, P, n, S, ncls, bias, T, tau, final_, head, orig, flags,
+                       logits, n_out, rec, nc, n);
 }
 
 // ----------------------------------------------------- fused exit head ----

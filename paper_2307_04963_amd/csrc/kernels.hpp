@@ -136,6 +136,17 @@ void exit_decide(const float* Z, int n, int ncls, const float* T, float tau, int
                  const int32_t* orig, uint8_t* flags, float* logits, int n_out, dycl_record* rec, hipStream_t s,
                  const int32_t* nc = nullptr);
 
+// Exit head over pooled features G [n][K] float32 with transposed weights
+// Wt [K][ncls] (ncls <= 1024): the linear cut into head_slices(K) K-slices
+// whose partial sums (P, head_partials_floats(K, n, ncls) floats) are added
+// in slice order with the bias, then the decision as exit_decide takes it.
+int head_slices(int K);
+bool head_sliced_fits(int K, int ncls);   // K <= 2048 (16 slices), ncls <= 1024
+size_t head_partials_floats(int K, int n, int ncls);
+void exit_head_sliced(const float* G, int n, int K, const float* Wt, const float* bias, int ncls, const float* T,
+                      float tau, int final_, int head, const int32_t* orig, uint8_t* flags, float* logits, int n_out,
+                      dycl_record* rec, float* P, hipStream_t s, const int32_t* nc = nullptr);
+
 // Fused exit head for small heads (C <= 2048 and a multiple of 4, ncls <=
 // 1024): pooling, head linear on the weights as stored W [ncls][C] (16-byte
 // aligned rows), and the exit decision, up to 8 rows per workgroup.  Same

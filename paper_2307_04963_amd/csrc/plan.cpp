@@ -302,6 +302,13 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     p->split_bytes = split_bytes;
   }
   p->d_Z = dev_alloc<float>(p, static_cast<size_t>(B) * sp.max_ncls, "head logits");
+  {
+    size_t hp = 0;   // partial sums of the sliced exit heads
+    for (const Node& nd : sp.nodes)
+      if (nd.kind == NodeKind::Exit && !nd.fused && k::head_sliced_fits(nd.hc, nd.ncls))
+        hp = std::max(hp, k::head_partials_floats(nd.hc, B, nd.ncls));
+    if (hp) p->d_headP = dev_alloc<float>(p, hp, "exit head partial sums");
+  }
   p->d_S = dev_alloc<float>(p, B, "halting sums");
   if (sp.any_decode) {
     p->d_tok[0] = dev_alloc<int32_t>(p, B, "previous tokens");
@@ -363,7 +370,7 @@ void plan_free(dycl_plan* p) {
   for (void* b : p->buffers)
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
-                     p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_S, p->d_zeros,
+                     p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_headP, p->d_S, p->d_zeros,
                      p->d_xpad, p->d_cws, p->d_Gpart, p->d_split, p->d_tok[0], p->d_tok[1], p->act.h[0],
                      p->act.h[1]};
   for (void* s : singles)
@@ -683,7 +690,14 @@ struct Run {
             });
             G = p->d_G;
           }
-          if (!nd.fused) {
+          if (!nd.fused && k::head_sliced_fits(nd.hc, nd.ncls)) {
+            // the head linear in K slices, then the slices' sum and the decision
+            launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, 4.0 * (n * (nd.hc + nd.ncls) + nd.ncls * nd.hc), [&] {
+              k::exit_head_sliced(G, n, nd.hc, p->head_t[nd.head_t], f32(nd.h_b), nd.ncls, f32(nd.h_T), nd.tau,
+                                  nd.final_ ? 1 : 0, nd.index, orig, p->d_flags, logits, sp.n_out, rec, p->d_headP,
+                                  s, rows.nc);
+            });
+          } else if (!nd.fused) {
             launch(P_HEAD, 2.0 * n * nd.hc * nd.ncls, 4.0 * (n * (nd.hc + nd.ncls) + nd.ncls * nd.hc), [&] {
               k::linear_t_f32(G, n, nd.hc, p->head_t[nd.head_t], f32(nd.h_b), nd.ncls, k::ACT_NONE, p->d_Z, s,
                               rows.nc, rows.hint);

@@ -179,6 +179,7 @@ struct dycl_plan {
   float* d_split = nullptr;      // K-split conv partial sums (largest layer at max_batch rows), or null
   size_t split_bytes = 0;
   float* d_Z = nullptr;          // [max_batch, max_ncls]
+  float* d_headP = nullptr;      // K-slice partial sums of the wide exit heads, or null
   float* d_S = nullptr;          // [max_batch]
   void* d_cws = nullptr;         // workspace of the large-n compaction (max_batch > 16384)
   uint16_t* d_zeros = nullptr;   // 256 zero bytes: source of convolution padding taps
