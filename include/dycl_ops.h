@@ -40,6 +40,10 @@ size_t dycl_op_compact_workspace(int64_t n);
  *   workspace    dycl_op_compact_workspace(n) bytes, 8-byte aligned (may be
  *                NULL when that is 0).
  * 0 <= n < 2^31; n == 0 writes counts = {0, 0}.
+ * Above 16384 flags the partition is one chained pass over blocks of 16384
+ * flags, 8192 with ids (each block waits, boundedly, for the counts of the
+ * blocks before it); if that wait ever ran out, counts reads {-1, -1} and
+ * the lists are incomplete.
  */
 int dycl_op_compact(const uint8_t* flags, const int32_t* orig, int64_t n, int32_t* idx1, int32_t* org1,
                     int32_t* idx0, int32_t* org0, int32_t* counts, void* workspace, size_t workspace_bytes,
@@ -50,16 +54,16 @@ int dycl_op_compact(const uint8_t* flags, const int32_t* orig, int64_t n, int32_
  * memory or pass a workspace: code under HIP graph capture, tight serving
  * loops, harnesses that forbid hipMalloc.  Same arguments, results and
  * errors as dycl_op_compact without the workspace pair; it calls no
- * allocating routine.  The block counts and offsets of the reduce-then-scan
- * form (or the ids of a small partition whose org1 / org0 is NULL) live in
- * a library-owned static device array of DYCL_OP_COMPACT_NOALLOC_SCRATCH
+ * allocating routine.  The block status words of the chained form (or the
+ * ids of a small partition whose org1 / org0 is NULL) live in a
+ * library-owned static device array of DYCL_OP_COMPACT_NOALLOC_SCRATCH
  * bytes, one per GPU the library runs on, held until the process ends; its
  * device address is resolved on the first call on each device.
  *   0 <= n <= DYCL_OP_COMPACT_NOALLOC_MAX_N (2^28); larger n returns
  *   DYCL_E_INVALID.  n == 0 writes counts = {0, 0} with a kernel.
  * Every call on one GPU shares that GPU's array, which keeps the last call's
- * contents (nothing in it needs clearing: each entry is written before it is
- * read): calls that overlap on one GPU (concurrent streams, threads) race
+ * contents (a call's first kernel clears what the chained form needs at
+ * zero): calls that overlap on one GPU (concurrent streams, threads) race
  * and must be serialised by the caller.
  */
 #define DYCL_OP_COMPACT_NOALLOC_MAX_N (1LL << 28)

@@ -314,8 +314,8 @@ int dycl_op_compact_noalloc(const uint8_t* flags, const int32_t* orig, int64_t n
       int32_t* w = reinterpret_cast<int32_t*>(ws);
       dycl::k::compact(flags, orig, static_cast<int>(n), idx1, org1 ? org1 : w, idx0, org0 ? org0 : w + n, counts, s);
     } else {
-      // block counts and offsets in the scratch: every entry below the
-      // block count is written before it is read, so nothing is cleared
+      // block status words in the scratch, cleared by the
+      // call's first kernel (not by a memset, so the call can be captured)
       dycl::k::compact_large(flags, orig, static_cast<size_t>(n), idx1, org1, idx0, org0, counts, ws, s);
     }
     if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_compact_noalloc: launch failed");

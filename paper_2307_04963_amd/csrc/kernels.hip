@@ -716,29 +716,33 @@ void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, in
 }
 
 // ------------------------------------------------- large-n compaction ----
-// Reduce-then-scan over blocks of 4096 flags: (1) every block counts its
-// set flags (16 per thread, one 16-byte load), (2) one workgroup turns the
-// counts into per-block output offsets, (3) every block ranks its flags
-// again by ballots, stages its partition in LDS and writes both lists with
-// coalesced stores.  Order is preserved (stable partition).
+// One pass, chained over blocks of 16384 flags (8192 when ids are carried).
+// A workgroup reads its block's flags (and ids) once, counts the ones,
+// publishes that count in the block's status word, ranks its elements and
+// stages the block's partition in LDS (block positions, and the ids); wave 0
+// then learns how many ones all earlier blocks hold by reading their status
+// words backwards, 64 a round, to the nearest one that already carries an
+// inclusive prefix, publishes the block's own inclusive prefix, and the
+// workgroup writes both runs with coalesced stores.  Order is preserved
+// (stable partition).  Flags cross HBM once and every index once; blocks are
+// large because each one's prefix costs a round trip through the chain.
+//
+// Status word: the top two bits say what it holds (0 nothing yet, 1 the
+// block's count, 2 the ones of blocks 0..b), the rest the value.  The words
+// and the counts are cleared by the call's first kernel.  The wait is
+// bounded (kSpinLimit polls in all): it cannot run out unless a predecessor
+// never publishes, which in-order dispatch rules out; a workgroup that still
+// runs out of polls writes counts {-1, -1} and nothing else instead of
+// waiting for ever.
 
-constexpr int kCompactBlock = 4096;
-
-__device__ __forceinline__ int flag_count16(const uint8_t* __restrict__ f, size_t i0, size_t n, uint8_t v[16]) {
-  if (i0 + 16 <= n) {
-    const uint4 q = *reinterpret_cast<const uint4*>(f + i0);
-    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int j = 0; j < 16; ++j) v[j] = (w[j >> 2] >> (8 * (j & 3))) & 0xff;
-  } else {
-#pragma unroll
-    for (int j = 0; j < 16; ++j) v[j] = (i0 + j < n) ? f[i0 + j] : 0;
-  }
-  int c = 0;
-#pragma unroll
-  for (int j = 0; j < 16; ++j) c += v[j] != 0;
-  return c;
-}
+constexpr int kCompactEPT = 64;                       // flags per thread, without ids
+constexpr int kCompactEPTI = 32;                      // with ids (their LDS staging halves the block)
+constexpr int kCompactBlock = 256 * kCompactEPT;
+constexpr int kCompactBlockI = 256 * kCompactEPTI;
+static_assert(kCompactEPTI <= kCompactEPT && kCompactEPT <= 256 && kCompactEPTI % 16 == 0,
+              "the workspace is sized by the smaller block; positions fit 16 bits");
+constexpr uint64_t kStCount = 1ull << 62, kStPrefix = 2ull << 62, kStValue = (1ull << 62) - 1;
+constexpr int kSpinLimit = 1 << 16;
 
 __device__ __forceinline__ int wave_incl_scan(int x) {
   const int lane = threadIdx.x & 63;
@@ -750,235 +754,206 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
   return x;
 }
 
-// Each workgroup counts kCountSub consecutive blocks: every thread loads its
-// 16 flags of each block (all loads in flight together), the waves reduce
-// by shuffles and LDS combines the four waves.
-constexpr int kCountSub = 8;
+__device__ __forceinline__ long long wave_sum_ll(long long v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
 
-__global__ __launch_bounds__(256) void compact_count_kernel(const uint8_t* __restrict__ flags, size_t n, int nb,
-                                                            int32_t* __restrict__ bcount, const int32_t* nc) {
-  __shared__ int ws[4][kCountSub];
+__device__ __forceinline__ void status_put(uint64_t* w, uint64_t v) {
+  __hip_atomic_store(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint64_t status_get(uint64_t* w) {
+  return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// a pause that grows with the polls already spent (1 to 16 sleeps of 64 clocks)
+__device__ __forceinline__ void backoff(int spins) {
+  const int k = spins < 4 ? 1 << spins : 16;
+  for (int i = 0; i < k; ++i) __builtin_amdgcn_s_sleep(1);
+}
+
+__global__ __launch_bounds__(256) void compact_clear_kernel(uint64_t* __restrict__ st, int nb, int32_t* counts) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < nb) st[i] = 0;
+  if (i == 0) {
+    counts[0] = 0;
+    counts[1] = 0;
+  }
+}
+
+// Block b = workgroup b: workgroups of a grid are dispatched in index order,
+// so the blocks a workgroup waits for have all been dispatched.
+template <bool IDS>
+__global__ __launch_bounds__(256) void compact_chain_kernel(const uint8_t* __restrict__ flags,
+                                                            const int32_t* __restrict__ orig, size_t n,
+                                                            uint64_t* st, int32_t* idx1, int32_t* org1,
+                                                            int32_t* idx0, int32_t* org0, int32_t* counts,
+                                                            const int32_t* nc) {
+  constexpr int EPT = IDS ? kCompactEPTI : kCompactEPT, NB = 256 * EPT;
+  __shared__ uint16_t spos[NB];              // block position of each staged element
+  __shared__ int32_t sorg[IDS ? NB : 1];
+  __shared__ int wsum[4];
+  __shared__ int s_fail;
+  __shared__ long long s_excl;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const size_t blk = static_cast<size_t>(blockIdx.x) * kCountSub * kCompactBlock;
-  const size_t g0 = blk + threadIdx.x * 16;
-  int c[kCountSub];
-  if (blk + static_cast<size_t>(kCountSub) * kCompactBlock <= n) {
-    uint4 q[kCountSub];
+  const int nbl = static_cast<int>((n + NB - 1) / NB);
+  const int b = blockIdx.x;
+  if (b >= nbl) return;
+  const size_t blk0 = static_cast<size_t>(b) * NB;
+  const int nblk = static_cast<int>(min(n - blk0, static_cast<size_t>(NB)));
+
+  // EPT consecutive flags per thread (16-byte loads; the ids likewise)
+  const int l0 = tid * EPT;
+  const size_t e = blk0 + l0;
+  const int nv = max(0, min(EPT, nblk - l0));
+  uint8_t v[EPT];
+  int32_t id[IDS ? EPT : 1];
+  if (nv == EPT) {
 #pragma unroll
-    for (int b = 0; b < kCountSub; ++b) q[b] = *reinterpret_cast<const uint4*>(flags + g0 + b * kCompactBlock);
+    for (int h = 0; h < EPT / 16; ++h) {
+      const uint4 q = *reinterpret_cast<const uint4*>(flags + e + 16 * h);
+      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-    for (int b = 0; b < kCountSub; ++b) {
-      const uint32_t w[4] = {q[b].x, q[b].y, q[b].z, q[b].w};
-      int k = 0;
+      for (int j = 0; j < 16; ++j) v[16 * h + j] = (w4[j >> 2] >> (8 * (j & 3))) & 0xff;
+    }
+    if constexpr (IDS) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) k += ((w[j >> 2] >> (8 * (j & 3))) & 0xff) != 0;
-      c[b] = k;
+      for (int j = 0; j < EPT / 4; ++j) {
+        const int4 o4 = *reinterpret_cast<const int4*>(orig + e + 4 * j);
+        id[4 * j] = o4.x;
+        id[4 * j + 1] = o4.y;
+        id[4 * j + 2] = o4.z;
+        id[4 * j + 3] = o4.w;
+      }
     }
   } else {
-    uint8_t v[16];
 #pragma unroll
-    for (int b = 0; b < kCountSub; ++b) {
-      const size_t i0 = g0 + b * kCompactBlock;
-      c[b] = i0 < n ? flag_count16(flags, i0, n, v) : 0;
+    for (int j = 0; j < EPT; ++j) {
+      v[j] = j < nv ? flags[e + j] : 0;
+      if constexpr (IDS) id[j] = j < nv ? orig[e + j] : 0;
     }
   }
+  int c = 0;
 #pragma unroll
-  for (int b = 0; b < kCountSub; ++b) {
-    const int x = wave_incl_scan(c[b]);
-    if (lane == 63) ws[wave][b] = x;
+  for (int j = 0; j < EPT; ++j) c += (j < nv && v[j] != 0);
+
+  // the block's count (waves in order), published before anything waits
+  const int incl = wave_incl_scan(c);
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int below = incl - c, agg = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (w < wave) below += wsum[w];
+    agg += wsum[w];
+  }
+  if (tid == 0) status_put(st + b, (b == 0 ? kStPrefix : kStCount) | static_cast<uint64_t>(agg));
+
+  // stage the partition: ones from the front, zeros from the back
+  int r1 = below;
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    if (j < nv) {
+      const int slot = v[j] ? r1 : NB - 1 - (l0 + j - r1);
+      spos[slot] = static_cast<uint16_t>(l0 + j);
+      if constexpr (IDS) sorg[slot] = id[j];
+      r1 += v[j] != 0;
+    }
+  }
+
+  // ones of the earlier blocks: wave 0 first waits for the block just
+  // before (one word, polled by one lane), then reads the status words
+  // backwards, 64 a round, to the nearest inclusive prefix
+  if (wave == 0) {
+    long long excl = 0;
+    int fail = 0, spins = 0;
+    if (b > 0) {
+      if (lane == 0)
+        while ((status_get(st + b - 1) >> 62) == 0 && spins <= kSpinLimit) backoff(spins++);
+      spins = __shfl(spins, 0, 64);
+      int top = b - 1;
+      while (true) {
+        const int k = top - lane;
+        // below block 0 reads as an empty prefix, so the walk always ends
+        const uint64_t w = k >= 0 ? status_get(st + k) : kStPrefix;
+        const uint64_t pre = __ballot((w >> 62) == 2);
+        const uint64_t empty = __ballot((w >> 62) == 0);
+        const int lim = pre ? __builtin_ctzll(pre) : 63;   // nearest word with a prefix
+        const uint64_t upto = lim == 63 ? ~0ull : ((2ull << lim) - 1);
+        if (empty & upto) {
+          if (++spins > kSpinLimit) {
+            fail = 1;
+            break;
+          }
+          backoff(spins);
+          continue;
+        }
+        excl += wave_sum_ll(lane <= lim ? static_cast<long long>(w & kStValue) : 0);
+        if (pre) break;
+        top -= 64;
+      }
+      if (lane == 0 && !fail) status_put(st + b, kStPrefix | static_cast<uint64_t>(excl + agg));
+    }
+    if (lane == 0) {
+      s_excl = excl;
+      s_fail = fail;
+      if (fail) {
+        counts[0] = -1;
+        counts[1] = -1;
+      } else if (b == nbl - 1) {
+        counts[0] = static_cast<int32_t>(excl + agg);
+        counts[1] = static_cast<int32_t>(static_cast<long long>(n) - (excl + agg));
+      }
+    }
   }
   __syncthreads();
-  if (threadIdx.x < kCountSub) {
-    const int b = blockIdx.x * kCountSub + threadIdx.x;
-    if (b < nb) bcount[b] = ws[0][threadIdx.x] + ws[1][threadIdx.x] + ws[2][threadIdx.x] + ws[3][threadIdx.x];
+  if (s_fail) return;
+  const long long base1 = s_excl, base0 = static_cast<long long>(blk0) - base1;
+  for (int k = tid; k < agg; k += 256) {
+    const int32_t row = static_cast<int32_t>(blk0 + spos[k]);
+    idx1[base1 + k] = row;
+    if (org1) org1[base1 + k] = IDS ? sorg[k] : row;
   }
-}
-
-// One workgroup, rounds of 16384 block counts: the counts are staged in LDS
-// with coalesced loads (all 16 per thread in flight together), each thread
-// prefix-sums 16 consecutive ones (its sum scanned across the workgroup:
-// shuffles within a wave, LDS across waves) and puts their offsets back in
-// place, and the offsets leave with coalesced stores.  Offsets within a
-// round fit 32 bits (at most 2^26).
-constexpr int kScanRound = 16 * 1024;
-
-__global__ __launch_bounds__(1024) void compact_scan_kernel(const int32_t* __restrict__ bcount, int nb, size_t n,
-                                                            int64_t* __restrict__ boff, int32_t* counts,
-                                                            const int32_t* nc) {
-  __shared__ __align__(16) int32_t sc[kScanRound];
-  __shared__ int ws[16];
-  if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int64_t carry = 0;                                // ones in the blocks of earlier rounds
-  for (int b0 = 0; b0 < nb; b0 += kScanRound) {
-    const int m = min(kScanRound, nb - b0);
-    int ld[kScanRound / 1024];
-#pragma unroll
-    for (int r = 0; r < kScanRound / 1024; ++r) {
-      const int k = r * 1024 + tid;
-      ld[r] = k < m ? bcount[b0 + k] : 0;
-    }
-#pragma unroll
-    for (int r = 0; r < kScanRound / 1024; ++r) sc[r * 1024 + tid] = ld[r];
-    __syncthreads();
-    int4 q[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) q[j] = reinterpret_cast<const int4*>(sc)[tid * 4 + j];
-    int c[16] = {q[0].x, q[0].y, q[0].z, q[0].w, q[1].x, q[1].y, q[1].z, q[1].w,
-                 q[2].x, q[2].y, q[2].z, q[2].w, q[3].x, q[3].y, q[3].z, q[3].w};
-    int sum = 0;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) sum += c[j];
-    const int x = wave_incl_scan(sum);
-    if (lane == 63) ws[wave] = x;
-    __syncthreads();
-    int run = x - sum, total = 0;
-#pragma unroll
-    for (int w = 0; w < 16; ++w) {
-      if (w < wave) run += ws[w];
-      total += ws[w];
-    }
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int cj = c[j];
-      c[j] = run;                                   // ones of this round before block tid * 16 + j
-      run += cj;
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      reinterpret_cast<int4*>(sc)[tid * 4 + j] = make_int4(c[4 * j], c[4 * j + 1], c[4 * j + 2], c[4 * j + 3]);
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kScanRound / 1024; ++r) {
-      const int k = r * 1024 + tid;
-      if (k < m) boff[b0 + k] = carry + sc[k];
-    }
-    carry += total;
-    __syncthreads();
-  }
-  if (tid == 0) {
-    counts[0] = static_cast<int32_t>(carry);
-    counts[1] = static_cast<int32_t>(static_cast<int64_t>(n) - carry);
-  }
-}
-
-// A block of 4096 flags in 4 rounds of 1024, 4 consecutive flags per lane
-// (one 32-bit load; the ids as one 16-byte load).  An element's rank among
-// the block's ones is the ones of earlier rounds, of earlier waves (LDS), of
-// lower lanes (for each of the 4 positions, mbcnt of that position's ballot)
-// and of the lane's own earlier elements; its rank among the zeros is its
-// block index minus that.  The block's partition is staged in LDS, ones from
-// the front and zeros from the back, and both runs are then written with
-// consecutive lanes on consecutive elements.
-__global__ __launch_bounds__(256) void compact_write_kernel(const uint8_t* __restrict__ flags,
-                                                            const int32_t* __restrict__ orig, size_t n,
-                                                            const int64_t* __restrict__ boff, int32_t* idx1,
-                                                            int32_t* org1, int32_t* idx0, int32_t* org0,
-                                                            const int32_t* nc) {
-  __shared__ int32_t sidx[kCompactBlock], sorg[kCompactBlock];
-  __shared__ int wc[4];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const size_t blk0 = static_cast<size_t>(blockIdx.x) * kCompactBlock;
-  if (nc) n = min(n, static_cast<size_t>(max(*nc, 0)));
-  if (blk0 >= n) return;
-  const int nblk = static_cast<int>(min(n - blk0, static_cast<size_t>(kCompactBlock)));
-  int ones = 0;                                     // ones in earlier rounds
-  for (int rd = 0; rd < kCompactBlock / 1024; ++rd) {
-    const int l0 = rd * 1024 + tid * 4;             // block index of the lane's first element
-    const size_t e = blk0 + l0;
-    const int nv = max(0, min(4, nblk - l0));
-    uint8_t v[4] = {0, 0, 0, 0};
-    int32_t id[4] = {0, 0, 0, 0};
-    if (nv == 4) {
-      const uint32_t w = *reinterpret_cast<const uint32_t*>(flags + e);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = (w >> (8 * j)) & 0xff;
-      if (orig) {
-        const int4 q = *reinterpret_cast<const int4*>(orig + e);
-        id[0] = q.x;
-        id[1] = q.y;
-        id[2] = q.z;
-        id[3] = q.w;
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (j < nv) {
-          v[j] = flags[e + j];
-          if (orig) id[j] = orig[e + j];
-        }
-    }
-    if (!orig)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) id[j] = static_cast<int32_t>(e + j);
-    int below = 0, wtot = 0;                        // ones of lower lanes; of the wave
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint64_t b = __ballot(j < nv && v[j] != 0);
-      below += __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b >> 32),
-                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(b), 0));
-      wtot += __popcll(b);
-    }
-    if (lane == 0) wc[wave] = wtot;
-    __syncthreads();
-    int r1 = ones + below, rtot = 0;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      if (w < wave) r1 += wc[w];
-      rtot += wc[w];
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j < nv) {
-        const int slot = v[j] ? r1 : kCompactBlock - 1 - (l0 + j - r1);
-        sidx[slot] = static_cast<int32_t>(e + j);
-        sorg[slot] = id[j];
-        r1 += v[j] != 0;
-      }
-    }
-    ones += rtot;
-    __syncthreads();
-  }
-  const int64_t base1 = boff[blockIdx.x], base0 = static_cast<int64_t>(blk0) - base1;
-  for (int k = tid; k < ones; k += 256) {
-    idx1[base1 + k] = sidx[k];
-    if (org1) org1[base1 + k] = sorg[k];
-  }
-  const int zeros = nblk - ones;
+  const int zeros = nblk - agg;
   for (int k = tid; k < zeros; k += 256) {
-    idx0[base0 + k] = sidx[kCompactBlock - 1 - k];
-    if (org0) org0[base0 + k] = sorg[kCompactBlock - 1 - k];
+    const int32_t row = static_cast<int32_t>(blk0 + spos[NB - 1 - k]);
+    idx0[base0 + k] = row;
+    if (org0) org0[base0 + k] = IDS ? sorg[NB - 1 - k] : row;
   }
 }
 
 size_t compact_workspace(size_t n) {
-  const size_t nb = (n + kCompactBlock - 1) / kCompactBlock;
-  return nb * (sizeof(int32_t) + sizeof(int64_t)) + 256;
+  const size_t nb = (n + kCompactBlockI - 1) / kCompactBlockI;
+  return nb * sizeof(uint64_t) + 256;
 }
 
 void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t* idx1, int32_t* org1, int32_t* idx0,
                    int32_t* org0, int32_t* counts, void* workspace, hipStream_t s, const int32_t* nc) {
-  const int nb = static_cast<int>((n + kCompactBlock - 1) / kCompactBlock);
-  int64_t* boff = static_cast<int64_t*>(workspace);
-  int32_t* bcount = reinterpret_cast<int32_t*>(boff + nb);
-  hipLaunchKernelGGL(compact_count_kernel, dim3((nb + kCountSub - 1) / kCountSub), dim3(256), 0, s, flags, n, nb,
-                     bcount, nc);
-  hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(1024), 0, s, bcount, nb, n, boff, counts, nc);
-  hipLaunchKernelGGL(compact_write_kernel, dim3(nb), dim3(256), 0, s, flags, orig, n, boff, idx1, org1, idx0, org0,
-                     nc);
+  const int NB = orig ? kCompactBlockI : kCompactBlock;
+  const int nb = static_cast<int>((n + NB - 1) / NB);
+  uint64_t* st = static_cast<uint64_t*>(workspace);
+  hipLaunchKernelGGL(compact_clear_kernel, dim3((nb + 255) / 256), dim3(256), 0, s, st, nb, counts);
+  if (nb <= 0) return;
+  if (orig)
+    hipLaunchKernelGGL(compact_chain_kernel<true>, dim3(nb), dim3(256), 0, s, flags, orig, n, st, idx1, org1, idx0,
+                       org0, counts, nc);
+  else
+    hipLaunchKernelGGL(compact_chain_kernel<false>, dim3(nb), dim3(256), 0, s, flags, orig, n, st, idx1, org1, idx0,
+                       org0, counts, nc);
 }
 
 // Library-owned scratch of the allocation-free compaction entry point: the
-// block counts and block offsets of up to kScratchCompactMaxN flags (or the
+// block status words of up to kScratchCompactMaxN flags (or the
 // two id lists of a small partition whose caller passes none).  Each GPU the
 // library runs on holds one copy until the process ends.  In host code the
 // array's name is not a device address: compact_scratch() resolves it once
 // per device and only that address is ever handed to a kernel.
 __device__ __align__(256) uint8_t scratch[kScratchBytes];
-static_assert(((kScratchCompactMaxN + kCompactBlock - 1) / kCompactBlock) * (sizeof(int32_t) + sizeof(int64_t)) + 256 <=
-                  kScratchBytes,
-              "scratch too small for the largest reduce-then-scan partition it takes");
+static_assert(((kScratchCompactMaxN + kCompactBlockI - 1) / kCompactBlockI) * sizeof(uint64_t) + 256 <= kScratchBytes,
+              "scratch too small for the largest chained partition it takes");
 static_assert(8 * 16384 <= kScratchBytes, "scratch too small for the ids of a single-workgroup partition");
 
 void* compact_scratch() {

@@ -172,9 +172,9 @@ void halt_head(const uint16_t* h, int n, int C, const float* w, const float* aux
 void compact(const uint8_t* flags, const int32_t* orig, int n, int32_t* idx1, int32_t* org1, int32_t* idx0,
              int32_t* org0, int32_t* counts, hipStream_t s, const int32_t* nc = nullptr);
 
-// The same partition for large n (reduce-then-scan over 4096-flag blocks);
-// org1 / org0 may be null.  workspace: compact_workspace(n) bytes, 8-byte
-// aligned.  n < 2^31.
+// The same partition for large n (one chained pass over 4096-flag blocks:
+// a clearing kernel, then the pass); org1 / org0 may be null.  workspace:
+// compact_workspace(n) bytes, 8-byte aligned.  n < 2^31.
 size_t compact_workspace(size_t n);
 void compact_large(const uint8_t* flags, const int32_t* orig, size_t n, int32_t* idx1, int32_t* org1, int32_t* idx0,
                    int32_t* org0, int32_t* counts, void* workspace, hipStream_t s, const int32_t* nc = nullptr);

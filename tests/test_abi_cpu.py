@@ -35,7 +35,7 @@ def test_exports_match_headers():
 def test_ops_reject_bad_arguments_without_gpu():
     assert lib.dycl_op_compact_workspace(0) == 0
     assert lib.dycl_op_compact_workspace(100) == 0
-    assert lib.dycl_op_compact_workspace(1 << 20) > (1 << 20) // 4096 * 12
+    assert lib.dycl_op_compact_workspace(1 << 20) >= (1 << 20) // 8192 * 8   # one status word per block
     assert lib.dycl_op_compact(None, None, -1, None, None, None, None, None, None, 0, None) == -1
     assert lib.dycl_op_compact(None, None, 5, None, None, None, None, None, None, 0, None) == -1
     assert lib.dycl_op_move_rows(None, None, None, None, 16, 3, None) == -1

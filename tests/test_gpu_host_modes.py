@@ -110,8 +110,8 @@ def test_device_mode_oracle_parity(name):
 
 
 def test_large_batch_partition_all_modes():
-    # above 16384 rows a decision's partition takes the reduce-then-scan
-    # kernels; device and graph modes hand them the live count on the device
+    # above 16384 rows a decision's partition takes the chained single-pass
+    # kernel; device and graph modes hand it the live count on the device
     rt = _rt()
     B = 40000
     wl, plan = _plan("mlp_exit", max_batch=B)

@@ -1,6 +1,6 @@
 """Routing primitives through include/dycl_ops.h on the GPU: the stable
-two-way partition (single-workgroup form up to 16384 rows, reduce-then-scan
-above) bit-exact against numpy at every density (none,
+two-way partition (single-workgroup form up to 16384 rows, one chained pass
+over blocks of 4096 above) bit-exact against numpy at every density (none,
 rare, half, all set) and ragged sizes, also on a reused workspace that
 starts out dirty, and row gathers / scatters byte-exact."""
 
@@ -50,13 +50,13 @@ def test_compact_is_a_stable_partition(n, density):
 
 
 def test_compact_scan_carries_across_rounds():
-    # 2^26 + 4097 rows: 16385 blocks of 4096 flags, one more than a scan round
-    # holds, so the block offsets of the second round start from the first
-    # round's total
+    # 2^26 + 4097 rows: 16385 blocks of 4096 flags, so a block's prefix is
+    # carried through many look-back windows of 64 blocks, and the last,
+    # all-set block starts from the total of all the others
     import torch
     L = _lib()
     n = (1 << 26) + 4097
-    print(f"[compact] n={n} (two scan rounds)", flush=True)
+    print(f"[compact] n={n} (16385 chained blocks)", flush=True)
     rng = np.random.default_rng(26)
     flags = (rng.random(n, dtype=np.float32) < 0.5).astype(np.uint8)
     flags[-4097:] = 1                       # the second round's block: all set
@@ -81,7 +81,7 @@ def test_compact_scan_carries_across_rounds():
 
 
 def test_compact_reuses_a_dirty_workspace():
-    # every call rewrites the per-block counts and offsets it reads: a
+    # every call clears the block status words and the ticket it uses: a
     # workspace full of garbage, then reused by a smaller call, gives exact
     # partitions
     import torch
@@ -130,6 +130,32 @@ def test_compact_empty_and_null_ids():
     k = (n + 2) // 3
     np.testing.assert_array_equal(i1[:k].cpu().numpy(), np.arange(0, n, 3))
     assert counts.cpu().tolist() == [k, n - k]
+
+
+def test_compact_without_ids_at_full_size():
+    # the form the partition itself needs (flags in, row indices out, no
+    # ids), at 2^26 + 12345 rows, as the bandwidth measurement runs it
+    import torch
+    L = _lib()
+    n = (1 << 26) + 12345
+    print(f"[compact] n={n} without ids", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(3)
+    f = (torch.rand(n, device="cuda", generator=g) < 0.5).to(torch.uint8)
+    i1 = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    i0 = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    counts = torch.zeros(2, dtype=torch.int32, device="cuda")
+    ws_bytes = L.lib.dycl_op_compact_workspace(n)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    L.check(L.lib.dycl_op_compact(C.c_void_p(f.data_ptr()), None, n, C.c_void_p(i1.data_ptr()), None,
+                                  C.c_void_p(i0.data_ptr()), None, C.c_void_p(counts.data_ptr()),
+                                  C.c_void_p(ws.data_ptr()), ws_bytes, None))
+    torch.cuda.synchronize()
+    flags = f.cpu().numpy()
+    ones = np.flatnonzero(flags).astype(np.int32)
+    zeros = np.flatnonzero(flags == 0).astype(np.int32)
+    assert counts.cpu().tolist() == [len(ones), len(zeros)]
+    np.testing.assert_array_equal(i1.cpu().numpy()[:len(ones)], ones)
+    np.testing.assert_array_equal(i0.cpu().numpy()[:len(zeros)], zeros)
 
 
 @pytest.mark.parametrize("row_bytes,n,rows", [(16, 7, 10), (2048, 333, 1000), (128 * 1024, 40, 64)])
