@@ -72,6 +72,7 @@ struct ConvP {
   void* dst;
   int act, out_f32;
   const uint16_t* zeros;   // >= 16 zero bytes: the source of padding taps
+  float* gap;              // conv_lds_kernel: 32-row chunk column sums of the bf16 output, or null
 };
 
 // round to nearest even (v_cvt_pk_bf16_f32; NaN stays NaN), as every
@@ -640,6 +641,32 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
             ov.z = pack_bf16(vv[4], vv[5]);
             ov.w = pack_bf16(vv[6], vv[7]);
             *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.dst) + o) = ov;
+            if (p.gap) {
+              // the stored values back into the staging rows, for the
+              // chunk's column sums below
+              const uint32_t ow[4] = {ov.x, ov.y, ov.z, ov.w};
+              float* e8 = ep + rl * EPW + g * 8;
+              *reinterpret_cast<float4*>(e8) = make_float4(__uint_as_float(ow[0] << 16), __uint_as_float(ow[0] & 0xffff0000u),
+                                                           __uint_as_float(ow[1] << 16), __uint_as_float(ow[1] & 0xffff0000u));
+              *reinterpret_cast<float4*>(e8 + 4) = make_float4(__uint_as_float(ow[2] << 16), __uint_as_float(ow[2] & 0xffff0000u),
+                                                               __uint_as_float(ow[3] << 16), __uint_as_float(ow[3] & 0xffff0000u));
+            }
+          }
+        }
+      }
+      if constexpr (ACT != ACT_LSTM) {
+        const int row0 = m0 + wm * WTM + a * 32;   // a 32-row chunk: all rows < M or none (HoWo % 32 == 0)
+        if (p.gap && !partial && row0 < M) {
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own rows: in-order LDS
+#pragma unroll
+          for (int c0 = 0; c0 < WTN; c0 += 64) {
+            const int c = c0 + lane, col = n0 + wn * WTN + c;
+            if (c < WTN && col < p.cout) {
+              float t = 0.f;
+#pragma unroll 8
+              for (int r = 0; r < 32; ++r) t += ep[r * EPW + c];
+              p.gap[static_cast<size_t>(row0 / 32) * p.cout + col] = t;
+            }
           }
         }
       }
@@ -1714,9 +1741,9 @@ int conv_cout_pad(int cout) {
   return (cout + 31) / 32 * 32;
 }
 
-void conv_bf16(const ConvArgs& a, hipStream_t s) {
-  if (a.pool) return;   // only conv_rgb_stem fuses a max-pool (its dst is the pooled tensor)
-  if (a.cin == 3 && conv_rgb_stem(a, s)) return;
+bool conv_bf16(const ConvArgs& a, hipStream_t s) {
+  if (a.pool) return false;   // only conv_rgb_stem fuses a max-pool (its dst is the pooled tensor)
+  if (a.cin == 3 && conv_rgb_stem(a, s)) return false;
   ConvP p;
   p.src = a.src;
   p.src2 = a.src2;
@@ -1753,6 +1780,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.part = nullptr;
   p.cell_in = a.cell_in;
   p.cell_out = a.cell_out;
+  p.gap = nullptr;
   p.kfold = a.kfold;
   p.fsp = a.fold_sp;
   p.fbp = a.fold_bp;
@@ -1791,7 +1819,7 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
       else if (a.k == 3) go<128, 32, 4, 1, 3, true>(p, s);
       else go<128, 32, 4, 1, 1, true>(p, s);
     }
-    return;
+    return false;
   }
   // tile shapes follow the expected live rows (the grid covers all n)
   const int Mh = (a.nhint > 0 && a.nhint < a.n ? a.nhint : a.n) * a.Ho * a.Wo;
@@ -1802,8 +1830,8 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
   // rows: a layer with row lists takes the register-weight halo kernel
   // (image mode) or the implicit GEMM
   const bool listed = a.src_rows || a.src2_rows || a.res_rows || a.dst_rows;
-  if (conv3_narrow(a, s)) return;   // 16 / 32 channels: row lists allowed
-  if (vec_out && (listed ? conv3_wres(a, s) : (conv3_wres(a, s) || conv3_halo(a, s)))) return;
+  if (conv3_narrow(a, s)) return false;   // 16 / 32 channels: row lists allowed
+  if (vec_out && (listed ? conv3_wres(a, s) : (conv3_wres(a, s) || conv3_halo(a, s)))) return false;
   if (vec_out) {
     // deep K on few pixels per image: K ranges of one tile on several
     // workgroups, fp32 partials summed in a fixed order by a second kernel
@@ -1836,15 +1864,17 @@ void conv_bf16(const ConvArgs& a, hipStream_t s) {
         finish(ksplit_finish_kernel<ACT_GELU>);
       else
         finish(ksplit_finish_kernel<ACT_NONE>);
-      return;
+      return false;
     }
+    if (a.gap_part && !a.out_f32 && !a.dst_rows && a.act != ACT_LSTM && (a.Ho * a.Wo) % 32 == 0)
+      p.gap = a.gap_part;
     if (a.k == 1)
       dispatch_lds<1>(c, p, s);
     else if (a.k == 3)
       dispatch_lds<3>(c, p, s);
     else
       dispatch_lds<7>(c, p, s);
-    return;
+    return p.gap != nullptr;
   }
   const TileCfg c = a.cout >= 128 ? choose(kWide, Mh, a.cout)
                     : a.cout >= 64 ? choose(kMid, Mh, a.cout)

@@ -78,8 +78,18 @@ struct ConvArgs {
   // holds the pooled tensor [n, (Ho - 1) / 2 + 1, (Wo - 1) / 2 + 1, cout]
   // (conv_rgb_stem with ReLU only)
   int pool = 0;
+  // global average pooling of the output taken in the epilogue: when set,
+  // Ho * Wo % 32 == 0, the output is bf16 without a dst list and the layer
+  // runs on the implicit-GEMM kernel without a K split, the sum of each
+  // output column over each 32-row chunk of layer rows (image * Ho * Wo +
+  // pixel; the bf16 values as stored, added in row order) goes to
+  // gap_part[chunk][cout]; conv_bf16 then returns true
+  float* gap_part = nullptr;
 };
-void conv_bf16(const ConvArgs& a, hipStream_t s);
+bool conv_bf16(const ConvArgs& a, hipStream_t s);
+// the pooled features of n images from those chunk sums: G[r][c] = (sum of
+// the HW / 32 chunks of image r, in order) / HW
+void gap_chunks(const float* Q, int n, int HW, int C, float* G, hipStream_t s, const int32_t* nc = nullptr);
 
 // 7x7 stride-2 stems on 3-channel (RGB) input with 64 output channels,
 // W % 8 == 0, output rows of at most 112 pixels: a dedicated kernel reads

@@ -285,6 +285,28 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     if (nd.kind == NodeKind::Exit && !nd.fused && sp.dt == DType::BF16) split_pool = true;
   if (split_pool)
     p->d_Gpart = dev_alloc<float>(p, static_cast<size_t>(k::kGapMaxSplit) * B * sp.max_head_c, "pooling partials");
+  {
+    // an exit head whose input a top-level conv has just written pools from
+    // 32-row chunk sums taken in that conv's epilogue (when the conv's kernel
+    // takes them; else the exit pools the tensor itself)
+    size_t q = 0;
+    std::vector<int> writer(sp.tensors.size(), -1);
+    for (size_t i = 0; i < p->spec.nodes.size(); ++i) {
+      Node& nd = p->spec.nodes[i];
+      if (nd.kind == NodeKind::Exit && !nd.fused && sp.dt == DType::BF16 && nd.src >= 0 && writer[nd.src] >= 0 &&
+          (nd.H * nd.W) % 32 == 0) {
+        Node& cv = p->spec.nodes[writer[nd.src]];
+        if (cv.act != k::ACT_LSTM && !cv.pool && cv.dst_list == 0 && cv.cout == nd.hc) {
+          cv.gap_pool = nd.gap_pool = true;
+          q = std::max(q, static_cast<size_t>(B) * (nd.H * nd.W / 32) * nd.hc);
+        }
+      }
+      // only a conv that directly precedes the exit, on the same rows, counts
+      std::fill(writer.begin(), writer.end(), -1);
+      if (nd.kind == NodeKind::Conv && nd.dst >= 0 && nd.body.empty()) writer[nd.dst] = static_cast<int>(i);
+    }
+    if (q) p->d_gapQ = dev_alloc<float>(p, q, "pooling chunk sums");
+  }
   // K-split partial sums: the largest any bf16 conv layer needs at B rows
   size_t split_bytes = 0;
   std::function<void(const std::vector<Node>&)> walk = [&](const std::vector<Node>& nodes) {
@@ -371,7 +393,7 @@ void plan_free(dycl_plan* p) {
     if (b) hipFree(b);
   void* singles[] = {p->d_blob, p->d_flags, p->d_idx1, p->d_org1, p->d_idx0, p->d_org0, p->d_orig[0],
                      p->d_orig[1], p->d_iota, p->d_counts, p->d_G, p->d_Z, p->d_headP, p->d_S, p->d_zeros,
-                     p->d_xpad, p->d_cws, p->d_Gpart, p->d_split, p->d_tok[0], p->d_tok[1], p->act.h[0],
+                     p->d_xpad, p->d_cws, p->d_Gpart, p->d_gapQ, p->d_split, p->d_tok[0], p->d_tok[1], p->act.h[0],
                      p->act.h[1]};
   for (void* s : singles)
     if (s) hipFree(s);
@@ -410,6 +432,7 @@ struct Run {
   std::string label;         // the node being enqueued (profiling labels)
   const int32_t* orig;       // original ids of the current rows
   int orig_next = 0;         // which d_orig buffer the next compaction fills
+  int gap_tensor = -1;       // tensor whose pooling chunk sums the last conv left in d_gapQ
 
   hipEvent_t event() {
     if (p->ev_free.empty()) {
@@ -589,7 +612,8 @@ struct Run {
     }
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
                                 static_cast<double>(nd.cout) * nd.k * nd.k * cin);
-    launch(P_CONV, flops, bytes, [&] { k::conv_bf16(a, s); });
+    if (nd.gap_pool) a.gap_part = p->d_gapQ;
+    launch(P_CONV, flops, bytes, [&] { gap_tensor = k::conv_bf16(a, s) ? nd.dst : -1; });
   }
 
   // what a profiled launch belongs to: a layer by the tensor it writes (a
@@ -684,6 +708,12 @@ struct Run {
                            nd.ncls, f32(nd.h_T), nd.tau, nd.final_ ? 1 : 0, nd.index, orig, p->d_flags, logits,
                            sp.n_out, rec, s, rows.nc, rows.hint);
             });
+          } else if (sp.dt == DType::BF16 && nd.gap_pool && gap_tensor == nd.src) {
+            // the producing conv left 32-row chunk sums of this tensor
+            launch(P_HEAD, 0, 4.0 * n * (HW / 32 + 1) * nd.hc, [&] {
+              k::gap_chunks(p->d_gapQ, n, HW, nd.hc, p->d_G, s, rows.nc);
+            });
+            G = p->d_G;
           } else if (sp.dt == DType::BF16) {
             launch(P_HEAD, 0, 2.0 * n * HW * nd.hc + 4.0 * n * nd.hc, [&] {
               k::gap_bf16(static_cast<const uint16_t*>(tp[nd.src]), n, HW, nd.hc, p->d_G, p->d_Gpart, s, rows.nc);

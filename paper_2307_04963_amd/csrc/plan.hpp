@@ -87,6 +87,9 @@ struct Node {
   int ncls = 0, hc = 0;
   int head_t = -1;      // index of the transposed fp32 weights (exit heads, fp32 linear layers), or -1
   bool fused = false;   // exit head small enough for the one-kernel path
+  // a conv whose output an exit head pools, with the pooling's partial sums
+  // taken in its epilogue (conv), or that exit head (Exit)
+  bool gap_pool = false;
   float tau = 0.f;
   bool final_ = false;
   int index = 0;        // exit head / gate / loop step
@@ -176,6 +179,7 @@ struct dycl_plan {
   int32_t* h_counts = nullptr;   // pinned
   float* d_G = nullptr;          // [max_batch, max_head_c]
   float* d_Gpart = nullptr;      // [kGapMaxSplit, max_batch, max_head_c] split pooling partials, or null
+  float* d_gapQ = nullptr;       // [max_batch * HW / 32, C] pooling partials from a conv epilogue, or null
   float* d_split = nullptr;      // K-split conv partial sums (largest layer at max_batch rows), or null
   size_t split_bytes = 0;
   float* d_Z = nullptr;          // [max_batch, max_ncls]
