@@ -44,8 +44,10 @@ T* dev_alloc(dycl_plan* p, size_t count, const char* what) {
   void* ptr = nullptr;
   const size_t bytes = std::max<size_t>(count * sizeof(T), 256);
   hipError_t e = hipMalloc(&ptr, bytes);
-  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) {
+    (void)hipGetLastError();   // leave no error behind for the next launch check
     throw OomError(std::string(what) + ": hipMalloc of " + std::to_string(bytes) + " bytes failed");
+  }
   hip_check(e, what);
   p->workspace_bytes += bytes;
   return static_cast<T*>(ptr);
