@@ -416,10 +416,8 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
   auto issue = [&](int kt, int stage) __attribute__((always_inline)) {
     char* sb = smem + stage * STAGE;
     kt += kb;
-    if constexpr (NS >= 2) {
-      // a folded projection's steps (the last kfold of the layout) come first
-      if (p.kfold) kt = kt < p.kfold ? kt + (nk_all - p.kfold) : kt - p.kfold;
-    }
+    // a folded projection's steps (the last kfold of the layout) come first
+    if (p.kfold) kt = kt < p.kfold ? kt + (nk_all - p.kfold) : kt - p.kfold;
     const int kidx = kt * 64 + lchunk * 8;
     int tap = 0, ci = kidx;
     if constexpr (KS != 1) {
@@ -489,7 +487,7 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
   // rounding), divided by the block's scale, so the block's own steps add
   // to it and the epilogue's scale / shift finish the residual sum
   float fsp[TN], fbp[TN], finv[TN];
-  if constexpr (NS >= 2) {
+  {
     if (p.kfold) {
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
@@ -502,7 +500,7 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
     }
   }
   auto fold_round = [&]() __attribute__((always_inline)) {
-    if constexpr (NS >= 2) {
+    {
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
@@ -513,6 +511,27 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
     }
   };
 
+  const bool partial = p.ksplit > 1;   // raw sums; the split reduction finishes them
+  // residual vectors of the rows and 8-channel groups this lane finishes in
+  // the epilogue (below)
+  constexpr int G = WTN / 8;           // 8-channel groups per row
+  constexpr int VI = 32 * G / 64;      // groups per lane in a 32-row block
+  uint4 rv[TM][VI];
+  auto load_res = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int v = 0; v < VI; ++v) {
+        const int idx = v * 64 + lane;
+        const int rl = idx / G, g = idx - (idx / G) * G;
+        const int row = m0 + wm * WTM + a * 32 + rl;
+        const int col = n0 + wn * WTN + g * 8;
+        rv[a][v] = (row < M && col < p.cout)
+                       ? *reinterpret_cast<const uint4*>(p.res + row_at(p.rrows, row, HoWo) * p.cout + col)
+                       : make_uint4(0, 0, 0, 0);
+      }
+  };
+
   // NS-stage pipeline: the loads of step kt+NS-1 are issued while step kt
   // is computed; the stage they fill was read in step kt-1, which every wave
   // finished before the barrier of step kt
@@ -520,11 +539,17 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
   for (int i = 0; i < NS - 1; ++i)
     if (i < nk) issue(i, i);
   if constexpr (NS == 1) {
-    // one K step (Kp == 64): no pipeline, a small LDS footprint, more
-    // workgroups per CU for these memory-bound layers
-    issue(0, 0);
-    wait_vm_barrier<0>();
-    compute(0);
+    // one stage, the K steps one after another (one step, or a few on a
+    // memory-bound layer): a small LDS footprint, more workgroups per CU,
+    // whose number (not the bytes in flight per workgroup) sets the speed
+    // of these layers
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt) __syncthreads();   // every wave is done reading the stage
+      issue(kt, 0);
+      wait_vm_barrier<0>();
+      compute(0);
+      if (kt + 1 == p.kfold) fold_round();
+    }
   } else if (NS == 2 && nk == 2) {
     // both K steps fit the two stages: the second is requested at once, so
     // its latency overlaps the first one's rather than following its MFMAs
@@ -554,30 +579,13 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
   __syncthreads();   // the main loop's last tiles are no longer read
   float* ep = reinterpret_cast<float*>(smem) + wave * 32 * EPW;
   float sc[TN], sh[TN];
-  const bool partial = p.ksplit > 1;   // raw sums; the split reduction finishes them
 #pragma unroll
   for (int b = 0; b < TN; ++b) {
     const int col = n0 + wn * WTN + b * 32 + (lane & 31);
     sc[b] = (!partial && p.scale && col < p.cout) ? p.scale[col] : 1.0f;
     sh[b] = (!partial && p.shift && col < p.cout) ? p.shift[col] : 0.0f;
   }
-  constexpr int G = WTN / 8;           // 8-channel groups per row
-  constexpr int VI = 32 * G / 64;      // groups per lane in a 32-row block
-  uint4 rv[TM][VI];
-  if (p.res && !partial) {
-#pragma unroll
-    for (int a = 0; a < TM; ++a)
-#pragma unroll
-      for (int v = 0; v < VI; ++v) {
-        const int idx = v * 64 + lane;
-        const int rl = idx / G, g = idx - (idx / G) * G;
-        const int row = m0 + wm * WTM + a * 32 + rl;
-        const int col = n0 + wn * WTN + g * 8;
-        rv[a][v] = (row < M && col < p.cout)
-                       ? *reinterpret_cast<const uint4*>(p.res + row_at(p.rrows, row, HoWo) * p.cout + col)
-                       : make_uint4(0, 0, 0, 0);
-      }
-  }
+  if (p.res && !partial) load_res();
   // the activation is chosen once, outside the epilogue's loops
   auto epilogue = [&](auto act_c) __attribute__((always_inline)) {
     constexpr int ACT = decltype(act_c)::value;
@@ -1490,13 +1498,14 @@ void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
 // in ceil(tiles / resident) rounds.  Tiles are compared by rounds times tile
 // area, the time of the slowest CU (measured on the layer shapes of the
 // workloads; 256 x 256 tiles lost on every one of them)
-TileCfg choose_lds(int M, int cout, int Kp) {
+TileCfg choose_lds(int M, int cout, int Kp, bool k1) {
   const TileCfg c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2}, c32{128, 32, 4, 1};
   if (cout < 64) return c32;
-  // one K step: memory-bound; 128 x 64 tiles (24 KB of LDS, five workgroups
-  // per CU by registers) keep the most rows in flight (measured against
-  // 128 x 128, 64 x 64 and 256 x 256 on the ResNet 1x1 layers)
-  if (Kp <= 64) return c12864;
+  // one K step, or a 1x1 layer of up to four: memory-bound; 128 x 64 tiles
+  // (24 KB of LDS, five workgroups per CU by registers) keep the most rows
+  // in flight (measured against 128 x 128, 64 x 128, 64 x 64 and 256 x 64
+  // on the ResNet-50 1x1 layers)
+  if (Kp <= 64 || (k1 && Kp <= 256)) return c12864;
   constexpr long kCUs = 256;
   const long r128 = (tiles_of(c128, M, cout) + 2 * kCUs - 1) / (2 * kCUs);
   const long t12864 = tiles_of(c12864, M, cout), r12864 = (t12864 + 3 * kCUs - 1) / (3 * kCUs);
@@ -1508,16 +1517,22 @@ TileCfg choose_lds(int M, int cout, int Kp) {
   return t12864 > 256 ? c12864 : c64;
 }
 
-// stages: one for a single K step; four for 64 x 64 tiles with eight or
-// more K steps (64 KB of LDS: still two workgroups per CU, three steps of
-// loads in flight; measured 1-6 % faster end to end), else two
+// stages: one for a 1x1 layer of up to four K steps (taken in turn: these
+// layers are bound by the workgroups a CU holds, five with one 24 KB stage
+// against three with two; measured 10-15 % faster on the ResNet-50 1x1
+// shapes with K = 128 .. 256); four for 64 x 64 tiles with eight or more K
+// steps (64 KB of LDS: still two workgroups per CU, three steps of loads in
+// flight; measured 1-6 % faster end to end), else two
 template <int BM, int BN, int WM, int WN, int KS>
 void go_lds(const ConvP& p, hipStream_t s, int S) {
   const dim3 grid(p.mt * p.nt * S);
   constexpr bool small = BM == 64 && BN == 64;
-  if (p.Kp == 64)
-    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
-  else if (small && p.Kp >= 512)
+  bool one = false;
+  if constexpr (KS == 1) one = p.Kp <= 256 && S == 1;
+  if (one) {
+    if constexpr (KS == 1)
+      hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
+  } else if (small && p.Kp >= 512)
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, small ? 4 : 2>), grid, dim3(64 * WM * WN), 0, s, p);
   else
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), grid, dim3(64 * WM * WN), 0, s, p);
@@ -1840,7 +1855,7 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold && !special &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
-                            : choose_lds(Mh, a.cout, p.Kp);
+                            : choose_lds(Mh, a.cout, p.Kp, a.k == 1);
     p.mt = (p.M + c.bm - 1) / c.bm;
     p.nt = (a.cout + c.bn - 1) / c.bn;
     if (split) {

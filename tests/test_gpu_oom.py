@@ -1,9 +1,11 @@
 """Plan creation that cannot get its device memory (include/dycl.h,
-DYCL_E_OOM): a ResNet-50 plan for 2^20 images asks for activation buffers
-of terabytes.  The call returns DYCL_E_OOM with a message naming the
-allocation, hands back no plan, frees what it had allocated (device free
-memory is where it was, over repeated attempts), and leaves the runtime
-usable: a plan of a normal size then builds and runs."""
+DYCL_E_OOM): with all but about 2 GiB of the GPU held by another
+allocation, a ResNet-50 plan for 2048 images (activation buffers of several
+GiB each) cannot be built.  The call returns DYCL_E_OOM with a message
+naming the allocation, hands back no plan, frees what it had allocated
+(device free memory is where it was, over repeated attempts), and leaves
+the runtime usable: once the other allocation is gone, a plan of a normal
+size builds and runs."""
 
 import ctypes as C
 
@@ -26,17 +28,23 @@ def test_oversized_plan_returns_oom_and_leaks_nothing():
     spec = lower_json(wl.arch, man).encode()
     buf = C.create_string_buffer(blob, len(blob))
     torch.cuda.synchronize()
+    free, _ = torch.cuda.mem_get_info()
+    hold = torch.empty(max(free - (2 << 30), 0), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
     free0 = torch.cuda.mem_get_info()[0]
+    print(f"[oom] holding {hold.numel() >> 20} MiB, {free0 >> 20} MiB free", flush=True)
     for attempt in range(3):
-        print(f"[oom] resnet50_exit max_batch=2^20 attempt {attempt}", flush=True)
+        print(f"[oom] resnet50_exit max_batch=2048 attempt {attempt}", flush=True)
         h = C.c_void_p(1)
-        rc = _lib.lib.dycl_plan_create(spec, C.cast(buf, C.c_void_p), len(blob), 1 << 20, 0, C.byref(h))
+        rc = _lib.lib.dycl_plan_create(spec, C.cast(buf, C.c_void_p), len(blob), 2048, 0, C.byref(h))
         assert rc == DYCL_E_OOM, (rc, _lib.last_error())
         assert not h.value
         assert "hipMalloc" in _lib.last_error()
     torch.cuda.synchronize()
     free1 = torch.cuda.mem_get_info()[0]
     assert abs(free1 - free0) < (64 << 20), (free0, free1)
+    del hold
+    torch.cuda.empty_cache()
 
     print("[oom] a normal plan afterwards", flush=True)
     plan = runtime.Plan.from_workload(wl, 4)
