@@ -1501,11 +1501,11 @@ void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
 TileCfg choose_lds(int M, int cout, int Kp, bool k1) {
   const TileCfg c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2}, c32{128, 32, 4, 1};
   if (cout < 64) return c32;
-  // one K step, or a 1x1 layer of up to four: memory-bound; 128 x 64 tiles
-  // (24 KB of LDS, five workgroups per CU by registers) keep the most rows
-  // in flight (measured against 128 x 128, 64 x 128, 64 x 64 and 256 x 64
-  // on the ResNet-50 1x1 layers)
-  if (Kp <= 64 || (k1 && Kp <= 256)) return c12864;
+  // one K step, or a 1x1 convolution of up to 16: 128 x 64 tiles (24 KB of
+  // LDS, five workgroups per CU by registers) keep the most rows in flight
+  // (measured against 128 x 128, 64 x 128, 64 x 64 and 256 x 64 on the
+  // ResNet-50 1x1 layers)
+  if (Kp <= 64 || (k1 && Kp <= 1024)) return c12864;
   constexpr long kCUs = 256;
   const long r128 = (tiles_of(c128, M, cout) + 2 * kCUs - 1) / (2 * kCUs);
   const long t12864 = tiles_of(c12864, M, cout), r12864 = (t12864 + 3 * kCUs - 1) / (3 * kCUs);
@@ -1517,10 +1517,10 @@ TileCfg choose_lds(int M, int cout, int Kp, bool k1) {
   return t12864 > 256 ? c12864 : c64;
 }
 
-// stages: one for a 1x1 layer of up to four K steps (taken in turn: these
-// layers are bound by the workgroups a CU holds, five with one 24 KB stage
-// against three with two; measured 10-15 % faster on the ResNet-50 1x1
-// shapes with K = 128 .. 256); four for 64 x 64 tiles with eight or more K
+// stages: one for a 1x1 convolution of up to 16 K steps (taken in turn:
+// these layers are bound by the workgroups a CU holds, five with one 24 KB
+// stage against three with two; measured 2-20 % faster on the ResNet-50 1x1
+// shapes with K = 128 .. 1024); four for 64 x 64 tiles with eight or more K
 // steps (64 KB of LDS: still two workgroups per CU, three steps of loads in
 // flight; measured 1-6 % faster end to end), else two
 template <int BM, int BN, int WM, int WN, int KS>
@@ -1528,7 +1528,7 @@ void go_lds(const ConvP& p, hipStream_t s, int S) {
   const dim3 grid(p.mt * p.nt * S);
   constexpr bool small = BM == 64 && BN == 64;
   bool one = false;
-  if constexpr (KS == 1) one = p.Kp <= 256 && S == 1;
+  if constexpr (KS == 1) one = p.Kp <= 1024 && S == 1 && p.Ho * p.Wo > 1;
   if (one) {
     if constexpr (KS == 1)
       hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
@@ -1855,7 +1855,7 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold && !special &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
-                            : choose_lds(Mh, a.cout, p.Kp, a.k == 1);
+                            : choose_lds(Mh, a.cout, p.Kp, a.k == 1 && a.Ho * a.Wo > 1);
     p.mt = (p.M + c.bm - 1) / c.bm;
     p.nt = (a.cout + c.bn - 1) / c.bn;
     if (split) {
