@@ -73,6 +73,7 @@ struct ConvP {
   int act, out_f32;
   const uint16_t* zeros;   // >= 16 zero bytes: the source of padding taps
   float* gap;              // conv_lds_kernel: 32-row chunk column sums of the bf16 output, or null
+  int rev;                 // conv_lds_kernel: each XCD walks its tiles last to first
 };
 
 // round to nearest even (v_cvt_pk_bf16_f32; NaN stays NaN), as every
@@ -375,7 +376,7 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
   if (static_cast<int>(blockIdx.x) >= T * p.ksplit) return;
   const int split = blockIdx.x / T;
   const int wg = blockIdx.x - split * T;
-  const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (wg >> 3) : wg;
+  const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (p.rev ? (T8 >> 3) - 1 - (wg >> 3) : (wg >> 3)) : wg;
   const int mtile = t / p.nt;
   const int m0 = mtile * BM, n0 = (t - mtile * p.nt) * BN;
 
@@ -1796,6 +1797,7 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
   p.cell_in = a.cell_in;
   p.cell_out = a.cell_out;
   p.gap = nullptr;
+  p.rev = a.rev;
   p.kfold = a.kfold;
   p.fsp = a.fold_sp;
   p.fbp = a.fold_bp;

@@ -85,6 +85,11 @@ struct ConvArgs {
   // pixel; the bf16 values as stored, added in row order) goes to
   // gap_part[chunk][cout]; conv_bf16 then returns true
   float* gap_part = nullptr;
+  // 1: the implicit GEMM walks each XCD's tiles last to first (the results
+  // do not depend on the order); alternating it from one layer to the next
+  // lets a layer start on the rows its producer wrote last, which the
+  // memory-side cache still holds
+  int rev = 0;
 };
 bool conv_bf16(const ConvArgs& a, hipStream_t s);
 // the pooled features of n images from those chunk sums: G[r][c] = (sum of

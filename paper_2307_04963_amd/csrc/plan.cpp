@@ -435,6 +435,7 @@ struct Run {
   const int32_t* orig;       // original ids of the current rows
   int orig_next = 0;         // which d_orig buffer the next compaction fills
   int gap_tensor = -1;       // tensor whose pooling chunk sums the last conv left in d_gapQ
+  int conv_launches = 0;     // alternates the implicit GEMM's tile order from one layer to the next
 
   hipEvent_t event() {
     if (p->ev_free.empty()) {
@@ -615,6 +616,7 @@ struct Run {
     const double bytes = 2.0 * (static_cast<double>(n) * (nd.H * nd.W * cin + M / n * nd.cout * (nd.res >= 0 ? 2 : 1)) +
                                 static_cast<double>(nd.cout) * nd.k * nd.k * cin);
     if (nd.gap_pool) a.gap_part = p->d_gapQ;
+    a.rev = conv_launches++ & 1;
     launch(P_CONV, flops, bytes, [&] { gap_tensor = k::conv_bf16(a, s) ? nd.dst : -1; });
   }
 
