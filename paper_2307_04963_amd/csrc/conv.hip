@@ -664,17 +664,28 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
         }
       }
       if constexpr (ACT != ACT_LSTM) {
-        const int row0 = m0 + wm * WTM + a * 32;   // a 32-row chunk: all rows < M or none (HoWo % 32 == 0)
+        const int row0 = m0 + wm * WTM + a * 32;   // a 32-row chunk of layer rows
         if (p.gap && !partial && row0 < M) {
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own rows: in-order LDS
+          // rows before `bnd` belong to the chunk's first image, the rest to
+          // the next one (an image has at least 32 rows; rows past M land in
+          // the second sum of the last image's chunk, which is never read)
+          const int bnd = min(32, (row0 / HoWo + 1) * HoWo - row0);
 #pragma unroll
           for (int c0 = 0; c0 < WTN; c0 += 64) {
             const int c = c0 + lane, col = n0 + wn * WTN + c;
             if (c < WTN && col < p.cout) {
-              float t = 0.f;
+              float t0 = 0.f, t1 = 0.f;
+              if (bnd == 32) {
 #pragma unroll 8
-              for (int r = 0; r < 32; ++r) t += ep[r * EPW + c];
-              p.gap[static_cast<size_t>(row0 / 32) * p.cout + col] = t;
+                for (int r = 0; r < 32; ++r) t0 += ep[r * EPW + c];
+              } else {
+                for (int r = 0; r < bnd; ++r) t0 += ep[r * EPW + c];
+                for (int r = bnd; r < 32; ++r) t1 += ep[r * EPW + c];
+              }
+              float* q = p.gap + static_cast<size_t>(row0 / 32) * 2 * p.cout + col;
+              q[0] = t0;
+              if (bnd < 32) q[p.cout] = t1;   // read only for a chunk that crosses into the next image
             }
           }
         }
@@ -1883,8 +1894,7 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
         finish(ksplit_finish_kernel<ACT_NONE>);
       return false;
     }
-    if (a.gap_part && !a.out_f32 && !a.dst_rows && a.act != ACT_LSTM && (a.Ho * a.Wo) % 32 == 0)
-      p.gap = a.gap_part;
+    if (a.gap_part && !a.out_f32 && !a.dst_rows && a.act != ACT_LSTM && a.Ho * a.Wo >= 32) p.gap = a.gap_part;
     if (a.k == 1)
       dispatch_lds<1>(c, p, s);
     else if (a.k == 3)

@@ -127,31 +127,33 @@ __global__ void gap_merge_kernel(const float* __restrict__ P, int n, int HW, int
 }
 
 // pooled features from the 32-row chunk sums a conv epilogue left: one
-// thread per (image, channel), the image's chunks added in order (loaded
-// eight at a time), then divided by HW as gap_merge_kernel does
+// thread per (image, channel); the chunks image r overlaps, in order, each
+// contributing its first part when the chunk starts in image r and its
+// second part when it starts in the image before (loaded eight at a time),
+// then divided by HW as gap_merge_kernel does
 __global__ __launch_bounds__(256) void gap_chunks_kernel(const float* __restrict__ Q, int n, int HW, int C,
                                                          float* __restrict__ G, const int32_t* nc) {
   const size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= static_cast<size_t>(live(nc, n)) * C) return;
   const size_t r = i / C, c = i - r * C;
-  const int nch = HW / 32;
-  const float* q = Q + r * nch * C + c;
-  float t = 0.f;
-  int j = 0;
-  for (; j + 8 <= nch; j += 8) {
+  const size_t j0 = r * HW / 32, j1 = ((r + 1) * HW - 1) / 32;
+  // only the first chunk can start in the image before (HW >= 32)
+  float t = Q[(2 * j0 + ((r * HW) % 32 ? 1 : 0)) * C + c];
+  size_t j = j0 + 1;
+  for (; j + 8 <= j1 + 1; j += 8) {
     float v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = q[static_cast<size_t>(j + u) * C];
+    for (int u = 0; u < 8; ++u) v[u] = Q[2 * (j + u) * C + c];
 #pragma unroll
     for (int u = 0; u < 8; ++u) t += v[u];
   }
-  for (; j < nch; ++j) t += q[static_cast<size_t>(j) * C];
+  for (; j <= j1; ++j) t += Q[2 * j * C + c];
   G[i] = t * (1.0f / static_cast<float>(HW));
 }
 
 void gap_chunks(const float* Q, int n, int HW, int C, float* G, hipStream_t s, const int32_t* nc) {
   if (n <= 0) return;
-  if (HW % 32) throw std::invalid_argument("gap_chunks: HW must be a multiple of 32");
+  if (HW < 32) throw std::invalid_argument("gap_chunks: an image needs at least 32 rows");
   const size_t total = static_cast<size_t>(n) * C;
   hipLaunchKernelGGL(gap_chunks_kernel, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, s, Q, n, HW,
                      C, G, nc);

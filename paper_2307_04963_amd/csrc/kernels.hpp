@@ -79,11 +79,12 @@ struct ConvArgs {
   // (conv_rgb_stem with ReLU only)
   int pool = 0;
   // global average pooling of the output taken in the epilogue: when set,
-  // Ho * Wo % 32 == 0, the output is bf16 without a dst list and the layer
-  // runs on the implicit-GEMM kernel without a K split, the sum of each
-  // output column over each 32-row chunk of layer rows (image * Ho * Wo +
-  // pixel; the bf16 values as stored, added in row order) goes to
-  // gap_part[chunk][cout]; conv_bf16 then returns true
+  // Ho * Wo >= 32, the output is bf16 without a dst list and the layer runs
+  // on the implicit-GEMM kernel without a K split, each output column's sum
+  // over each 32-row chunk of layer rows (image * Ho * Wo + pixel; the bf16
+  // values as stored, added in row order) goes to gap_part[chunk][0][cout],
+  // split at an image boundary inside the chunk: the rows of the next image
+  // to gap_part[chunk][1][cout]; conv_bf16 then returns true
   float* gap_part = nullptr;
   // 1: the implicit GEMM walks each XCD's tiles last to first (the results
   // do not depend on the order); alternating it from one layer to the next
@@ -93,7 +94,7 @@ struct ConvArgs {
 };
 bool conv_bf16(const ConvArgs& a, hipStream_t s);
 // the pooled features of n images from those chunk sums: G[r][c] = (sum of
-// the HW / 32 chunks of image r, in order) / HW
+// image r's parts of the chunks it overlaps, in chunk order) / HW
 void gap_chunks(const float* Q, int n, int HW, int C, float* G, hipStream_t s, const int32_t* nc = nullptr);
 
 // 7x7 stride-2 stems on 3-channel (RGB) input with 64 output channels,

@@ -296,11 +296,11 @@ int plan_build(dycl_plan* p, const std::string& json, const void* weights, size_
     for (size_t i = 0; i < p->spec.nodes.size(); ++i) {
       Node& nd = p->spec.nodes[i];
       if (nd.kind == NodeKind::Exit && !nd.fused && sp.dt == DType::BF16 && nd.src >= 0 && writer[nd.src] >= 0 &&
-          (nd.H * nd.W) % 32 == 0) {
+          nd.H * nd.W >= 32) {
         Node& cv = p->spec.nodes[writer[nd.src]];
         if (cv.act != k::ACT_LSTM && !cv.pool && cv.dst_list == 0 && cv.cout == nd.hc) {
           cv.gap_pool = nd.gap_pool = true;
-          q = std::max(q, static_cast<size_t>(B) * (nd.H * nd.W / 32) * nd.hc);
+          q = std::max(q, (static_cast<size_t>(B) * nd.H * nd.W + 31) / 32 * 2 * nd.hc);
         }
       }
       // only a conv that directly precedes the exit, on the same rows, counts
@@ -714,7 +714,7 @@ struct Run {
             });
           } else if (sp.dt == DType::BF16 && nd.gap_pool && gap_tensor == nd.src) {
             // the producing conv left 32-row chunk sums of this tensor
-            launch(P_HEAD, 0, 4.0 * n * (HW / 32 + 1) * nd.hc, [&] {
+            launch(P_HEAD, 0, 4.0 * n * (HW / 32.0 + 2) * nd.hc, [&] {
               k::gap_chunks(p->d_gapQ, n, HW, nd.hc, p->d_G, s, rows.nc);
             });
             G = p->d_G;

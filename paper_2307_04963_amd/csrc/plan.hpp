@@ -179,7 +179,7 @@ struct dycl_plan {
   int32_t* h_counts = nullptr;   // pinned
   float* d_G = nullptr;          // [max_batch, max_head_c]
   float* d_Gpart = nullptr;      // [kGapMaxSplit, max_batch, max_head_c] split pooling partials, or null
-  float* d_gapQ = nullptr;       // [max_batch * HW / 32, C] pooling partials from a conv epilogue, or null
+  float* d_gapQ = nullptr;       // [ceil(max_batch * HW / 32), 2, C] pooling chunk sums from a conv epilogue, or null
   float* d_split = nullptr;      // K-split conv partial sums (largest layer at max_batch rows), or null
   size_t split_bytes = 0;
   float* d_Z = nullptr;          // [max_batch, max_ncls]
