@@ -1510,14 +1510,14 @@ void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
 // in ceil(tiles / resident) rounds.  Tiles are compared by rounds times tile
 // area, the time of the slowest CU (measured on the layer shapes of the
 // workloads; 256 x 256 tiles lost on every one of them)
-TileCfg choose_lds(int M, int cout, int Kp, bool k1) {
+TileCfg choose_lds(int M, int cout, int Kp) {
   const TileCfg c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2}, c32{128, 32, 4, 1};
   if (cout < 64) return c32;
-  // one K step, or a 1x1 convolution of up to 16: 128 x 64 tiles (24 KB of
-  // LDS, five workgroups per CU by registers) keep the most rows in flight
-  // (measured against 128 x 128, 64 x 128, 64 x 64 and 256 x 64 on the
-  // ResNet-50 1x1 layers)
-  if (Kp <= 64 || (k1 && Kp <= 1024)) return c12864;
+  // one K step: memory-bound; 128 x 64 tiles (24 KB of LDS, five
+  // workgroups per CU by registers) keep the most rows in flight (measured
+  // against 128 x 128, 64 x 128, 64 x 64 and 256 x 64 on the ResNet-50 1x1
+  // layers)
+  if (Kp <= 64) return c12864;
   constexpr long kCUs = 256;
   const long r128 = (tiles_of(c128, M, cout) + 2 * kCUs - 1) / (2 * kCUs);
   const long t12864 = tiles_of(c12864, M, cout), r12864 = (t12864 + 3 * kCUs - 1) / (3 * kCUs);
@@ -1529,21 +1529,22 @@ TileCfg choose_lds(int M, int cout, int Kp, bool k1) {
   return t12864 > 256 ? c12864 : c64;
 }
 
-// stages: one for a 1x1 convolution of up to 16 K steps (taken in turn:
-// these layers are bound by the workgroups a CU holds, five with one 24 KB
-// stage against three with two; measured 2-20 % faster on the ResNet-50 1x1
-// shapes with K = 128 .. 1024); four for 64 x 64 tiles with eight or more K
-// steps (64 KB of LDS: still two workgroups per CU, three steps of loads in
-// flight; measured 1-6 % faster end to end), else two
+// stages: one (`one`, 128 x 64 tiles only: the K steps taken in turn) where
+// the workgroups a CU holds bound the layer, five with one 24 KB stage
+// against three with two: measured 2-20 % faster on the ResNet-50 1x1
+// shapes with K = 128 .. 1024 and 8-16 % on its strided 3x3 layers with 2.5
+// or more tiles per CU (slower with fewer); four for 64 x 64 tiles with
+// eight or more K steps (64 KB of LDS: still two workgroups per CU, three
+// steps of loads in flight; measured 1-6 % faster end to end), else two
 template <int BM, int BN, int WM, int WN, int KS>
-void go_lds(const ConvP& p, hipStream_t s, int S) {
+void go_lds(const ConvP& p, hipStream_t s, int S, bool one) {
   const dim3 grid(p.mt * p.nt * S);
   constexpr bool small = BM == 64 && BN == 64;
-  bool one = false;
-  if constexpr (KS == 1) one = p.Kp <= 1024 && S == 1 && p.Ho * p.Wo > 1;
-  if (one) {
-    if constexpr (KS == 1)
+  if (one && S == 1) {
+    if constexpr (BM == 128 && BN == 64)
       hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
+    else
+      throw std::invalid_argument("conv_bf16: the one-stage implicit GEMM takes 128 x 64 tiles only");
   } else if (small && p.Kp >= 512)
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, small ? 4 : 2>), grid, dim3(64 * WM * WN), 0, s, p);
   else
@@ -1551,12 +1552,12 @@ void go_lds(const ConvP& p, hipStream_t s, int S) {
 }
 
 template <int KS>
-void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s, int S = 1) {
+void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s, int S = 1, bool one = false) {
   switch (c.bm * 1000 + c.bn) {
-    case 128128: go_lds<128, 128, 2, 2, KS>(p, s, S); break;
-    case 128064: go_lds<128, 64, 2, 2, KS>(p, s, S); break;
-    case 64064: go_lds<64, 64, 2, 2, KS>(p, s, S); break;
-    default: go_lds<128, 32, 4, 1, KS>(p, s, S); break;
+    case 128128: go_lds<128, 128, 2, 2, KS>(p, s, S, one); break;
+    case 128064: go_lds<128, 64, 2, 2, KS>(p, s, S, one); break;
+    case 64064: go_lds<64, 64, 2, 2, KS>(p, s, S, one); break;
+    default: go_lds<128, 32, 4, 1, KS>(p, s, S, one); break;
   }
 }
 
@@ -1867,8 +1868,13 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     const int S = conv_ksplit(a.Ho, a.Wo, a.cout, p.K, a.out_f32 != 0);
     const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold && !special &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
+    // one LDS stage on 128 x 64 tiles: a spatial 1x1 layer with K <= 1024,
+    // or any other spatial layer with at least 512 such tiles
+    const long t12864 = (static_cast<long>(Mh) + 127) / 128 * ((a.cout + 63) / 64);
+    const bool one = !split && a.cout >= 64 && a.Ho * a.Wo > 1 && (a.k == 1 ? p.Kp <= 1024 : t12864 >= 512);
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
-                            : choose_lds(Mh, a.cout, p.Kp, a.k == 1 && a.Ho * a.Wo > 1);
+                      : one ? TileCfg{128, 64, 2, 2}
+                            : choose_lds(Mh, a.cout, p.Kp);
     p.mt = (p.M + c.bm - 1) / c.bm;
     p.nt = (a.cout + c.bn - 1) / c.bn;
     if (split) {
@@ -1896,11 +1902,11 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     }
     if (a.gap_part && !a.out_f32 && !a.dst_rows && a.act != ACT_LSTM && a.Ho * a.Wo >= 32) p.gap = a.gap_part;
     if (a.k == 1)
-      dispatch_lds<1>(c, p, s);
+      dispatch_lds<1>(c, p, s, 1, one);
     else if (a.k == 3)
-      dispatch_lds<3>(c, p, s);
+      dispatch_lds<3>(c, p, s, 1, one);
     else
-      dispatch_lds<7>(c, p, s);
+      dispatch_lds<7>(c, p, s, 1, one);
     return p.gap != nullptr;
   }
   const TileCfg c = a.cout >= 128 ? choose(kWide, Mh, a.cout)
