@@ -81,6 +81,11 @@ CASES = [
     (2000, 8, 8, 128, 256, 3, 2, 1, False, 1),  # 128-pixel tiles, several units per workgroup
     (2500, 8, 8, 128, 256, 3, 2, 1, True, 1),   # 256-pixel tiles, several units per workgroup
     (3, 6, 6, 600, 64, 1, 1, 0, False, 1),      # K = 600: the last step is partly padding
+    (24, 56, 56, 64, 256, 1, 1, 0, True, 1),    # one stage, 128 x 256 tiles (588 of them), residual
+    (24, 56, 56, 128, 256, 1, 1, 0, False, 2),  # one stage, 128 x 256 tiles, two K steps in turn, GELU
+    (48, 28, 28, 384, 512, 1, 1, 0, True, 1),   # one stage, 128 x 256 tiles, six K steps, residual
+    (40, 28, 28, 512, 128, 1, 1, 0, False, 1),  # one stage, 128 x 64 tiles, eight K steps
+    (42, 56, 56, 128, 128, 3, 2, 1, False, 1),  # strided 3x3 on one stage (516 tiles of 128 x 64)
 ]
 
 
