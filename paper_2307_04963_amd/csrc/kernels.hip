@@ -1224,7 +1224,24 @@ __global__ __launch_bounds__(256) void decode_step_kernel(const float* __restric
   const int V4 = V / 4;
   float bv = -INFINITY;
   int bi = V;
-  for (int j = lane; j < V4; j += 64) {
+  // sixteen 16-byte loads in flight per lane before the comparisons (the
+  // winner, the largest value and the lowest index among equals, does not
+  // depend on the order in which a lane visits its values)
+  int j = lane;
+  for (; j + 64 * 15 < V4; j += 64 * 16) {
+    float4 q[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) q[u] = zr[j + 64 * u];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int i0 = 4 * (j + 64 * u);
+      better(q[u].x, i0, bv, bi);
+      better(q[u].y, i0 + 1, bv, bi);
+      better(q[u].z, i0 + 2, bv, bi);
+      better(q[u].w, i0 + 3, bv, bi);
+    }
+  }
+  for (; j < V4; j += 64) {
     const float4 q = zr[j];
     better(q.x, 4 * j, bv, bi);
     better(q.y, 4 * j + 1, bv, bi);
@@ -1248,7 +1265,7 @@ __global__ __launch_bounds__(256) void decode_step_kernel(const float* __restric
   }
   if (done) {
     float4* lr = reinterpret_cast<float4*>(logits + static_cast<size_t>(o) * V);
-    for (int j = lane; j < V4; j += 64) lr[j] = zr[j];
+    for (int jj = lane; jj < V4; jj += 64) lr[jj] = zr[jj];
   }
 }
 
