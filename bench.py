@@ -21,8 +21,11 @@ Prints one JSON line:
   cpu_baseline the oracle (plain per-sample CPU interpreter) on a bounded
                sample of the same workload, on every host core (parallel
                across samples) and on one core;
-  other_workloads  samples/s of the other four workloads at their own
-               batches (device host mode, same step count).
+  other_workloads  samples/s of every other workload at its own batch
+               (device host mode, same step count);
+  hbm_kernels  the routing primitives at HBM-bound sizes: the 2^26-flag
+               partition (flags to row indices, and carrying ids) and a
+               gather of 1.5 MiB rows.
 """
 
 from __future__ import annotations
