@@ -129,7 +129,7 @@ __global__ void gap_merge_kernel(const float* __restrict__ P, int n, int HW, int
 // pooled features from the 32-row chunk sums a conv epilogue left: one
 // thread per (image, channel); the chunks image r overlaps, in order, each
 // contributing its first part when the chunk starts in image r and its
-// second part when it starts in the image before (loaded eight at a time),
+// second part when it starts in the image before (up to 32 loads in flight),
 // then divided by HW as gap_merge_kernel does
 __global__ __launch_bounds__(256) void gap_chunks_kernel(const float* __restrict__ Q, int n, int HW, int C,
                                                          float* __restrict__ G, const int32_t* nc) {
@@ -140,6 +140,13 @@ __global__ __launch_bounds__(256) void gap_chunks_kernel(const float* __restrict
   // only the first chunk can start in the image before (HW >= 32)
   float t = Q[(2 * j0 + ((r * HW) % 32 ? 1 : 0)) * C + c];
   size_t j = j0 + 1;
+  for (; j + 32 <= j1 + 1; j += 32) {
+    float v[32];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) v[u] = Q[2 * (j + u) * C + c];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) t += v[u];
+  }
   for (; j + 8 <= j1 + 1; j += 8) {
     float v[8];
 #pragma unroll
