@@ -362,7 +362,7 @@ __global__ __launch_bounds__(256) void head_partial_kernel(const float* __restri
                                                            const float* __restrict__ Wt, int N, int S,
                                                            float* __restrict__ P, int nP, const int32_t* nc) {
   constexpr int R = 8, KSMAX = 132;
-  __shared__ float xs[R][KSMAX];
+  __shared__ __align__(16) float xs[KSMAX][R];   // k-major: a k's 8 rows in two 16-byte reads
   __shared__ float red[4][R][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gy = (N + 63) / 64;
@@ -397,7 +397,7 @@ __global__ __launch_bounds__(256) void head_partial_kernel(const float* __restri
     const int e = threadIdx.x + 256 * i;
     if (e < R * ks) {
       const int r = e / ks, kk = e - r * ks;
-      xs[r][kk] = m0 + r < n ? xv[i] : 0.f;
+      xs[kk][r] = m0 + r < n ? xv[i] : 0.f;
     }
   }
   __syncthreads();
@@ -407,9 +407,13 @@ __global__ __launch_bounds__(256) void head_partial_kernel(const float* __restri
 #pragma unroll
   for (int i = 0; i < KI; ++i) {
     const int kk = w + 4 * i;
-    if (kk < ks)
+    if (kk < ks) {
+      const float4 x0 = *reinterpret_cast<const float4*>(&xs[kk][0]);
+      const float4 x1 = *reinterpret_cast<const float4*>(&xs[kk][4]);
+      const float xr[R] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
-      for (int r = 0; r < R; ++r) acc[r] = fmaf(xs[r][kk], wv[i], acc[r]);
+      for (int r = 0; r < R; ++r) acc[r] = fmaf(xr[r], wv[i], acc[r]);
+    }
   }
 #pragma unroll
   for (int r = 0; r < R; ++r) red[w][r][lane] = acc[r];
