@@ -712,8 +712,11 @@ __global__ __launch_bounds__(1024) void compact_kernel(const uint8_t* __restrict
   for (int start = 0; start < n; start += 1024) {
     const int i = start + tid;
     const bool valid = i < n;
-    const bool f = valid && flags[i] != 0;
-    const bool g = valid && flags[i] == 0;
+    // the row's id requested with its flag: one memory round trip, not two
+    const int32_t id = valid && orig ? orig[i] : i;
+    const uint8_t fl = valid ? flags[i] : 0;
+    const bool f = valid && fl != 0;
+    const bool g = valid && fl == 0;
     const uint64_t b1 = __ballot(f);
     const uint64_t b0 = __ballot(g);
     const int r1 = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b1 >> 32),
@@ -738,11 +741,11 @@ __global__ __launch_bounds__(1024) void compact_kernel(const uint8_t* __restrict
     }
     if (f) {
       idx1[off1 + r1] = i;
-      org1[off1 + r1] = orig ? orig[i] : i;
+      org1[off1 + r1] = id;
     }
     if (g) {
       idx0[off0 + r0] = i;
-      org0[off0 + r0] = orig ? orig[i] : i;
+      org0[off0 + r0] = id;
     }
     base1 += t1;
     base0 += t0;
