@@ -64,7 +64,11 @@ typedef struct {
  *                 "gate" (pool, linear, sigmoid, run a sub-list of nodes
  *                 on the samples that execute), "halt" (halting unit of a
  *                 bounded loop, unrolled) and "output" (final linear on the
- *                 loop's parked states).  Copied, not retained.
+ *                 loop's parked states).  Optional "pair_pointwise": false
+ *                 runs every layer in its own launch (by default a
+ *                 bottleneck's last 1x1 convolution and the next 1x1
+ *                 convolution share one; the results are the same bits
+ *                 either way).  Copied, not retained.
  *   weights       host pointer to the weight blob the spec's offsets index;
  *                 copied to the device, not retained.
  *   weights_bytes size of that blob.
@@ -194,8 +198,8 @@ int dycl_profile_launches(dycl_plan* plan, double* rows, int cap);
 /*
  * Label of launch i of the rows dycl_profile_launches returned: the node it
  * belongs to - a layer by the tensor it writes (with the projection folded
- * into it, or the fused max-pool), a decision as "exit k", "gate k" or
- * "halt k".  "" for an index out of range or an invalid plan.  The string
+ * into it, or the fused max-pool; "a + b" for two 1x1 layers in one
+ * launch), a decision as "exit k", "gate k" or "halt k".  "" for an index out of range or an invalid plan.  The string
  * lives in the plan until its next profiled run.
  */
 const char* dycl_profile_launch_label(const dycl_plan* plan, int i);

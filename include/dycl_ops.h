@@ -140,6 +140,26 @@ int dycl_op_conv_maxpool(const uint16_t* x, int n, int H, int W, int cin, const 
                          int stride, int pad, const float* scale, const float* shift, int act, uint16_t* y,
                          void* hip_stream);
 
+/*
+ * A bottleneck block's last 1x1 convolution and the next block's first 1x1
+ * convolution, which reads nothing but its output, in one launch (two
+ * layers of one sub-DNN node in succession, Sec. 5.3; dycl_run runs such
+ * pairs this way unless the spec says "pair_pointwise": false):
+ *   y3 = dycl_op_conv(x, packed3, c3, k 1, stride 1, pad 0, scale3, shift3, res, act 1)
+ *   y1 = dycl_op_conv(y3, packed1, c1, k 1, stride 1, pad 0, scale1, shift1, NULL, act 1)
+ * bit for bit; each tile of y3 stays on chip for the second contraction, so
+ * y3 is written once and never read back.  Taken for cin % 64 == 0, 64 <=
+ * cin <= 1024, c3 256, c1 64 (ResNet-50's first stage) and ReLU on both;
+ * other shapes return DYCL_E_INVALID.  x [n][H][W][cin], res [n][H][W][c3]
+ * or NULL, y3 [n][H][W][c3], y1 [n][H][W][c1]; packed3 / packed1 from
+ * dycl_op_conv_pack (k 1; cin and c3 input channels); scale / shift [cout]
+ * float32, all four required; device pointers, 16-byte aligned; n >= 0 (0
+ * does nothing).  Work is queued on hip_stream.
+ */
+int dycl_op_conv_pair(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed3, const float* scale3,
+                      const float* shift3, const uint16_t* res, int c3, uint16_t* y3, const uint16_t* packed1,
+                      const float* scale1, const float* shift1, int c1, uint16_t* y1, void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -21,7 +21,8 @@ EXPORTS = ["dycl_plan_create", "dycl_run", "dycl_run_seq", "dycl_plan_set_host_m
            "dycl_profile_read", "dycl_profile_launches", "dycl_profile_launch_label", "dycl_profile_class", "dycl_spec_check", "dycl_plan_destroy", "dycl_last_error"]
 # every symbol include/dycl_ops.h declares
 OPS_EXPORTS = ["dycl_op_compact_workspace", "dycl_op_compact", "dycl_op_compact_noalloc", "dycl_op_move_rows", "dycl_op_conv_packed_bytes",
-               "dycl_op_conv_pack", "dycl_op_conv_workspace_bytes", "dycl_op_conv", "dycl_op_conv_maxpool"]
+               "dycl_op_conv_pack", "dycl_op_conv_workspace_bytes", "dycl_op_conv", "dycl_op_conv_maxpool",
+               "dycl_op_conv_pair"]
 
 
 class DyclError(RuntimeError):
@@ -91,6 +92,8 @@ def _load():
     lib.dycl_op_conv.restype = i32
     lib.dycl_op_conv_maxpool.argtypes = [vp, i32, i32, i32, i32, vp, i32, i32, i32, i32, vp, vp, i32, vp, vp]
     lib.dycl_op_conv_maxpool.restype = i32
+    lib.dycl_op_conv_pair.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, vp, i32, vp, vp]
+    lib.dycl_op_conv_pair.restype = i32
     return lib
 
 

@@ -1,5 +1,6 @@
 // C ABI: argument checks, error mapping, and the thread-local message.
 // Nothing thrown inside the library crosses this boundary.
+#include <algorithm>
 #include <cstring>
 #include <new>
 #include <string>
@@ -469,3 +470,51 @@ int dycl_op_conv_maxpool(const uint16_t* x, int n, int H, int W, int cin, const 
 }
 
 }  // extern "C"
+
+int dycl_op_conv_pair(const uint16_t* x, int n, int H, int W, int cin, const uint16_t* packed3, const float* scale3,
+                      const float* shift3, const uint16_t* res, int c3, uint16_t* y3, const uint16_t* packed1,
+                      const float* scale1, const float* shift1, int c1, uint16_t* y1, void* hip_stream) {
+  if (n < 0) return fail(DYCL_E_INVALID, "dycl_op_conv_pair: n < 0");
+  if (H < 1 || W < 1 || !dycl::k::conv_pair_fits(cin, 0, c3, c1, dycl::k::ACT_RELU, dycl::k::ACT_RELU))
+    return fail(DYCL_E_INVALID, "dycl_op_conv_pair: needs H, W >= 1, cin % 64 == 0 in [64, 1024], c3 256, c1 64");
+  const long lim = 1L << 31;
+  if (static_cast<long>(n) * H * W * std::max(cin, c3) >= lim)
+    return fail(DYCL_E_INVALID, "dycl_op_conv_pair: a tensor reaches 2^31 elements");
+  if (n == 0) return DYCL_OK;
+  if (!x || !packed3 || !y3 || !packed1 || !y1 || !scale3 || !shift3 || !scale1 || !shift1)
+    return fail(DYCL_E_INVALID, "dycl_op_conv_pair: null tensor, weights or scale / shift vector");
+  const void* ptrs[] = {x, packed3, scale3, shift3, res, y3, packed1, scale1, shift1, y1};
+  for (const void* q : ptrs)
+    if (reinterpret_cast<uintptr_t>(q) & 15)
+      return fail(DYCL_E_INVALID, "dycl_op_conv_pair: every pointer must be 16-byte aligned");
+  return guarded([&] {
+    const uint16_t* zeros = dycl::k::zero_page();
+    if (!zeros) throw dycl::HipError("dycl_op_conv_pair: zero page unavailable");
+    dycl::k::PairArgs a;
+    a.x = x;
+    a.K3 = cin;
+    a.w3 = packed3;
+    a.Kp3 = static_cast<int>(dycl_op_conv_packed_bytes(c3, 1, cin) / 2 / dycl::k::conv_cout_pad(c3));
+    a.scale3 = scale3;
+    a.shift3 = shift3;
+    a.res = res;
+    a.y3 = y3;
+    a.C3 = c3;
+    a.w1 = packed1;
+    a.Kp1 = static_cast<int>(dycl_op_conv_packed_bytes(c1, 1, c3) / 2 / dycl::k::conv_cout_pad(c1));
+    a.scale1 = scale1;
+    a.shift1 = shift1;
+    a.y1 = y1;
+    a.C1 = c1;
+    a.act3 = dycl::k::ACT_RELU;
+    a.act1 = dycl::k::ACT_RELU;
+    a.n = n;
+    a.H = H;
+    a.W = W;
+    a.zeros = zeros;
+    if (!dycl::k::conv_pair(a, static_cast<hipStream_t>(hip_stream)))
+      throw dycl::HipError("dycl_op_conv_pair: the fused kernel declined the arguments");
+    if (hipGetLastError() != hipSuccess) throw dycl::HipError("dycl_op_conv_pair: launch failed");
+    return DYCL_OK;
+  });
+}

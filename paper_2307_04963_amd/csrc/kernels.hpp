@@ -93,6 +93,51 @@ struct ConvArgs {
   int rev = 0;
 };
 bool conv_bf16(const ConvArgs& a, hipStream_t s);
+
+// A bottleneck block's last 1x1 layer and the next block's first 1x1 layer
+// in one kernel (both stride 1, no row lists):
+//   y3 = act3(scale3 * (x W3^T) + shift3 + res)   [n * H * W][C3]
+//   y1 = act1(scale1 * (y3 W1^T) + shift1)        [n * H * W][C1]
+// with packed weights w3 [>= C3][Kp3] and w1 [>= C1][Kp1] (C3 used).  The
+// first layer may carry a folded projection shortcut instead of a residual
+// (x2 set; ConvArgs::kfold and its vectors): x2 [n][H2][W2][K2] read at
+// stride s2, whose K steps are the last K2 / 64 of w3.  Both outputs are bit
+// for bit those of the two layers launched one by one through conv_bf16.
+// Every pointer 16-byte aligned; ncount, when set, is the device count of
+// live images (<= n).  conv_pair_fits says whether the kernel takes a shape,
+// conv_pair_takes whether it takes an argument set; conv_pair returns false
+// (launching nothing) when the arguments do not qualify.
+struct PairArgs {
+  const uint16_t* x = nullptr;
+  int K3 = 0;                          // channels of x
+  const uint16_t* x2 = nullptr;        // a folded projection's input, or null
+  int K2 = 0, H2 = 0, W2 = 0, s2 = 1;
+  const float* fold_sp = nullptr;
+  const float* fold_bp = nullptr;
+  const float* fold_inv = nullptr;
+  const uint16_t* w3 = nullptr;
+  int Kp3 = 0;
+  const float* scale3 = nullptr;
+  const float* shift3 = nullptr;
+  const uint16_t* res = nullptr;       // or null
+  uint16_t* y3 = nullptr;
+  int C3 = 0;
+  const uint16_t* w1 = nullptr;
+  int Kp1 = 0;
+  const float* scale1 = nullptr;
+  const float* shift1 = nullptr;
+  uint16_t* y1 = nullptr;
+  int C1 = 0;
+  int act3 = 0, act1 = 0;
+  int n = 0, H = 0, W = 0;
+  const int32_t* ncount = nullptr;
+  const uint16_t* zeros = nullptr;
+  int rev = 0;   // as ConvArgs::rev
+};
+bool conv_pair_fits(int K3, int K2, int C3, int C1, int act3, int act1);
+bool conv_pair_takes(const PairArgs& a);
+bool conv_pair(const PairArgs& a, hipStream_t s);
+
 // the pooled features of n images from those chunk sums: G[r][c] = (sum of
 // image r's parts of the chunks it overlaps, in chunk order) / HW
 void gap_chunks(const float* Q, int n, int HW, int C, float* G, hipStream_t s, const int32_t* nc = nullptr);

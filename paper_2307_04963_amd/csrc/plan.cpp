@@ -620,6 +620,67 @@ struct Run {
     launch(P_CONV, flops, bytes, [&] { gap_tensor = k::conv_bf16(a, s) ? nd.dst : -1; });
   }
 
+  // a conv and the 1x1 conv after it in one launch (Spec::pair_pointwise);
+  // false: the kernel does not take this argument set and nothing ran
+  bool pair(const Node& c, const Node& d, Rows r) {
+    const Spec& sp = p->spec;
+    if (d.kind != NodeKind::Conv || d.gap_pool || c.gap_pool) return false;
+    const int n = r.n;
+    const Packed& q3 = sp.packed[c.packed];
+    const Packed& q1 = sp.packed[d.packed];
+    k::PairArgs a;
+    a.x = static_cast<const uint16_t*>(tp[c.src]);
+    a.K3 = c.cin1;
+    if (c.fold) {
+      const float* fs = p->fold_shift[c.fold_shift];
+      a.x2 = static_cast<const uint16_t*>(tp[c.src2]);
+      a.K2 = c.cin2;
+      a.H2 = sp.tensors[c.src2].H;
+      a.W2 = sp.tensors[c.src2].W;
+      a.s2 = c.s2;
+      a.scale3 = fs;
+      a.shift3 = fs + c.cout;
+      a.fold_sp = fs + 2 * c.cout;
+      a.fold_bp = fs + 3 * c.cout;
+      a.fold_inv = fs + 4 * c.cout;
+    } else {
+      a.scale3 = f32(c.scale_off);
+      a.shift3 = f32(c.shift_off);
+      a.res = c.res >= 0 ? static_cast<const uint16_t*>(tp[c.res]) : nullptr;
+    }
+    a.w3 = q3.dev;
+    a.Kp3 = q3.Kp;
+    a.y3 = static_cast<uint16_t*>(tp[c.dst]);
+    a.C3 = c.cout;
+    a.w1 = q1.dev;
+    a.Kp1 = q1.Kp;
+    a.scale1 = f32(d.scale_off);
+    a.shift1 = f32(d.shift_off);
+    a.y1 = static_cast<uint16_t*>(tp[d.dst]);
+    a.C1 = d.cout;
+    a.act3 = c.act;
+    a.act1 = d.act;
+    a.n = n;
+    a.H = c.Ho;
+    a.W = c.Wo;
+    a.ncount = r.nc;
+    a.zeros = p->d_zeros;
+    a.rev = conv_launches & 1;
+    if (!k::conv_pair_takes(a)) return false;
+    const double M = static_cast<double>(n) * c.Ho * c.Wo;
+    const double x2 = c.fold ? static_cast<double>(n) * c.Ho * c.Wo * c.cin2 : 0.0;   // read at the output pixels
+    const double flops = 2.0 * M * (static_cast<double>(c.cout) * (c.cin1 + c.cin2) + static_cast<double>(d.cout) * d.cin1);
+    const double bytes = 2.0 * (M * (c.cin1 + c.cout * (c.res >= 0 ? 2.0 : 1.0) + d.cout) + x2 +
+                                static_cast<double>(c.cout) * (c.cin1 + c.cin2) + static_cast<double>(d.cout) * d.cin1);
+    if (p->profile) label = node_label(c) + " + " + node_label(d);
+    launch(P_CONV, flops, bytes, [&] {
+      if (!k::conv_pair(a, s)) throw HipError("conv pair: arguments the kernel does not take");
+    });
+    ++conv_launches;
+    gap_tensor = -1;
+    return true;
+  }
+
   // what a profiled launch belongs to: a layer by the tensor it writes (a
   // folded projection named with it), a decision by its kind and index
   std::string node_label(const Node& nd) const {
@@ -690,7 +751,13 @@ struct Run {
       if (p->profile) label = node_label(nd);
       switch (nd.kind) {
         case NodeKind::Conv:
-          if (n > 0) conv(nd, rows);
+          if (n > 0) {
+            if (nd.pair && ni + 1 < last && pair(nd, nodes[ni + 1], rows)) {
+              ++ni;   // the second conv ran in the same launch
+              break;
+            }
+            conv(nd, rows);
+          }
           break;
         case NodeKind::MaxPool:
           if (n > 0) {

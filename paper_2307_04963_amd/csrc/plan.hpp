@@ -90,6 +90,9 @@ struct Node {
   // a conv whose output an exit head pools, with the pooling's partial sums
   // taken in its epilogue (conv), or that exit head (Exit)
   bool gap_pool = false;
+  // this conv and the next node (a 1x1 conv reading only its output) run as
+  // one kernel (conv_pair) when the kernel takes them
+  bool pair = false;
   float tau = 0.f;
   bool final_ = false;
   int index = 0;        // exit head / gate / loop step
@@ -141,6 +144,7 @@ struct Spec {
   int fused_gates = 0;     // gates whose gathers and scatters are fused into the body convolutions
   int fused_pools = 0;     // max-pools fused into the stem convolution that feeds them
   int fused_projections = 0;   // 1x1 projection shortcuts folded into the block's last 1x1 convolution
+  int fused_pairs = 0;         // 1x1 convolutions run in one kernel with the 1x1 convolution before them
   int n_fold_shift = 0;        // constant vectors of the folded projections
   int n_lstm_shift = 0;        // interleaved biases of the LSTM steps
   bool any_decode = false;     // a greedy decoding loop: runs emit tokens
@@ -157,6 +161,7 @@ struct Spec {
   void fuse_gate_moves();
   void fuse_stem_pools();
   void fuse_projections();
+  void pair_pointwise();
 };
 
 }  // namespace dycl

@@ -623,6 +623,37 @@ void Spec::fuse_projections() {
   }
 }
 
+// A bottleneck block's last 1x1 convolution and the next block's first 1x1
+// convolution, which reads nothing but its output, in one kernel that keeps
+// each tile of the first output on chip for the second contraction
+// (conv_pair): the second layer no longer reads that output back.  Top-level
+// nodes in direct succession on the same rows, no row lists.  The inputs of
+// the first stay live through the second, since one launch reads them while
+// it writes the second's output.
+void Spec::pair_pointwise() {
+  if (dt != DType::BF16) return;
+  auto plain = [&](const Node& n) {
+    return n.kind == NodeKind::Conv && n.body.empty() && n.k == 1 && n.stride == 1 && n.pad == 0 && !n.pad_in &&
+           !n.pool && n.act != k::ACT_LSTM && n.packed >= 0 && !n.src_list && !n.src2_list && !n.res_list &&
+           !n.dst_list;
+  };
+  for (size_t i = 0; i + 1 < nodes.size(); ++i) {
+    Node& c = nodes[i];
+    const Node& d = nodes[i + 1];
+    if (!plain(c) || !plain(d) || c.pair) continue;
+    if (c.fold ? (c.src2 < 0 || c.res >= 0) : (c.src2 >= 0 || c.scale_off < 0 || c.shift_off < 0)) continue;
+    if (d.src != c.dst || d.src2 >= 0 || d.res >= 0 || d.fold || d.scale_off < 0 || d.shift_off < 0 ||
+        d.cin1 != c.cout || d.H != c.Ho || d.W != c.Wo || tensors[c.dst].external || tensors[c.dst].unused)
+      continue;
+    if (!k::conv_pair_fits(c.cin1, c.fold ? c.cin2 : 0, c.cout, d.cout, c.act, d.act)) continue;
+    c.pair = true;
+    for (int t : {c.src, c.src2, c.res})
+      if (t >= 0) tensors[t].last = std::max(tensors[t].last, d.seq_pre);
+    ++fused_pairs;
+    ++i;   // the second conv is taken
+  }
+}
+
 // The gather of an exit's carried tensor fused into its readers (a row
 // gather is a copy that computes nothing): when every reader of the carried
 // copy is a bf16 convolution that takes it as its main input before the next
@@ -856,6 +887,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch, c
   fuse_original_order_reads();
   fuse_exit_gathers();
   fuse_gate_moves();
+  if (j.get_bool("pair_pointwise", true)) pair_pointwise();
 
   // every tensor that is moved between row groups must be a whole number of
   // 16-byte vectors, and a whole batch of it must be indexable with 32-bit
@@ -871,7 +903,7 @@ void Spec::parse(const std::string& json, size_t weights_bytes, int max_batch, c
   os << "nodes=" << nodes_total << " decisions=" << decisions << " tensors=" << tensors.size()
      << " packed_weights=" << packed.size() << " fused_gathers=" << fused_gathers
      << " fused_gates=" << fused_gates << " fused_pools=" << fused_pools
-     << " fused_projections=" << fused_projections << " n_out=" << n_out
+     << " fused_projections=" << fused_projections << " fused_pairs=" << fused_pairs << " n_out=" << n_out
      << " dtype=" << dts;
   summary = os.str();
   host_w = nullptr;   // the caller's blob is not kept

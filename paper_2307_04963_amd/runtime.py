@@ -186,6 +186,21 @@ def conv_maxpool(x: torch.Tensor, packed: torch.Tensor, cout: int, k: int, strid
     return y
 
 
+def conv_pair(x: torch.Tensor, packed3: torch.Tensor, scale3: torch.Tensor, shift3: torch.Tensor, res, c3: int,
+              packed1: torch.Tensor, scale1: torch.Tensor, shift1: torch.Tensor, c1: int, stream=None):
+    """dycl_op_conv_pair on device tensors: x [n, H, W, cin] bf16, the two
+    layers' packed 1x1 weights, float32 scale / shift vectors and an optional
+    bf16 residual of the first; returns (y3 [n, H, W, c3], y1 [n, H, W, c1])."""
+    n, H, W, cin = x.shape
+    y3 = torch.empty((n, H, W, c3), dtype=torch.bfloat16, device=x.device)
+    y1 = torch.empty((n, H, W, c1), dtype=torch.bfloat16, device=x.device)
+    s = stream if stream is not None else torch.cuda.current_stream(x.device)
+    check(lib.dycl_op_conv_pair(x.data_ptr(), n, H, W, cin, packed3.data_ptr(), scale3.data_ptr(), shift3.data_ptr(),
+                                None if res is None else res.data_ptr(), c3, y3.data_ptr(), packed1.data_ptr(),
+                                scale1.data_ptr(), shift1.data_ptr(), c1, y1.data_ptr(), s.cuda_stream))
+    return y3, y1
+
+
 def conv(x: torch.Tensor, packed: torch.Tensor, cout: int, k: int, stride: int, pad: int, scale=None, shift=None,
          res=None, act: int = 0, out: torch.Tensor | None = None, stream=None, workspace="auto") -> torch.Tensor:
     """dycl_op_conv on device tensors: x [n, H, W, cin] bf16, packed weights

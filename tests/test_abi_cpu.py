@@ -82,6 +82,9 @@ def test_every_workload_spec_validates(name):
     # each stage's projection shortcut (stride 1, then 2) folds into its block's last 1x1 conv
     fpr = int(re.search(r"fused_projections=(\d+)", msg).group(1))
     assert fpr == (4 if name == "resnet50_exit" else 0)
+    # both first-stage block boundaries (256 -> 64 channels) run as one-launch pairs
+    fpa = int(re.search(r"fused_pairs=(\d+)", msg).group(1))
+    assert fpa == (2 if name == "resnet50_exit" else 0)
     # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
     if name == "act_loop":
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16
@@ -167,6 +170,42 @@ def test_projection_folded_only_into_its_sole_linear_reader():
         rc, msg = _check(json.dumps(sp), nb)
         assert rc == 0, msg
         assert f"fused_projections={want}" in msg, (want, msg)
+
+
+def test_pointwise_pairs_only_where_the_second_reads_only_the_first():
+    # y = relu(bn(conv1x1(x, 64 -> 256)) + r); z = relu(bn(conv1x1(y, 256 -> 64)))
+    w3 = 256 * 64 * 2
+    w1 = 64 * 256 * 2
+    vec = w3 + w1                       # four float32 vectors, 256 floats apart
+    head_w = vec + 4 * 256 * 4
+
+    def spec(second_res=False, second_k=1, c3=256, first_res=True, switch=None, between=False):
+        v = lambda i: vec + i * 1024  # noqa: E731
+        nodes = [{"op": "conv", "src": "x", "dst": "r", "k": 1, "cout": c3, "act": "relu", "w": {"off": 0}},
+                 {"op": "conv", "src": "r", "dst": "a", "k": 1, "cout": 64, "act": "relu", "w": {"off": w3}},
+                 {"op": "conv", "src": "a", "dst": "y", "k": 1, "cout": c3, "act": "relu", "w": {"off": 0},
+                  "scale": v(0), "shift": v(1), "res": "r" if first_res else None},
+                 {"op": "conv", "src": "y", "dst": "z", "k": second_k, "pad": second_k // 2, "cout": 64,
+                  "act": "relu", "w": {"off": w3}, "scale": v(2), "shift": v(3),
+                  "res": "a" if second_res else None},
+                 {"op": "exit", "src": "z", "w": head_w, "b": head_w + 64 * 10 * 4, "ncls": 10, "index": 0,
+                  "final": True}]
+        if between:
+            nodes.insert(3, {"op": "maxpool", "src": "y", "dst": "yp"})
+            nodes[4]["src"] = "yp"
+        sp = {"version": 1, "dtype": "bf16", "input": {"name": "x", "shape": [8, 8, 64]}, "n_out": 10,
+              "nodes": nodes}
+        if switch is not None:
+            sp["pair_pointwise"] = switch
+        return sp
+
+    nb = head_w + 64 * 10 * 4 + 64 + 64 * 256 * 9 * 2
+    cases = ((spec(), 1), (spec(first_res=False), 1), (spec(switch=False), 0), (spec(second_res=True), 0),
+             (spec(second_k=3), 0), (spec(c3=128), 0), (spec(between=True), 0))
+    for sp, want in cases:
+        rc, msg = _check(json.dumps(sp), nb)
+        assert rc == 0, msg
+        assert f"fused_pairs={want}" in msg, (want, msg)
 
 
 def _mlp_spec():
