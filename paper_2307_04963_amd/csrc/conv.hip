@@ -1070,7 +1070,7 @@ __global__ __launch_bounds__(512) void conv3_wres_kernel(Conv3P p) {
 // ------------------------------ 3x3 conv, halo tiles, streamed weights ----
 // For 3x3 / stride 1 / pad 1 layers with Cin and Cout multiples of 64.  A
 // persistent workgroup walks a contiguous range of work units, a unit being
-// one BM-pixel output tile (128 or 256; the row / image geometry of the
+// one BM-pixel output tile (128 as launched; the row / image geometry of the
 // kernel above) times BN output channels.  The K loop runs over 64-channel chunks and,
 // inside a chunk, the nine taps: one step = one tap of one chunk = 64 of K.
 //  * the input patch of a chunk (the tile's pixels plus the one-pixel halo,
@@ -1666,8 +1666,12 @@ bool conv3_wres(const ConvArgs& a, hipStream_t s) {
   return true;
 }
 
-// the streamed-weights 3x3 kernel (Cin, Cout multiples of 64): 256-pixel
-// tiles when they are at least 3/4 used and give every CU work, else 128
+// the streamed-weights 3x3 kernel (Cin, Cout multiples of 64) on 128-pixel
+// tiles: measured 2-5 % faster than 256-pixel tiles on the ResNet-50
+// stage-2 / 3 and ResNet-18 stage-2 layers (interleaved runs, best of four
+// each), and a shape whose 128-pixel patch does not fit LDS fits no
+// 256-pixel patch either, once the smallest images (taken by the implicit
+// GEMM, below) are set aside
 bool conv3_halo(const ConvArgs& a, hipStream_t s) {
   if (!is_halo_layer(a) || a.cout > kHMaxC) return false;
   // images so small that the halo more than doubles the patch (4 x 4: 36
@@ -1679,12 +1683,8 @@ bool conv3_halo(const ConvArgs& a, hipStream_t s) {
   // grid) is then laid out for all n
   const int nh = a.nhint > 0 && a.nhint < a.n ? a.nhint : a.n;
   HaloGeom g;
-  int bm = 256;
-  if (!halo_geom(nh, a.H, a.W, 256, halo_cap(256), g) ||
-      4L * nh * a.H * a.W < 3L * 256 * g.mtiles || (long)g.mtiles * (a.cout / 128) < cus) {
-    bm = 128;
-    if (!halo_geom(nh, a.H, a.W, 128, halo_cap(128), g)) return false;
-  }
+  constexpr int bm = 128;
+  if (!halo_geom(nh, a.H, a.W, bm, halo_cap(bm), g)) return false;
   const int bn = (a.cout % 128 == 0 && conv_cout_pad(a.cout) % 128 == 0 && (long)g.mtiles * (a.cout / 128) >= cus)
                      ? 128 : 64;
   if (!halo_geom(a.n, a.H, a.W, bm, halo_cap(bm), g)) return false;
@@ -1712,8 +1712,7 @@ bool conv3_halo(const ConvArgs& a, hipStream_t s) {
   p.nch = a.cin / 64;
   p.nc = a.ncount;
   const int grid = p.units < cus ? p.units : cus;
-  // four compute waves: 128 x 64 (pixels x channels) each for 256-pixel
-  // tiles, 64 x BN/2 for 128-pixel tiles; plus four loader waves
+  // four compute waves of 64 x BN/2 (pixels x channels), four loader waves
   auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(512), 0, s, p); };
 #define DYCL_H(BM, BN, NS)                                                              \
   if (p.res) {                                                                          \
@@ -1725,18 +1724,10 @@ bool conv3_halo(const ConvArgs& a, hipStream_t s) {
     else if (a.act == ACT_GELU) go(conv3h_kernel<BM, BN, BM / 64, ACT_GELU, false, NS>); \
     else go(conv3h_kernel<BM, BN, BM / 64, ACT_NONE, false, NS>);                       \
   }
-  if (bm == 256) {
-    if (bn == 128) {
-      DYCL_H(256, 128, 3)
-    } else {
-      DYCL_H(256, 64, 6)
-    }
+  if (bn == 128) {
+    DYCL_H(128, 128, 5)
   } else {
-    if (bn == 128) {
-      DYCL_H(128, 128, 5)
-    } else {
-      DYCL_H(128, 64, 8)
-    }
+    DYCL_H(128, 64, 8)
   }
 #undef DYCL_H
   return true;
