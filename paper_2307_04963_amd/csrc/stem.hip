@@ -81,12 +81,15 @@ struct StemP {
 };
 
 // the larger of two non-negative bf16 values is the one with the larger
-// bits: element-wise maxima of 8 bf16 by 16-bit integer maxima
-__device__ __forceinline__ uint4 max_bf16x8(uint4 a, uint4 b) {
-  auto m = [](uint32_t x, uint32_t y) {
-    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, x), __builtin_bit_cast(u16x2, y)));
-  };
-  return make_uint4(m(a.x, b.x), m(a.y, b.y), m(a.z, b.z), m(a.w, b.w));
+// bits: element-wise maxima of 8 bf16 by 16-bit integer maxima.  The pooled
+// path works on vector types throughout: with the struct type uint4, a
+// choice between a loaded value and a constant became a choice between
+// addresses, i.e. a generic (flat) load, whose wait also waited for the
+// next unit's input loads in flight
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4 max_bf16x8(u32x4 a, u32x4 b) {
+  return __builtin_bit_cast(u32x4, __builtin_elementwise_max(__builtin_bit_cast(u16x8, a), __builtin_bit_cast(u16x8, b)));
 }
 
 template <int ACT>
@@ -324,8 +327,8 @@ __global__ __launch_bounds__(256, 2) void stem_rgb_kernel(StemP p) {
       uint16_t* const ew = el + wave * 16 * kEStride;
       uint16_t* const hp = reinterpret_cast<uint16_t*>(pl);   // [kRows][WP][64]
       const int t8 = lane >> 3, q = lane & 7;
-      const uint4 zero = make_uint4(0, 0, 0, 0);
-      uint4 prev = zero;   // the previous block's pixel 15
+      const u32x4 zero = {0u, 0u, 0u, 0u};
+      u32x4 prev = zero;   // the previous block's pixel 15
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
@@ -341,17 +344,18 @@ __global__ __launch_bounds__(256, 2) void stem_rgb_kernel(StemP p) {
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         const int c1 = 2 * t8;
-        const uint4 center = *reinterpret_cast<const uint4*>(ew + c1 * kEStride + q * 8);
-        const uint4 right = *reinterpret_cast<const uint4*>(ew + (c1 + 1) * kEStride + q * 8);
-        const uint4 left = t8 > 0 ? *reinterpret_cast<const uint4*>(ew + (c1 - 1) * kEStride + q * 8) : prev;
-        const uint4 last = *reinterpret_cast<const uint4*>(ew + 15 * kEStride + q * 8);
+        const u32x4 center = *reinterpret_cast<const u32x4*>(ew + c1 * kEStride + q * 8);
+        const u32x4 right = *reinterpret_cast<const u32x4*>(ew + (c1 + 1) * kEStride + q * 8);
+        const u32x4 lft = *reinterpret_cast<const u32x4*>(ew + (t8 > 0 ? c1 - 1 : 0) * kEStride + q * 8);
+        const u32x4 left = t8 > 0 ? lft : prev;
+        const u32x4 last = *reinterpret_cast<const u32x4*>(ew + 15 * kEStride + q * 8);
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // reads done before the next block's staging
         const int ow = mb * 16 + c1;
-        uint4 m = ow < p.Wo ? center : zero;
+        u32x4 m = ow < p.Wo ? center : zero;
         if (ow + 1 < p.Wo) m = max_bf16x8(m, right);
         if (ow >= 1 && ow - 1 < p.Wo) m = max_bf16x8(m, left);
         if (oh >= p.Ho) m = zero;
-        *reinterpret_cast<uint4*>(hp + (wave * G::WP + mb * 8 + t8) * kCout + q * 8) = m;
+        *reinterpret_cast<u32x4*>(hp + (wave * G::WP + mb * 8 + t8) * kCout + q * 8) = m;
         prev = last;
       }
       __syncthreads();   // every row's maxima are in LDS
@@ -364,17 +368,18 @@ __global__ __launch_bounds__(256, 2) void stem_rgb_kernel(StemP p) {
           const int po = 2 * j + pr;
           if (po >= p.Hp) continue;
           const int o = pw * kCout + qq * 8;
-          const uint4 r1 = *reinterpret_cast<const uint4*>(hp + (pr * 2) * G::WP * kCout + o);
-          const uint4 r2 = *reinterpret_cast<const uint4*>(hp + (pr * 2 + 1) * G::WP * kCout + o);
-          const uint4 r0 = pr ? *reinterpret_cast<const uint4*>(hp + G::WP * kCout + o)
-                              : (j > 0 ? *reinterpret_cast<const uint4*>(cl + o) : zero);
-          *reinterpret_cast<uint4*>(p.y + ((static_cast<size_t>(img) * p.Hp + po) * p.Wp + pw) * kCout + qq * 8) =
+          const u32x4 r1 = *reinterpret_cast<const u32x4*>(hp + (pr * 2) * G::WP * kCout + o);
+          const u32x4 r2 = *reinterpret_cast<const u32x4*>(hp + (pr * 2 + 1) * G::WP * kCout + o);
+          const u32x4 ra = *reinterpret_cast<const u32x4*>(hp + G::WP * kCout + o);
+          const u32x4 rc = *reinterpret_cast<const u32x4*>(cl + o);
+          const u32x4 r0 = pr ? ra : (j > 0 ? rc : zero);
+          *reinterpret_cast<u32x4*>(p.y + ((static_cast<size_t>(img) * p.Hp + po) * p.Wp + pw) * kCout + qq * 8) =
               max_bf16x8(max_bf16x8(r0, r1), r2);
         }
       }
       __syncthreads();   // the carried row is read
       for (int e = tid; e < WP8; e += 256)   // the unit's last stem row is carried
-        *reinterpret_cast<uint4*>(cl + e * 8) = *reinterpret_cast<const uint4*>(hp + 3 * G::WP * kCout + e * 8);
+        *reinterpret_cast<u32x4*>(cl + e * 8) = *reinterpret_cast<const u32x4*>(hp + 3 * G::WP * kCout + e * 8);
     } else {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
