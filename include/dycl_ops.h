@@ -148,9 +148,11 @@ int dycl_op_conv_maxpool(const uint16_t* x, int n, int H, int W, int cin, const 
  *   y3 = dycl_op_conv(x, packed3, c3, k 1, stride 1, pad 0, scale3, shift3, res, act 1)
  *   y1 = dycl_op_conv(y3, packed1, c1, k 1, stride 1, pad 0, scale1, shift1, NULL, act 1)
  * bit for bit; each tile of y3 stays on chip for the second contraction, so
- * y3 is written once and never read back.  Taken for cin % 64 == 0, 64 <=
- * cin <= 1024, c3 256, c1 64 (ResNet-50's first stage) and ReLU on both;
- * other shapes return DYCL_E_INVALID.  x [n][H][W][cin], res [n][H][W][c3]
+ * y3 is written once and never read back.  Taken for ReLU on both and
+ * either c3 256, c1 64, cin % 64 == 0 with 64 <= cin <= 1024 (ResNet-50's
+ * first stage) or c3 512, c1 128, cin 128 (its second stage, the first
+ * layer's output channels taken 128 at a time); other shapes return
+ * DYCL_E_INVALID.  x [n][H][W][cin], res [n][H][W][c3]
  * or NULL, y3 [n][H][W][c3], y1 [n][H][W][c1]; packed3 / packed1 from
  * dycl_op_conv_pack (k 1; cin and c3 input channels); scale / shift [cout]
  * float32, all four required; device pointers, 16-byte aligned; n >= 0 (0

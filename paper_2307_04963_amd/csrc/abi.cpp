@@ -476,7 +476,9 @@ int dycl_op_conv_pair(const uint16_t* x, int n, int H, int W, int cin, const uin
                       const float* scale1, const float* shift1, int c1, uint16_t* y1, void* hip_stream) {
   if (n < 0) return fail(DYCL_E_INVALID, "dycl_op_conv_pair: n < 0");
   if (H < 1 || W < 1 || !dycl::k::conv_pair_fits(cin, 0, c3, c1, dycl::k::ACT_RELU, dycl::k::ACT_RELU))
-    return fail(DYCL_E_INVALID, "dycl_op_conv_pair: needs H, W >= 1, cin % 64 == 0 in [64, 1024], c3 256, c1 64");
+    return fail(DYCL_E_INVALID,
+                "dycl_op_conv_pair: needs H, W >= 1 and c3 256, c1 64, cin % 64 == 0 in [64, 1024] or c3 512, c1 128, "
+                "cin 128");
   const long lim = 1L << 31;
   if (static_cast<long>(n) * H * W * std::max(cin, c3) >= lim)
     return fail(DYCL_E_INVALID, "dycl_op_conv_pair: a tensor reaches 2^31 elements");

@@ -95,7 +95,8 @@ struct ConvArgs {
 bool conv_bf16(const ConvArgs& a, hipStream_t s);
 
 // A bottleneck block's last 1x1 layer and the next block's first 1x1 layer
-// in one kernel (both stride 1, no row lists):
+// in one kernel (both stride 1, no row lists; 256 -> 64 channels, or 512 ->
+// 128 without a fold):
 //   y3 = act3(scale3 * (x W3^T) + shift3 + res)   [n * H * W][C3]
 //   y1 = act1(scale1 * (y3 W1^T) + shift1)        [n * H * W][C1]
 // with packed weights w3 [>= C3][Kp3] and w1 [>= C1][Kp1] (C3 used).  The

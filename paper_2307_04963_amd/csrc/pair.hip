@@ -331,13 +331,193 @@ __global__ __launch_bounds__(kThr) __attribute__((amdgpu_waves_per_eu(4))) void 
   }
 }
 
+// Wider blocks (C3 = 512: ResNet-50's second stage) do not fit W3, the
+// tile's y3 rows and W1 side by side in LDS.  Here the first layer's
+// output channels are taken in chunks of 128: per chunk its W3 rows (all of
+// K, 32 KB) and residual columns come in, the chunk's y3 columns are
+// finished in place and stored, W1's matching 128 K columns (requested
+// with the rest) take the place of W3, and the second contraction adds that
+// K range to its sums: one round of requests per chunk.  The second layer
+// runs over K in chunk order, 16 at a time, as the single layer does, so
+// the bits are again those of the two layers run one by one.  The tile's x
+// rows (both K steps) stay in LDS for all chunks.  LDS 69 KB: two
+// workgroups per CU.
+//   wave (wl & 3, wl >> 2) = 32 channels x 32 pixels, in both contractions
+template <int C3, int C1, int K3, int ACT3, int ACT1, bool RES>
+__global__ __launch_bounds__(kThr) __attribute__((amdgpu_waves_per_eu(4))) void conv_pair_chunked_kernel(PairP p) {
+  constexpr int CW = 128;                     // y3 channels per chunk
+  constexpr int NCH = C3 / CW;
+  constexpr int XROW = K3 * 2;                // bytes of an x row (all K steps)
+  constexpr int X_BYTES = kRowsT * XROW;
+  constexpr int WROW = 256;                   // bytes of a W3 chunk row (K3 = 128) and of a W1 chunk row (CW = 128)
+  constexpr int W_BYTES = 128 * WROW;         // 128 rows: CW rows of W3, or the C1 rows of W1
+  constexpr int AROW = CW * 2;                // bytes of a y3 chunk row
+  constexpr int A_BYTES = kRowsT * AROW;
+  constexpr int NV = 2 * C3 + 2 * C1;         // [s3 | b3 | s1 | b1]
+  static_assert(C3 % CW == 0 && C1 == 128 && K3 == 128, "laid out for 128 -> 512 -> 128 channels");
+  static_assert(XROW == WROW && AROW == WROW, "all LDS rows 256 bytes: 16 chunks, swizzled by row & 15");
+  static_assert(kRowsT * C1 * 2 <= X_BYTES, "the y1 staging takes the place of x");
+  static_assert(NV / 4 <= kThr, "one vector load per thread at most");
+  constexpr int JX = X_BYTES / 16 / kThr, JW = W_BYTES / 16 / kThr, JA = A_BYTES / 16 / kThr;
+  static_assert(JW == 4, "four W1 vectors per thread");
+  __shared__ __align__(16) char smem[X_BYTES + W_BYTES + A_BYTES + NV * 4];
+  char* const sx = smem;                              // x rows, then the y1 staging
+  char* const sw = smem + X_BYTES;                    // a W3 chunk, then a W1 chunk
+  char* const sa = smem + X_BYTES + W_BYTES;          // a residual chunk, then a y3 chunk
+  float* const sv = reinterpret_cast<float*>(smem + X_BYTES + W_BYTES + A_BYTES);
+
+  const int HW = p.H * p.W;
+  const int M = (p.nc ? min(*p.nc, p.nmax) : p.nmax) * HW;
+  const int T = (M + kRowsT - 1) / kRowsT;
+  const int wg = blockIdx.x;
+  if (wg >= T) return;
+  const int T8 = (T >> 3) << 3;
+  const int t = wg < T8 ? (wg & 7) * (T8 >> 3) + (p.rev ? (T8 >> 3) - 1 - (wg >> 3) : (wg >> 3)) : wg;
+  const int m0 = t * kRowsT;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  // slot q of a region of 256-byte rows: row q / 16, physical chunk q % 16
+  // holding logical chunk (q % 16) ^ (row & 15)
+  auto lchunk = [](int q) { return (q & 15) ^ ((q >> 4) & 15); };
+  if (tid < NV / 4) {
+    const int q = tid * 4;
+    const float* g = q < C3 ? p.v3[0] + q : q < 2 * C3 ? p.v3[1] + (q - C3) : q < 2 * C3 + C1 ? p.sc1 + (q - 2 * C3)
+                                                                                             : p.sh1 + (q - 2 * C3 - C1);
+    to_lds(g, reinterpret_cast<char*>(sv) + wave * 1024);
+  }
+#pragma unroll
+  for (int j = 0; j < JX; ++j) {
+    const int q = j * kThr + tid, m = m0 + (q >> 4);
+    to_lds(m < M ? p.x + static_cast<size_t>(m) * K3 + lchunk(q) * 8 : p.zeros, sx + (j * kThr + wave * 64) * 16);
+  }
+
+  const int wc = wave & 3, wp = wave >> 2;
+  const int lsw = lane & 15;
+  f32x16 acc1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc1[r] = 0.f;
+  // 16 MFMA steps of K = 16 over 256-byte rows: A rows at pa, B rows at pb
+  auto mma16 = [&](f32x16& acc, const char* pa, const char* pb) __attribute__((always_inline)) {
+    bf16x8 af[2], bx[2];
+    auto fetch = [&](int s, int slot) __attribute__((always_inline)) {
+      const int phys = ((2 * s + (lane >> 5)) ^ lsw) * 16;
+      af[slot] = *reinterpret_cast<const bf16x8*>(pa + phys);
+      bx[slot] = *reinterpret_cast<const bf16x8*>(pb + phys);
+    };
+    fetch(0, 0);
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      if (s + 1 < 8) fetch(s + 1, (s + 1) & 1);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1], bx[s & 1], acc, 0, 0, 0);
+    }
+  };
+
+  for (int c = 0; c < NCH; ++c) {
+    if (c) lds_sync();   // the previous chunk's W1 and y3 are no longer read
+    // W3 rows c CW .. + CW (all of K) and the residual's chunk columns
+#pragma unroll
+    for (int j = 0; j < JW; ++j) {
+      const int q = j * kThr + tid;
+      to_lds(p.w3 + static_cast<size_t>(c * CW + (q >> 4)) * p.Kp3 + lchunk(q) * 8, sw + (j * kThr + wave * 64) * 16);
+    }
+    if (RES) {
+#pragma unroll
+      for (int j = 0; j < JA; ++j) {
+        const int q = j * kThr + tid, m = m0 + (q >> 4);
+        to_lds(m < M ? p.res + static_cast<size_t>(m) * C3 + c * CW + lchunk(q) * 8 : p.zeros,
+               sa + (j * kThr + wave * 64) * 16);
+      }
+    }
+    // W1 columns c CW .. + CW of all C1 rows into registers (they go to the
+    // space of W3 after the epilogue), requested and awaited with the rest:
+    // with direct-to-LDS loads and register loads in flight, the compiler
+    // waits for all of them before any LDS read anyway
+    auto w1_at = [&](int j) __attribute__((always_inline)) {
+      const int q = j * kThr + tid;
+      return *reinterpret_cast<const uint4*>(p.w1 + static_cast<size_t>(q >> 4) * p.Kp1 + c * CW + lchunk(q) * 8);
+    };
+    const uint4 w1a = w1_at(0), w1b = w1_at(1), w1c = w1_at(2), w1d = w1_at(3);
+    vm_barrier<0>();
+    f32x16 acc3;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc3[r] = 0.f;
+    mma16(acc3, sw + (32 * wc + (lane & 31)) * WROW, sx + (32 * wp + (lane & 31)) * XROW);
+    lds_sync();   // every wave is done reading W3
+    {
+      const int row = 32 * wp + (lane & 31);
+      char* const arow = sa + row * AROW + (lane >> 5) * 8;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int cl = 32 * wc + 8 * g + 4 * (lane >> 5), c0 = c * CW + cl;
+        uint2* const e = reinterpret_cast<uint2*>(arow + (((cl >> 3) ^ (row & 15)) * 16));
+        const float4 sc = *reinterpret_cast<const float4*>(sv + c0);
+        const float4 sh = *reinterpret_cast<const float4*>(sv + C3 + c0);
+        float v0 = fmaf(acc3[4 * g + 0], sc.x, sh.x);
+        float v1 = fmaf(acc3[4 * g + 1], sc.y, sh.y);
+        float v2 = fmaf(acc3[4 * g + 2], sc.z, sh.z);
+        float v3 = fmaf(acc3[4 * g + 3], sc.w, sh.w);
+        if (RES) {
+          const uint2 r = *e;
+          v0 += __uint_as_float(r.x << 16);
+          v1 += __uint_as_float(r.x & 0xffff0000u);
+          v2 += __uint_as_float(r.y << 16);
+          v3 += __uint_as_float(r.y & 0xffff0000u);
+        }
+        *e = make_uint2(pack2(act_of<ACT3>(v0), act_of<ACT3>(v1)), pack2(act_of<ACT3>(v2), act_of<ACT3>(v3)));
+      }
+    }
+    auto w1_put = [&](int j, const uint4& v) __attribute__((always_inline)) {
+      const int q = j * kThr + tid;
+      *reinterpret_cast<uint4*>(sw + q * 16) = v;   // slot q: row q / 16, physical chunk q % 16
+    };
+    w1_put(0, w1a);
+    w1_put(1, w1b);
+    w1_put(2, w1c);
+    w1_put(3, w1d);
+    lds_sync();   // the chunk's y3 columns and W1 columns are complete
+#pragma unroll
+    for (int j = 0; j < JA; ++j) {
+      const int q = j * kThr + tid, row = q >> 4, lc = lchunk(q);
+      if (m0 + row < M)
+        *reinterpret_cast<uint4*>(p.y3 + static_cast<size_t>(m0 + row) * C3 + c * CW + lc * 8) =
+            *reinterpret_cast<const uint4*>(sa + q * 16);
+    }
+    mma16(acc1, sw + (32 * wc + (lane & 31)) * WROW, sa + (32 * wp + (lane & 31)) * AROW);
+  }
+  lds_sync();   // x is no longer read: its space takes the y1 staging
+  {
+    const int px = 32 * wp + (lane & 31);
+    char* const yrow = sx + px * (C1 * 2) + (lane >> 5) * 8;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int c0 = 32 * wc + 8 * g + 4 * (lane >> 5);
+      const float4 sc = *reinterpret_cast<const float4*>(sv + 2 * C3 + c0);
+      const float4 sh = *reinterpret_cast<const float4*>(sv + 2 * C3 + C1 + c0);
+      const float v0 = act_of<ACT1>(fmaf(acc1[4 * g + 0], sc.x, sh.x));
+      const float v1 = act_of<ACT1>(fmaf(acc1[4 * g + 1], sc.y, sh.y));
+      const float v2 = act_of<ACT1>(fmaf(acc1[4 * g + 2], sc.z, sh.z));
+      const float v3 = act_of<ACT1>(fmaf(acc1[4 * g + 3], sc.w, sh.w));
+      *reinterpret_cast<uint2*>(yrow + (((c0 >> 3) ^ (px & 15)) * 16)) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+    }
+  }
+  lds_sync();
+#pragma unroll
+  for (int j = 0; j < kRowsT * C1 * 2 / 16 / kThr; ++j) {
+    const int q = j * kThr + tid, row = q >> 4;
+    if (m0 + row < M)
+      *reinterpret_cast<uint4*>(p.y1 + static_cast<size_t>(m0 + row) * C1 + lchunk(q) * 8) =
+          *reinterpret_cast<const uint4*>(sx + q * 16);
+  }
+}
+
 bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
 
 }  // namespace
 
 bool conv_pair_fits(int K3, int K2, int C3, int C1, int act3, int act1) {
-  return C3 == 256 && C1 == 64 && K3 >= 64 && K3 % 64 == 0 && K2 >= 0 && K2 % 64 == 0 && K3 + K2 <= 1024 &&
-         act3 == ACT_RELU && act1 == ACT_RELU;
+  if (act3 != ACT_RELU || act1 != ACT_RELU) return false;
+  if (C3 == 512) return C1 == 128 && K3 == 128 && K2 == 0;   // the chunked kernel: no fold
+  return C3 == 256 && C1 == 64 && K3 >= 64 && K3 % 64 == 0 && K2 >= 0 && K2 % 64 == 0 && K3 + K2 <= 1024;
 }
 
 bool conv_pair_takes(const PairArgs& a) {
@@ -391,7 +571,11 @@ bool conv_pair(const PairArgs& a, hipStream_t s) {
   p.Kp1 = a.Kp1;
   p.rev = a.rev;
   const dim3 grid(static_cast<unsigned>((M + kRowsT - 1) / kRowsT));
-  if (fold)
+  if (a.C3 == 512 && a.res)
+    hipLaunchKernelGGL((conv_pair_chunked_kernel<512, 128, 128, ACT_RELU, ACT_RELU, true>), grid, dim3(kThr), 0, s, p);
+  else if (a.C3 == 512)
+    hipLaunchKernelGGL((conv_pair_chunked_kernel<512, 128, 128, ACT_RELU, ACT_RELU, false>), grid, dim3(kThr), 0, s, p);
+  else if (fold)
     hipLaunchKernelGGL((conv_pair_kernel<256, 64, ACT_RELU, ACT_RELU, false, true>), grid, dim3(kThr), 0, s, p);
   else if (a.res)
     hipLaunchKernelGGL((conv_pair_kernel<256, 64, ACT_RELU, ACT_RELU, true, false>), grid, dim3(kThr), 0, s, p);

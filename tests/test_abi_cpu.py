@@ -82,9 +82,11 @@ def test_every_workload_spec_validates(name):
     # each stage's projection shortcut (stride 1, then 2) folds into its block's last 1x1 conv
     fpr = int(re.search(r"fused_projections=(\d+)", msg).group(1))
     assert fpr == (4 if name == "resnet50_exit" else 0)
-    # both first-stage block boundaries (256 -> 64 channels) run as one-launch pairs
+    # block boundaries run as one-launch pairs: both of the first stage (256 -> 64
+    # channels, one with a folded projection) and the two plain ones of the second
+    # (512 -> 128)
     fpa = int(re.search(r"fused_pairs=(\d+)", msg).group(1))
-    assert fpa == (2 if name == "resnet50_exit" else 0)
+    assert fpa == (4 if name == "resnet50_exit" else 0)
     # the bounded loop is unrolled: one halting test per step (Sec. 5.2 rewriting)
     if name == "act_loop":
         assert sum(n["op"] == "halt" for n in spec["nodes"]) == 16

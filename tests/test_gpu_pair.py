@@ -4,7 +4,9 @@ and the next block's first 1x1 layer, which reads nothing but its output
 
 * dycl_op_conv_pair against dycl_op_conv called twice, bit for bit on every
   element (ragged last tile, one row, several K steps, with and without the
-  residual, the full ResNet-50 first-stage shape at batch 256), and both of
+  residual, the full ResNet-50 first-stage shape at batch 256; 512 -> 128
+  channels in chunks, up to the second-stage shape at the rows that reach
+  it), and both of
   its outputs against the oracle's float64 convolutions on sampled images
   within the fp32 accumulation bound (the second layer's reference takes the
   first layer's bf16 output as its input, as the network does).
@@ -12,7 +14,8 @@ and the next block's first 1x1 layer, which reads nothing but its output
   records and branch counts with the pairing on and off
   ("pair_pointwise": false), in the sync and device host modes; the pairing
   covers both first-stage boundaries, one of them a block whose projection
-  shortcut is folded into the pair's first layer.
+  shortcut is folded into the pair's first layer, and the two plain
+  second-stage boundaries (512 channels, taken 128 at a time).
 """
 
 import json
@@ -56,20 +59,22 @@ def _check_1x1(x, w, sc, sh, r, got, imgs, what):
 
 
 CASES = [
-    # n, H, W, cin, residual
-    (2, 7, 7, 64, True),        # 98 rows: a ragged second tile
-    (1, 1, 1, 64, True),        # one row
-    (3, 9, 9, 128, False),      # two K steps, no residual
-    (5, 14, 14, 1024, True),    # sixteen K steps
-    (256, 56, 56, 64, True),    # ResNet-50's first stage at batch 256
+    # n, H, W, cin, residual, c3, c1
+    (2, 7, 7, 64, True, 256, 64),         # 98 rows: a ragged second tile
+    (1, 1, 1, 64, True, 256, 64),         # one row
+    (3, 9, 9, 128, False, 256, 64),       # two K steps, no residual
+    (5, 14, 14, 1024, True, 256, 64),     # sixteen K steps
+    (256, 56, 56, 64, True, 256, 64),     # ResNet-50's first stage at batch 256
+    (3, 7, 7, 128, True, 512, 128),       # 512 channels in chunks of 128: ragged last tile
+    (2, 5, 5, 128, False, 512, 128),      # no residual
+    (182, 28, 28, 128, True, 512, 128),   # ResNet-50's second stage at the rows that reach it
 ]
 
 
-@pytest.mark.parametrize("case", CASES, ids=lambda c: "n{}_{}x{}_cin{}_res{}".format(*c))
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "n{}_{}x{}_cin{}_res{}_c{}".format(*c[:6]))
 def test_conv_pair_op(case):
     from paper_2307_04963_amd import runtime
-    n, H, W, cin, residual = case
-    c3, c1 = 256, 64
+    n, H, W, cin, residual, c3, c1 = case
     print(f"[pair-op] n={n} {H}x{W} cin={cin} residual={residual}", flush=True)
     rng = np.random.default_rng(n * 1000 + cin)
     x = bf16_bits_to_f32(to_bf16_bits(rng.standard_normal((n, H, W, cin)).astype(np.float32)))
@@ -102,7 +107,7 @@ def test_conv_pair_op_rejects_other_shapes():
     p = torch.zeros(1 << 16, dtype=torch.int16, device="cuda")
     v = torch.ones(512, dtype=torch.float32, device="cuda")
     with pytest.raises(DyclError):
-        runtime.conv_pair(x, p, v, v, None, 512, p, v, v, 128)   # the kernel is laid out for 256 -> 64
+        runtime.conv_pair(x, p, v, v, None, 512, p, v, v, 128)   # 512 -> 128 takes cin 128 only
     with pytest.raises(DyclError):
         runtime.conv_pair(x[..., :32].contiguous(), p, v, v, None, 256, p, v, v, 64)   # cin % 64 != 0
 
@@ -117,12 +122,13 @@ def test_resnet50_plan_same_bits_with_and_without_pairs():
     on = runtime.Plan(json.dumps(spec), blob, B)
     off = runtime.Plan(json.dumps(dict(spec, pair_pointwise=False)), blob, B)
     x, aux = wl.inputs(B)
-    # the pairing took both first-stage boundaries (labels of the profiled launches)
+    # the pairing took both first-stage boundaries and two of the second stage
+    # (labels of the profiled launches)
     on.profile(True)
     runtime.run_numpy(on, wl, x, aux)
     labels = [r["label"] for r in on.profile_launches() if " + " in r["label"]]
     on.profile(False)
-    assert len(labels) == 2, labels
+    assert len(labels) == 4, labels
     for mode in ("sync", "device"):
         print(f"[pair-plan] {name} B={B} mode={mode}", flush=True)
         on.set_host_mode(mode)
