@@ -551,15 +551,31 @@ __global__ __launch_bounds__(64 * WM* WN) __attribute__((amdgpu_waves_per_eu(NS 
       compute(0);
       if (kt + 1 == p.kfold) fold_round();
     }
-  } else if (NS == 2 && nk == 2) {
-    // both K steps fit the two stages: the second is requested at once, so
-    // its latency overlaps the first one's rather than following its MFMAs
-    issue(1, 1);
-    wait_vm_barrier<JA + JB>();
-    compute(0);
-    if (p.kfold == 1) fold_round();
-    wait_vm_barrier<0>();
-    compute(1);
+  } else if (NS == 2) {
+    // rounds of two K steps requested together: the second step's latency
+    // overlaps the first's, and a layer of nk steps waits on ceil(nk / 2)
+    // round trips (measured 5-25 % faster than keeping one step in flight
+    // behind the MFMAs, on every layer shape tried, and ahead of four
+    // pipelined stages on 64 x 64 tiles)
+    for (int kt = 0; kt < nk; kt += 2) {
+      if (kt) {
+        __syncthreads();   // every wave is done reading both stages
+        issue(kt, 0);
+      }
+      if (kt + 1 < nk) {
+        issue(kt + 1, 1);
+        wait_vm_barrier<JA + JB>();   // step kt has landed; kt + 1 may be in flight
+      } else {
+        wait_vm_barrier<0>();
+      }
+      compute(0);
+      if (kt + 1 == p.kfold) fold_round();
+      if (kt + 1 < nk) {
+        wait_vm_barrier<0>();
+        compute(1);
+        if (kt + 2 == p.kfold) fold_round();
+      }
+    }
   } else {
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + NS - 2 < nk)
@@ -1525,21 +1541,22 @@ TileCfg choose_lds(int M, int cout, int Kp) {
   // one tile column spans a short-K layer's channels, so that each input
   // pixel (the bulk of its traffic) is fetched by one workgroup
   if (cout >= 128 && (2 * r128 <= r12864 || (cout == 128 && Kp <= 256))) return c128;
-  // 64 x 64 only when 128 x 64 would leave most CUs with one workgroup
-  return t12864 > 256 ? c12864 : c64;
+  // 64 x 64 when 128 x 64 would give fewer than ~1.5 tiles per CU (with
+  // rounds of two K steps: the ResNet-18 stage-4 strided 3x3 layer 33 -> 29
+  // us, the ACT loop's short steps 10-15 % faster; at 2.5 tiles per CU
+  // 128 x 64 stays ahead)
+  return t12864 >= 400 ? c12864 : c64;
 }
 
-// stages: one (`one`, 128 x 64 tiles only: the K steps taken in turn) where
-// the workgroups a CU holds bound the layer, five with one 24 KB stage
-// against three with two: measured 2-20 % faster on the ResNet-50 1x1
-// shapes with K = 128 .. 1024 and 8-16 % on its strided 3x3 layers with 2.5
-// or more tiles per CU (slower with fewer); four for 64 x 64 tiles with
-// eight or more K steps (64 KB of LDS: still two workgroups per CU, three
-// steps of loads in flight; measured 1-6 % faster end to end), else two
+// stages: one (`one`, 128 x 64 or 128 x 256 tiles only: the K steps taken
+// in turn) where the workgroups a CU holds bound the layer, five with one
+// 24 KB stage against three with two: measured 2-20 % faster on the
+// ResNet-50 1x1 shapes with many tiles and 8-16 % on its strided 3x3
+// layers with 2.5 or more tiles per CU (slower with fewer); else two,
+// filled in rounds of two K steps
 template <int BM, int BN, int WM, int WN, int KS>
 void go_lds(const ConvP& p, hipStream_t s, int S, bool one) {
   const dim3 grid(p.mt * p.nt * S);
-  constexpr bool small = BM == 64 && BN == 64;
   if (one && S == 1) {
     if constexpr (BM == 128 && (BN == 64 || BN == 256))
       hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 1>), grid, dim3(64 * WM * WN), 0, s, p);
@@ -1547,10 +1564,9 @@ void go_lds(const ConvP& p, hipStream_t s, int S, bool one) {
       throw std::invalid_argument("conv_bf16: the one-stage implicit GEMM takes 128 x 64 or 128 x 256 tiles only");
   } else if constexpr (BN == 256) {
     throw std::invalid_argument("conv_bf16: 128 x 256 tiles are one-stage only");
-  } else if (small && p.Kp >= 512)
-    hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, small ? 4 : 2>), grid, dim3(64 * WM * WN), 0, s, p);
-  else
+  } else {
     hipLaunchKernelGGL((conv_lds_kernel<BM, BN, WM, WN, KS, 2>), grid, dim3(64 * WM * WN), 0, s, p);
+  }
 }
 
 template <int KS>
@@ -1862,8 +1878,11 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     const int S = conv_ksplit(a.Ho, a.Wo, a.cout, p.K, a.out_f32 != 0);
     const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold && !special &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
-    // one LDS stage on 128 x 64 tiles: a spatial 1x1 layer with K <= 1024,
-    // or any other spatial layer with at least 512 such tiles; on 128 x 256
+    // one LDS stage on 128 x 64 tiles: a spatial 1x1 layer with K <= 512, or
+    // K <= 1024 and at least 1024 such tiles (deep K on fewer tiles waits on
+    // fewer round trips in rounds of two K steps: ResNet-50 stage-3/4
+    // reductions 5-8 % faster), or any other spatial layer with at least 512
+    // such tiles; on 128 x 256
     // tiles (eight waves, whole 512-byte row pieces per workgroup: the
     // output-heavy layers' stores were the limit) when Cout is a multiple of
     // 256 and there are at least 512 of them (measured 4-15 % faster on the
@@ -1871,7 +1890,8 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     // tiles per CU, slower with fewer)
     const long t12864 = (static_cast<long>(Mh) + 127) / 128 * ((a.cout + 63) / 64);
     const long t128256 = (static_cast<long>(Mh) + 127) / 128 * ((a.cout + 255) / 256);
-    const bool one = !split && a.cout >= 64 && a.Ho * a.Wo > 1 && (a.k == 1 ? p.Kp <= 1024 : t12864 >= 512);
+    const bool one = !split && a.cout >= 64 && a.Ho * a.Wo > 1 &&
+                     (a.k == 1 ? p.Kp <= 512 || (p.Kp <= 1024 && t12864 >= 1024) : t12864 >= 512);
     const bool wide = one && a.cout % 256 == 0 && t128256 >= 512;
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
                       : wide ? TileCfg{128, 256, 2, 4}
