@@ -69,11 +69,14 @@ CASES = [
     (3, 16, 16, 8, 16, 3, 1, 1, True, 2),
     (6, 11, 16, 8, 64, 3, 1, 1, True, 0),       # 8 -> 64 stays on the register-weight halo kernel
     (5, 12, 12, 64, 24, 3, 1, 1, True, 2),      # Cout not a multiple of 8
-    (37, 4, 4, 512, 512, 3, 1, 1, False, 1),    # K split in 4, ragged last row tile
-    (37, 8, 8, 512, 512, 3, 2, 1, True, 1),     # strided, K split in 4
+    (37, 4, 4, 512, 512, 3, 1, 1, False, 1),    # deep K on 4x4 outputs, unsplit, ragged last row tile
+    (37, 8, 8, 512, 512, 3, 2, 1, True, 1),     # strided to 4x4, unsplit
     (5, 4, 4, 512, 384, 3, 1, 1, True, 2),      # three 128-channel tiles, GELU
-    (11, 7, 7, 512, 256, 3, 2, 1, False, 0),    # 7x7 -> 4x4, K split in 4
-    (6, 4, 4, 4608, 256, 1, 1, 0, False, 1),    # 1x1 with K = 4608, split in 4
+    (11, 7, 7, 512, 256, 3, 2, 1, False, 0),    # 7x7 -> 4x4, unsplit
+    (6, 4, 4, 4608, 256, 1, 1, 0, False, 1),    # 1x1 with K = 4608 on 16 pixels, unsplit
+    (37, 14, 14, 512, 512, 3, 2, 1, True, 1),   # strided 14x14 -> 7x7, K split in 4
+    (11, 12, 12, 512, 256, 3, 2, 1, False, 0),  # 12x12 -> 6x6, K split in 4
+    (6, 6, 6, 4608, 256, 1, 1, 0, False, 1),    # 1x1 with K = 4608 on 36 pixels, split in 4
     # deep K without a split: strided, deep 1x1, ragged channel tiles, many tiles
     (7, 9, 9, 64, 96, 3, 2, 1, True, 1),        # half-used second channel tile
     (3, 16, 16, 1024, 256, 1, 1, 0, True, 0),   # deep 1x1 with residual
@@ -140,7 +143,15 @@ def test_conv_op(case):
     _case(*case, seed=hash(case) % (2 ** 31))
 
 
-@pytest.mark.parametrize("case", [c for c in CASES if c[4] >= 256 and c[1] * c[2] <= 64], ids=str)
+def _split(c):
+    """Cases whose layer dycl_op_conv splits over K (deep K on 17-64 output
+    pixels per image)."""
+    n, H, W, cin, cout, k, stride, pad = c[:8]
+    Ho, Wo = (H + 2 * pad - k) // stride + 1, (W + 2 * pad - k) // stride + 1
+    return cout >= 256 and cout % 64 == 0 and k * k * cin >= 4608 and 16 < Ho * Wo <= 64 and (k != 3 or stride != 1)
+
+
+@pytest.mark.parametrize("case", [c for c in CASES if _split(c)], ids=str)
 def test_conv_op_unsplit_without_workspace(case):
     # the same layers without a workspace: one K range per tile
     _case(*case, seed=hash(case) % (2 ** 31), workspace=None)
@@ -151,11 +162,12 @@ def test_conv_op_split_rows_are_independent():
     # depends on the layer shape, not on n)
     from paper_2307_04963_amd import runtime
     rng = np.random.default_rng(11)
-    x = _bits(rng.standard_normal((100, 4, 4, 512))).cuda().view(torch.bfloat16)
+    x = _bits(rng.standard_normal((100, 14, 14, 512))).cuda().view(torch.bfloat16)
     w = to_bf16_bits(rng.uniform(-0.02, 0.02, (512, 3, 3, 512)).astype(np.float32))
     packed = torch.from_numpy(runtime.pack_conv_weights(w).view(np.int16)).cuda()
-    a = runtime.conv(x, packed, 512, 3, 1, 1, None, None, None, 1)
-    b = runtime.conv(x[:13].contiguous(), packed, 512, 3, 1, 1, None, None, None, 1)
+    assert runtime.conv_workspace_bytes(100, 14, 14, 512, 512, 3, 2, 1) > 0   # split over K
+    a = runtime.conv(x, packed, 512, 3, 2, 1, None, None, None, 1)
+    b = runtime.conv(x[:13].contiguous(), packed, 512, 3, 2, 1, None, None, None, 1)
     torch.cuda.synchronize()
     assert torch.equal(a[:13].view(torch.int16), b.view(torch.int16))
 
