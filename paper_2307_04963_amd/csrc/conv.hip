@@ -1527,7 +1527,8 @@ void dispatch_staged(const TileCfg& c, const ConvP& p, hipStream_t s) {
 // area, the time of the slowest CU (measured on the layer shapes of the
 // workloads; 256 x 256 tiles lost on every one of them)
 TileCfg choose_lds(int M, int cout, int Kp) {
-  const TileCfg c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2}, c32{128, 32, 4, 1};
+  const TileCfg c128{128, 128, 2, 2}, c12864{128, 64, 2, 2}, c64{64, 64, 2, 2}, c64128{64, 128, 2, 2},
+      c32{128, 32, 4, 1};
   if (cout < 64) return c32;
   // one K step: memory-bound; 128 x 64 tiles (24 KB of LDS, five
   // workgroups per CU by registers) keep the most rows in flight (measured
@@ -1537,15 +1538,17 @@ TileCfg choose_lds(int M, int cout, int Kp) {
   constexpr long kCUs = 256;
   const long r128 = (tiles_of(c128, M, cout) + 2 * kCUs - 1) / (2 * kCUs);
   const long t12864 = tiles_of(c12864, M, cout), r12864 = (t12864 + 3 * kCUs - 1) / (3 * kCUs);
+  // few tiles (a layer bound by its chains of K rounds): 64 x 64 below ~1.5
+  // tiles of 128 x 64 per CU, 64 x 128 below four (measured with rounds of
+  // two K steps: ResNet-50's strided stage-3 3x3 49 -> 42 us, its stage-3/4
+  // reductions and stage-4 expansions 4-10 % faster than 128 x 64)
+  if (t12864 < 400) return c64;
+  if (t12864 < 1024 && cout % 128 == 0) return c64128;
   // 128 x 128 when its rounds of double-area tiles take no longer, or when
   // one tile column spans a short-K layer's channels, so that each input
   // pixel (the bulk of its traffic) is fetched by one workgroup
   if (cout >= 128 && (2 * r128 <= r12864 || (cout == 128 && Kp <= 256))) return c128;
-  // 64 x 64 when 128 x 64 would give fewer than ~1.5 tiles per CU (with
-  // rounds of two K steps: the ResNet-18 stage-4 strided 3x3 layer 33 -> 29
-  // us, the ACT loop's short steps 10-15 % faster; at 2.5 tiles per CU
-  // 128 x 64 stays ahead)
-  return t12864 >= 400 ? c12864 : c64;
+  return c12864;
 }
 
 // stages: one (`one`, 128 x 64 or 128 x 256 tiles only: the K steps taken
@@ -1576,6 +1579,7 @@ void dispatch_lds(const TileCfg& c, const ConvP& p, hipStream_t s, int S = 1, bo
     case 128064: go_lds<128, 64, 2, 2, KS>(p, s, S, one); break;
     case 128256: go_lds<128, 256, 2, 4, KS>(p, s, S, one); break;
     case 64064: go_lds<64, 64, 2, 2, KS>(p, s, S, one); break;
+    case 64128: go_lds<64, 128, 2, 2, KS>(p, s, S, one); break;
     default: go_lds<128, 32, 4, 1, KS>(p, s, S, one); break;
   }
 }
@@ -1880,11 +1884,10 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     const int S = conv_ksplit(a.Ho, a.Wo, a.cout, p.K, a.out_f32 != 0);
     const bool split = S > 1 && a.splitws && !a.res_rows && !a.dst_rows && !a.kfold && !special &&
                        a.splitws_bytes >= static_cast<size_t>(S) * p.M * a.cout * sizeof(float);
-    // one LDS stage on 128 x 64 tiles: a spatial 1x1 layer with K <= 512, or
-    // K <= 1024 and at least 1024 such tiles (deep K on fewer tiles waits on
-    // fewer round trips in rounds of two K steps: ResNet-50 stage-3/4
-    // reductions 5-8 % faster), or any other spatial layer with at least 512
-    // such tiles; on 128 x 256
+    // one LDS stage on 128 x 64 tiles: a spatial layer with at least 1024
+    // such tiles (and K <= 1024 for a 1x1 layer); fewer tiles wait on fewer
+    // round trips in rounds of two K steps (the ResNet-50 stage-3/4 layers
+    // 4-15 % faster); on 128 x 256
     // tiles (eight waves, whole 512-byte row pieces per workgroup: the
     // output-heavy layers' stores were the limit) when Cout is a multiple of
     // 256 and there are at least 512 of them (measured 4-15 % faster on the
@@ -1892,8 +1895,7 @@ bool conv_bf16(const ConvArgs& a, hipStream_t s) {
     // tiles per CU, slower with fewer)
     const long t12864 = (static_cast<long>(Mh) + 127) / 128 * ((a.cout + 63) / 64);
     const long t128256 = (static_cast<long>(Mh) + 127) / 128 * ((a.cout + 255) / 256);
-    const bool one = !split && a.cout >= 64 && a.Ho * a.Wo > 1 &&
-                     (a.k == 1 ? p.Kp <= 512 || (p.Kp <= 1024 && t12864 >= 1024) : t12864 >= 512);
+    const bool one = !split && a.cout >= 64 && a.Ho * a.Wo > 1 && t12864 >= 1024 && (a.k != 1 || p.Kp <= 1024);
     const bool wide = one && a.cout % 256 == 0 && t128256 >= 512;
     const TileCfg c = split ? (a.cout % 128 == 0 ? TileCfg{128, 128, 2, 2} : TileCfg{128, 64, 2, 2})
                       : wide ? TileCfg{128, 256, 2, 4}

@@ -88,7 +88,10 @@ CASES = [
     (24, 56, 56, 128, 256, 1, 1, 0, False, 2),  # one stage, 128 x 256 tiles, two K steps in turn, GELU
     (48, 28, 28, 384, 512, 1, 1, 0, True, 1),   # one stage, 128 x 256 tiles, six K steps, residual
     (40, 28, 28, 512, 128, 1, 1, 0, False, 1),  # one stage, 128 x 64 tiles, eight K steps
-    (42, 56, 56, 128, 128, 3, 2, 1, False, 1),  # strided 3x3 on one stage (516 tiles of 128 x 64)
+    (42, 56, 56, 128, 128, 3, 2, 1, False, 1),  # strided 3x3, 516 tiles of 128 x 64: 64 x 128 tiles
+    (107, 14, 14, 1024, 256, 1, 1, 0, False, 1),  # 656 tiles: 64 x 128, rounds of two K steps
+    (107, 28, 28, 256, 256, 3, 2, 1, True, 1),    # strided 3x3 on 64 x 128 tiles, residual
+    (30, 14, 14, 1024, 256, 1, 1, 0, True, 2),    # 184 tiles: 64 x 64, GELU
 ]
 
 
