@@ -1770,11 +1770,11 @@ const uint16_t* zero_page() {
 }
 
 int conv_ksplit(int Ho, int Wo, int cout, int K, bool out_f32) {
-  // measured with rounds of two K steps: K = 4608 on 7x7 outputs (ResNet-50
-  // stage 4, 51 images) gains from four ranges (42 -> 34 us); on 4x4 outputs
-  // (ResNet-18 stage 4, 255-774 images) one range is 8-16 % faster; K = 2304
-  // loses from two (the partial sums cost more than the idle CUs)
-  if (out_f32 || Ho * Wo > 64 || Ho * Wo <= 16 || K < 4608 || cout < 256 || cout % 64) return 1;
+  // measured: K = 4608 on 4x4 and 7x7 outputs gains from four ranges
+  // (ResNet-50 stage 4, 51 images: 42 -> 34 us; ResNet-18 stage 4, 255
+  // images: its step 1.218 -> 1.201 ms, same box, interleaved runs), K =
+  // 2304 loses from two (the partial sums cost more than the idle CUs)
+  if (out_f32 || Ho * Wo > 64 || K < 4608 || cout < 256 || cout % 64) return 1;
   return 4;
 }
 

@@ -290,12 +290,12 @@ def test_conv_pack_and_validation():
     assert "aligned" in _lib.last_error()
     assert lib.dycl_op_conv(*args(ws=C.c_void_p(264), wsb=4096)) == -1   # misaligned workspace
     assert lib.dycl_op_conv(*args(n=0)) == 0                              # nothing to do
-    # K split workspace: deep K on 17-64 output pixels per image only, sized by
-    # S * n * Ho * Wo * cout fp32
+    # K split workspace: deep K on at most 64 output pixels per image only,
+    # sized by S * n * Ho * Wo * cout fp32
     assert lib.dycl_op_conv_workspace_bytes(255, 14, 14, 512, 512, 3, 2, 1) == 4 * 255 * 49 * 512 * 4
     assert lib.dycl_op_conv_workspace_bytes(255, 6, 6, 4608, 256, 1, 1, 0) == 4 * 255 * 36 * 256 * 4
-    assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 512, 512, 3, 1, 1) == 0     # 16 pixels per image
-    assert lib.dycl_op_conv_workspace_bytes(255, 8, 8, 512, 512, 3, 2, 1) == 0     # 16 pixels per image
+    assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 512, 512, 3, 1, 1) == 4 * 255 * 16 * 512 * 4
+    assert lib.dycl_op_conv_workspace_bytes(255, 8, 8, 512, 512, 3, 2, 1) == 4 * 255 * 16 * 512 * 4
     assert lib.dycl_op_conv_workspace_bytes(255, 8, 8, 256, 512, 3, 2, 1) == 0     # K = 2304
     assert lib.dycl_op_conv_workspace_bytes(255, 16, 16, 512, 512, 3, 1, 1) == 0   # 256 pixels per image
     assert lib.dycl_op_conv_workspace_bytes(255, 4, 4, 128, 512, 3, 1, 1) == 0     # K = 1152
