@@ -109,11 +109,13 @@ __global__ __launch_bounds__(kThr) __attribute__((amdgpu_waves_per_eu(4))) void 
   static_assert(kRowsT * C1 * 2 <= X_BYTES, "the y1 staging takes the place of x");
   static_assert(X_BYTES == 16 * kThr && CPR == 32, "one x load per thread; 32 chunks per y3 row");
   static_assert(NV / 4 <= kThr, "one vector load per thread at most");
-  __shared__ __align__(16) char smem[S_BYTES + A_BYTES + NV * 4];
-  char* const sw = smem;                   // W3, then W1
-  char* const sx = smem + W3_BYTES;        // x, then the y1 staging
-  char* const sa = smem + S_BYTES;         // the residual, then y3
-  float* const sv = reinterpret_cast<float*>(smem + S_BYTES + A_BYTES);
+  // separate LDS objects, so that the compiler can tell a direct-to-LDS
+  // load into one from a read of another (and does not wait for the loads
+  // in flight before reading the vectors)
+  __shared__ __align__(16) char sw[W3_BYTES];   // W3, then W1
+  __shared__ __align__(16) char sx[X_BYTES];    // x, then the y1 staging
+  __shared__ __align__(16) char sa[A_BYTES];    // the residual, then y3
+  __shared__ __align__(16) float sv[NV];
 
   const int HW = p.H * p.W;
   const int M = (p.nc ? min(*p.nc, p.nmax) : p.nmax) * HW;
@@ -188,14 +190,36 @@ __global__ __launch_bounds__(kThr) __attribute__((amdgpu_waves_per_eu(4))) void 
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc3[b][r] = 0.f;
+  // the projection's sums become its output as the unfused layer stores it
+  // (scale, shift, bf16), divided by the block's scale: done while the
+  // block's first K step is in flight
+  auto fold_round = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c0 = 64 * wc + 32 * b + 8 * g + 4 * (lane >> 5);
+        const float4 sp = *reinterpret_cast<const float4*>(sv + 2 * C3 + c0);
+        const float4 bp = *reinterpret_cast<const float4*>(sv + 3 * C3 + c0);
+        const float4 iv = *reinterpret_cast<const float4*>(sv + 4 * C3 + c0);
+        const float spv[4] = {sp.x, sp.y, sp.z, sp.w}, bpv[4] = {bp.x, bp.y, bp.z, bp.w},
+                    ivv[4] = {iv.x, iv.y, iv.z, iv.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          acc3[b][4 * g + i] =
+              __uint_as_float(static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(
+                                  fmaf(acc3[b][4 * g + i], spv[i], bpv[i]))))
+                              << 16) *
+              ivv[i];
+      }
+  };
   for (int kt = 0; kt < nk3; ++kt) {
     if (kt) {
       lds_sync();   // every wave is done reading the previous step
       issue_xw(kt);
-      vm_barrier<0>();
-    } else {
-      vm_barrier<0>();
+      if (FOLD && kt == kfold) fold_round();
     }
+    vm_barrier<0>();
     const int lsw = (lane >> 1) & 7;
     const char* pa = sw + (64 * wc + (lane & 31)) * 128;
     const char* pb = sx + (32 * wp + (lane & 31)) * 128;
@@ -213,28 +237,6 @@ __global__ __launch_bounds__(kThr) __attribute__((amdgpu_waves_per_eu(4))) void 
 #pragma unroll
       for (int b = 0; b < 2; ++b)
         acc3[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][b], bx[s & 1], acc3[b], 0, 0, 0);
-    }
-    if (FOLD && kt + 1 == kfold) {
-      // the projection's sums become its output as the unfused layer
-      // stores it (scale, shift, bf16), divided by the block's scale
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c0 = 64 * wc + 32 * b + 8 * g + 4 * (lane >> 5);
-          const float4 sp = *reinterpret_cast<const float4*>(sv + 2 * C3 + c0);
-          const float4 bp = *reinterpret_cast<const float4*>(sv + 3 * C3 + c0);
-          const float4 iv = *reinterpret_cast<const float4*>(sv + 4 * C3 + c0);
-          const float spv[4] = {sp.x, sp.y, sp.z, sp.w}, bpv[4] = {bp.x, bp.y, bp.z, bp.w},
-                      ivv[4] = {iv.x, iv.y, iv.z, iv.w};
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            acc3[b][4 * g + i] =
-                __uint_as_float(static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(
-                                    fmaf(acc3[b][4 * g + i], spv[i], bpv[i]))))
-                                << 16) *
-                ivv[i];
-        }
     }
   }
   lds_sync();   // every wave is done reading W3 and x
