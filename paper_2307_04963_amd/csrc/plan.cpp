@@ -638,6 +638,8 @@ struct Run {
       a.H2 = sp.tensors[c.src2].H;
       a.W2 = sp.tensors[c.src2].W;
       a.s2 = c.s2;
+      // the pair kernel indexes the projection input's pixels in 32 bits
+      if (static_cast<long>(r.n) * a.H2 * a.W2 > 0x7fffffffL) return false;
       a.scale3 = fs;
       a.shift3 = fs + c.cout;
       a.fold_sp = fs + 2 * c.cout;
