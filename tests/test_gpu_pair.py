@@ -10,7 +10,7 @@ and the next block's first 1x1 layer, which reads nothing but its output
   its outputs against the oracle's float64 convolutions on sampled images
   within the fp32 accumulation bound (the second layer's reference takes the
   first layer's bf16 output as its input, as the network does).
-* The ResNet-50 early-exit plan at its benchmark batch: the same logits,
+* The ResNet-50 early-exit plan at its benchmark batch and at 37 images: the same logits,
   records and branch counts with the pairing on and off
   ("pair_pointwise": false), in the sync and device host modes; the pairing
   covers both first-stage boundaries, one of them a block whose projection
@@ -112,10 +112,13 @@ def test_conv_pair_op_rejects_other_shapes():
         runtime.conv_pair(x[..., :32].contiguous(), p, v, v, None, 256, p, v, v, 64)   # cin % 64 != 0
 
 
-def test_resnet50_plan_same_bits_with_and_without_pairs():
+@pytest.mark.parametrize("batch", [None, 37], ids=["benchmark_batch", "b37"])
+def test_resnet50_plan_same_bits_with_and_without_pairs(batch):
+    """At the benchmark batch and at 37 images (ragged last tiles at every
+    stage; the exits leave odd live counts, read on the device)."""
     from paper_2307_04963_amd import lowering, runtime
     name = "resnet50_exit"
-    B = configs.DEFAULT_BATCH[name]
+    B = batch or configs.DEFAULT_BATCH[name]
     wl = configs.build(name)
     blob, man = wl.blob()
     spec = lowering.lower(wl.arch, man)
@@ -123,12 +126,13 @@ def test_resnet50_plan_same_bits_with_and_without_pairs():
     off = runtime.Plan(json.dumps(dict(spec, pair_pointwise=False)), blob, B)
     x, aux = wl.inputs(B)
     # the pairing took both first-stage boundaries and two of the second stage
-    # (labels of the profiled launches)
+    # (labels of the profiled launches; the second stage's pairs run when
+    # some rows reach it)
     on.profile(True)
-    runtime.run_numpy(on, wl, x, aux)
+    res = runtime.run_numpy(on, wl, x, aux)
     labels = [r["label"] for r in on.profile_launches() if " + " in r["label"]]
     on.profile(False)
-    assert len(labels) == 4, labels
+    assert len(labels) == (4 if res["counts"][0][1] > 0 else 2), labels
     for mode in ("sync", "device"):
         print(f"[pair-plan] {name} B={B} mode={mode}", flush=True)
         on.set_host_mode(mode)
